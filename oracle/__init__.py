@@ -1,0 +1,192 @@
+"""Python wrapper of the LDA oracle (plain single-threaded C, fp64).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  It shares no code
+with the GPU library (``paper_2007_08725_amd``) and the library never calls it.
+
+Every function follows the paper's definitions (arXiv 2007.08725):
+  * ``iterate``  -- one synchronous ESCA iteration, Sec. 2.2 Eq. 1-2, drawn in
+                    the three-branch canonical order of Sec. 3.2 Eq. 5;
+                    ``mode="dense"`` is the brute-force form over all K topics,
+                    ``mode="sparse"`` the decomposition over nz(D[d]).
+  * ``llpt``     -- log-likelihood per token (log2), Sec. 2.2.
+  * ``build_counts`` -- D (CSR), W (dense), T = column sums of W, Sec. 2.2.
+  * ``philox``, ``uniform``, ``init_topics`` -- Philox4x32-10 draws
+                    (Salmon et al., SC'11); the paper only says u ~ U[0,1].
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "lda_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "_lda_oracle.so")
+_lib = None
+
+STAT_NAMES = ("flagged", "skip3", "sest_violations", "skip_not_k1", "fallback", "skip_after_s", "nnz_scanned")
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc: -O2, IEEE fp64, no FMA contraction."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-std=c11", "-fPIC", "-shared",
+                        "-o", tmp, _SRC, "-lm"], check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB_PATH)
+        P, I64, I32, U64, U32, D = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64,
+                                    ctypes.c_uint32, ctypes.c_double)
+        lib.ora_philox4x32_10.argtypes = [P, P, P]
+        lib.ora_uniform.argtypes = [U64, U32, U64]
+        lib.ora_uniform.restype = D
+        lib.ora_init_topic.argtypes = [U64, U64, I32]
+        lib.ora_init_topic.restype = I32
+        lib.ora_init.argtypes = [I64, I32, U64, P]
+        lib.ora_build_counts.argtypes = [I64, P, P, P, I32, I32, I32, P, P, P, P, P, P]
+        lib.ora_iterate.argtypes = [ctypes.c_int, ctypes.c_int, I64, P, P, I32, I32, I32, D, D, U64, U32, P, I64, P,
+                                    P, P, P, P]
+        lib.ora_llpt.argtypes = [ctypes.c_int, I64, P, P, P, I32, I32, I32, D, D]
+        lib.ora_llpt.restype = D
+        lib.ora_draw_given_u.argtypes = [ctypes.c_int, I64, P, P, P, I32, I32, I32, D, D, I64, D, P, P]
+        lib.ora_draw_given_u.restype = I32
+        lib.ora_what_row.argtypes = [I64, P, P, P, I32, I32, I32, D, I32, P]
+        lib.ora_word_stats.argtypes = [I64, P, P, P, I32, I32, I32, D, D, P, P, P, P, P, P]
+        _lib = lib
+    return _lib
+
+
+def _p(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def philox(ctr, key) -> np.ndarray:
+    """Philox4x32-10 of one 128-bit counter (4 x uint32) under a 64-bit key (2 x uint32)."""
+    lib = _load()
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.empty(4, dtype=np.uint32)
+    lib.ora_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def uniform(seed: int, t: int, i: int) -> float:
+    return float(_load().ora_uniform(seed, t, i))
+
+
+def init_topics(n: int, K: int, seed: int) -> np.ndarray:
+    z = np.empty(n, dtype=np.int32)
+    _load().ora_init(n, K, seed, _p(z))
+    return z
+
+
+def build_counts(word, doc, z, M: int, V: int, K: int) -> dict:
+    lib = _load()
+    word, doc, z = _i32(word), _i32(doc), _i32(z)
+    n = word.shape[0]
+    out = dict(len=np.empty(M, np.int64), doff=np.empty(M + 1, np.int64), dtop=np.empty(max(n, 1), np.int32),
+               dcnt=np.empty(max(n, 1), np.int32), W=np.empty((V, K), np.int32), T=np.empty(K, np.int64))
+    rc = lib.ora_build_counts(n, _p(word), _p(doc), _p(z), M, V, K, _p(out["len"]), _p(out["doff"]),
+                              _p(out["dtop"]), _p(out["dcnt"]), _p(out["W"]), _p(out["T"]))
+    if rc:
+        raise ValueError("ora_build_counts failed (%d)" % rc)
+    nnz = int(out["doff"][M])
+    out["dtop"] = out["dtop"][:nnz].copy()
+    out["dcnt"] = out["dcnt"][:nnz].copy()
+    return out
+
+
+def iterate(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float, seed: int, t: int,
+            mode: str = "sparse", g: int = 2, idx=None, want_Z: bool = False):
+    """One synchronous iteration from the snapshot built from ``z``.
+
+    Returns ``(z_new, flags, stats[, Z])``; with ``idx`` only those tokens are
+    drawn and the outputs are aligned with ``idx``.  flags bit0 = draw within
+    1e-9*Z of a CDF edge, bit1 = step-3 skip test fired.
+    """
+    lib = _load()
+    word, doc, z = _i32(word), _i32(doc), _i32(z)
+    n = word.shape[0]
+    if idx is not None:
+        idx = np.ascontiguousarray(idx, dtype=np.int64)
+        m = idx.shape[0]
+    else:
+        m = n
+    z_out = np.empty(m, np.int32)
+    flags = np.empty(m, np.uint8)
+    Z = np.empty(m, np.float64) if want_Z else None
+    stats = np.zeros(8, np.int64)
+    rc = lib.ora_iterate(0 if mode == "sparse" else 1, g, n, _p(word), _p(doc), M, V, K, alpha, beta, seed, t, _p(z),
+                         m if idx is not None else 0, _p(idx), _p(z_out), _p(flags), _p(Z), _p(stats))
+    if rc:
+        raise ValueError("ora_iterate failed (%d)" % rc)
+    st = {name: int(stats[j]) for j, name in enumerate(STAT_NAMES)}
+    if want_Z:
+        return z_out, flags, st, Z
+    return z_out, flags, st
+
+
+def llpt(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float, mode: str = "sparse") -> float:
+    word, doc, z = _i32(word), _i32(doc), _i32(z)
+    return float(_load().ora_llpt(0 if mode == "sparse" else 1, word.shape[0], _p(word), _p(doc), _p(z), M, V, K,
+                                  alpha, beta))
+
+
+def word_stats(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float) -> dict:
+    lib = _load()
+    word, doc, z = _i32(word), _i32(doc), _i32(z)
+    out = dict(K1=np.empty(V, np.int32), K2=np.empty(V, np.int32), a1=np.empty(V), a2=np.empty(V), a3=np.empty(V),
+               Qp=np.empty(V))
+    rc = lib.ora_word_stats(word.shape[0], _p(word), _p(doc), _p(z), M, V, K, alpha, beta, _p(out["K1"]),
+                            _p(out["K2"]), _p(out["a1"]), _p(out["a2"]), _p(out["a3"]), _p(out["Qp"]))
+    if rc:
+        raise ValueError("ora_word_stats failed (%d)" % rc)
+    return out
+
+
+def run(word, doc, *, M: int, V: int, K: int, alpha: float, beta: float, seed: int, iters: int, t0: int = 0,
+        z0=None, mode: str = "sparse"):
+    """Initial topics (or ``z0``), then ``iters`` synchronous iterations.  Returns the list of z after each."""
+    z = init_topics(len(word), K, seed) if z0 is None else _i32(z0)
+    traj = [z]
+    for t in range(t0, t0 + iters):
+        z, _, _ = iterate(word, doc, z, M=M, V=V, K=K, alpha=alpha, beta=beta, seed=seed, t=t, mode=mode)
+        traj.append(z)
+    return traj
+
+
+def draw_given_u(word, doc, z, i: int, u: float, *, M: int, V: int, K: int, alpha: float, beta: float,
+                 mode: str = "sparse"):
+    """Draw token ``i`` of the snapshot built from ``z`` with the uniform ``u``.  Returns (topic, Z, flag)."""
+    word, doc, z = _i32(word), _i32(doc), _i32(z)
+    Z = ctypes.c_double(0.0)
+    f = ctypes.c_uint8(0)
+    k = _load().ora_draw_given_u(0 if mode == "sparse" else 1, word.shape[0], _p(word), _p(doc), _p(z), M, V, K,
+                                 alpha, beta, i, u, ctypes.byref(Z), ctypes.byref(f))
+    if k < 0:
+        raise ValueError("ora_draw_given_u: bad argument")
+    return int(k), float(Z.value), int(f.value)
+
+
+def what_row(word, doc, z, v: int, *, M: int, V: int, K: int, beta: float) -> np.ndarray:
+    """W^[v][k] = (W[v][k]+beta) / (T[k]+V*beta) for every topic k (Eq. 2)."""
+    word, doc, z = _i32(word), _i32(doc), _i32(z)
+    out = np.empty(K)
+    if _load().ora_what_row(word.shape[0], _p(word), _p(doc), _p(z), M, V, K, beta, v, _p(out)):
+        raise ValueError("ora_what_row failed")
+    return out

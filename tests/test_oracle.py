@@ -1,0 +1,319 @@
+"""Pins for the oracle (CPU only).
+
+Each test ties the oracle to something other than itself: the paper's worked
+example (Sec. 2.2), rocRAND's Philox4x32-10, the closed-form conditional of
+Eq. 1 (exact segment layout and a chi-square test), closed-form limits of the
+LLPT, brute-force count tables, and the agreement of two independent forms
+(dense brute force vs sparse decomposition).
+"""
+import json
+import math
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+from scipy import stats as sps
+
+import oracle as ora
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+GOLDEN = os.path.join(HERE, "golden")
+
+
+def _counts_np(word, doc, z, M, V, K):
+    D = np.zeros((M, K), np.int64)
+    W = np.zeros((V, K), np.int64)
+    np.add.at(D, (np.asarray(doc), np.asarray(z)), 1)
+    np.add.at(W, (np.asarray(word), np.asarray(z)), 1)
+    return D, W, W.sum(axis=0)
+
+
+def _eq1_layout(word, doc, z, M, V, K, alpha, beta, i):
+    """Canonical segments [K1 | S' asc | Q' asc] written from Eq. 1 and Eq. 5 with numpy."""
+    D, W, T = _counts_np(word, doc, z, M, V, K)
+    wh = (W[word[i]] + beta) / (T + V * beta)
+    d = doc[i]
+    k1 = int(np.argmax(wh))  # first maximum = lowest topic id
+    segs = [(k1, (D[d, k1] + alpha) * wh[k1])]
+    segs += [(k, D[d, k] * wh[k]) for k in range(K) if k != k1 and D[d, k] > 0]
+    segs += [(k, alpha * wh[k]) for k in range(K) if k != k1]
+    p = (D[d] + alpha) * wh  # Eq. 1 numerator
+    return segs, p / p.sum()
+
+
+def _tiny_case():
+    """3 docs, 5 words, 4 topics (the closed-form brute-force case)."""
+    word = np.array([0, 1, 2, 0, 3, 4, 1, 2, 0, 3, 3, 4], np.int32)
+    doc = np.array([0, 0, 0, 0, 0, 1, 1, 1, 2, 2, 2, 2], np.int32)
+    z = np.array([0, 1, 2, 3, 0, 1, 1, 2, 3, 3, 0, 2], np.int32)
+    return word, doc, z, dict(M=3, V=5, K=4, alpha=0.5, beta=0.01)
+
+
+def _random_corpus(rng, max_m=20, max_v=30, kmin=2, kmax=8, max_n=200):
+    M = int(rng.integers(1, max_m + 1))
+    V = int(rng.integers(1, max_v + 1))
+    K = int(rng.integers(kmin, kmax + 1))
+    n = int(rng.integers(1, max_n + 1))
+    word = rng.integers(0, V, n).astype(np.int32)
+    doc = rng.integers(0, M, n).astype(np.int32)
+    return word, doc, M, V, K
+
+
+# ---------------------------------------------------------------- worked example
+
+@pytest.fixture(scope="module")
+def wex():
+    with open(os.path.join(GOLDEN, "worked_example.json")) as f:
+        return json.load(f)
+
+
+def _wex_args(w):
+    return (np.array(w["word"], np.int32), np.array(w["doc"], np.int32), np.array(w["topic"], np.int32),
+            dict(M=w["M"], V=w["V"], K=w["K"], alpha=w["alpha"], beta=w["beta"]))
+
+
+def test_worked_example_counts(wex):
+    word, doc, z, kw = _wex_args(wex)
+    c = ora.build_counts(word, doc, z, kw["M"], kw["V"], kw["K"])
+    assert c["T"].tolist() == wex["printed"]["T"]
+    assert c["W"][0].tolist() == wex["printed"]["W0"]
+    d2 = np.zeros(kw["K"], np.int64)
+    sl = slice(c["doff"][2], c["doff"][3])
+    d2[c["dtop"][sl]] = c["dcnt"][sl]
+    assert d2.tolist() == wex["printed"]["D2"]
+    assert c["len"].tolist() == [2, 2, 3]
+
+
+def test_worked_example_what_and_two_branch(wex):
+    """W^[0] o alpha, W^[0] o D[2], the Q prefix, the branch test and the new topic (Sec. 2.2)."""
+    word, doc, z, kw = _wex_args(wex)
+    pr = wex["printed"]
+    wh = ora.what_row(word, doc, z, 0, M=kw["M"], V=kw["V"], K=kw["K"], beta=kw["beta"])
+    np.testing.assert_allclose(kw["alpha"] * wh, pr["alpha_times_What0"], rtol=2e-3)
+    np.testing.assert_allclose(wh * np.array(pr["D2"]), pr["What0_times_D2"], rtol=2e-3, atol=5e-5)
+    q = np.cumsum(kw["alpha"] * wh)
+    np.testing.assert_allclose(q, pr["Q_prefix"], rtol=2e-3)
+    S = float(np.sum(wh * np.array(pr["D2"])))
+    Q = float(q[-1])
+    u = pr["u"]
+    assert not (u <= S / (S + Q))           # the Q branch is taken
+    x = (1 - u) * (S + Q)
+    assert x == pytest.approx(pr["reflected_u_times_SQ"], rel=2e-3)
+    assert int(np.argmax(q > x)) == pr["new_topic"]   # descending the Q tree
+    # the oracle's canonical three-branch draw with the same u gives the same topic
+    k, Z, flag = ora.draw_given_u(word, doc, z, wex["token_index"], u, **kw)
+    assert k == pr["new_topic"]
+    kd, Zd, flagd = ora.draw_given_u(word, doc, z, wex["token_index"], u, mode="dense", **kw)
+    assert (kd, Zd, flagd) == (k, Z, flag)
+
+
+def test_worked_example_three_branch(wex):
+    """K1/K2, a1..a3, M, S', S_est, Q', Z of Eq. 5-9 on the example token."""
+    word, doc, z, kw = _wex_args(wex)
+    dv = wex["derived_three_branch_not_printed"]
+    ws = ora.word_stats(word, doc, z, **kw)
+    assert (ws["K1"][0], ws["K2"][0]) == (dv["K1"], dv["K2"])
+    for key in ("a1", "a2", "a3"):
+        assert ws[key][0] == pytest.approx(dv[key], rel=1e-4)
+    assert ws["Qp"][0] == pytest.approx(dv["Q_prime"], rel=1e-5)
+    _, Z, flag = ora.draw_given_u(word, doc, z, wex["token_index"], wex["printed"]["u"], **kw)
+    assert Z == pytest.approx(dv["Z"], rel=1e-6)
+    assert bool(flag & 2) == dv["skip3"]
+    Mm = ws["a1"][0] * (0 + kw["alpha"])
+    assert Mm == pytest.approx(dv["Mmax"], rel=1e-6)
+    assert Z - Mm - ws["Qp"][0] == pytest.approx(dv["S_prime"], rel=1e-5)
+
+
+# ------------------------------------------------------------------- Philox
+
+def test_philox_matches_rocrand():
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    exe = os.path.join(os.environ.get("TMPDIR", "/tmp"), "rocrand_philox_kat_%d" % os.getpid())
+    subprocess.run([hipcc, "-O1", "-o", exe, os.path.join(HERE, "pins", "rocrand_philox_kat.cpp")], check=True,
+                   capture_output=True)
+    rng = np.random.default_rng(5)
+    cases = [(42, 0, 0, 0, 0), (42, 5, 0, 3, 0), (2**64 - 1, 2**32 - 1, 2**30 - 1, 2**32 - 1, 2**32 - 1)]
+    for _ in range(200):
+        cases.append((int(rng.integers(0, 2**63)), int(rng.integers(0, 2**32)), int(rng.integers(0, 2**30)),
+                      int(rng.integers(0, 2**32)), int(rng.integers(0, 2))))
+    inp = "".join("%d %d %d %d %d\n" % c for c in cases)
+    out = subprocess.run([exe], input=inp, capture_output=True, text=True, check=True).stdout.split("\n")
+    os.unlink(exe)
+    for c, line in zip(cases, out):
+        want = [int(x) for x in line.split()]
+        got = ora.philox(c[1:], [c[0] & 0xFFFFFFFF, c[0] >> 32]).tolist()
+        assert got == want, c
+
+
+def test_uniform_and_init_are_uniform():
+    n = 200_000
+    z = ora.init_topics(n, 16, 42)
+    obs = np.bincount(z, minlength=16)
+    assert sps.chisquare(obs).pvalue > 1e-3
+    u = np.array([ora.uniform(42, 3, i) for i in range(20_000)])
+    assert u.min() >= 0.0 and u.max() < 1.0
+    assert sps.kstest(u, "uniform").pvalue > 1e-3
+    # the counter layout keys on (token, iteration): different t give different draws
+    assert ora.uniform(42, 0, 7) != ora.uniform(42, 1, 7)
+    assert ora.uniform(42, 0, 7) != ora.uniform(43, 0, 7)
+
+
+# --------------------------------------------------------- closed form, Eq. 1
+
+@pytest.mark.parametrize("mode", ["sparse", "dense"])
+def test_canonical_layout_from_eq1(mode):
+    """Every segment of [K1 | S' | Q'] built from Eq. 1/5 maps to its topic; edges are flagged."""
+    cases = [_tiny_case()]
+    rng = np.random.default_rng(17)
+    for _ in range(6):
+        word, doc, M, V, K = _random_corpus(rng, max_n=40)
+        z = rng.integers(0, K, len(word)).astype(np.int32)
+        cases.append((word, doc, z, dict(M=M, V=V, K=K, alpha=float(rng.uniform(0.05, 3)), beta=0.01)))
+    for word, doc, z, kw in cases:
+        for i in range(len(word)):
+            segs, _ = _eq1_layout(word, doc, z, kw["M"], kw["V"], kw["K"], kw["alpha"], kw["beta"], i)
+            w = np.array([s[1] for s in segs])
+            cum = np.concatenate([[0.0], np.cumsum(w)])
+            Z = cum[-1]
+            for j, (k, width) in enumerate(segs):
+                if width <= 1e-6 * Z:
+                    continue
+                got, Zo, flag = ora.draw_given_u(word, doc, z, i, 0.5 * (cum[j] + cum[j + 1]) / Z, mode=mode, **kw)
+                assert got == k and not (flag & 1)
+                assert Zo == pytest.approx(Z, rel=1e-12)
+            # a draw exactly on an inner edge is flagged as near-boundary
+            j = 1
+            if cum[j] / Z < 1.0:
+                _, _, flag = ora.draw_given_u(word, doc, z, i, cum[j] / Z, mode=mode, **kw)
+                assert flag & 1
+
+
+def test_chi2_against_closed_form():
+    """10^6 Philox-driven draws on the 3-doc/5-word/4-topic case vs Eq. 1 (chi-square, p = 0.001)."""
+    word, doc, z, kw = _tiny_case()
+    n = len(word)
+    iters = 1_000_000 // n + 1
+    hist = np.zeros((n, kw["K"]), np.int64)
+    for t in range(iters):
+        zn, _, _ = ora.iterate(word, doc, z, seed=2024, t=t, **kw)
+        hist[np.arange(n), zn] += 1
+    total = 0.0
+    for i in range(n):
+        _, p = _eq1_layout(word, doc, z, kw["M"], kw["V"], kw["K"], kw["alpha"], kw["beta"], i)
+        exp = p * iters
+        chi = float(((hist[i] - exp) ** 2 / exp).sum())
+        assert chi < sps.chi2.ppf(0.999, kw["K"] - 1), (i, hist[i], exp)
+        total += chi
+    assert total < sps.chi2.ppf(0.999, n * (kw["K"] - 1))
+
+
+# ------------------------------------------------- dense == sparse, bit-exact
+
+def test_dense_and_sparse_forms_bit_identical():
+    rng = np.random.default_rng(123)
+    for seed in range(20):
+        word, doc, M, V, K = _random_corpus(rng)
+        kw = dict(M=M, V=V, K=K, alpha=float(rng.choice([50.0 / K, 0.1, 1.0])), beta=0.01)
+        z = ora.init_topics(len(word), K, seed)
+        for t in range(20):
+            zs, fs, ss, Zs = ora.iterate(word, doc, z, seed=seed, t=t, mode="sparse", want_Z=True, **kw)
+            zd, fd, sd, Zd = ora.iterate(word, doc, z, seed=seed, t=t, mode="dense", want_Z=True, **kw)
+            assert np.array_equal(zs, zd) and np.array_equal(fs, fd)
+            assert np.array_equal(Zs.view(np.uint64), Zd.view(np.uint64))
+            assert ss == sd
+            assert ss["sest_violations"] == 0 and ss["skip_not_k1"] == 0
+            z = zs
+
+
+def test_subset_draws_equal_full_draws():
+    rng = np.random.default_rng(9)
+    word, doc, M, V, K = _random_corpus(rng, max_n=300)
+    kw = dict(M=M, V=V, K=K, alpha=0.3, beta=0.01)
+    z = ora.init_topics(len(word), K, 1)
+    full, ff, _ = ora.iterate(word, doc, z, seed=1, t=4, **kw)
+    idx = rng.choice(len(word), size=min(50, len(word)), replace=False)
+    sub, fs, _ = ora.iterate(word, doc, z, seed=1, t=4, idx=idx, **kw)
+    assert np.array_equal(full[idx], sub) and np.array_equal(ff[idx], fs)
+
+
+# ------------------------------------------------------------ count tables
+
+def test_count_tables_match_brute_force():
+    rng = np.random.default_rng(3)
+    for _ in range(10):
+        word, doc, M, V, K = _random_corpus(rng, max_n=500)
+        z = rng.integers(0, K, len(word)).astype(np.int32)
+        c = ora.build_counts(word, doc, z, M, V, K)
+        D, W, T = _counts_np(word, doc, z, M, V, K)
+        assert np.array_equal(c["W"], W) and np.array_equal(c["T"], T)
+        for d in range(M):
+            sl = slice(c["doff"][d], c["doff"][d + 1])
+            tops = c["dtop"][sl]
+            assert np.all(np.diff(tops) > 0)          # ascending, unique
+            assert np.all(c["dcnt"][sl] > 0)
+            row = np.zeros(K, np.int64)
+            row[tops] = c["dcnt"][sl]
+            assert np.array_equal(row, D[d])
+        # invariants: sum_k D = len, sum_d D = sum_v W = T, sum T = N
+        assert np.array_equal(D.sum(1), c["len"])
+        assert np.array_equal(D.sum(0), T) and np.array_equal(W.sum(0), T)
+        assert T.sum() == len(word)
+
+
+# -------------------------------------------------------------- skip exactness
+
+@pytest.fixture(scope="module")
+def c1():
+    import lda_synth
+    return lda_synth.make_corpus("c1")
+
+
+def test_skip_bound_and_exactness_on_c1(c1):
+    """S' <= S_est on every token and 'skip => K1' on all 10 iterations of c1 (Eq. 8-9)."""
+    kw = dict(M=c1.n_docs, V=c1.V, K=c1.K, alpha=c1.alpha, beta=c1.beta)
+    z = ora.init_topics(c1.N, c1.K, 42)
+    skips = []
+    for t in range(10):
+        z1, f1, st1 = ora.iterate(c1.word, c1.doc, z, seed=42, t=t, g=1, **kw)
+        z2, f2, st2 = ora.iterate(c1.word, c1.doc, z, seed=42, t=t, g=2, **kw)
+        assert np.array_equal(z1, z2)       # g changes statistics, never draws
+        for st in (st1, st2):
+            assert st["sest_violations"] == 0 and st["skip_not_k1"] == 0
+        assert st2["skip3"] >= st1["skip3"]  # a tighter bound skips at least as often
+        skips.append(st2["skip3"])
+        assert st2["flagged"] < 1e-3 * c1.N
+        z = z2
+    assert skips[-1] > skips[0]
+
+
+# ---------------------------------------------------------------------- LLPT
+
+def test_llpt_closed_form_limits():
+    rng = np.random.default_rng(8)
+    for _ in range(5):
+        word, doc, M, V, K = _random_corpus(rng, max_n=300)
+        z = rng.integers(0, K, len(word)).astype(np.int32)
+        # one word: W^[0][k] = 1 for every k, and the doc mixture sums to 1 -> LLPT = 0
+        w1 = np.zeros_like(word)
+        for mode in ("sparse", "dense"):
+            assert abs(ora.llpt(w1, doc, z, M=M, V=1, K=K, alpha=0.7, beta=0.01, mode=mode)) < 1e-12
+        # beta -> infinity: W^ -> 1/V for every k -> LLPT = -log2 V
+        for mode in ("sparse", "dense"):
+            got = ora.llpt(word, doc, z, M=M, V=V, K=K, alpha=0.7, beta=1e13, mode=mode)
+            assert got == pytest.approx(-math.log2(V), abs=1e-9)
+        a = ora.llpt(word, doc, z, M=M, V=V, K=K, alpha=0.2, beta=0.01, mode="sparse")
+        b = ora.llpt(word, doc, z, M=M, V=V, K=K, alpha=0.2, beta=0.01, mode="dense")
+        assert a == pytest.approx(b, rel=1e-13)
+
+
+def test_llpt_rises_on_c1(c1):
+    """LLPT increases as sampling proceeds (Sec. 2.2, evaluation metric)."""
+    kw = dict(M=c1.n_docs, V=c1.V, K=c1.K, alpha=c1.alpha, beta=c1.beta)
+    traj = ora.run(c1.word, c1.doc, seed=42, iters=10, **kw)
+    ll = [ora.llpt(c1.word, c1.doc, z, **kw) for z in traj]
+    assert all(b > a for a, b in zip(ll, ll[1:]))
+    assert ll[-1] > ll[0] + 0.03
