@@ -1,0 +1,778 @@
+// Device kernels of liblda for gfx950 (CDNA4, wave64).
+//
+// One synchronous iteration (Sec. 2.2, 3.2, 4.3):
+//   k_begin      den[k] = T[k] + V*beta; scheduler counters reset
+//   k_word_pre   per word: top-3 of W^[v] (K1, K2, a1..a3), Q' and sum W^   (step 1, Sec. 3.2)
+//   k_doc_pass   per document: C1, C2 by lookup in the D row, u, M, S_est
+//                and the skip test; writes K1 or "undecided" into the
+//                word-ordered topic slot                                   (steps 2-3, Sec. 3.3)
+//   k_sampler    per region of a word: W^ row and Q' block prefix in LDS,
+//                then for every undecided token S' over nz(D[d]) and the
+//                final draw over [K1 | S' | Q']                            (steps 4-6, Sec. 4.3)
+//   k_zero_split, k_rebuild_w, k_rebuild_d
+//                count tables of the new assignment: dense rows of W by
+//                histogram (integer atomics for split words), sparse rows of
+//                W and rows of D as packed (topic << 16 | count) entries, T
+//                                                                          (Sec. 4.2-4.3)
+// All floating point is fp64 (IEEE divide for W^), built without
+// contraction so that the values match a plain sequential evaluation.
+#include "lda_internal.h"
+
+namespace lda {
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kGroup = 16;  // lanes that cooperate on one token in the sampler
+constexpr uint32_t kGroupMask = (1u << kGroup) - 1u;
+
+// ------------------------------------------------------------- Philox ----
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of
+//   (c0, c1, c2, c3) -> (hi(M1*c2) ^ c1 ^ k0, lo(M1*c2), hi(M0*c0) ^ c3 ^ k1, lo(M0*c0))
+// with the key bumped by the Weyl constants between rounds.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
+    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+// u in [0,1) for token i (input order) at iteration t: counter (i, 0, t, 0).
+__device__ __forceinline__ double uniform_draw(uint64_t seed, uint32_t t, uint32_t i) {
+  const uint4 x = philox4x32_10(make_uint4(i, 0u, t, 0u), uint32_t(seed), uint32_t(seed >> 32));
+  const uint64_t bits = (uint64_t(x.x) << 32) | uint64_t(x.y);
+  return double(bits >> 11) * 0x1p-53;
+}
+
+// Count of topic k in a packed row with ascending topics (0 if absent).
+__device__ __forceinline__ uint32_t row_lookup(const uint32_t *__restrict__ row, uint32_t nnz, uint32_t k) {
+  uint32_t lo = 0, hi = nnz;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if ((row[mid] >> 16) < k) lo = mid + 1;
+    else hi = mid;
+  }
+  return (lo < nnz && (row[lo] >> 16) == k) ? (row[lo] & 0xFFFFu) : 0u;
+}
+
+// W^[v][k] exactly as the paper defines it: an IEEE fp64 divide.
+__device__ __forceinline__ double what(uint32_t count, double beta, double den) { return (double(count) + beta) / den; }
+
+// -------------------------------------------------- wave / group helpers --
+template <int W>
+__device__ __forceinline__ double group_sum(double v) {
+#pragma unroll
+  for (int o = W / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, W);
+  return v;
+}
+
+template <int W>
+__device__ __forceinline__ uint32_t group_sum_u32(uint32_t v) {
+#pragma unroll
+  for (int o = W / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, W);
+  return v;
+}
+
+template <int W>
+__device__ __forceinline__ unsigned long long group_sum_u64(unsigned long long v) {
+#pragma unroll
+  for (int o = W / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, W);
+  return v;
+}
+
+template <int W>
+__device__ __forceinline__ double group_incl_scan(double v, int li) {
+#pragma unroll
+  for (int o = 1; o < W; o <<= 1) {
+    const double y = __shfl_up(v, o, W);
+    if (li >= o) v += y;
+  }
+  return v;
+}
+
+struct Top3 {
+  double v[3];
+  uint32_t k[3];
+};
+
+__device__ __forceinline__ bool better(double va, uint32_t ka, double vb, uint32_t kb) {
+  return va > vb || (va == vb && ka < kb);
+}
+
+__device__ __forceinline__ void top3_insert(Top3 &t, double v, uint32_t k) {
+  if (!better(v, k, t.v[2], t.k[2])) return;
+  t.v[2] = v;
+  t.k[2] = k;
+  if (better(t.v[2], t.k[2], t.v[1], t.k[1])) {
+    double tv = t.v[1]; uint32_t tk = t.k[1];
+    t.v[1] = t.v[2]; t.k[1] = t.k[2];
+    t.v[2] = tv; t.k[2] = tk;
+  }
+  if (better(t.v[1], t.k[1], t.v[0], t.k[0])) {
+    double tv = t.v[0]; uint32_t tk = t.k[0];
+    t.v[0] = t.v[1]; t.k[0] = t.k[1];
+    t.v[1] = tv; t.k[1] = tk;
+  }
+}
+
+// Block-wide sum of a double over 256 threads (fixed order).
+__device__ double block_sum(double v, double *scratch) {
+  v = group_sum<kWave>(v);
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  __syncthreads();
+  if (lane == 0) scratch[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+  for (int q = 0; q < kBlock / kWave; ++q) s += scratch[q];
+  __syncthreads();
+  return s;
+}
+
+// Block-wide exclusive prefix of a uint32 over 256 threads; *total gets the sum.
+__device__ uint32_t block_exclusive_u32(uint32_t v, uint32_t *scratch, uint32_t *total) {
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  uint32_t incl = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t y = __shfl_up(incl, o, kWave);
+    if (lane >= o) incl += y;
+  }
+  __syncthreads();
+  if (lane == kWave - 1) scratch[wave] = incl;
+  __syncthreads();
+  uint32_t off = 0, all = 0;
+  for (int q = 0; q < kBlock / kWave; ++q) {
+    if (q < wave) off += scratch[q];
+    all += scratch[q];
+  }
+  *total = all;
+  return off + incl - v;
+}
+
+// First index in [0, nnz) whose packed topic is >= k.
+__device__ __forceinline__ uint32_t row_lower_bound(const uint32_t *__restrict__ row, uint32_t nnz, uint32_t k) {
+  uint32_t lo = 0, hi = nnz;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if ((row[mid] >> 16) < k) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// ------------------------------------------------------------ kernels ----
+
+__global__ void k_init_topics(const uint32_t *__restrict__ wt_key, uint16_t *__restrict__ z_w, int64_t n, int32_t K,
+                              uint64_t seed) {
+  for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < n; j += int64_t(gridDim.x) * blockDim.x) {
+    const uint32_t i = wt_key[j];
+    const uint4 x = philox4x32_10(make_uint4(i, 0u, 0u, 1u), uint32_t(seed), uint32_t(seed >> 32));
+    z_w[j] = uint16_t((uint64_t(x.x) * uint64_t(uint32_t(K))) >> 32);
+  }
+}
+
+__global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, int32_t K, double vbeta,
+                        uint32_t *__restrict__ counters, unsigned long long *__restrict__ stats) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k < K) den[k] = double(T[k]) + vbeta;
+  if (blockIdx.x == 0 && threadIdx.x < 8) {
+    counters[threadIdx.x] = 0u;
+    if (stats) stats[threadIdx.x] = 0ull;
+  }
+}
+
+// Step 1 of Sec. 3.2 and the per-word Q' of Sec. 2.2 ("Q tree once per word").
+__global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const int K = p.K;
+  __shared__ double sv[kBlock * 3];
+  __shared__ uint32_t sk[kBlock * 3];
+  __shared__ double scratch[kBlock / kWave];
+  const bool dense = r < p.n_dense;
+  const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
+  const uint32_t *ents = nullptr;
+  uint32_t nnz = 0;
+  if (!dense) {
+    const int s = r - p.n_dense;
+    ents = d.ws_ent + d.ws_cap[s];
+    nnz = d.ws_nnz[s];
+  }
+  // sparse rows: each thread walks a contiguous chunk of topics
+  const int cs = (K + kBlock - 1) / kBlock;
+  const int c0 = min(K, tid * cs), c1 = min(K, c0 + cs);
+
+  Top3 t;
+  for (int q = 0; q < 3; ++q) {
+    t.v[q] = -1.0;
+    t.k[q] = 0xFFFFFFFFu;
+  }
+  if (dense) {
+    for (int k = tid; k < K; k += kBlock) top3_insert(t, what(uint32_t(wrow[k]), p.beta, d.den[k]), uint32_t(k));
+  } else {
+    uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
+    for (int k = c0; k < c1; ++k) {
+      uint32_t c = 0;
+      if (e < nnz && (ents[e] >> 16) == uint32_t(k)) c = ents[e++] & 0xFFFFu;
+      top3_insert(t, what(c, p.beta, d.den[k]), uint32_t(k));
+    }
+  }
+  for (int q = 0; q < 3; ++q) {
+    sv[tid * 3 + q] = t.v[q];
+    sk[tid * 3 + q] = t.k[q];
+  }
+  __syncthreads();
+  for (int stride = kBlock / 2; stride > 0; stride >>= 1) {
+    if (tid < stride) {
+      for (int q = 0; q < 3; ++q) top3_insert(t, sv[(tid + stride) * 3 + q], sk[(tid + stride) * 3 + q]);
+    }
+    __syncthreads();
+    if (tid < stride) {
+      for (int q = 0; q < 3; ++q) {
+        sv[tid * 3 + q] = t.v[q];
+        sk[tid * 3 + q] = t.k[q];
+      }
+    }
+    __syncthreads();
+  }
+  const uint32_t K1 = sk[0], K2 = sk[1];
+  const double a1 = sv[0], a2 = sv[1], a3 = K >= 3 ? sv[2] : 0.0;
+
+  double q = 0.0, sw = 0.0;
+  if (dense) {
+    for (int k = tid; k < K; k += kBlock) {
+      const double w = what(uint32_t(wrow[k]), p.beta, d.den[k]);
+      sw += w;
+      if (uint32_t(k) != K1) q += p.alpha * w;
+    }
+  } else {
+    uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
+    for (int k = c0; k < c1; ++k) {
+      uint32_t c = 0;
+      if (e < nnz && (ents[e] >> 16) == uint32_t(k)) c = ents[e++] & 0xFFFFu;
+      const double w = what(c, p.beta, d.den[k]);
+      sw += w;
+      if (uint32_t(k) != K1) q += p.alpha * w;
+    }
+  }
+  q = block_sum(q, scratch);
+  sw = block_sum(sw, scratch);
+  if (tid == 0) {
+    WordRec rec;
+    rec.a1 = a1;
+    rec.a2 = a2;
+    rec.a3 = a3;
+    rec.qp = q;
+    rec.sumw = sw;
+    rec.k1 = K1;
+    rec.k2 = K2;
+    d.wrec[r] = rec;
+  }
+}
+
+// Steps 2 and 3: per document, C1 = D[d][K1], C2 = D[d][K2], u, M, S_est and
+// the skip test (Eq. 7 and 9).  One wave per document; documents are handed
+// out in batches through an atomic counter.
+constexpr uint32_t kDocBatch = 32;
+
+__global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint32_t t,
+                                                     unsigned long long *__restrict__ stats) {
+  const int lane = threadIdx.x & (kWave - 1);
+  unsigned long long nskip = 0;
+  const uint32_t M = uint32_t(p.M);
+  for (;;) {
+    uint32_t d0 = 0;
+    if (lane == 0) d0 = atomicAdd(&d.counters[CNT_DOCPASS], kDocBatch);
+    d0 = __shfl(d0, 0);
+    if (d0 >= M) break;
+    const uint32_t d1 = min(M, d0 + kDocBatch);
+    for (uint32_t dd = d0; dd < d1; ++dd) {
+      const uint32_t b = d.doc_off[dd], e = d.doc_off[dd + 1];
+      const uint32_t len = e - b;
+      const uint32_t *row = d.d_ent + d.d_cap[dd];
+      const uint32_t nnz = d.d_nnz[dd];
+      for (uint32_t pp = b + lane; pp < e; pp += kWave) {
+        const uint32_t v = d.dt_word[pp];
+        const WordRec rec = d.wrec[v];
+        const uint32_t C1 = row_lookup(row, nnz, rec.k1);
+        const uint32_t C2 = row_lookup(row, nnz, rec.k2);
+        const uint32_t key = p.key_identity ? pp : d.dt_key[pp];
+        const double u = uniform_draw(p.seed, t, key);
+        const double Mm = rec.a1 * (double(C1) + p.alpha);
+        const double Sest = p.g == 1 ? rec.a2 * double(len - C1)
+                                     : rec.a2 * double(C2) + rec.a3 * double(len - C1 - C2);
+        const bool skip = !p.no_skip && (u * (Mm + Sest + rec.qp) < Mm);
+        d.z_w[d.dt_wpos[pp]] = skip ? uint16_t(rec.k1) : kUndecided;
+        nskip += skip ? 1ull : 0ull;
+      }
+    }
+  }
+  nskip = group_sum_u64<kWave>(nskip);
+  if (lane == 0 && nskip) atomicAdd(&stats[ST_SKIP3], nskip);
+}
+
+// Steps 4-6 for the undecided tokens of one region; the W^ row of the word
+// sits in LDS (Sec. 4.3, last paragraph) together with the Q' prefix over
+// blocks of kGroup topics.
+__global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32_t t,
+                                                    unsigned long long *__restrict__ stats) {
+  extern __shared__ double lds[];
+  const int K = p.K;
+  const int nb = (K + kGroup - 1) / kGroup;
+  double *wh = lds;         // [K]
+  double *qb = lds + K;     // [nb + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup
+  __shared__ uint32_t s_reg[3];
+  __shared__ int s_valid;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int grp = lane / kGroup, li = lane % kGroup;
+  uint32_t cur = 0xFFFFFFFFu, K1 = 0;
+  double a1 = 0.0, qp = 0.0;
+  unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0, n_reg = 0, n_dreg = 0;
+
+  for (;;) {
+    if (tid == 0) {
+      const uint32_t r = atomicAdd(&d.counters[CNT_SAMPLER], 1u);
+      s_valid = int64_t(r) < p.n_regions;
+      if (s_valid) {
+        s_reg[0] = d.region[3 * size_t(r)];
+        s_reg[1] = d.region[3 * size_t(r) + 1];
+        s_reg[2] = d.region[3 * size_t(r) + 2];
+      }
+    }
+    __syncthreads();
+    if (!s_valid) break;
+    const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2];
+    if (tid == 0) {
+      n_reg++;
+      if (int32_t(v) < p.n_dense) n_dreg++;
+    }
+    if (v != cur) {
+      cur = v;
+      const WordRec rec = d.wrec[v];
+      K1 = rec.k1;
+      a1 = rec.a1;
+      qp = rec.qp;
+      if (int32_t(v) < p.n_dense) {
+        const int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
+        for (int k = tid; k < K; k += kBlock) wh[k] = what(uint32_t(wrow[k]), p.beta, d.den[k]);
+      } else {
+        const int s = int(v) - p.n_dense;
+        const uint32_t *ents = d.ws_ent + d.ws_cap[s];
+        const uint32_t nnz = d.ws_nnz[s];
+        for (int k = tid; k < K; k += kBlock) wh[k] = what(0u, p.beta, d.den[k]);
+        __syncthreads();
+        for (uint32_t q = tid; q < nnz; q += kBlock) {
+          const uint32_t ent = ents[q];
+          wh[ent >> 16] = what(ent & 0xFFFFu, p.beta, d.den[ent >> 16]);
+        }
+      }
+      __syncthreads();
+      for (int blk = tid; blk < nb; blk += kBlock) {
+        double s = 0.0;
+        const int k1 = min(K, (blk + 1) * kGroup);
+        for (int k = blk * kGroup; k < k1; ++k)
+          if (uint32_t(k) != K1) s += p.alpha * wh[k];
+        qb[blk + 1] = s;
+      }
+      __syncthreads();
+      if (wave == 0) {
+        // in-place exclusive-to-inclusive prefix: qb[b+1] = qb[b] + block sum
+        const int per = (nb + kWave - 1) / kWave;
+        const int q0 = min(nb, lane * per), q1 = min(nb, q0 + per);
+        double s = 0.0;
+        for (int q = q0; q < q1; ++q) s += qb[q + 1];
+        double run = group_incl_scan<kWave>(s, lane) - s;
+        for (int q = q0; q < q1; ++q) {
+          run += qb[q + 1];
+          qb[q + 1] = run;
+        }
+        if (lane == 0) qb[0] = 0.0;
+      }
+      __syncthreads();
+    }
+
+    for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += kBlock) {
+      const uint32_t j = base + uint32_t(lane);
+      const bool und = j < e && d.z_w[j] == kUndecided;
+      unsigned long long mask = __ballot(und);
+      while (mask) {
+        unsigned long long m = mask;
+        for (int q = 0; q < grp; ++q) m &= m - 1ull;
+        for (int q = 0; q < kWave / kGroup; ++q) mask &= mask - 1ull;
+        if (m == 0ull) continue;
+        const uint32_t jt = base + uint32_t(__ffsll(m) - 1);
+        const uint32_t doc = d.wt_doc[jt];
+        const uint32_t key = d.wt_key[jt];
+        const uint32_t *row = d.d_ent + d.d_cap[doc];
+        const uint32_t nnz = d.d_nnz[doc];
+        // S' over nz(D[d]) \ {K1} and C1 = D[d][K1]
+        double acc = 0.0;
+        uint32_t c1 = 0;
+        for (uint32_t q = li; q < nnz; q += kGroup) {
+          const uint32_t ent = row[q];
+          const uint32_t k = ent >> 16, c = ent & 0xFFFFu;
+          if (k == K1) c1 = c;
+          else acc += double(c) * wh[k];
+        }
+        const double S = group_sum<kGroup>(acc);
+        const uint32_t C1 = group_sum_u32<kGroup>(c1);
+        const double Mm = a1 * (double(C1) + p.alpha);
+        const double Z = (Mm + S) + qp;
+        const double x = uniform_draw(p.seed, t, key) * Z;
+        uint32_t topic = K1;
+        if (x < Mm) {
+          if (li == 0) n_after_s++;
+        } else {
+          double cbase = Mm;
+          bool found = false;
+          for (uint32_t e0 = 0; e0 < nnz; e0 += kGroup) {
+            const uint32_t q = e0 + uint32_t(li);
+            double term = 0.0;
+            uint32_t k = 0;
+            if (q < nnz) {
+              const uint32_t ent = row[q];
+              k = ent >> 16;
+              if (k != K1) term = double(ent & 0xFFFFu) * wh[k];
+            }
+            const double incl = group_incl_scan<kGroup>(term, li);
+            const bool hit = term > 0.0 && x < cbase + incl;
+            const uint32_t hm = uint32_t(__ballot(hit) >> (grp * kGroup)) & kGroupMask;
+            if (hm) {
+              topic = __shfl(k, __ffs(hm) - 1, kGroup);
+              found = true;
+              break;
+            }
+            cbase += __shfl(incl, kGroup - 1, kGroup);
+          }
+          if (!found) {
+            const double xq = x - cbase;
+            if (!(xq < qb[nb])) {
+              topic = (K1 == uint32_t(K - 1)) ? uint32_t(K - 2) : uint32_t(K - 1);  // last positive segment
+            } else {
+              int lo = 0, hi = nb - 1;
+              while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (qb[mid] <= xq) lo = mid;
+                else hi = mid - 1;
+              }
+              const int k = lo * kGroup + li;
+              const double term = (k < K && uint32_t(k) != K1) ? p.alpha * wh[k] : 0.0;
+              const double incl = group_incl_scan<kGroup>(term, li);
+              const bool hit = term > 0.0 && xq < qb[lo] + incl;
+              const uint32_t hm = uint32_t(__ballot(hit) >> (grp * kGroup)) & kGroupMask;
+              if (hm) {
+                topic = uint32_t(lo * kGroup + __ffs(hm) - 1);
+              } else {
+                const uint32_t pm = uint32_t(__ballot(term > 0.0) >> (grp * kGroup)) & kGroupMask;
+                topic = uint32_t(lo * kGroup + 31 - __clz(pm));
+              }
+            }
+          }
+        }
+        if (li == 0) {
+          d.z_w[jt] = uint16_t(topic);
+          n_sampled++;
+          nnz_sum += nnz;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  n_sampled = group_sum_u64<kWave>(n_sampled);
+  n_after_s = group_sum_u64<kWave>(n_after_s);
+  nnz_sum = group_sum_u64<kWave>(nnz_sum);
+  if (lane == 0) {
+    if (n_sampled) atomicAdd(&stats[ST_SAMPLED], n_sampled);
+    if (n_after_s) atomicAdd(&stats[ST_SKIP_AFTER_S], n_after_s);
+    if (nnz_sum) atomicAdd(&stats[ST_NNZ], nnz_sum);
+  }
+  if (tid == 0) {
+    if (n_reg) atomicAdd(&stats[ST_REGIONS], n_reg);
+    if (n_dreg) atomicAdd(&stats[ST_DENSE_REGIONS], n_dreg);
+  }
+}
+
+// Rows of split dense words are accumulated with atomics; clear them and T.
+__global__ void k_zero_split(DevState d, Params p) {
+  const int64_t total = int64_t(p.n_dense) * p.K;
+  for (int64_t x = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; x < total; x += int64_t(gridDim.x) * blockDim.x) {
+    if (d.split[x / p.K]) d.w_dense[x] = 0;
+  }
+  for (int64_t k = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; k < p.K; k += int64_t(gridDim.x) * blockDim.x)
+    d.T[k] = 0u;
+}
+
+// W rebuild from the word-ordered topics: LDS histogram per region; dense
+// rows written whole (or added with atomics when the word is split), sparse
+// rows compacted to ascending packed entries; T accumulated per workgroup.
+__global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
+  extern __shared__ uint32_t ldsu[];
+  const int K = p.K;
+  uint32_t *hist = ldsu;      // [K]
+  uint32_t *tloc = ldsu + K;  // [K]
+  __shared__ uint32_t s_reg[3];
+  __shared__ int s_valid;
+  __shared__ uint32_t s_scan[kBlock / kWave];
+  const int tid = threadIdx.x;
+  uint32_t bad = 0;
+  for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
+  for (;;) {
+    if (tid == 0) {
+      const uint32_t r = atomicAdd(&d.counters[CNT_REBUILD_W], 1u);
+      s_valid = int64_t(r) < p.n_regions;
+      if (s_valid) {
+        s_reg[0] = d.region[3 * size_t(r)];
+        s_reg[1] = d.region[3 * size_t(r) + 1];
+        s_reg[2] = d.region[3 * size_t(r) + 2];
+      }
+    }
+    for (int k = tid; k < K; k += kBlock) hist[k] = 0u;
+    __syncthreads();
+    if (!s_valid) break;
+    const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2];
+    for (uint32_t j = b + tid; j < e; j += kBlock) {
+      const uint32_t z = d.z_w[j];
+      if (z < uint32_t(K)) atomicAdd(&hist[z], 1u);
+      else bad++;
+    }
+    __syncthreads();
+    if (int32_t(v) < p.n_dense) {
+      int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
+      if (d.split[v]) {
+        for (int k = tid; k < K; k += kBlock)
+          if (hist[k]) atomicAdd(&wrow[k], int32_t(hist[k]));
+      } else {
+        for (int k = tid; k < K; k += kBlock) wrow[k] = int32_t(hist[k]);
+      }
+    } else {
+      const int s = int(v) - p.n_dense;
+      const int cs = (K + kBlock - 1) / kBlock;
+      const int c0 = min(K, tid * cs), c1 = min(K, c0 + cs);
+      uint32_t cnt = 0;
+      for (int k = c0; k < c1; ++k) cnt += hist[k] ? 1u : 0u;
+      uint32_t total = 0;
+      uint32_t off = block_exclusive_u32(cnt, s_scan, &total);
+      uint32_t *out = d.ws_ent + d.ws_cap[s];
+      for (int k = c0; k < c1; ++k)
+        if (hist[k]) out[off++] = (uint32_t(k) << 16) | hist[k];
+      if (tid == 0) d.ws_nnz[s] = total;
+    }
+    for (int k = tid; k < K; k += kBlock) tloc[k] += hist[k];
+    __syncthreads();
+  }
+  for (int k = tid; k < K; k += kBlock)
+    if (tloc[k]) atomicAdd(&d.T[k], tloc[k]);
+  if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
+}
+
+// D rebuild: per document gather the new topics through the inverted index
+// (doc order -> word-order slot), histogram in a per-wave LDS table of
+// 16-bit counters, and emit ascending packed entries.
+__global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
+  extern __shared__ uint32_t ldsu[];
+  const int K = p.K;
+  const int half = (K + 1) / 2;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  uint32_t *hist = ldsu + size_t(wave) * size_t(half);
+  for (int q = lane; q < half; q += kWave) hist[q] = 0u;
+  const uint32_t M = uint32_t(p.M);
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  uint32_t bad = 0;
+  for (;;) {
+    uint32_t d0 = 0;
+    if (lane == 0) d0 = atomicAdd(&d.counters[CNT_REBUILD_D], kDocBatch);
+    d0 = __shfl(d0, 0);
+    if (d0 >= M) break;
+    const uint32_t d1 = min(M, d0 + kDocBatch);
+    for (uint32_t dd = d0; dd < d1; ++dd) {
+      const uint32_t b = d.doc_off[dd], e = d.doc_off[dd + 1];
+      for (uint32_t pp = b + lane; pp < e; pp += kWave) {
+        const uint32_t z = d.z_w[d.dt_wpos[pp]];
+        if (z < uint32_t(K)) atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
+        else bad++;
+      }
+      __threadfence_block();
+      uint32_t *out = d.d_ent + d.d_cap[dd];
+      uint32_t base = 0;
+      for (int q0 = 0; q0 < half; q0 += kWave) {
+        const int q = q0 + lane;
+        uint32_t w = 0;
+        if (q < half) {
+          w = hist[q];
+          hist[q] = 0u;
+        }
+        const uint32_t lo = w & 0xFFFFu, hi = w >> 16;
+        const unsigned long long m0 = __ballot(lo != 0u), m1 = __ballot(hi != 0u);
+        const uint32_t rank = uint32_t(__popcll(m0 & lt) + __popcll(m1 & lt));
+        if (lo) out[base + rank] = (uint32_t(2 * q) << 16) | lo;
+        if (hi) out[base + rank + (lo ? 1u : 0u)] = (uint32_t(2 * q + 1) << 16) | hi;
+        base += uint32_t(__popcll(m0) + __popcll(m1));
+      }
+      if (lane == 0) d.d_nnz[dd] = base;
+      __threadfence_block();
+    }
+  }
+  if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
+}
+
+// LLPT terms per region (Sec. 2.2): for every token,
+//   log2( (sum_{k in nz(D[d])} D[d][k] W^[v][k] + alpha * sum_k W^[v][k]) / (len(d) + K alpha) ),
+// summed in a fixed order so that the result does not depend on the schedule.
+__global__ __launch_bounds__(kBlock) void k_loglik(DevState d, Params p) {
+  extern __shared__ double lds[];
+  const int K = p.K;
+  double *wh = lds;
+  __shared__ uint32_t s_reg[3];
+  __shared__ int s_valid;
+  __shared__ uint32_t s_r;
+  __shared__ double s_part[kBlock / kGroup];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int gid = tid / kGroup, li = lane % kGroup;  // 16 groups per block
+  uint32_t cur = 0xFFFFFFFFu;
+  double sumw = 0.0;
+  const double Kalpha = double(K) * p.alpha;
+  for (;;) {
+    if (tid == 0) {
+      const uint32_t r = atomicAdd(&d.counters[CNT_LOGLIK], 1u);
+      s_r = r;
+      s_valid = int64_t(r) < p.n_regions;
+      if (s_valid) {
+        s_reg[0] = d.region[3 * size_t(r)];
+        s_reg[1] = d.region[3 * size_t(r) + 1];
+        s_reg[2] = d.region[3 * size_t(r) + 2];
+      }
+    }
+    __syncthreads();
+    if (!s_valid) break;
+    const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2], r = s_r;
+    if (v != cur) {
+      cur = v;
+      sumw = d.wrec[v].sumw;
+      if (int32_t(v) < p.n_dense) {
+        const int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
+        for (int k = tid; k < K; k += kBlock) wh[k] = what(uint32_t(wrow[k]), p.beta, d.den[k]);
+      } else {
+        const int s = int(v) - p.n_dense;
+        const uint32_t *ents = d.ws_ent + d.ws_cap[s];
+        const uint32_t nnz = d.ws_nnz[s];
+        for (int k = tid; k < K; k += kBlock) wh[k] = what(0u, p.beta, d.den[k]);
+        __syncthreads();
+        for (uint32_t q = tid; q < nnz; q += kBlock) {
+          const uint32_t ent = ents[q];
+          wh[ent >> 16] = what(ent & 0xFFFFu, p.beta, d.den[ent >> 16]);
+        }
+      }
+      __syncthreads();
+    }
+    double part = 0.0;
+    for (uint32_t j = b + uint32_t(gid); j < e; j += kBlock / kGroup) {
+      const uint32_t doc = d.wt_doc[j];
+      const uint32_t *row = d.d_ent + d.d_cap[doc];
+      const uint32_t nnz = d.d_nnz[doc];
+      double acc = 0.0;
+      for (uint32_t q = li; q < nnz; q += kGroup) {
+        const uint32_t ent = row[q];
+        acc += double(ent & 0xFFFFu) * wh[ent >> 16];
+      }
+      const double num = group_sum<kGroup>(acc) + p.alpha * sumw;
+      const double len = double(d.doc_off[doc + 1] - d.doc_off[doc]);
+      part += log2(num / (len + Kalpha));
+    }
+    if (li == 0) s_part[gid] = part;
+    __syncthreads();
+    if (tid == 0) {
+      double s = 0.0;
+      for (int q = 0; q < kBlock / kGroup; ++q) s += s_part[q];
+      d.ll_part[r] = s;
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_loglik_reduce(const double *__restrict__ part, int64_t n,
+                                                          double *__restrict__ out) {
+  __shared__ double scratch[kBlock / kWave];
+  double s = 0.0;
+  for (int64_t q = threadIdx.x; q < n; q += kBlock) s += part[q];
+  s = block_sum(s, scratch);
+  if (threadIdx.x == 0) out[0] = s;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------- launchers ----
+
+// Dynamic LDS above 64 KB per workgroup has to be requested for the kernel.
+template <typename F>
+hipError_t allow_lds(F *kernel, size_t bytes) {
+  if (bytes <= 65536) return hipSuccess;
+  return hipFuncSetAttribute(reinterpret_cast<const void *>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                             int(bytes));
+}
+
+hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s) {
+  const int64_t blocks = std::min<int64_t>((p.n + kBlock - 1) / kBlock, int64_t(p.grid_docs) * 8);
+  hipLaunchKernelGGL(k_init_topics, dim3(uint32_t(blocks)), dim3(kBlock), 0, s, d.wt_key, d.z_w, p.n, p.K, p.seed);
+  return hipGetLastError();
+}
+
+hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_t s) {
+  hipLaunchKernelGGL(k_begin, dim3((p.K + kBlock - 1) / kBlock), dim3(kBlock), 0, s, d.T, d.den, p.K, p.vbeta,
+                     d.counters, d.stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s) {
+  hipLaunchKernelGGL(k_word_pre, dim3(uint32_t(p.n_present)), dim3(kBlock), 0, s, d, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
+  hipLaunchKernelGGL(k_doc_pass, dim3(uint32_t(p.grid_docs)), dim3(kBlock), 0, s, d, p, t, d.stats);
+  return hipGetLastError();
+}
+
+size_t sampler_lds_bytes(int K) { return sizeof(double) * (size_t(K) + size_t((K + kGroup - 1) / kGroup) + 1); }
+
+hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
+  hipError_t err = allow_lds(k_sampler, sampler_lds_bytes(p.K));
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_sampler, dim3(uint32_t(p.grid_regions)), dim3(kBlock), sampler_lds_bytes(p.K), s, d, p, t,
+                     d.stats);
+  return hipGetLastError();
+}
+
+hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s) {
+  const int64_t zb = std::min<int64_t>((int64_t(p.n_dense) * p.K + kBlock - 1) / kBlock + 1, 65536);
+  hipLaunchKernelGGL(k_zero_split, dim3(uint32_t(zb)), dim3(kBlock), 0, s, d, p);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  err = allow_lds(k_rebuild_w, sizeof(uint32_t) * 2 * size_t(p.K));
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_rebuild_w, dim3(uint32_t(p.grid_regions)), dim3(kBlock), sizeof(uint32_t) * 2 * size_t(p.K),
+                     s, d, p);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const size_t half = size_t((p.K + 1) / 2);
+  err = allow_lds(k_rebuild_d, sizeof(uint32_t) * half * (kBlock / kWave));
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kBlock),
+                     sizeof(uint32_t) * half * (kBlock / kWave), s, d, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s) {
+  hipError_t err0 = allow_lds(k_loglik, sizeof(double) * size_t(p.K));
+  if (err0 != hipSuccess) return err0;
+  hipLaunchKernelGGL(k_loglik, dim3(uint32_t(p.grid_regions)), dim3(kBlock), sizeof(double) * size_t(p.K), s, d, p);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_loglik_reduce, dim3(1), dim3(kBlock), 0, s, d.ll_part, p.n_regions, d.ll_out);
+  return hipGetLastError();
+}
+
+}  // namespace lda

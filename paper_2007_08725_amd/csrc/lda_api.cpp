@@ -1,0 +1,482 @@
+// C ABI of liblda (include/lda.h): handle lifetime, validation, device
+// memory, the per-iteration launch sequence and the host-side exports.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "lda_internal.h"
+
+using namespace lda;
+
+namespace {
+
+thread_local std::string g_create_error = "no error";
+constexpr int kStatSlots = 256;   // iterations between two statistics read-backs
+constexpr int kEventsPerIter = 5;
+
+}  // namespace
+
+struct lda_handle {
+  Layout L;  // host copy of the layout (only the parts needed later are kept)
+  DevState d{};
+  Params p{};
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  int device = 0;
+  void *(*dev_alloc)(size_t, void *) = nullptr;
+  void (*dev_free)(void *, void *) = nullptr;
+  void *alloc_ctx = nullptr;
+  std::vector<void *> allocations;
+  unsigned long long *stats_base = nullptr;  // [kStatSlots * kStatsPerIter]
+  std::vector<hipEvent_t> events;            // [kStatSlots * kEventsPerIter]
+  int64_t iteration = 0;
+  bool poisoned = false;
+  std::string err = "no error";
+};
+
+namespace {
+
+lda_status fail(lda_handle *h, lda_status st, const std::string &msg) {
+  if (h) {
+    h->err = msg;
+    if (st == LDA_E_DEVICE) h->poisoned = true;
+  } else {
+    g_create_error = msg;
+  }
+  return st;
+}
+
+lda_status hip_fail(lda_handle *h, hipError_t e, const char *what) {
+  return fail(h, e == hipErrorOutOfMemory ? LDA_E_NOMEM : LDA_E_DEVICE,
+              std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(h, expr)                                  \
+  do {                                                    \
+    hipError_t e_ = (expr);                               \
+    if (e_ != hipSuccess) return hip_fail((h), e_, #expr); \
+  } while (0)
+
+template <typename T>
+lda_status dalloc(lda_handle *h, T **out, size_t count) {
+  size_t bytes = std::max<size_t>(count, 1) * sizeof(T);
+  bytes = (bytes + 255) & ~size_t(255);
+  void *ptr = nullptr;
+  if (h->dev_alloc) {
+    ptr = h->dev_alloc(bytes, h->alloc_ctx);
+    if (!ptr) return fail(h, LDA_E_NOMEM, "device allocation of " + std::to_string(bytes) + " bytes failed");
+  } else {
+    hipError_t e = hipMalloc(&ptr, bytes);
+    if (e != hipSuccess) return fail(h, LDA_E_NOMEM, "hipMalloc(" + std::to_string(bytes) + "): " + hipGetErrorString(e));
+  }
+  h->allocations.push_back(ptr);
+  *out = static_cast<T *>(ptr);
+  return LDA_OK;
+}
+
+template <typename T>
+lda_status upload(lda_handle *h, T *dst, const std::vector<T> &src) {
+  if (src.empty()) return LDA_OK;
+  HIP_TRY(h, hipMemcpyAsync(dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice, h->stream));
+  return LDA_OK;
+}
+
+#define LDA_TRY(expr)                 \
+  do {                                \
+    lda_status s_ = (expr);           \
+    if (s_ != LDA_OK) return s_;      \
+  } while (0)
+
+lda_status check_handle(lda_handle *h) {
+  if (!h) return LDA_E_ARG;
+  if (h->poisoned) return LDA_E_STATE;
+  return LDA_OK;
+}
+
+lda_status check_errors(lda_handle *h, const unsigned long long *st) {
+  if (st[ST_ERRORS]) return fail(h, LDA_E_DEVICE, "kernel found " + std::to_string(st[ST_ERRORS]) + " undecided topic slots");
+  return LDA_OK;
+}
+
+// Count tables of the current assignment z_w (Sec. 4.3 update step).
+lda_status rebuild_counts(lda_handle *h) {
+  DevState d = h->d;
+  d.stats = h->stats_base;
+  HIP_TRY(h, launch_begin_iteration(d, h->p, h->stream));
+  HIP_TRY(h, launch_rebuild(d, h->p, h->stream));
+  return LDA_OK;
+}
+
+lda_status create_device(lda_handle *h, const lda_options *o) {
+  Layout &L = h->L;
+  HIP_TRY(h, hipGetDevice(&h->device));
+  int cus = 0, lds_max = 0;
+  HIP_TRY(h, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device));
+  HIP_TRY(h, hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device));
+  const size_t need = sizeof(double) * (size_t(L.K) + size_t(L.K) / 16 + 2) + 256;
+  if (need > size_t(lds_max))
+    return fail(h, LDA_E_RANGE, "K = " + std::to_string(L.K) + " needs " + std::to_string(need) +
+                                    " bytes of LDS per workgroup; the device allows " + std::to_string(lds_max));
+  if (o && o->stream) {
+    h->stream = static_cast<hipStream_t>(o->stream);
+  } else {
+    HIP_TRY(h, hipStreamCreateWithFlags(&h->stream, hipStreamNonBlocking));
+    h->own_stream = true;
+  }
+  Params &p = h->p;
+  p.grid_regions = std::max(1, cus * 8);
+  p.grid_docs = std::max(1, cus * 8);
+
+  const size_t n = size_t(L.n);
+  DevState &d = h->d;
+  LDA_TRY(dalloc(h, &d.doc_off, L.doc_off.size()));
+  LDA_TRY(dalloc(h, &d.dt_word, n));
+  if (!L.key_identity) LDA_TRY(dalloc(h, &d.dt_key, n));
+  LDA_TRY(dalloc(h, &d.dt_wpos, n));
+  LDA_TRY(dalloc(h, &d.word_off, L.word_off.size()));
+  LDA_TRY(dalloc(h, &d.wt_doc, n));
+  LDA_TRY(dalloc(h, &d.wt_key, n));
+  LDA_TRY(dalloc(h, &d.region, L.region.size()));
+  LDA_TRY(dalloc(h, &d.split, L.split.size()));
+  LDA_TRY(dalloc(h, &d.z_w, n));
+  LDA_TRY(dalloc(h, &d.d_cap, L.d_cap.size()));
+  LDA_TRY(dalloc(h, &d.d_nnz, size_t(L.M)));
+  LDA_TRY(dalloc(h, &d.d_ent, size_t(L.d_cap.back())));
+  LDA_TRY(dalloc(h, &d.w_dense, size_t(L.n_dense) * size_t(L.K)));
+  LDA_TRY(dalloc(h, &d.ws_cap, L.ws_cap.size()));
+  LDA_TRY(dalloc(h, &d.ws_nnz, L.ws_cap.size()));
+  LDA_TRY(dalloc(h, &d.ws_ent, size_t(L.ws_cap.back())));
+  LDA_TRY(dalloc(h, &d.T, size_t(L.K)));
+  LDA_TRY(dalloc(h, &d.den, size_t(L.K)));
+  LDA_TRY(dalloc(h, &d.wrec, size_t(L.n_present)));
+  LDA_TRY(dalloc(h, &d.counters, 8));
+  LDA_TRY(dalloc(h, &h->stats_base, size_t(kStatSlots) * kStatsPerIter));
+  LDA_TRY(dalloc(h, &d.ll_part, size_t(L.n_regions)));
+  LDA_TRY(dalloc(h, &d.ll_out, 1));
+  d.stats = h->stats_base;
+
+  LDA_TRY(upload(h, d.doc_off, L.doc_off));
+  LDA_TRY(upload(h, d.dt_word, L.dt_word));
+  if (!L.key_identity) LDA_TRY(upload(h, d.dt_key, L.dt_key));
+  LDA_TRY(upload(h, d.dt_wpos, L.dt_wpos));
+  LDA_TRY(upload(h, d.word_off, L.word_off));
+  LDA_TRY(upload(h, d.wt_doc, L.wt_doc));
+  LDA_TRY(upload(h, d.wt_key, L.wt_key));
+  LDA_TRY(upload(h, d.region, L.region));
+  LDA_TRY(upload(h, d.split, L.split));
+  LDA_TRY(upload(h, d.d_cap, L.d_cap));
+  LDA_TRY(upload(h, d.ws_cap, L.ws_cap));
+  HIP_TRY(h, hipMemsetAsync(h->stats_base, 0, sizeof(unsigned long long) * kStatSlots * kStatsPerIter, h->stream));
+  HIP_TRY(h, launch_init_topics(d, p, h->stream));
+  LDA_TRY(rebuild_counts(h));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  unsigned long long st[kStatsPerIter];
+  HIP_TRY(h, hipMemcpy(st, h->stats_base, sizeof(st), hipMemcpyDeviceToHost));
+  LDA_TRY(check_errors(h, st));
+  // the doc- and word-order staging arrays are no longer needed on the host
+  std::vector<uint32_t>().swap(L.dt_word);
+  std::vector<uint32_t>().swap(L.dt_key);
+  std::vector<uint32_t>().swap(L.dt_wpos);
+  std::vector<uint32_t>().swap(L.wt_doc);
+  return LDA_OK;
+}
+
+void release(lda_handle *h) {
+  if (!h) return;
+  if (h->stream) (void)hipStreamSynchronize(h->stream);
+  for (hipEvent_t ev : h->events)
+    if (ev) (void)hipEventDestroy(ev);
+  for (void *ptr : h->allocations) {
+    if (h->dev_alloc) h->dev_free(ptr, h->alloc_ctx);
+    else (void)hipFree(ptr);
+  }
+  if (h->own_stream && h->stream) (void)hipStreamDestroy(h->stream);
+  delete h;
+}
+
+}  // namespace
+
+extern "C" {
+
+lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens, int32_t V, int32_t K, double alpha,
+                      double beta, uint64_t seed, const lda_options *opts, lda_handle **out) {
+  if (!out) return fail(nullptr, LDA_E_ARG, "out is NULL");
+  *out = nullptr;
+  if (!word || !doc) return fail(nullptr, LDA_E_ARG, "word or doc is NULL");
+  if (n_tokens <= 0) return fail(nullptr, LDA_E_ARG, "n_tokens must be positive");
+  if (V <= 0) return fail(nullptr, LDA_E_ARG, "V must be positive");
+  if (K < 2 || K > LDA_MAX_TOPICS) return fail(nullptr, LDA_E_ARG, "K must be in [2, 16384]");
+  if (!std::isfinite(alpha) || !(alpha > 0.0)) return fail(nullptr, LDA_E_ARG, "alpha must be finite and positive");
+  if (!std::isfinite(beta) || !(beta > 0.0)) return fail(nullptr, LDA_E_ARG, "beta must be finite and positive");
+  int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0;
+  if (opts) {
+    if (opts->g != 0 && opts->g != 1 && opts->g != 2) return fail(nullptr, LDA_E_ARG, "g must be 1 or 2");
+    if (opts->g) g = opts->g;
+    if (opts->region_tokens < 0) return fail(nullptr, LDA_E_ARG, "region_tokens must be >= 0");
+    if (opts->region_tokens) R = opts->region_tokens;
+    if ((opts->dev_alloc == nullptr) != (opts->dev_free == nullptr))
+      return fail(nullptr, LDA_E_ARG, "dev_alloc and dev_free must be given together");
+    no_skip = opts->no_skip ? 1 : 0;
+  }
+  lda_handle *h = new (std::nothrow) lda_handle();
+  if (!h) return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
+  std::string msg;
+  lda_status st;
+  try {
+    st = build_layout(word, doc, n_tokens, V, K, R, h->L, msg);
+  } catch (const std::bad_alloc &) {
+    st = LDA_E_NOMEM;
+    msg = "host allocation failed while building the layout";
+  }
+  if (st != LDA_OK) {
+    delete h;
+    return fail(nullptr, st, msg);
+  }
+  if (opts) {
+    h->dev_alloc = opts->dev_alloc;
+    h->dev_free = opts->dev_free;
+    h->alloc_ctx = opts->alloc_ctx;
+  }
+  Params &p = h->p;
+  p.n = n_tokens;
+  p.M = h->L.M;
+  p.V = V;
+  p.K = K;
+  p.n_present = h->L.n_present;
+  p.n_dense = h->L.n_dense;
+  p.n_regions = h->L.n_regions;
+  p.alpha = alpha;
+  p.beta = beta;
+  p.vbeta = double(V) * beta;
+  p.seed = seed;
+  p.g = g;
+  p.no_skip = no_skip;
+  p.key_identity = h->L.key_identity ? 1 : 0;
+  try {
+    st = create_device(h, opts);
+  } catch (const std::bad_alloc &) {
+    st = fail(h, LDA_E_NOMEM, "host allocation failed");
+  }
+  if (st != LDA_OK) {
+    g_create_error = h->err;
+    release(h);
+    return st;
+  }
+  *out = h;
+  return LDA_OK;
+}
+
+lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
+  LDA_TRY(check_handle(h));
+  if (n_iters < 0) return fail(h, LDA_E_ARG, "n_iters must be >= 0");
+  if (stats && h->events.empty()) {
+    h->events.assign(size_t(kStatSlots) * kEventsPerIter, nullptr);
+    for (auto &ev : h->events) HIP_TRY(h, hipEventCreate(&ev));
+  }
+  for (int32_t done = 0; done < n_iters;) {
+    const int32_t chunk = std::min<int32_t>(n_iters - done, kStatSlots);
+    for (int32_t c = 0; c < chunk; ++c) {
+      const uint32_t t = uint32_t(h->iteration);
+      DevState d = h->d;
+      d.stats = h->stats_base + size_t(c) * kStatsPerIter;
+      hipEvent_t *ev = stats ? &h->events[size_t(c) * kEventsPerIter] : nullptr;
+      if (ev) HIP_TRY(h, hipEventRecord(ev[0], h->stream));
+      HIP_TRY(h, launch_begin_iteration(d, h->p, h->stream));
+      HIP_TRY(h, launch_word_pre(d, h->p, h->stream));
+      if (ev) HIP_TRY(h, hipEventRecord(ev[1], h->stream));
+      HIP_TRY(h, launch_doc_pass(d, h->p, t, h->stream));
+      if (ev) HIP_TRY(h, hipEventRecord(ev[2], h->stream));
+      HIP_TRY(h, launch_sampler(d, h->p, t, h->stream));
+      if (ev) HIP_TRY(h, hipEventRecord(ev[3], h->stream));
+      HIP_TRY(h, launch_rebuild(d, h->p, h->stream));
+      if (ev) HIP_TRY(h, hipEventRecord(ev[4], h->stream));
+      h->iteration++;
+    }
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    std::vector<unsigned long long> st(static_cast<size_t>(chunk) * kStatsPerIter);
+    HIP_TRY(h, hipMemcpy(st.data(), h->stats_base, st.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+    for (int32_t c = 0; c < chunk; ++c) {
+      const unsigned long long *s = &st[size_t(c) * kStatsPerIter];
+      LDA_TRY(check_errors(h, s));
+      if (!stats) continue;
+      lda_iter_stats &o = stats[done + c];
+      hipEvent_t *ev = &h->events[size_t(c) * kEventsPerIter];
+      float ms_all = 0, ms_doc = 0, ms_smp = 0, ms_reb = 0;
+      HIP_TRY(h, hipEventElapsedTime(&ms_all, ev[0], ev[4]));
+      HIP_TRY(h, hipEventElapsedTime(&ms_doc, ev[1], ev[2]));
+      HIP_TRY(h, hipEventElapsedTime(&ms_smp, ev[2], ev[3]));
+      HIP_TRY(h, hipEventElapsedTime(&ms_reb, ev[3], ev[4]));
+      o.iteration = h->iteration - chunk + c;
+      o.ms_iter = ms_all;
+      o.ms_docpass = ms_doc;
+      o.ms_sampler = ms_smp;
+      o.ms_rebuild = ms_reb;
+      o.skip_step3 = int64_t(s[ST_SKIP3]);
+      o.skip_after_s = int64_t(s[ST_SKIP_AFTER_S]);
+      o.sampled = int64_t(s[ST_SAMPLED]);
+      o.nnz_scanned = int64_t(s[ST_NNZ]);
+      o.regions = int64_t(s[ST_REGIONS]);
+      o.dense_regions = int64_t(s[ST_DENSE_REGIONS]);
+    }
+    done += chunk;
+  }
+  return LDA_OK;
+}
+
+lda_status lda_get_counts(lda_handle *h, lda_counts *out) {
+  LDA_TRY(check_handle(h));
+  if (!out) return fail(h, LDA_E_ARG, "out is NULL");
+  const Layout &L = h->L;
+  const size_t n = size_t(L.n);
+  const int32_t K = L.K;
+  std::vector<uint32_t> d_nnz(static_cast<size_t>(L.M)), ws_nnz(L.ws_cap.size() - 1);
+  HIP_TRY(h, hipMemcpyAsync(d_nnz.data(), h->d.d_nnz, d_nnz.size() * 4, hipMemcpyDeviceToHost, h->stream));
+  if (!ws_nnz.empty())
+    HIP_TRY(h, hipMemcpyAsync(ws_nnz.data(), h->d.ws_nnz, ws_nnz.size() * 4, hipMemcpyDeviceToHost, h->stream));
+  std::vector<int32_t> wd(static_cast<size_t>(L.n_dense) * static_cast<size_t>(K));
+  if (!wd.empty())
+    HIP_TRY(h, hipMemcpyAsync(wd.data(), h->d.w_dense, wd.size() * 4, hipMemcpyDeviceToHost, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  int64_t nnz_D = 0, nnz_W = 0;
+  for (uint32_t x : d_nnz) nnz_D += x;
+  for (uint32_t x : ws_nnz) nnz_W += x;
+  for (int32_t x : wd) nnz_W += x != 0;
+  out->iteration = h->iteration;
+  out->M = L.M;
+  out->V = L.V;
+  out->K = K;
+  out->n_tokens = L.n;
+  out->nnz_D = nnz_D;
+  out->nnz_W = nnz_W;
+  if (!out->z && !out->T && !out->D_off && !out->D_topic && !out->D_count && !out->W_off && !out->W_topic &&
+      !out->W_count)
+    return LDA_OK;  // size query
+  if (out->z) {
+    std::vector<uint16_t> zw(n);
+    HIP_TRY(h, hipMemcpy(zw.data(), h->d.z_w, n * 2, hipMemcpyDeviceToHost));
+    for (size_t j = 0; j < n; ++j) out->z[L.wt_key[j]] = int32_t(zw[j]);
+  }
+  if (out->T) {
+    std::vector<uint32_t> tk(static_cast<size_t>(K));
+    HIP_TRY(h, hipMemcpy(tk.data(), h->d.T, size_t(K) * 4, hipMemcpyDeviceToHost));
+    for (int32_t k = 0; k < K; ++k) out->T[k] = tk[size_t(k)];
+  }
+  if (out->D_off || out->D_topic || out->D_count) {
+    if (!out->D_off || !out->D_topic || !out->D_count) return fail(h, LDA_E_ARG, "D arrays must be given together");
+    std::vector<uint32_t> ent(static_cast<size_t>(L.d_cap.back()));
+    if (!ent.empty()) HIP_TRY(h, hipMemcpy(ent.data(), h->d.d_ent, ent.size() * 4, hipMemcpyDeviceToHost));
+    int64_t o = 0;
+    for (int32_t dd = 0; dd < L.M; ++dd) {
+      out->D_off[dd] = o;
+      for (uint32_t q = 0; q < d_nnz[size_t(dd)]; ++q) {
+        const uint32_t e = ent[size_t(L.d_cap[size_t(dd)]) + q];
+        out->D_topic[o] = int32_t(e >> 16);
+        out->D_count[o] = int32_t(e & 0xFFFFu);
+        ++o;
+      }
+    }
+    out->D_off[L.M] = o;
+  }
+  if (out->W_off || out->W_topic || out->W_count) {
+    if (!out->W_off || !out->W_topic || !out->W_count) return fail(h, LDA_E_ARG, "W arrays must be given together");
+    std::vector<uint32_t> went(static_cast<size_t>(L.ws_cap.back()));
+    if (!went.empty()) HIP_TRY(h, hipMemcpy(went.data(), h->d.ws_ent, went.size() * 4, hipMemcpyDeviceToHost));
+    int64_t o = 0;
+    for (int32_t v = 0; v < L.V; ++v) {
+      out->W_off[v] = o;
+      const int32_t r = L.relabel[size_t(v)];
+      if (r >= L.n_present) continue;
+      if (r < L.n_dense) {
+        const int32_t *row = &wd[size_t(r) * size_t(K)];
+        for (int32_t k = 0; k < K; ++k)
+          if (row[k]) {
+            out->W_topic[o] = k;
+            out->W_count[o] = row[k];
+            ++o;
+          }
+      } else {
+        const size_t s = size_t(r - L.n_dense);
+        for (uint32_t q = 0; q < ws_nnz[s]; ++q) {
+          const uint32_t e = went[size_t(L.ws_cap[s]) + q];
+          out->W_topic[o] = int32_t(e >> 16);
+          out->W_count[o] = int32_t(e & 0xFFFFu);
+          ++o;
+        }
+      }
+    }
+    out->W_off[L.V] = o;
+  }
+  return LDA_OK;
+}
+
+lda_status lda_loglik(lda_handle *h, double *llpt) {
+  LDA_TRY(check_handle(h));
+  if (!llpt) return fail(h, LDA_E_ARG, "llpt is NULL");
+  DevState d = h->d;
+  d.stats = h->stats_base;
+  HIP_TRY(h, launch_begin_iteration(d, h->p, h->stream));
+  HIP_TRY(h, launch_word_pre(d, h->p, h->stream));
+  HIP_TRY(h, launch_loglik(d, h->p, h->stream));
+  double sum = 0.0;
+  HIP_TRY(h, hipMemcpyAsync(&sum, h->d.ll_out, sizeof(double), hipMemcpyDeviceToHost, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  *llpt = sum / double(h->L.n);
+  return LDA_OK;
+}
+
+lda_status lda_set_assignments(lda_handle *h, const int32_t *z, int64_t iteration) {
+  LDA_TRY(check_handle(h));
+  if (!z) return fail(h, LDA_E_ARG, "z is NULL");
+  if (iteration < 0 || iteration >= (int64_t(1) << 32)) return fail(h, LDA_E_ARG, "iteration out of range");
+  const Layout &L = h->L;
+  const size_t n = size_t(L.n);
+  std::vector<uint16_t> zw(n);
+  for (size_t j = 0; j < n; ++j) {
+    const int32_t v = z[L.wt_key[j]];
+    if (v < 0 || v >= L.K) return fail(h, LDA_E_ARG, "topic out of range at token " + std::to_string(L.wt_key[j]));
+    zw[j] = uint16_t(v);
+  }
+  HIP_TRY(h, hipMemcpyAsync(h->d.z_w, zw.data(), n * 2, hipMemcpyHostToDevice, h->stream));
+  LDA_TRY(rebuild_counts(h));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  unsigned long long st[kStatsPerIter];
+  HIP_TRY(h, hipMemcpy(st, h->stats_base, sizeof(st), hipMemcpyDeviceToHost));
+  LDA_TRY(check_errors(h, st));
+  h->iteration = iteration;
+  return LDA_OK;
+}
+
+void lda_destroy(lda_handle *h) { release(h); }
+
+const char *lda_last_error(const lda_handle *h) { return h ? h->err.c_str() : g_create_error.c_str(); }
+
+lda_status lda_describe_layout(const int32_t *word, const int32_t *doc, int64_t n_tokens, int32_t V, int32_t K,
+                               int32_t region_tokens, int32_t *relabel, int32_t *n_present, int32_t *n_dense,
+                               int64_t *n_regions, int32_t *n_docs, uint32_t *word_off, uint32_t *wt_key,
+                               uint32_t *region) {
+  if (!word || !doc || n_tokens <= 0 || V <= 0 || K < 2 || K > LDA_MAX_TOPICS || region_tokens < 0)
+    return fail(nullptr, LDA_E_ARG, "bad argument");
+  Layout L;
+  std::string msg;
+  lda_status st;
+  try {
+    st = build_layout(word, doc, n_tokens, V, K, region_tokens ? region_tokens : kDefaultRegionTokens, L, msg);
+  } catch (const std::bad_alloc &) {
+    return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
+  }
+  if (st != LDA_OK) return fail(nullptr, st, msg);
+  if (n_present) *n_present = L.n_present;
+  if (n_dense) *n_dense = L.n_dense;
+  if (n_regions) *n_regions = L.n_regions;
+  if (n_docs) *n_docs = L.M;
+  if (relabel) std::memcpy(relabel, L.relabel.data(), L.relabel.size() * 4);
+  if (word_off) std::memcpy(word_off, L.word_off.data(), L.word_off.size() * 4);
+  if (wt_key) std::memcpy(wt_key, L.wt_key.data(), L.wt_key.size() * 4);
+  if (region) std::memcpy(region, L.region.data(), L.region.size() * 4);
+  return LDA_OK;
+}
+
+}  // extern "C"

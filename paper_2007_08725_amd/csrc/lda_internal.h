@@ -1,0 +1,108 @@
+// Internal declarations of liblda: host layout, device state and kernel
+// launchers.  Device code targets gfx950 (CDNA4, wave64) only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/lda.h"
+
+namespace lda {
+
+// Reserved value of a 16-bit topic slot: "not decided by the step-3 test".
+constexpr uint16_t kUndecided = 0xFFFF;
+constexpr int kDefaultRegionTokens = 10000;  // Sec. 5.1
+constexpr int kBlock = 256;                  // threads per workgroup (4 wave64)
+
+// ----------------------------------------------------------------- layout --
+// Host-side token layout (Sec. 4.2-4.3 and 5.1).
+//   doc order : tokens stably sorted by document
+//   word order: tokens stably sorted by relabelled word (within a word the
+//               documents ascend, since the source is doc order)
+struct Layout {
+  int64_t n = 0;
+  int32_t M = 0, V = 0, K = 0;
+  int32_t n_present = 0;  // words with at least one token (relabelled ids 0..)
+  int32_t n_dense = 0;    // relabelled ids [0, n_dense) have count > K
+  std::vector<int32_t> relabel;   // [V] caller id -> new id
+  std::vector<int32_t> inv;       // [n_present] new id -> caller id
+  std::vector<uint32_t> count;    // [n_present] tokens per new id
+  std::vector<uint32_t> doc_off;  // [M+1]
+  std::vector<uint32_t> word_off; // [n_present+1]
+  std::vector<uint32_t> dt_word;  // [n] new word id of each doc-ordered token
+  std::vector<uint32_t> dt_key;   // [n] input index of each doc-ordered token (empty if identity)
+  std::vector<uint32_t> dt_wpos;  // [n] word-order position of each doc-ordered token
+  std::vector<uint32_t> wt_doc;   // [n] doc id of each word-ordered token
+  std::vector<uint32_t> wt_key;   // [n] input index of each word-ordered token
+  std::vector<uint32_t> d_cap;    // [M+1] offsets of D rows, capacity min(len, K)
+  std::vector<uint32_t> ws_cap;   // [n_present-n_dense+1] offsets of sparse W rows, capacity = count
+  std::vector<uint32_t> region;   // [3*n_regions] (word, begin, end)
+  std::vector<uint8_t> split;     // [n_dense] 1 if the dense word has more than one region
+  int64_t n_regions = 0;
+  int64_t n_dense_regions = 0;
+  bool key_identity = false;      // input already doc-sorted: input index == doc-order position
+};
+
+// Validates and builds the layout; returns LDA_OK or an error with msg set.
+lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t K, int32_t R,
+                        Layout &L, std::string &msg);
+
+// ---------------------------------------------------------- device state --
+struct WordRec {  // per relabelled word, refreshed every iteration (Sec. 3.2, steps 1 and 4)
+  double a1, a2, a3;  // top-3 values of W^[v]
+  double qp;          // Q' = sum_{k != K1} alpha * W^[v][k]
+  double sumw;        // sum_k W^[v][k] (log-likelihood)
+  uint32_t k1, k2;    // top-2 topic ids (lowest id on ties)
+};
+
+struct DevState {
+  // layout
+  uint32_t *doc_off, *dt_word, *dt_key, *dt_wpos, *word_off, *wt_doc, *wt_key;
+  uint32_t *region;   // 3 per region
+  uint8_t *split;     // per dense word
+  // assignment, word order
+  uint16_t *z_w;
+  // counts
+  uint32_t *d_cap, *d_nnz, *d_ent;
+  int32_t *w_dense;
+  uint32_t *ws_cap, *ws_nnz, *ws_ent;
+  uint32_t *T;
+  double *den;
+  WordRec *wrec;
+  // scheduler counters and statistics
+  uint32_t *counters;           // [8]
+  unsigned long long *stats;    // [8]
+  double *ll_part;              // [n_regions]
+  double *ll_out;               // [1]
+};
+
+struct Params {
+  int64_t n;
+  int32_t M, V, K, n_present, n_dense;
+  int64_t n_regions;
+  double alpha, beta, vbeta;
+  uint64_t seed;
+  int32_t g;
+  int32_t no_skip;
+  int32_t key_identity;
+  int32_t grid_regions;  // persistent workgroups for region kernels
+  int32_t grid_docs;     // persistent workgroups for doc kernels
+};
+
+enum { CNT_SAMPLER = 0, CNT_REBUILD_W = 1, CNT_DOCPASS = 2, CNT_REBUILD_D = 3, CNT_LOGLIK = 4 };
+enum { ST_SKIP3 = 0, ST_SKIP_AFTER_S = 1, ST_SAMPLED = 2, ST_NNZ = 3, ST_REGIONS = 4, ST_DENSE_REGIONS = 5, ST_ERRORS = 6 };
+constexpr int kStatsPerIter = 8;
+
+// Kernel launchers (all asynchronous on `s`); return hipGetLastError().
+hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
+hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
+hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s);
+
+}  // namespace lda

@@ -1,0 +1,251 @@
+"""GPU parity: the HIP path (through the C ABI) against the oracle.
+
+Bars (per draw): every GPU/oracle topic mismatch is a flagged near-boundary
+draw and there are fewer than 1e-6*N of them; D, W and T are bit-exact given
+the GPU's assignment; LLPT agrees with the oracle to 1e-12 relative on the same
+assignment (1e-3 after trajectories diverge).
+"""
+import numpy as np
+import pytest
+
+import lda_synth
+import oracle
+from gpu_common import (SEED, check_counts_are_histograms, compare_draws, corpus_kw, make_lda, oracle_step,
+                        say)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def c1():
+    return lda_synth.make_corpus("c1")
+
+
+@pytest.fixture(scope="module")
+def c1_traj(c1):
+    """Oracle trajectory of c1: initial topics, then 10 iterations with flags and stats."""
+    z = oracle.init_topics(c1.N, c1.K, SEED)
+    out = [(z, None, None)]
+    for t in range(c1.spec.iters):
+        zn, f, st = oracle_step(c1, z, t)
+        out.append((zn, f, st))
+        z = zn
+    return out
+
+
+def test_init_topics_match_oracle(c1, c1_traj):
+    say("init c1 N=%d" % c1.N)
+    with make_lda(c1) as m:
+        cnt = m.counts()
+    assert cnt["iteration"] == 0
+    assert np.array_equal(cnt["z"], c1_traj[0][0])
+    check_counts_are_histograms(c1, cnt, c1.K)
+
+
+def test_c1_every_iteration_from_oracle_snapshot(c1, c1_traj):
+    """At each t the GPU starts from the oracle's z_t and must reproduce z_{t+1}."""
+    with make_lda(c1) as m:
+        for t in range(c1.spec.iters):
+            say("c1 snapshot t=%d" % t)
+            m.set_assignments(c1_traj[t][0], t)
+            st = m.iterate(1, stats=True)[0]
+            cnt = m.counts()
+            zo, flags, ost = c1_traj[t + 1]
+            compare_draws(cnt["z"], zo, flags, c1.N)
+            check_counts_are_histograms(c1, cnt, c1.K)
+            assert st["iteration"] == t and cnt["iteration"] == t + 1
+            assert st["skip_step3"] + st["sampled"] == c1.N
+            assert abs(st["skip_step3"] - ost["skip3"]) <= ost["flagged"] + 2
+            assert st["ms_sampler"] > 0.0
+
+
+def test_c1_free_running_trajectory_and_llpt(c1, c1_traj):
+    with make_lda(c1) as m:
+        ll0 = m.loglik()
+        m.iterate(c1.spec.iters)
+        cnt = m.counts()
+        ll = m.loglik()
+    kw = corpus_kw(c1)
+    zo = c1_traj[-1][0]
+    lo0 = oracle.llpt(c1.word, c1.doc, c1_traj[0][0], **kw)
+    assert ll0 == pytest.approx(lo0, rel=1e-12)
+    lo = oracle.llpt(c1.word, c1.doc, zo, **kw)
+    if np.array_equal(cnt["z"], zo):
+        assert ll == pytest.approx(lo, rel=1e-12)
+    else:
+        assert ll == pytest.approx(lo, rel=1e-3)
+    # the GPU's LLPT on its own state equals the oracle's LLPT on that same state
+    assert ll == pytest.approx(oracle.llpt(c1.word, c1.doc, cnt["z"], **kw), rel=1e-12)
+    assert ll > ll0
+
+
+@pytest.mark.parametrize("opts", [dict(region_tokens=7), dict(region_tokens=100), dict(g=1), dict(no_skip=True),
+                                  dict(torch_allocator=False, torch_stream=False)])
+def test_schedule_invariance(c1, opts):
+    """Region size, S_est depth, the skip test, allocator and stream never change the draws."""
+    say("invariance %s" % opts)
+    with make_lda(c1) as a:
+        a.iterate(3)
+        za = a.counts(D=False, W=False)["z"]
+    with make_lda(c1, **opts) as b:
+        b.iterate(3)
+        zb = b.counts(D=False, W=False)["z"]
+    assert np.array_equal(za, zb)
+
+
+def test_determinism_and_resume(c1):
+    with make_lda(c1) as a:
+        a.iterate(10)
+        z10 = a.counts(D=False, W=False)["z"]
+    with make_lda(c1) as b:
+        b.iterate(5)
+        z5 = b.counts(D=False, W=False)["z"]
+    with make_lda(c1) as c:
+        c.set_assignments(z5, 5)
+        c.iterate(5)
+        cnt = c.counts()
+    assert cnt["iteration"] == 10
+    assert np.array_equal(cnt["z"], z10)
+    check_counts_are_histograms(c1, cnt, c1.K)
+
+
+REDUCED = [
+    # (name, overrides): corpus shapes of the five workloads at sizes the oracle finishes in seconds;
+    # every one has words with more than 10,000 tokens (split into several regions)
+    ("c2", dict(n_docs=2500)),
+    ("c3", dict(n_docs=12000)),
+    ("c4", dict(n_docs=1200, V=20000)),
+    ("c5", dict(n_docs=3000, V=100000)),
+]
+
+
+@pytest.mark.parametrize("name,over", REDUCED, ids=[r[0] for r in REDUCED])
+def test_reduced_config_snapshots(name, over):
+    c = lda_synth.make_corpus(name, **over)
+    say("reduced %s N=%d V=%d K=%d" % (name, c.N, c.V, c.K))
+    z = oracle.init_topics(c.N, c.K, SEED)
+    with make_lda(c) as m:
+        assert np.array_equal(m.counts(D=False, W=False)["z"], z)
+        for t in range(2):
+            zo, flags, ost = oracle_step(c, z, t)
+            m.set_assignments(z, t)
+            st = m.iterate(1, stats=True)[0]
+            cnt = m.counts()
+            compare_draws(cnt["z"], zo, flags, c.N)
+            check_counts_are_histograms(c, cnt, c.K)
+            assert st["skip_step3"] + st["sampled"] == c.N
+            assert st["regions"] > c.V // 50
+            z = zo
+        ll = m.loglik()
+    assert ll == pytest.approx(oracle.llpt(c.word, c.doc, cnt["z"], **corpus_kw(c)), rel=1e-12)
+
+
+def test_shuffled_input_order():
+    """Input not sorted by document: keys and z stay in the caller's order."""
+    c = lda_synth.generate(lda_synth.SPECS["c1"], n_docs=300, shuffle=True)
+    z = oracle.init_topics(c.N, c.K, SEED)
+    zo, flags, _ = oracle_step(c, z, 0)
+    with make_lda(c) as m:
+        assert np.array_equal(m.counts(D=False, W=False)["z"], z)
+        m.iterate(1)
+        cnt = m.counts()
+    compare_draws(cnt["z"], zo, flags, c.N)
+    check_counts_are_histograms(c, cnt, c.K)
+
+
+class _Tiny:
+    def __init__(self, word, doc, V, K, alpha, beta=0.01):
+        self.word = np.asarray(word, np.int32)
+        self.doc = np.asarray(doc, np.int32)
+        self.V, self.K, self.alpha, self.beta = V, K, alpha, beta
+        self.n_docs = int(self.doc.max()) + 1
+        self.N = self.word.shape[0]
+
+
+def _edge_cases():
+    rng = np.random.default_rng(77)
+    yield "single_token", _Tiny([0], [0], 1, 2, 0.5)
+    yield "empty_docs", _Tiny([1, 2, 2, 0], [3, 3, 9, 9], 5, 3, 0.3)
+    yield "K2", _Tiny(rng.integers(0, 6, 400), np.sort(rng.integers(0, 20, 400)), 6, 2, 25.0)
+    n = 30000
+    yield "one_word_many_regions", _Tiny(np.zeros(n, np.int32), np.sort(rng.integers(0, 50, n)), 1, 8, 0.1)
+    yield "longest_doc", _Tiny(rng.integers(0, 50, 65535), np.zeros(65535, np.int32), 50, 16, 0.2)
+    yield "max_topics", _Tiny(rng.integers(0, 40, 3000), np.sort(rng.integers(0, 30, 3000)), 40, 16384, 0.01)
+    yield "ragged_K", _Tiny(rng.integers(0, 300, 20000), np.sort(rng.integers(0, 200, 20000)), 300, 1013, 0.05)
+
+
+@pytest.mark.parametrize("name,c", list(_edge_cases()), ids=[e[0] for e in _edge_cases()])
+def test_edge_cases(name, c):
+    say("edge %s N=%d K=%d" % (name, c.N, c.K))
+    kw = dict(M=c.n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta)
+    z = oracle.init_topics(c.N, c.K, SEED)
+    with lda_make(c) as m:
+        for t in range(3):
+            zo, flags, _ = oracle.iterate(c.word, c.doc, z, seed=SEED, t=t, **kw)
+            m.set_assignments(z, t)
+            m.iterate(1)
+            cnt = m.counts()
+            compare_draws(cnt["z"], zo, flags, c.N)
+            check_counts_are_histograms(c, cnt, c.K)
+            z = zo
+        ll = m.loglik()
+    assert ll == pytest.approx(oracle.llpt(c.word, c.doc, cnt["z"], **kw), rel=1e-12, abs=1e-14)
+
+
+def lda_make(c, **kw):
+    import paper_2007_08725_amd as lda
+    return lda.LDA(c.word, c.doc, c.V, c.K, c.alpha, c.beta, SEED, **kw)
+
+
+def test_allocator_failure_reports_nomem(c1):
+    import ctypes
+
+    import paper_2007_08725_amd as lda
+    lib = lda.load_library()
+    calls = {"n": 0}
+
+    def alloc(nbytes, ctx):
+        calls["n"] += 1
+        return None if calls["n"] == 4 else _pool.alloc(nbytes)
+
+    def free(ptr, ctx):
+        _pool.free(ptr)
+
+    class Pool:
+        def __init__(self):
+            import torch
+            self.torch = torch
+            self.live = {}
+
+        def alloc(self, n):
+            t = self.torch.empty(int(n), dtype=self.torch.uint8, device="cuda")
+            self.live[t.data_ptr()] = t
+            return t.data_ptr()
+
+        def free(self, p):
+            self.live.pop(p)
+
+    global _pool
+    _pool = Pool()
+    fa, ff = lda.ALLOC_FN(alloc), lda.FREE_FN(free)
+    o = lda.Options()
+    o.dev_alloc, o.dev_free = fa, ff
+    h = ctypes.c_void_p()
+    w = np.ascontiguousarray(c1.word)
+    d = np.ascontiguousarray(c1.doc)
+    st = lib.lda_create(ctypes.c_void_p(w.ctypes.data), ctypes.c_void_p(d.ctypes.data), c1.N, c1.V, c1.K, c1.alpha,
+                        c1.beta, SEED, ctypes.byref(o), ctypes.byref(h))
+    assert st == lda.LDA_E_NOMEM and not h.value
+    assert not _pool.live  # everything allocated before the failure was released
+    assert b"allocation" in lib.lda_last_error(None)
+
+
+def test_set_assignments_rejects_bad_topics(c1):
+    import paper_2007_08725_amd as lda
+    with make_lda(c1) as m:
+        z = np.zeros(c1.N, np.int32)
+        z[5] = c1.K
+        with pytest.raises(lda.LDAError) as ei:
+            m.set_assignments(z, 0)
+        assert ei.value.status == lda.LDA_E_ARG
+        m.iterate(1)  # the handle is still usable
