@@ -1,0 +1,172 @@
+#!/usr/bin/env python3
+"""Benchmark of the synchronous LDA iteration on one MI355X.
+
+Workload (default): the large planted corpus -- 8.2M documents with
+lognormal lengths (mean 90, sigma 0.8), ~738M tokens, V = 141,000 with a
+Zipf(1.1) vocabulary base, 500 planted topics -- fit with K = 1,000,
+alpha = 0.05, beta = 0.01.  It stands in for PubMed (Sec. 6).  A step is one
+full synchronous iteration: per-topic and per-word precompute, the
+per-document C1/C2 + skip pass, the word-major sampler and the count rebuild.
+
+Prints one JSON line: tokens/s over the timed steps, the sampler kernel's
+algorithmic HBM bytes per launch divided by its HIP-event duration against the
+8 TB/s peak, and the oracle timed on a bounded sample of the same workload.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "k_sampler_c3_counters.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2007_08725_amd", "csrc", "kernels.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def sampler_alg_bytes(st, N):
+    """Bytes the sampler must move per launch (see the design notes):
+    2 B topic slot per token; per sampled token its doc id and key (8 B), the
+    D-row offset and length (8 B), the D row (4 B per entry) and the new topic
+    (2 B); the W rows (4*K per dense word, 4*nnz per sparse word); the region
+    and word records (12 + 48 B per region)."""
+    return (2 * N + 18 * st["sampled"] + 4 * st["nnz_scanned"] + st["row_bytes"] + 60 * st["regions"])
+
+
+def traffic_from_profile(alg_per_launch):
+    """HBM bytes per sampler launch from the committed counter summary, if it
+    was taken on the current kernel source; else None."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    txt = open(PMC_SUMMARY).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", txt)
+    b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m or not b:
+        return None
+    sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    if sha != m.group(1):
+        return None
+    return float(b.group(1))
+
+
+def cpu_baseline(c, n_docs):
+    """The oracle as it stands: one synchronous iteration on the first n_docs documents."""
+    import numpy as np
+    import oracle
+
+    m = int(np.searchsorted(c.doc, n_docs))
+    w, d = c.word[:m], c.doc[:m]
+    z = oracle.init_topics(m, c.K, 42)
+    t0 = time.perf_counter()
+    oracle.iterate(w, d, z, M=n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta, seed=42, t=0)
+    dt = time.perf_counter() - t0
+    return {"value": m / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": "one synchronous iteration (counts rebuilt from the Philox initial topics, per-word "
+                      "precompute over all %d words, every token drawn) on the first %d documents = %d tokens "
+                      "of the same corpus, single thread, %.1f s" % (c.V, n_docs, m, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--cpu-docs", type=int, default=50000, help="documents in the oracle's timed sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported "
+              "(the multi-GPU design is described but not built)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import lda_synth
+    import paper_2007_08725_amd as lda
+
+    torch.cuda.set_device(0)
+    t0 = time.perf_counter()
+    c = lda_synth.make_corpus(args.workload)
+    log("generated %s: N=%d docs=%d V=%d K=%d in %.1f s" % (args.workload, c.N, c.n_docs, c.V, c.K,
+                                                            time.perf_counter() - t0))
+    t0 = time.perf_counter()
+    m = lda.LDA(c.word, c.doc, c.V, c.K, c.alpha, c.beta, lda_synth.SAMPLER_SEED)
+    torch.cuda.synchronize()
+    t_create = time.perf_counter() - t0
+    log("lda_create %.1f s" % t_create)
+
+    if args.calib_copy:
+        a = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    if args.warmup:
+        m.iterate(args.warmup)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    st = m.iterate(args.steps, stats=True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    log("timed %d steps in %.3f s" % (args.steps, elapsed))
+    llpt = m.loglik()
+
+    N = c.N
+    value = N * args.steps / elapsed
+    ms_sampler = np.array([s["ms_sampler"] for s in st])
+    alg = np.array([sampler_alg_bytes(s, N) for s in st], dtype=np.float64)
+    achieved = alg.sum() / (ms_sampler.sum() * 1e-3) / 1e9
+    alg_per_launch = float(alg.mean())
+    traffic = traffic_from_profile(alg_per_launch)
+    stage_ms = {k: float(np.mean([s[k] for s in st])) for k in
+                ("ms_precompute", "ms_docpass", "ms_sampler", "ms_rebuild", "ms_iter")}
+    line = {
+        "metric": "sampled tokens/sec per iteration + sampler HBM GB/s vs peak, K=1000",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic planted-LDA corpus (seeded), random initial topics",
+        "config": {"workload": "%s: %d docs, %d tokens, V=%d, K=%d, alpha=%g, beta=%g, iterations %d-%d" % (
+            args.workload, c.n_docs, N, c.V, c.K, c.alpha, c.beta, args.warmup, args.warmup + args.steps - 1),
+            "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "kernel": "k_sampler",
+                     "alg_bytes_per_launch": alg_per_launch, "avg_launch_ms": float(ms_sampler.mean())},
+        "breakdown_ms": stage_ms,
+        "skip_step3_frac": float(np.mean([s["skip_step3"] for s in st]) / N),
+        "llpt_after": llpt,
+        "create_s": t_create,
+    }
+    m.close()
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a sample ...")
+        line["cpu_baseline"] = cpu_baseline(c, args.cpu_docs)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -81,12 +81,14 @@ typedef struct {
   double ms_sampler;     /* device time of the word-major sampler kernel */
   double ms_docpass;     /* device time of the per-document C1/C2 + skip kernel */
   double ms_rebuild;     /* device time of the count rebuild kernels */
+  double ms_precompute;  /* device time of the per-topic and per-word precompute */
   int64_t skip_step3;    /* tokens set to K1 by the step-3 test */
   int64_t skip_after_s;  /* tokens drawn as K1 by the second max-topic test */
   int64_t sampled;       /* tokens whose S' was built (not skipped at step 3) */
   int64_t nnz_scanned;   /* sum of nnz(D[d]) over the sampled tokens */
   int64_t regions;       /* regions handed out by the scheduler */
   int64_t dense_regions; /* of which regions of dense (full-row) words */
+  int64_t row_bytes;     /* bytes of W rows the sampler needs: 4*K per dense word, 4*nnz per sparse word */
 } lda_iter_stats;
 
 /* Count tables in the caller's ids.  Caller-allocated; a call with every array

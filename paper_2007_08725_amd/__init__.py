@@ -35,9 +35,10 @@ class Options(ctypes.Structure):
 
 class IterStats(ctypes.Structure):
     _fields_ = [("iteration", ctypes.c_int64), ("ms_iter", ctypes.c_double), ("ms_sampler", ctypes.c_double),
-                ("ms_docpass", ctypes.c_double), ("ms_rebuild", ctypes.c_double), ("skip_step3", ctypes.c_int64),
-                ("skip_after_s", ctypes.c_int64), ("sampled", ctypes.c_int64), ("nnz_scanned", ctypes.c_int64),
-                ("regions", ctypes.c_int64), ("dense_regions", ctypes.c_int64)]
+                ("ms_docpass", ctypes.c_double), ("ms_rebuild", ctypes.c_double), ("ms_precompute", ctypes.c_double),
+                ("skip_step3", ctypes.c_int64), ("skip_after_s", ctypes.c_int64), ("sampled", ctypes.c_int64),
+                ("nnz_scanned", ctypes.c_int64), ("regions", ctypes.c_int64), ("dense_regions", ctypes.c_int64),
+                ("row_bytes", ctypes.c_int64)]
 
 
 class Counts(ctypes.Structure):

@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
   const int grp = lane / kGroup, li = lane % kGroup;
   uint32_t cur = 0xFFFFFFFFu, K1 = 0;
   double a1 = 0.0, qp = 0.0;
-  unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0, n_reg = 0, n_dreg = 0;
+  unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0, n_reg = 0, n_dreg = 0, row_bytes = 0;
 
   for (;;) {
     if (tid == 0) {
@@ -349,6 +349,8 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
     if (tid == 0) {
       n_reg++;
       if (int32_t(v) < p.n_dense) n_dreg++;
+      if (b == d.word_off[v])
+        row_bytes += int32_t(v) < p.n_dense ? 4ull * uint64_t(K) : 4ull * d.ws_nnz[int(v) - p.n_dense];
     }
     if (v != cur) {
       cur = v;
@@ -493,6 +495,7 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
   if (tid == 0) {
     if (n_reg) atomicAdd(&stats[ST_REGIONS], n_reg);
     if (n_dreg) atomicAdd(&stats[ST_DENSE_REGIONS], n_dreg);
+    if (row_bytes) atomicAdd(&stats[ST_ROW_BYTES], row_bytes);
   }
 }
 

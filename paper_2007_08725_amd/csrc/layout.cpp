@@ -1,4 +1,4 @@
-// Host-side token layout (runs once inside lda_create).
+// Token layout, host side (runs once inside lda_create).
 //
 //   Sec. 4.2: words are relabelled by descending token count so that the
 //             dense words (count > K) form a prefix of the id space; a sparse
@@ -10,6 +10,10 @@
 //   Sec. 5.1: every word is cut into regions of at most R consecutive
 //             word-ordered tokens (large-word dissection); the regions are
 //             the units the atomic scheduler hands out.
+//
+// scan_tokens and plan_from_counts are shared by the device builder (the
+// sorts run on the GPU, see layout_gpu.hip) and by build_layout, the
+// all-host reference used by lda_describe_layout.
 #include <algorithm>
 #include <cmath>
 #include <numeric>
@@ -18,10 +22,10 @@
 
 namespace lda {
 
-lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t K, int32_t R,
-                        Layout &L, std::string &msg) {
-  if (n <= 0 || V <= 0 || K < 2 || R <= 0) {
-    msg = "build_layout: bad sizes";
+lda_status scan_tokens(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t &M, bool &doc_sorted,
+                       std::string &msg) {
+  if (n <= 0 || V <= 0) {
+    msg = "bad sizes";
     return LDA_E_ARG;
   }
   if (n >= (int64_t(1) << 32)) {
@@ -29,38 +33,37 @@ lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int3
     return LDA_E_RANGE;
   }
   int64_t maxdoc = -1;
+  bool sorted = true;
+  int32_t prev = 0;
   for (int64_t i = 0; i < n; i++) {
-    if (word[i] < 0 || word[i] >= V) {
+    const int32_t w = word[i], d = doc[i];
+    if (w < 0 || w >= V) {
       msg = "word id out of range at token " + std::to_string(i);
       return LDA_E_ARG;
     }
-    if (doc[i] < 0) {
+    if (d < 0) {
       msg = "negative doc id at token " + std::to_string(i);
       return LDA_E_ARG;
     }
-    if (doc[i] > maxdoc) maxdoc = doc[i];
+    if (d > maxdoc) maxdoc = d;
+    if (d < prev) sorted = false;
+    prev = d;
   }
-  L = Layout();
-  L.n = n;
-  L.V = V;
-  L.K = K;
-  L.M = int32_t(maxdoc + 1);
-  const int32_t M = L.M;
+  M = int32_t(maxdoc + 1);
+  doc_sorted = sorted;
+  return LDA_OK;
+}
 
-  // document lengths and doc-order offsets
-  L.doc_off.assign(size_t(M) + 1, 0);
-  for (int64_t i = 0; i < n; i++) L.doc_off[size_t(doc[i]) + 1]++;
+lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t R, Layout &L, std::string &msg) {
+  const int32_t V = int32_t(cnt.size());
+  const int32_t M = int32_t(L.doc_off.size()) - 1;
   for (int32_t d = 0; d < M; d++) {
-    if (L.doc_off[size_t(d) + 1] > uint32_t(LDA_MAX_DOC_LEN)) {
+    if (L.doc_off[size_t(d) + 1] - L.doc_off[size_t(d)] > uint32_t(LDA_MAX_DOC_LEN)) {
       msg = "document " + std::to_string(d) + " has more than 65535 tokens";
       return LDA_E_RANGE;
     }
   }
-  for (int32_t d = 0; d < M; d++) L.doc_off[size_t(d) + 1] += L.doc_off[size_t(d)];
-
   // relabel: descending count, ties by ascending caller id (stable sort)
-  std::vector<uint32_t> cnt(static_cast<size_t>(V), 0u);
-  for (int64_t i = 0; i < n; i++) cnt[size_t(word[i])]++;
   std::vector<int32_t> order(static_cast<size_t>(V));
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return cnt[size_t(a)] > cnt[size_t(b)]; });
@@ -68,7 +71,7 @@ lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int3
   for (int32_t r = 0; r < V; r++) L.relabel[size_t(order[size_t(r)])] = r;
   int32_t np = 0, nd = 0;
   for (int32_t r = 0; r < V; r++) {
-    uint32_t c = cnt[size_t(order[size_t(r)])];
+    const uint32_t c = cnt[size_t(order[size_t(r)])];
     if (c > 0) np++;
     // dense iff the count exceeds K (Sec. 4.2); a count above 65535 cannot be
     // packed in a 16-bit sparse entry, so such a word is dense as well
@@ -79,46 +82,13 @@ lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int3
   L.inv.assign(order.begin(), order.begin() + np);
   L.count.resize(size_t(np));
   for (int32_t r = 0; r < np; r++) L.count[size_t(r)] = cnt[size_t(order[size_t(r)])];
-  std::vector<uint32_t>().swap(cnt);
-
-  // doc order: stable counting sort by document
-  bool identity = true;
-  for (int64_t i = 1; i < n && identity; i++)
-    if (doc[i] < doc[i - 1]) identity = false;
-  L.key_identity = identity;
-  L.dt_word.resize(size_t(n));
-  if (!identity) L.dt_key.resize(size_t(n));
-  {
-    std::vector<uint32_t> pos(L.doc_off.begin(), L.doc_off.end() - 1);
-    for (int64_t i = 0; i < n; i++) {
-      uint32_t p = pos[size_t(doc[i])]++;
-      L.dt_word[p] = uint32_t(L.relabel[size_t(word[i])]);
-      if (!identity) L.dt_key[p] = uint32_t(i);
-    }
-  }
-
-  // word order: stable counting sort of the doc-ordered tokens by new word id
   L.word_off.assign(size_t(np) + 1, 0);
   for (int32_t r = 0; r < np; r++) L.word_off[size_t(r) + 1] = L.word_off[size_t(r)] + L.count[size_t(r)];
-  L.dt_wpos.resize(size_t(n));
-  L.wt_doc.resize(size_t(n));
-  L.wt_key.resize(size_t(n));
-  {
-    std::vector<uint32_t> cur(L.word_off.begin(), L.word_off.end() - 1);
-    for (int32_t d = 0; d < M; d++) {
-      for (uint32_t p = L.doc_off[size_t(d)]; p < L.doc_off[size_t(d) + 1]; p++) {
-        uint32_t j = cur[L.dt_word[p]]++;
-        L.dt_wpos[p] = j;
-        L.wt_doc[j] = uint32_t(d);
-        L.wt_key[j] = identity ? p : L.dt_key[p];
-      }
-    }
-  }
 
   // capacities: D rows min(len, K) (Sec. 4.2), sparse W rows = token count
   L.d_cap.assign(size_t(M) + 1, 0);
   for (int32_t d = 0; d < M; d++) {
-    uint32_t len = L.doc_off[size_t(d) + 1] - L.doc_off[size_t(d)];
+    const uint32_t len = L.doc_off[size_t(d) + 1] - L.doc_off[size_t(d)];
     L.d_cap[size_t(d) + 1] = L.d_cap[size_t(d)] + std::min<uint32_t>(len, uint32_t(K));
   }
   const int32_t ns = np - nd;
@@ -129,21 +99,67 @@ lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int3
   // of near-equal size; a sparse word is always one region
   L.split.assign(size_t(nd), 0);
   L.region.clear();
+  L.n_dense_regions = 0;
   for (int32_t r = 0; r < np; r++) {
-    uint32_t b = L.word_off[size_t(r)], c = L.count[size_t(r)];
+    const uint32_t b = L.word_off[size_t(r)], c = L.count[size_t(r)];
     uint64_t nreg = 1;
     if (r < nd) nreg = (uint64_t(c) + uint64_t(R) - 1) / uint64_t(R);
     if (r < nd && nreg > 1) L.split[size_t(r)] = 1;
     for (uint64_t q = 0; q < nreg; q++) {
-      uint32_t rb = b + uint32_t(uint64_t(c) * q / nreg);
-      uint32_t re = b + uint32_t(uint64_t(c) * (q + 1) / nreg);
       L.region.push_back(uint32_t(r));
-      L.region.push_back(rb);
-      L.region.push_back(re);
+      L.region.push_back(b + uint32_t(uint64_t(c) * q / nreg));
+      L.region.push_back(b + uint32_t(uint64_t(c) * (q + 1) / nreg));
       if (r < nd) L.n_dense_regions++;
     }
   }
   L.n_regions = int64_t(L.region.size() / 3);
+  return LDA_OK;
+}
+
+lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t K, int32_t R,
+                        Layout &L, std::string &msg) {
+  if (K < 2 || R <= 0) {
+    msg = "build_layout: bad sizes";
+    return LDA_E_ARG;
+  }
+  int32_t M = 0;
+  bool identity = false;
+  lda_status st = scan_tokens(word, doc, n, V, M, identity, msg);
+  if (st != LDA_OK) return st;
+  L = Layout();
+  L.n = n;
+  L.V = V;
+  L.K = K;
+  L.M = M;
+  L.key_identity = identity;
+
+  L.doc_off.assign(size_t(M) + 1, 0);
+  for (int64_t i = 0; i < n; i++) L.doc_off[size_t(doc[i]) + 1]++;
+  for (int32_t d = 0; d < M; d++) L.doc_off[size_t(d) + 1] += L.doc_off[size_t(d)];
+  std::vector<uint32_t> cnt(static_cast<size_t>(V), 0u);
+  for (int64_t i = 0; i < n; i++) cnt[size_t(word[i])]++;
+  st = plan_from_counts(cnt, K, R, L, msg);
+  if (st != LDA_OK) return st;
+
+  // doc order: stable counting sort by document
+  std::vector<uint32_t> dt_word(static_cast<size_t>(n)), dt_key;
+  if (!identity) dt_key.resize(size_t(n));
+  {
+    std::vector<uint32_t> pos(L.doc_off.begin(), L.doc_off.end() - 1);
+    for (int64_t i = 0; i < n; i++) {
+      const uint32_t p = pos[size_t(doc[i])]++;
+      dt_word[p] = uint32_t(L.relabel[size_t(word[i])]);
+      if (!identity) dt_key[p] = uint32_t(i);
+    }
+  }
+  // word order: stable counting sort of the doc-ordered tokens by new word id
+  L.wt_key.resize(size_t(n));
+  {
+    std::vector<uint32_t> cur(L.word_off.begin(), L.word_off.end() - 1);
+    for (int32_t d = 0; d < M; d++)
+      for (uint32_t p = L.doc_off[size_t(d)]; p < L.doc_off[size_t(d) + 1]; p++)
+        L.wt_key[cur[dt_word[p]]++] = identity ? p : dt_key[p];
+  }
   return LDA_OK;
 }
 

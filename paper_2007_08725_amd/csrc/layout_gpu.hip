@@ -1,0 +1,129 @@
+// Token layout on the device (lda_create): the two stable orders of Sec. 4.3
+// built with rocPRIM radix sorts, plus the gathers/scatters that link them.
+//
+//   doc order : stable sort of input indices by document (skipped when the
+//               input is already sorted by document)
+//   word order: stable sort of doc-order positions by caller word id, then a
+//               permutation of whole word segments into relabelled order
+//               (descending count, Sec. 4.2), so that within a word the
+//               documents ascend.
+#include <rocprim/device/device_radix_sort.hpp>
+#include <rocprim/iterator/counting_iterator.hpp>
+
+#include "lda_internal.h"
+
+namespace lda {
+namespace {
+
+constexpr int kThreads = 256;
+
+inline uint32_t grid_for(int64_t n) {
+  const int64_t b = (n + kThreads - 1) / kThreads;
+  return uint32_t(std::min<int64_t>(std::max<int64_t>(b, 1), 1 << 20));
+}
+
+__global__ void k_gather_u32(uint32_t *__restrict__ dst, const int32_t *__restrict__ src,
+                             const uint32_t *__restrict__ idx, int64_t n) {
+  for (int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; p < n; p += int64_t(gridDim.x) * blockDim.x)
+    dst[p] = uint32_t(src[idx[p]]);
+}
+
+// off[b] = first position whose key is >= b, for b in [0, nbins]; keys ascending.
+__global__ void k_boundaries(const uint32_t *__restrict__ keys, int64_t n, uint32_t nbins, uint32_t *__restrict__ off) {
+  for (int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; p < n; p += int64_t(gridDim.x) * blockDim.x) {
+    const uint32_t k = keys[p];
+    const int64_t prev = p == 0 ? -1 : int64_t(keys[p - 1]);
+    for (int64_t b = prev + 1; b <= int64_t(k); ++b) off[b] = uint32_t(p);
+    if (p == n - 1)
+      for (int64_t b = int64_t(k) + 1; b <= int64_t(nbins); ++b) off[b] = uint32_t(n);
+  }
+}
+
+// Word-order slot of every token: its position in the caller-id sort, moved
+// with its whole word segment to the relabelled segment start.
+__global__ void k_word_order(const uint32_t *__restrict__ wkey, const uint32_t *__restrict__ wpos, int64_t n,
+                             const int32_t *__restrict__ relabel, const uint32_t *__restrict__ woff_orig,
+                             const uint32_t *__restrict__ woff_new, const uint32_t *__restrict__ doc_sorted,
+                             const int32_t *__restrict__ doc_in, const uint32_t *__restrict__ dt_key,
+                             uint32_t *__restrict__ dt_word, uint32_t *__restrict__ dt_wpos,
+                             uint32_t *__restrict__ wt_doc, uint32_t *__restrict__ wt_key) {
+  for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < n; q += int64_t(gridDim.x) * blockDim.x) {
+    const uint32_t v = wkey[q];
+    const uint32_t r = uint32_t(relabel[v]);
+    const uint32_t j = woff_new[r] + (uint32_t(q) - woff_orig[v]);
+    const uint32_t p = wpos[q];
+    dt_word[p] = r;
+    dt_wpos[p] = j;
+    wt_doc[j] = doc_sorted ? doc_sorted[p] : uint32_t(doc_in[p]);
+    wt_key[j] = dt_key ? dt_key[p] : p;
+  }
+}
+
+__global__ void k_scatter_z(const uint16_t *__restrict__ z_w, const uint32_t *__restrict__ wt_key, int64_t n,
+                            int32_t *__restrict__ z_in) {
+  for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < n; j += int64_t(gridDim.x) * blockDim.x)
+    z_in[wt_key[j]] = int32_t(z_w[j]);
+}
+
+__global__ void k_gather_z(const int32_t *__restrict__ z_in, const uint32_t *__restrict__ wt_key, int64_t n,
+                           int32_t K, uint16_t *__restrict__ z_w, unsigned long long *__restrict__ bad) {
+  unsigned long long nbad = 0;
+  for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < n; j += int64_t(gridDim.x) * blockDim.x) {
+    const int32_t z = z_in[wt_key[j]];
+    if (z >= 0 && z < K) z_w[j] = uint16_t(z);
+    else {
+      z_w[j] = 0;
+      nbad++;
+    }
+  }
+  if (nbad) atomicAdd(bad, nbad);
+}
+
+}  // namespace
+
+unsigned bits_for(uint64_t max_value) {
+  unsigned b = 1;
+  while (b < 32 && (max_value >> b)) ++b;
+  return b;
+}
+
+hipError_t sort_pairs_u32(void *tmp, size_t &tmp_bytes, const uint32_t *keys_in, uint32_t *keys_out,
+                          const uint32_t *vals_in, uint32_t *vals_out, int64_t n, unsigned end_bit, hipStream_t s) {
+  const size_t size = size_t(n);
+  if (vals_in)
+    return rocprim::radix_sort_pairs(tmp, tmp_bytes, keys_in, keys_out, vals_in, vals_out, size, 0u, end_bit, s);
+  return rocprim::radix_sort_pairs(tmp, tmp_bytes, keys_in, keys_out, rocprim::counting_iterator<uint32_t>(0u),
+                                   vals_out, size, 0u, end_bit, s);
+}
+
+hipError_t launch_gather_u32(uint32_t *dst, const int32_t *src, const uint32_t *idx, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(k_gather_u32, dim3(grid_for(n)), dim3(kThreads), 0, s, dst, src, idx, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_boundaries(const uint32_t *keys, int64_t n, uint32_t nbins, uint32_t *off, hipStream_t s) {
+  hipLaunchKernelGGL(k_boundaries, dim3(grid_for(n)), dim3(kThreads), 0, s, keys, n, nbins, off);
+  return hipGetLastError();
+}
+
+hipError_t launch_word_order(const uint32_t *wkey, const uint32_t *wpos, int64_t n, const int32_t *relabel,
+                             const uint32_t *woff_orig, const uint32_t *woff_new, const uint32_t *doc_sorted,
+                             const int32_t *doc_in, const uint32_t *dt_key, uint32_t *dt_word, uint32_t *dt_wpos,
+                             uint32_t *wt_doc, uint32_t *wt_key, hipStream_t s) {
+  hipLaunchKernelGGL(k_word_order, dim3(grid_for(n)), dim3(kThreads), 0, s, wkey, wpos, n, relabel, woff_orig,
+                     woff_new, doc_sorted, doc_in, dt_key, dt_word, dt_wpos, wt_doc, wt_key);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_z(const uint16_t *z_w, const uint32_t *wt_key, int64_t n, int32_t *z_in, hipStream_t s) {
+  hipLaunchKernelGGL(k_scatter_z, dim3(grid_for(n)), dim3(kThreads), 0, s, z_w, wt_key, n, z_in);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_z(const int32_t *z_in, const uint32_t *wt_key, int64_t n, int32_t K, uint16_t *z_w,
+                           unsigned long long *bad, hipStream_t s) {
+  hipLaunchKernelGGL(k_gather_z, dim3(grid_for(n)), dim3(kThreads), 0, s, z_in, wt_key, n, K, z_w, bad);
+  return hipGetLastError();
+}
+
+}  // namespace lda

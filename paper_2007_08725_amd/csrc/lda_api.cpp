@@ -110,7 +110,32 @@ lda_status rebuild_counts(lda_handle *h) {
   return LDA_OK;
 }
 
-lda_status create_device(lda_handle *h, const lda_options *o) {
+template <typename T>
+void dfree(lda_handle *h, T *&ptr) {
+  if (!ptr) return;
+  void *v = static_cast<void *>(ptr);
+  auto it = std::find(h->allocations.begin(), h->allocations.end(), v);
+  if (it != h->allocations.end()) h->allocations.erase(it);
+  if (h->dev_alloc) h->dev_free(v, h->alloc_ctx);
+  else (void)hipFree(v);
+  ptr = nullptr;
+}
+
+lda_status sort_pairs(lda_handle *h, const uint32_t *keys_in, uint32_t *keys_out, const uint32_t *vals_in,
+                      uint32_t *vals_out, unsigned end_bit) {
+  size_t bytes = 0;
+  HIP_TRY(h, sort_pairs_u32(nullptr, bytes, keys_in, keys_out, vals_in, vals_out, h->L.n, end_bit, h->stream));
+  uint8_t *tmp = nullptr;
+  LDA_TRY(dalloc(h, &tmp, bytes));
+  HIP_TRY(h, sort_pairs_u32(tmp, bytes, keys_in, keys_out, vals_in, vals_out, h->L.n, end_bit, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  dfree(h, tmp);
+  return LDA_OK;
+}
+
+// Device layout (Sec. 4.2-4.3, 5.1): both token orders are built with radix
+// sorts on the GPU; only per-word and per-document counts visit the host.
+lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *word, const int32_t *doc, int32_t R) {
   Layout &L = h->L;
   HIP_TRY(h, hipGetDevice(&h->device));
   int cus = 0, lds_max = 0;
@@ -129,16 +154,81 @@ lda_status create_device(lda_handle *h, const lda_options *o) {
   Params &p = h->p;
   p.grid_regions = std::max(1, cus * 8);
   p.grid_docs = std::max(1, cus * 8);
-
   const size_t n = size_t(L.n);
+  const bool identity = L.key_identity;
   DevState &d = h->d;
-  LDA_TRY(dalloc(h, &d.doc_off, L.doc_off.size()));
-  LDA_TRY(dalloc(h, &d.dt_word, n));
-  if (!L.key_identity) LDA_TRY(dalloc(h, &d.dt_key, n));
-  LDA_TRY(dalloc(h, &d.dt_wpos, n));
+
+  // 1. the token list on the device
+  int32_t *word_d = nullptr, *doc_d = nullptr;
+  LDA_TRY(dalloc(h, &word_d, n));
+  LDA_TRY(dalloc(h, &doc_d, n));
+  HIP_TRY(h, hipMemcpyAsync(word_d, word, n * 4, hipMemcpyHostToDevice, h->stream));
+  HIP_TRY(h, hipMemcpyAsync(doc_d, doc, n * 4, hipMemcpyHostToDevice, h->stream));
+
+  // 2. doc order: stable sort of input indices by document
+  uint32_t *doc_sorted = nullptr;
+  if (!identity) {
+    LDA_TRY(dalloc(h, &doc_sorted, n));
+    LDA_TRY(dalloc(h, &d.dt_key, n));
+    LDA_TRY(sort_pairs(h, reinterpret_cast<const uint32_t *>(doc_d), doc_sorted, nullptr, d.dt_key,
+                       bits_for(uint64_t(L.M) - 1)));
+  }
+  const uint32_t *doc_keys = identity ? reinterpret_cast<const uint32_t *>(doc_d) : doc_sorted;
+  LDA_TRY(dalloc(h, &d.doc_off, size_t(L.M) + 1));
+  HIP_TRY(h, launch_boundaries(doc_keys, L.n, uint32_t(L.M), d.doc_off, h->stream));
+
+  // 3. caller word ids in doc order, stably sorted by word
+  uint32_t *w_orig = nullptr;
+  if (!identity) {
+    LDA_TRY(dalloc(h, &w_orig, n));
+    HIP_TRY(h, launch_gather_u32(w_orig, word_d, d.dt_key, L.n, h->stream));
+  }
+  uint32_t *wkey = nullptr, *wpos = nullptr, *woff_orig = nullptr;
+  LDA_TRY(dalloc(h, &wkey, n));
+  LDA_TRY(dalloc(h, &wpos, n));
+  LDA_TRY(sort_pairs(h, identity ? reinterpret_cast<const uint32_t *>(word_d) : w_orig, wkey, nullptr, wpos,
+                     bits_for(uint64_t(L.V) - 1)));
+  dfree(h, w_orig);
+  LDA_TRY(dalloc(h, &woff_orig, size_t(L.V) + 1));
+  HIP_TRY(h, launch_boundaries(wkey, L.n, uint32_t(L.V), woff_orig, h->stream));
+
+  // 4. counts to the host: relabel, capacities and regions
+  std::vector<uint32_t> woff_h(size_t(L.V) + 1);
+  L.doc_off.resize(size_t(L.M) + 1);
+  HIP_TRY(h, hipMemcpyAsync(woff_h.data(), woff_orig, woff_h.size() * 4, hipMemcpyDeviceToHost, h->stream));
+  HIP_TRY(h, hipMemcpyAsync(L.doc_off.data(), d.doc_off, L.doc_off.size() * 4, hipMemcpyDeviceToHost, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  std::vector<uint32_t> cnt(static_cast<size_t>(L.V));
+  for (int32_t v = 0; v < L.V; ++v) cnt[size_t(v)] = woff_h[size_t(v) + 1] - woff_h[size_t(v)];
+  std::string msg;
+  lda_status st = plan_from_counts(cnt, L.K, R, L, msg);
+  if (st != LDA_OK) return fail(h, st, msg);
+  p.n_present = L.n_present;
+  p.n_dense = L.n_dense;
+  p.n_regions = L.n_regions;
+
+  // 5. word order in relabelled ids and the links between the two orders
+  int32_t *relabel_d = nullptr;
+  LDA_TRY(dalloc(h, &relabel_d, size_t(L.V)));
   LDA_TRY(dalloc(h, &d.word_off, L.word_off.size()));
+  LDA_TRY(upload(h, relabel_d, L.relabel));
+  LDA_TRY(upload(h, d.word_off, L.word_off));
+  LDA_TRY(dalloc(h, &d.dt_word, n));
+  LDA_TRY(dalloc(h, &d.dt_wpos, n));
   LDA_TRY(dalloc(h, &d.wt_doc, n));
   LDA_TRY(dalloc(h, &d.wt_key, n));
+  HIP_TRY(h, launch_word_order(wkey, wpos, L.n, relabel_d, woff_orig, d.word_off, doc_sorted, doc_d, d.dt_key,
+                               d.dt_word, d.dt_wpos, d.wt_doc, d.wt_key, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  dfree(h, relabel_d);
+  dfree(h, woff_orig);
+  dfree(h, wpos);
+  dfree(h, wkey);
+  dfree(h, doc_sorted);
+  dfree(h, doc_d);
+  dfree(h, word_d);
+
+  // 6. count tables and scheduler state
   LDA_TRY(dalloc(h, &d.region, L.region.size()));
   LDA_TRY(dalloc(h, &d.split, L.split.size()));
   LDA_TRY(dalloc(h, &d.z_w, n));
@@ -157,14 +247,6 @@ lda_status create_device(lda_handle *h, const lda_options *o) {
   LDA_TRY(dalloc(h, &d.ll_part, size_t(L.n_regions)));
   LDA_TRY(dalloc(h, &d.ll_out, 1));
   d.stats = h->stats_base;
-
-  LDA_TRY(upload(h, d.doc_off, L.doc_off));
-  LDA_TRY(upload(h, d.dt_word, L.dt_word));
-  if (!L.key_identity) LDA_TRY(upload(h, d.dt_key, L.dt_key));
-  LDA_TRY(upload(h, d.dt_wpos, L.dt_wpos));
-  LDA_TRY(upload(h, d.word_off, L.word_off));
-  LDA_TRY(upload(h, d.wt_doc, L.wt_doc));
-  LDA_TRY(upload(h, d.wt_key, L.wt_key));
   LDA_TRY(upload(h, d.region, L.region));
   LDA_TRY(upload(h, d.split, L.split));
   LDA_TRY(upload(h, d.d_cap, L.d_cap));
@@ -173,14 +255,10 @@ lda_status create_device(lda_handle *h, const lda_options *o) {
   HIP_TRY(h, launch_init_topics(d, p, h->stream));
   LDA_TRY(rebuild_counts(h));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
-  unsigned long long st[kStatsPerIter];
-  HIP_TRY(h, hipMemcpy(st, h->stats_base, sizeof(st), hipMemcpyDeviceToHost));
-  LDA_TRY(check_errors(h, st));
-  // the doc- and word-order staging arrays are no longer needed on the host
-  std::vector<uint32_t>().swap(L.dt_word);
-  std::vector<uint32_t>().swap(L.dt_key);
-  std::vector<uint32_t>().swap(L.dt_wpos);
-  std::vector<uint32_t>().swap(L.wt_doc);
+  unsigned long long stt[kStatsPerIter];
+  HIP_TRY(h, hipMemcpy(stt, h->stats_base, sizeof(stt), hipMemcpyDeviceToHost));
+  LDA_TRY(check_errors(h, stt));
+  std::vector<uint32_t>().swap(L.region);
   return LDA_OK;
 }
 
@@ -224,17 +302,18 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   lda_handle *h = new (std::nothrow) lda_handle();
   if (!h) return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
   std::string msg;
-  lda_status st;
-  try {
-    st = build_layout(word, doc, n_tokens, V, K, R, h->L, msg);
-  } catch (const std::bad_alloc &) {
-    st = LDA_E_NOMEM;
-    msg = "host allocation failed while building the layout";
-  }
+  int32_t M = 0;
+  bool sorted = false;
+  lda_status st = scan_tokens(word, doc, n_tokens, V, M, sorted, msg);
   if (st != LDA_OK) {
     delete h;
     return fail(nullptr, st, msg);
   }
+  h->L.n = n_tokens;
+  h->L.V = V;
+  h->L.K = K;
+  h->L.M = M;
+  h->L.key_identity = sorted;
   if (opts) {
     h->dev_alloc = opts->dev_alloc;
     h->dev_free = opts->dev_free;
@@ -242,21 +321,18 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   }
   Params &p = h->p;
   p.n = n_tokens;
-  p.M = h->L.M;
+  p.M = M;
   p.V = V;
   p.K = K;
-  p.n_present = h->L.n_present;
-  p.n_dense = h->L.n_dense;
-  p.n_regions = h->L.n_regions;
   p.alpha = alpha;
   p.beta = beta;
   p.vbeta = double(V) * beta;
   p.seed = seed;
   p.g = g;
   p.no_skip = no_skip;
-  p.key_identity = h->L.key_identity ? 1 : 0;
+  p.key_identity = sorted ? 1 : 0;
   try {
-    st = create_device(h, opts);
+    st = create_device(h, opts, word, doc, R);
   } catch (const std::bad_alloc &) {
     st = fail(h, LDA_E_NOMEM, "host allocation failed");
   }
@@ -304,8 +380,9 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       if (!stats) continue;
       lda_iter_stats &o = stats[done + c];
       hipEvent_t *ev = &h->events[size_t(c) * kEventsPerIter];
-      float ms_all = 0, ms_doc = 0, ms_smp = 0, ms_reb = 0;
+      float ms_all = 0, ms_pre = 0, ms_doc = 0, ms_smp = 0, ms_reb = 0;
       HIP_TRY(h, hipEventElapsedTime(&ms_all, ev[0], ev[4]));
+      HIP_TRY(h, hipEventElapsedTime(&ms_pre, ev[0], ev[1]));
       HIP_TRY(h, hipEventElapsedTime(&ms_doc, ev[1], ev[2]));
       HIP_TRY(h, hipEventElapsedTime(&ms_smp, ev[2], ev[3]));
       HIP_TRY(h, hipEventElapsedTime(&ms_reb, ev[3], ev[4]));
@@ -314,12 +391,14 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       o.ms_docpass = ms_doc;
       o.ms_sampler = ms_smp;
       o.ms_rebuild = ms_reb;
+      o.ms_precompute = ms_pre;
       o.skip_step3 = int64_t(s[ST_SKIP3]);
       o.skip_after_s = int64_t(s[ST_SKIP_AFTER_S]);
       o.sampled = int64_t(s[ST_SAMPLED]);
       o.nnz_scanned = int64_t(s[ST_NNZ]);
       o.regions = int64_t(s[ST_REGIONS]);
       o.dense_regions = int64_t(s[ST_DENSE_REGIONS]);
+      o.row_bytes = int64_t(s[ST_ROW_BYTES]);
     }
     done += chunk;
   }
@@ -355,9 +434,12 @@ lda_status lda_get_counts(lda_handle *h, lda_counts *out) {
       !out->W_count)
     return LDA_OK;  // size query
   if (out->z) {
-    std::vector<uint16_t> zw(n);
-    HIP_TRY(h, hipMemcpy(zw.data(), h->d.z_w, n * 2, hipMemcpyDeviceToHost));
-    for (size_t j = 0; j < n; ++j) out->z[L.wt_key[j]] = int32_t(zw[j]);
+    int32_t *zin = nullptr;
+    LDA_TRY(dalloc(h, &zin, n));
+    HIP_TRY(h, launch_scatter_z(h->d.z_w, h->d.wt_key, L.n, zin, h->stream));
+    HIP_TRY(h, hipMemcpyAsync(out->z, zin, n * 4, hipMemcpyDeviceToHost, h->stream));
+    HIP_TRY(h, hipStreamSynchronize(h->stream));
+    dfree(h, zin);
   }
   if (out->T) {
     std::vector<uint32_t> tk(static_cast<size_t>(K));
@@ -433,16 +515,20 @@ lda_status lda_set_assignments(lda_handle *h, const int32_t *z, int64_t iteratio
   if (iteration < 0 || iteration >= (int64_t(1) << 32)) return fail(h, LDA_E_ARG, "iteration out of range");
   const Layout &L = h->L;
   const size_t n = size_t(L.n);
-  std::vector<uint16_t> zw(n);
-  for (size_t j = 0; j < n; ++j) {
-    const int32_t v = z[L.wt_key[j]];
-    if (v < 0 || v >= L.K) return fail(h, LDA_E_ARG, "topic out of range at token " + std::to_string(L.wt_key[j]));
-    zw[j] = uint16_t(v);
-  }
-  HIP_TRY(h, hipMemcpyAsync(h->d.z_w, zw.data(), n * 2, hipMemcpyHostToDevice, h->stream));
+  for (size_t i = 0; i < n; ++i)
+    if (z[i] < 0 || z[i] >= L.K) return fail(h, LDA_E_ARG, "topic out of range at token " + std::to_string(i));
+  int32_t *zin = nullptr;
+  LDA_TRY(dalloc(h, &zin, n));
+  HIP_TRY(h, hipMemcpyAsync(zin, z, n * 4, hipMemcpyHostToDevice, h->stream));
+  HIP_TRY(h, hipMemsetAsync(h->stats_base, 0, sizeof(unsigned long long) * kStatsPerIter, h->stream));
+  HIP_TRY(h, launch_gather_z(zin, h->d.wt_key, L.n, L.K, h->d.z_w, h->stats_base + ST_ERRORS, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  dfree(h, zin);
+  unsigned long long st[kStatsPerIter];
+  HIP_TRY(h, hipMemcpy(st, h->stats_base, sizeof(st), hipMemcpyDeviceToHost));
+  LDA_TRY(check_errors(h, st));
   LDA_TRY(rebuild_counts(h));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
-  unsigned long long st[kStatsPerIter];
   HIP_TRY(h, hipMemcpy(st, h->stats_base, sizeof(st), hipMemcpyDeviceToHost));
   LDA_TRY(check_errors(h, st));
   h->iteration = iteration;

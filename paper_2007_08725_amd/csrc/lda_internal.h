@@ -32,11 +32,7 @@ struct Layout {
   std::vector<uint32_t> count;    // [n_present] tokens per new id
   std::vector<uint32_t> doc_off;  // [M+1]
   std::vector<uint32_t> word_off; // [n_present+1]
-  std::vector<uint32_t> dt_word;  // [n] new word id of each doc-ordered token
-  std::vector<uint32_t> dt_key;   // [n] input index of each doc-ordered token (empty if identity)
-  std::vector<uint32_t> dt_wpos;  // [n] word-order position of each doc-ordered token
-  std::vector<uint32_t> wt_doc;   // [n] doc id of each word-ordered token
-  std::vector<uint32_t> wt_key;   // [n] input index of each word-ordered token
+  std::vector<uint32_t> wt_key;   // [n] input index of each word-ordered token (host reference only)
   std::vector<uint32_t> d_cap;    // [M+1] offsets of D rows, capacity min(len, K)
   std::vector<uint32_t> ws_cap;   // [n_present-n_dense+1] offsets of sparse W rows, capacity = count
   std::vector<uint32_t> region;   // [3*n_regions] (word, begin, end)
@@ -46,9 +42,31 @@ struct Layout {
   bool key_identity = false;      // input already doc-sorted: input index == doc-order position
 };
 
-// Validates and builds the layout; returns LDA_OK or an error with msg set.
+// Validates ids (word in [0, V), doc >= 0, n < 2^32); M = max doc + 1 and
+// whether the input is already sorted by document.
+lda_status scan_tokens(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t &M, bool &doc_sorted,
+                       std::string &msg);
+// From the per-word token counts (caller ids) and L.doc_off: relabel, dense
+// prefix, relabelled word offsets, capacities and regions.  LDA_E_RANGE for a
+// document longer than LDA_MAX_DOC_LEN.
+lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t R, Layout &L, std::string &msg);
+// All-host reference of the layout (lda_describe_layout); fills L.wt_key.
 lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t K, int32_t R,
                         Layout &L, std::string &msg);
+
+// Device layout steps (layout_gpu.hip).
+unsigned bits_for(uint64_t max_value);
+hipError_t sort_pairs_u32(void *tmp, size_t &tmp_bytes, const uint32_t *keys_in, uint32_t *keys_out,
+                          const uint32_t *vals_in, uint32_t *vals_out, int64_t n, unsigned end_bit, hipStream_t s);
+hipError_t launch_gather_u32(uint32_t *dst, const int32_t *src, const uint32_t *idx, int64_t n, hipStream_t s);
+hipError_t launch_boundaries(const uint32_t *keys, int64_t n, uint32_t nbins, uint32_t *off, hipStream_t s);
+hipError_t launch_word_order(const uint32_t *wkey, const uint32_t *wpos, int64_t n, const int32_t *relabel,
+                             const uint32_t *woff_orig, const uint32_t *woff_new, const uint32_t *doc_sorted,
+                             const int32_t *doc_in, const uint32_t *dt_key, uint32_t *dt_word, uint32_t *dt_wpos,
+                             uint32_t *wt_doc, uint32_t *wt_key, hipStream_t s);
+hipError_t launch_scatter_z(const uint16_t *z_w, const uint32_t *wt_key, int64_t n, int32_t *z_in, hipStream_t s);
+hipError_t launch_gather_z(const int32_t *z_in, const uint32_t *wt_key, int64_t n, int32_t K, uint16_t *z_w,
+                           unsigned long long *bad, hipStream_t s);
 
 // ---------------------------------------------------------- device state --
 struct WordRec {  // per relabelled word, refreshed every iteration (Sec. 3.2, steps 1 and 4)
@@ -93,7 +111,7 @@ struct Params {
 };
 
 enum { CNT_SAMPLER = 0, CNT_REBUILD_W = 1, CNT_DOCPASS = 2, CNT_REBUILD_D = 3, CNT_LOGLIK = 4 };
-enum { ST_SKIP3 = 0, ST_SKIP_AFTER_S = 1, ST_SAMPLED = 2, ST_NNZ = 3, ST_REGIONS = 4, ST_DENSE_REGIONS = 5, ST_ERRORS = 6 };
+enum { ST_SKIP3 = 0, ST_SKIP_AFTER_S = 1, ST_SAMPLED = 2, ST_NNZ = 3, ST_REGIONS = 4, ST_DENSE_REGIONS = 5, ST_ERRORS = 6, ST_ROW_BYTES = 7 };
 constexpr int kStatsPerIter = 8;
 
 // Kernel launchers (all asynchronous on `s`); return hipGetLastError().

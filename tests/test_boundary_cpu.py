@@ -84,14 +84,19 @@ def test_create_argument_errors(lib):
     assert lib.lda_create(pw, pd, 3, 3, 4, 0.5, 0.01, 42, None, None) == lda.LDA_E_ARG
 
 
-def test_create_range_errors(lib):
+def test_layout_range_errors(lib):
     # a document with more than 65535 tokens does not fit the 16-bit counts
+    # (lda_create reports the same after its device sort; see the GPU tests)
     n = lda.MAX_DOC_LEN + 1
     w = np.zeros(n, np.int32)
     d = np.zeros(n, np.int32)
-    st, h = _create(lib, ctypes.c_void_p(w.ctypes.data), ctypes.c_void_p(d.ctypes.data), n, 1, 4, 0.5, 0.01)
-    assert st == lda.LDA_E_RANGE and not h.value
+    with pytest.raises(lda.LDAError) as ei:
+        lda.describe_layout(w, d, 1, 4)
+    assert ei.value.status == lda.LDA_E_RANGE
     assert b"65535" in lib.lda_last_error(None)
+    # exactly 65535 is allowed
+    L = lda.describe_layout(w[:-1], d[:-1], 1, 4)
+    assert L["n_docs"] == 1
 
 
 def test_handle_calls_reject_null(lib):

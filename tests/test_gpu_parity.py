@@ -249,3 +249,19 @@ def test_set_assignments_rejects_bad_topics(c1):
             m.set_assignments(z, 0)
         assert ei.value.status == lda.LDA_E_ARG
         m.iterate(1)  # the handle is still usable
+
+
+def test_create_rejects_too_long_document():
+    import ctypes
+
+    import paper_2007_08725_amd as lda
+    lib = lda.load_library()
+    n = lda.MAX_DOC_LEN + 1
+    w = np.zeros(n, np.int32)
+    d = np.zeros(n, np.int32)
+    d[-1] = 0
+    h = ctypes.c_void_p()
+    st = lib.lda_create(ctypes.c_void_p(w.ctypes.data), ctypes.c_void_p(d.ctypes.data), n, 1, 4, 0.5, 0.01, SEED,
+                        None, ctypes.byref(h))
+    assert st == lda.LDA_E_RANGE and not h.value
+    assert b"65535" in lib.lda_last_error(None)
