@@ -94,6 +94,24 @@ __device__ __forceinline__ double group_incl_scan(double v, int li) {
   return v;
 }
 
+// Shift a double right by S lanes inside each row of 16 lanes (DPP
+// row_shr); lanes below S read 0.
+template <int S>
+__device__ __forceinline__ double row_shr(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), 0x110 + S, 0xF, 0xF, true);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), 0x110 + S, 0xF, 0xF, true);
+  return __hiloint2double(hi, lo);
+}
+
+// Inclusive prefix sum over each row of 16 lanes.
+__device__ __forceinline__ double row_incl_scan(double v) {
+  v += row_shr<1>(v);
+  v += row_shr<2>(v);
+  v += row_shr<4>(v);
+  v += row_shr<8>(v);
+  return v;
+}
+
 struct Top3 {
   double v[3];
   uint32_t k[3];
@@ -305,7 +323,7 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
         const double Sest = p.g == 1 ? rec.a2 * double(len - C1)
                                      : rec.a2 * double(C2) + rec.a3 * double(len - C1 - C2);
         const bool skip = !p.no_skip && (u * (Mm + Sest + rec.qp) < Mm);
-        d.z_w[d.dt_wpos[pp]] = skip ? uint16_t(rec.k1) : kUndecided;
+        d.z_w[d.dt_wpos[pp]] = skip ? uint16_t(rec.k1) : uint16_t(kUndecidedBit | min(C1, uint32_t(kC1Unknown)));
         nskip += skip ? 1ull : 0ull;
       }
     }
@@ -317,6 +335,71 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
 // Steps 4-6 for the undecided tokens of one region; the W^ row of the word
 // sits in LDS (Sec. 4.3, last paragraph) together with the Q' prefix over
 // blocks of kGroup topics.
+//
+// Work split: a wave takes 64 consecutive word-ordered tokens; every lane
+// fetches its own token's document, key, D-row offset and length and draws its
+// own u, then the four 16-lane groups take the undecided tokens in turn.  A
+// group loads up to kChunk entries of the D row into registers at once (lane l
+// holds a contiguous run, so lane partial sums are in ascending topic order),
+// sums S' per lane, scans the 16 lane sums, and finds the selected entry by a
+// walk inside a single lane.  Rows longer than kChunk are taken in chunks.
+constexpr int kRowRegs = 16;                 // D entries per lane per chunk
+constexpr uint32_t kChunk = kGroup * kRowRegs;  // 256 entries per chunk
+static_assert(kGroup == 16, "the row scans use DPP rows of 16 lanes");
+
+// Load a chunk of nn D entries: lane li gets entries [li*c, li*c + c) with
+// c = ceil(nn / 16), topics ascending; slots past the chunk read as 0 (topic
+// 0, count 0).  Only slots i < bound are touched (bound is wave-uniform and
+// at least c); reads may run past the row into the padding.
+__device__ __forceinline__ void load_chunk(const uint32_t *__restrict__ row, uint32_t nn, int li, uint32_t bound,
+                                           uint32_t (&r)[kRowRegs]) {
+  const uint32_t c = (nn + kGroup - 1) / kGroup;
+  const uint32_t b = uint32_t(li) * c;
+  const uint32_t end = min(b + c, nn);
+  const uint32_t *p = row + b;
+#pragma unroll
+  for (int i = 0; i < kRowRegs; ++i) {
+    uint32_t v = 0u;
+    if (uint32_t(i) < bound) v = p[i];
+    r[i] = (b + uint32_t(i) < end) ? v : 0u;
+  }
+}
+
+// This lane's S' terms in ascending topic order (W^[K1] is 0 in LDS, so the
+// max-topic entry contributes nothing).
+__device__ __forceinline__ double lane_sum(const uint32_t (&r)[kRowRegs], const double *__restrict__ wh,
+                                           uint32_t bound) {
+  double s = 0.0;
+#pragma unroll
+  for (int i = 0; i < kRowRegs; ++i) {
+    if (uint32_t(i) < bound) s += double(r[i] & 0xFFFFu) * wh[r[i] >> 16];
+  }
+  return s;
+}
+
+// Walk this lane's entries from `cum` until x is passed; returns the topic
+// (the last positive entry if rounding leaves x beyond them, K1 if none).
+__device__ __forceinline__ uint32_t lane_walk(const uint32_t (&r)[kRowRegs], const double *__restrict__ wh,
+                                              uint32_t K1, double cum, double x, uint32_t bound) {
+  uint32_t last = K1, pick = K1;
+  bool done = false;
+#pragma unroll
+  for (int i = 0; i < kRowRegs; ++i) {
+    if (uint32_t(i) < bound) {
+      const uint32_t k = r[i] >> 16;
+      const double term = double(r[i] & 0xFFFFu) * wh[k];
+      const double next = cum + term;
+      const bool take = !done && term > 0.0;
+      cum = take ? next : cum;
+      last = take ? k : last;
+      const bool hit = take && x < next;
+      pick = hit ? k : pick;
+      done = done || hit;
+    }
+  }
+  return done ? pick : last;
+}
+
 __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32_t t,
                                                     unsigned long long *__restrict__ stats) {
   extern __shared__ double lds[];
@@ -373,16 +456,17 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
         }
       }
       __syncthreads();
+      // the max topic is its own branch: W^' has a 0 there (Eq. 5)
+      if (tid == 0) wh[K1] = 0.0;
+      __syncthreads();
       for (int blk = tid; blk < nb; blk += kBlock) {
         double s = 0.0;
         const int k1 = min(K, (blk + 1) * kGroup);
-        for (int k = blk * kGroup; k < k1; ++k)
-          if (uint32_t(k) != K1) s += p.alpha * wh[k];
+        for (int k = blk * kGroup; k < k1; ++k) s += p.alpha * wh[k];
         qb[blk + 1] = s;
       }
       __syncthreads();
       if (wave == 0) {
-        // in-place exclusive-to-inclusive prefix: qb[b+1] = qb[b] + block sum
         const int per = (nb + kWave - 1) / kWave;
         const int q0 = min(nb, lane * per), q1 = min(nb, q0 + per);
         double s = 0.0;
@@ -399,56 +483,79 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
 
     for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += kBlock) {
       const uint32_t j = base + uint32_t(lane);
-      const bool und = j < e && d.z_w[j] == kUndecided;
+      const uint32_t zz = j < e ? uint32_t(d.z_w[j]) : 0u;
+      const bool und = (zz & kUndecidedBit) != 0u;
+      uint32_t off = 0, nnz = 0, c1 = zz & 0x7FFFu;
+      double u = 0.0;
+      if (und) {
+        const uint32_t doc = d.wt_doc[j];
+        u = uniform_draw(p.seed, t, d.wt_key[j]);
+        off = d.d_cap[doc];
+        nnz = d.d_nnz[doc];
+        if (c1 == kC1Unknown) c1 = row_lookup(d.d_ent + off, nnz, K1);
+      }
       unsigned long long mask = __ballot(und);
       while (mask) {
         unsigned long long m = mask;
         for (int q = 0; q < grp; ++q) m &= m - 1ull;
         for (int q = 0; q < kWave / kGroup; ++q) mask &= mask - 1ull;
+        const int src = m ? __ffsll(m) - 1 : lane;
+        // every lane takes part in the permutes: a source lane may belong to
+        // a group that has no token in this round
+        const uint32_t t_off = __shfl(off, src);
+        const uint32_t nnz_src = __shfl(nnz, src);
+        const uint32_t t_c1 = __shfl(c1, src);
+        const double t_u = __shfl(u, src);
+        const uint32_t t_nnz = m ? nnz_src : 0u;
+        // wave-uniform register bound for the first chunk
+        uint32_t cw = (min(t_nnz, kChunk) + kGroup - 1) / kGroup;
+        cw = max(cw, uint32_t(__shfl_xor(int(cw), 16)));
+        cw = max(cw, uint32_t(__shfl_xor(int(cw), 32)));
+        const uint32_t bound0 = uint32_t(__builtin_amdgcn_readfirstlane(int(cw)));
         if (m == 0ull) continue;
-        const uint32_t jt = base + uint32_t(__ffsll(m) - 1);
-        const uint32_t doc = d.wt_doc[jt];
-        const uint32_t key = d.wt_key[jt];
-        const uint32_t *row = d.d_ent + d.d_cap[doc];
-        const uint32_t nnz = d.d_nnz[doc];
-        // S' over nz(D[d]) \ {K1} and C1 = D[d][K1]
-        double acc = 0.0;
-        uint32_t c1 = 0;
-        for (uint32_t q = li; q < nnz; q += kGroup) {
-          const uint32_t ent = row[q];
-          const uint32_t k = ent >> 16, c = ent & 0xFFFFu;
-          if (k == K1) c1 = c;
-          else acc += double(c) * wh[k];
+        const uint32_t *row = d.d_ent + t_off;
+        const uint32_t nch = (t_nnz + kChunk - 1) / kChunk;
+
+        // pass 1: S' through the same lane sums and row scan pass 2 uses
+        uint32_t r[kRowRegs];
+        double S = 0.0, lane_incl = 0.0, lane_s = 0.0;
+        for (uint32_t ch = 0; ch < nch; ++ch) {
+          const uint32_t bound = ch == 0 ? bound0 : uint32_t(kRowRegs);
+          load_chunk(row + ch * kChunk, min(kChunk, t_nnz - ch * kChunk), li, bound, r);
+          lane_s = lane_sum(r, wh, bound);
+          lane_incl = row_incl_scan(lane_s);
+          S += __shfl(lane_incl, kGroup - 1, kGroup);
         }
-        const double S = group_sum<kGroup>(acc);
-        const uint32_t C1 = group_sum_u32<kGroup>(c1);
-        const double Mm = a1 * (double(C1) + p.alpha);
+        const double Mm = a1 * (double(t_c1) + p.alpha);
         const double Z = (Mm + S) + qp;
-        const double x = uniform_draw(p.seed, t, key) * Z;
+        const double x = t_u * Z;
         uint32_t topic = K1;
         if (x < Mm) {
           if (li == 0) n_after_s++;
         } else {
+          // pass 2: the chunk, then the lane, then the entry where x falls
           double cbase = Mm;
           bool found = false;
-          for (uint32_t e0 = 0; e0 < nnz; e0 += kGroup) {
-            const uint32_t q = e0 + uint32_t(li);
-            double term = 0.0;
-            uint32_t k = 0;
-            if (q < nnz) {
-              const uint32_t ent = row[q];
-              k = ent >> 16;
-              if (k != K1) term = double(ent & 0xFFFFu) * wh[k];
+          for (uint32_t ch = 0; ch < nch && !found; ++ch) {
+            const uint32_t bound = ch == 0 ? bound0 : uint32_t(kRowRegs);
+            if (nch > 1) {
+              load_chunk(row + ch * kChunk, min(kChunk, t_nnz - ch * kChunk), li, bound, r);
+              lane_s = lane_sum(r, wh, bound);
+              lane_incl = row_incl_scan(lane_s);
             }
-            const double incl = group_incl_scan<kGroup>(term, li);
-            const bool hit = term > 0.0 && x < cbase + incl;
-            const uint32_t hm = uint32_t(__ballot(hit) >> (grp * kGroup)) & kGroupMask;
-            if (hm) {
-              topic = __shfl(k, __ffs(hm) - 1, kGroup);
+            const double total = __shfl(lane_incl, kGroup - 1, kGroup);
+            if (x < cbase + total) {
+              const bool hit = lane_s > 0.0 && x < cbase + lane_incl;
+              const uint32_t hm = uint32_t(__ballot(hit) >> (grp * kGroup)) & kGroupMask;
+              // rounding can leave x past every lane's end: take the last lane with terms
+              const uint32_t pm = uint32_t(__ballot(lane_s > 0.0) >> (grp * kGroup)) & kGroupMask;
+              const int sel = hm ? __ffs(hm) - 1 : (pm ? 31 - __clz(pm) : 0);
+              const double excl = __shfl(lane_incl - lane_s, sel, kGroup);
+              const uint32_t pick = lane_walk(r, wh, K1, cbase + excl, x, bound);
+              topic = __shfl(pick, sel, kGroup);
               found = true;
-              break;
             }
-            cbase += __shfl(incl, kGroup - 1, kGroup);
+            cbase += total;
           }
           if (!found) {
             const double xq = x - cbase;
@@ -462,8 +569,8 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
                 else hi = mid - 1;
               }
               const int k = lo * kGroup + li;
-              const double term = (k < K && uint32_t(k) != K1) ? p.alpha * wh[k] : 0.0;
-              const double incl = group_incl_scan<kGroup>(term, li);
+              const double term = k < K ? p.alpha * wh[k] : 0.0;
+              const double incl = row_incl_scan(term);
               const bool hit = term > 0.0 && xq < qb[lo] + incl;
               const uint32_t hm = uint32_t(__ballot(hit) >> (grp * kGroup)) & kGroupMask;
               if (hm) {
@@ -476,9 +583,9 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
           }
         }
         if (li == 0) {
-          d.z_w[jt] = uint16_t(topic);
+          d.z_w[base + uint32_t(src)] = uint16_t(topic);
           n_sampled++;
-          nnz_sum += nnz;
+          nnz_sum += t_nnz;
         }
       }
     }

@@ -234,7 +234,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.z_w, n));
   LDA_TRY(dalloc(h, &d.d_cap, L.d_cap.size()));
   LDA_TRY(dalloc(h, &d.d_nnz, size_t(L.M)));
-  LDA_TRY(dalloc(h, &d.d_ent, size_t(L.d_cap.back())));
+  LDA_TRY(dalloc(h, &d.d_ent, size_t(L.d_cap.back()) + kRowPad));
   LDA_TRY(dalloc(h, &d.w_dense, size_t(L.n_dense) * size_t(L.K)));
   LDA_TRY(dalloc(h, &d.ws_cap, L.ws_cap.size()));
   LDA_TRY(dalloc(h, &d.ws_nnz, L.ws_cap.size()));

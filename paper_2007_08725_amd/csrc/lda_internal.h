@@ -12,8 +12,14 @@
 
 namespace lda {
 
-// Reserved value of a 16-bit topic slot: "not decided by the step-3 test".
-constexpr uint16_t kUndecided = 0xFFFF;
+// A 16-bit topic slot holds a topic (< K <= 16384) or, for a token the
+// step-3 test left undecided, kUndecidedBit | C1 with C1 = D[d][K1]
+// (kC1Unknown when C1 does not fit in 15 bits).
+constexpr uint16_t kUndecidedBit = 0x8000;
+constexpr uint16_t kC1Unknown = 0x7FFF;
+// Slack entries after the last D row: the sampler reads whole register
+// chunks past the end of a row and discards what lies beyond it.
+constexpr uint32_t kRowPad = 64;
 constexpr int kDefaultRegionTokens = 10000;  // Sec. 5.1
 constexpr int kBlock = 256;                  // threads per workgroup (4 wave64)
 
