@@ -343,61 +343,164 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
 // holds a contiguous run, so lane partial sums are in ascending topic order),
 // sums S' per lane, scans the 16 lane sums, and finds the selected entry by a
 // walk inside a single lane.  Rows longer than kChunk are taken in chunks.
-constexpr int kRowRegs = 16;                 // D entries per lane per chunk
-constexpr uint32_t kChunk = kGroup * kRowRegs;  // 256 entries per chunk
 static_assert(kGroup == 16, "the row scans use DPP rows of 16 lanes");
+constexpr uint32_t kChunk = 256;  // D entries one group holds in registers (16 per lane)
 
-// Load a chunk of nn D entries: lane li gets entries [li*c, li*c + c) with
-// c = ceil(nn / 16), topics ascending; slots past the chunk read as 0 (topic
-// 0, count 0).  Only slots i < bound are touched (bound is wave-uniform and
-// at least c); reads may run past the row into the padding.
-__device__ __forceinline__ void load_chunk(const uint32_t *__restrict__ row, uint32_t nn, int li, uint32_t bound,
-                                           uint32_t (&r)[kRowRegs]) {
-  const uint32_t c = (nn + kGroup - 1) / kGroup;
-  const uint32_t b = uint32_t(li) * c;
-  const uint32_t end = min(b + c, nn);
-  const uint32_t *p = row + b;
+// Per-lane data of one batch of 64 word-ordered tokens (lane = token).
+struct BatchTok {
+  uint32_t off, nnz, c1;
+  double u;
+};
+
+// The word of the current region: W^ row (with W^[K1] = 0) and Q' block
+// prefix in LDS, and its per-word scalars.
+struct WordState {
+  const double *wh, *qb;
+  int nb, K;
+  uint32_t K1;
+  double a1, qp, alpha;
+};
+
+struct SamplerCounts {
+  unsigned long long sampled, after_s, nnz;
+};
+
+// Load C entries per lane from `row` (lane li gets entries [li*C, li*C + C),
+// topics ascending); entries at or past nn read as 0 (topic 0, count 0).
+// Reads may run past the row into the padding after the last row.
+template <int C>
+__device__ __forceinline__ void load_run(const uint32_t *__restrict__ row, uint32_t nn, int li, uint32_t (&r)[C]) {
+  const uint32_t q0 = uint32_t(li) * C;
 #pragma unroll
-  for (int i = 0; i < kRowRegs; ++i) {
-    uint32_t v = 0u;
-    if (uint32_t(i) < bound) v = p[i];
-    r[i] = (b + uint32_t(i) < end) ? v : 0u;
+  for (int i = 0; i < C; ++i) {
+    const uint32_t v = row[q0 + i];
+    r[i] = (q0 + uint32_t(i) < nn) ? v : 0u;
   }
 }
 
-// This lane's S' terms in ascending topic order (W^[K1] is 0 in LDS, so the
-// max-topic entry contributes nothing).
-__device__ __forceinline__ double lane_sum(const uint32_t (&r)[kRowRegs], const double *__restrict__ wh,
-                                           uint32_t bound) {
+// This lane's S' terms in ascending topic order (W^[K1] = 0 in LDS).
+template <int C>
+__device__ __forceinline__ double run_sum(const uint32_t (&r)[C], const double *__restrict__ wh) {
   double s = 0.0;
 #pragma unroll
-  for (int i = 0; i < kRowRegs; ++i) {
-    if (uint32_t(i) < bound) s += double(r[i] & 0xFFFFu) * wh[r[i] >> 16];
-  }
+  for (int i = 0; i < C; ++i) s += double(r[i] & 0xFFFFu) * wh[r[i] >> 16];
   return s;
 }
 
-// Walk this lane's entries from `cum` until x is passed; returns the topic
-// (the last positive entry if rounding leaves x beyond them, K1 if none).
-__device__ __forceinline__ uint32_t lane_walk(const uint32_t (&r)[kRowRegs], const double *__restrict__ wh,
-                                              uint32_t K1, double cum, double x, uint32_t bound) {
-  uint32_t last = K1, pick = K1;
-  bool done = false;
+// x lies in [base, base + row total): find the lane whose run holds it, move
+// that lane's C entries onto lanes 0..C-1, scan their terms and return the
+// topic of the entry where x falls (the last positive entry if rounding
+// leaves x past them).
+template <int C>
+__device__ __forceinline__ uint32_t pick_in_row(const uint32_t (&r)[C], double s, double incl, double base, double x,
+                                                const double *__restrict__ wh, int grp, int li) {
+  const uint32_t hm = uint32_t(__ballot(s > 0.0 && x < base + incl) >> (grp * kGroup)) & kGroupMask;
+  const uint32_t pm = uint32_t(__ballot(s > 0.0) >> (grp * kGroup)) & kGroupMask;
+  const int sel = hm ? __ffs(hm) - 1 : (pm ? 31 - __clz(pm) : 0);
+  const double start = base + __shfl(incl - s, sel, kGroup);
+  uint32_t mine = 0u;
 #pragma unroll
-  for (int i = 0; i < kRowRegs; ++i) {
-    if (uint32_t(i) < bound) {
-      const uint32_t k = r[i] >> 16;
-      const double term = double(r[i] & 0xFFFFu) * wh[k];
-      const double next = cum + term;
-      const bool take = !done && term > 0.0;
-      cum = take ? next : cum;
-      last = take ? k : last;
-      const bool hit = take && x < next;
-      pick = hit ? k : pick;
-      done = done || hit;
+  for (int i = 0; i < C; ++i) {
+    const uint32_t vi = __shfl(r[i], sel, kGroup);
+    mine = li == i ? vi : mine;
+  }
+  const double term = double(mine & 0xFFFFu) * wh[mine >> 16];
+  const double in2 = row_incl_scan(term);
+  const uint32_t hm2 = uint32_t(__ballot(term > 0.0 && x < start + in2) >> (grp * kGroup)) & kGroupMask;
+  const uint32_t pm2 = uint32_t(__ballot(term > 0.0) >> (grp * kGroup)) & kGroupMask;
+  const int h = hm2 ? __ffs(hm2) - 1 : (pm2 ? 31 - __clz(pm2) : 0);
+  return __shfl(mine >> 16, h, kGroup);
+}
+
+// Q' branch: xq measured from the start of the Q' segments.
+__device__ __forceinline__ uint32_t pick_in_q(double xq, const WordState &w, int grp, int li) {
+  if (!(xq < w.qb[w.nb])) return (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);
+  int lo = 0, hi = w.nb - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (w.qb[mid] <= xq) lo = mid;
+    else hi = mid - 1;
+  }
+  const int k = lo * kGroup + li;
+  const double term = k < w.K ? w.alpha * w.wh[k] : 0.0;
+  const double incl = row_incl_scan(term);
+  const uint32_t hm = uint32_t(__ballot(term > 0.0 && xq < w.qb[lo] + incl) >> (grp * kGroup)) & kGroupMask;
+  if (hm) return uint32_t(lo * kGroup + __ffs(hm) - 1);
+  const uint32_t pm = uint32_t(__ballot(term > 0.0) >> (grp * kGroup)) & kGroupMask;
+  return uint32_t(lo * kGroup + 31 - __clz(pm));
+}
+
+// Draw the tokens of `mask` whose D rows hold at most 16*C entries, four at a
+// time (one per 16-lane group); C is fixed per call so every group of a round
+// does the same amount of work.  C == 0 selects the long-row path, which
+// walks rows of any length in chunks of kChunk entries.
+template <int C>
+__device__ void draw_tokens(unsigned long long mask, const BatchTok &bt, const WordState &w,
+                            const uint32_t *__restrict__ d_ent, uint16_t *__restrict__ z_out, int lane, int grp,
+                            int li, SamplerCounts &cnt) {
+  while (mask) {
+    unsigned long long m = mask;
+    for (int q = 0; q < grp; ++q) m &= m - 1ull;
+    for (int q = 0; q < kWave / kGroup; ++q) mask &= mask - 1ull;
+    // every lane takes part in the permutes: a source lane may belong to a
+    // group that has no token in this round
+    const int src = m ? __ffsll(m) - 1 : lane;
+    const uint32_t t_off = __shfl(bt.off, src);
+    const uint32_t t_nnz = __shfl(bt.nnz, src);
+    const uint32_t t_c1 = __shfl(bt.c1, src);
+    const double t_u = __shfl(bt.u, src);
+    if (m == 0ull) continue;
+    const uint32_t *row = d_ent + t_off;
+    const double Mm = w.a1 * (double(t_c1) + w.alpha);
+    uint32_t topic = w.K1;
+    if constexpr (C > 0) {
+      uint32_t r[C];
+      load_run<C>(row, t_nnz, li, r);
+      const double s = run_sum<C>(r, w.wh);
+      const double incl = row_incl_scan(s);
+      const double S = __shfl(incl, kGroup - 1, kGroup);
+      const double x = t_u * ((Mm + S) + w.qp);
+      if (x < Mm) {
+        if (li == 0) cnt.after_s++;
+      } else if (x < Mm + S) {
+        topic = pick_in_row<C>(r, s, incl, Mm, x, w.wh, grp, li);
+      } else {
+        topic = pick_in_q(x - (Mm + S), w, grp, li);
+      }
+    } else {
+      const uint32_t nch = (t_nnz + kChunk - 1) / kChunk;
+      uint32_t r[16];
+      double S = 0.0;
+      for (uint32_t ch = 0; ch < nch; ++ch) {
+        load_run<16>(row + ch * kChunk, t_nnz - ch * kChunk, li, r);
+        S += __shfl(row_incl_scan(run_sum<16>(r, w.wh)), kGroup - 1, kGroup);
+      }
+      const double x = t_u * ((Mm + S) + w.qp);
+      if (x < Mm) {
+        if (li == 0) cnt.after_s++;
+      } else {
+        double cbase = Mm;
+        bool found = false;
+        for (uint32_t ch = 0; ch < nch && !found; ++ch) {
+          load_run<16>(row + ch * kChunk, t_nnz - ch * kChunk, li, r);
+          const double s = run_sum<16>(r, w.wh);
+          const double incl = row_incl_scan(s);
+          const double total = __shfl(incl, kGroup - 1, kGroup);
+          if (x < cbase + total) {
+            topic = pick_in_row<16>(r, s, incl, cbase, x, w.wh, grp, li);
+            found = true;
+          }
+          cbase += total;
+        }
+        if (!found) topic = pick_in_q(x - cbase, w, grp, li);
+      }
+    }
+    if (li == 0) {
+      z_out[src] = uint16_t(topic);
+      cnt.sampled++;
+      cnt.nnz += t_nnz;
     }
   }
-  return done ? pick : last;
 }
 
 __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32_t t,
@@ -414,7 +517,8 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
   const int grp = lane / kGroup, li = lane % kGroup;
   uint32_t cur = 0xFFFFFFFFu, K1 = 0;
   double a1 = 0.0, qp = 0.0;
-  unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0, n_reg = 0, n_dreg = 0, row_bytes = 0;
+  SamplerCounts cnt{0ull, 0ull, 0ull};
+  unsigned long long n_reg = 0, n_dreg = 0, row_bytes = 0;
 
   for (;;) {
     if (tid == 0) {
@@ -481,116 +585,33 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
       __syncthreads();
     }
 
+    const WordState w{wh, qb, nb, K, K1, a1, qp, p.alpha};
     for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += kBlock) {
       const uint32_t j = base + uint32_t(lane);
       const uint32_t zz = j < e ? uint32_t(d.z_w[j]) : 0u;
       const bool und = (zz & kUndecidedBit) != 0u;
-      uint32_t off = 0, nnz = 0, c1 = zz & 0x7FFFu;
-      double u = 0.0;
+      BatchTok bt{0u, 0u, zz & 0x7FFFu, 0.0};
       if (und) {
         const uint32_t doc = d.wt_doc[j];
-        u = uniform_draw(p.seed, t, d.wt_key[j]);
-        off = d.d_cap[doc];
-        nnz = d.d_nnz[doc];
-        if (c1 == kC1Unknown) c1 = row_lookup(d.d_ent + off, nnz, K1);
+        bt.u = uniform_draw(p.seed, t, d.wt_key[j]);
+        bt.off = d.d_cap[doc];
+        bt.nnz = d.d_nnz[doc];
+        if (bt.c1 == kC1Unknown) bt.c1 = row_lookup(d.d_ent + bt.off, bt.nnz, K1);
       }
-      unsigned long long mask = __ballot(und);
-      while (mask) {
-        unsigned long long m = mask;
-        for (int q = 0; q < grp; ++q) m &= m - 1ull;
-        for (int q = 0; q < kWave / kGroup; ++q) mask &= mask - 1ull;
-        const int src = m ? __ffsll(m) - 1 : lane;
-        // every lane takes part in the permutes: a source lane may belong to
-        // a group that has no token in this round
-        const uint32_t t_off = __shfl(off, src);
-        const uint32_t nnz_src = __shfl(nnz, src);
-        const uint32_t t_c1 = __shfl(c1, src);
-        const double t_u = __shfl(u, src);
-        const uint32_t t_nnz = m ? nnz_src : 0u;
-        // wave-uniform register bound for the first chunk
-        uint32_t cw = (min(t_nnz, kChunk) + kGroup - 1) / kGroup;
-        cw = max(cw, uint32_t(__shfl_xor(int(cw), 16)));
-        cw = max(cw, uint32_t(__shfl_xor(int(cw), 32)));
-        const uint32_t bound0 = uint32_t(__builtin_amdgcn_readfirstlane(int(cw)));
-        if (m == 0ull) continue;
-        const uint32_t *row = d.d_ent + t_off;
-        const uint32_t nch = (t_nnz + kChunk - 1) / kChunk;
-
-        // pass 1: S' through the same lane sums and row scan pass 2 uses
-        uint32_t r[kRowRegs];
-        double S = 0.0, lane_incl = 0.0, lane_s = 0.0;
-        for (uint32_t ch = 0; ch < nch; ++ch) {
-          const uint32_t bound = ch == 0 ? bound0 : uint32_t(kRowRegs);
-          load_chunk(row + ch * kChunk, min(kChunk, t_nnz - ch * kChunk), li, bound, r);
-          lane_s = lane_sum(r, wh, bound);
-          lane_incl = row_incl_scan(lane_s);
-          S += __shfl(lane_incl, kGroup - 1, kGroup);
-        }
-        const double Mm = a1 * (double(t_c1) + p.alpha);
-        const double Z = (Mm + S) + qp;
-        const double x = t_u * Z;
-        uint32_t topic = K1;
-        if (x < Mm) {
-          if (li == 0) n_after_s++;
-        } else {
-          // pass 2: the chunk, then the lane, then the entry where x falls
-          double cbase = Mm;
-          bool found = false;
-          for (uint32_t ch = 0; ch < nch && !found; ++ch) {
-            const uint32_t bound = ch == 0 ? bound0 : uint32_t(kRowRegs);
-            if (nch > 1) {
-              load_chunk(row + ch * kChunk, min(kChunk, t_nnz - ch * kChunk), li, bound, r);
-              lane_s = lane_sum(r, wh, bound);
-              lane_incl = row_incl_scan(lane_s);
-            }
-            const double total = __shfl(lane_incl, kGroup - 1, kGroup);
-            if (x < cbase + total) {
-              const bool hit = lane_s > 0.0 && x < cbase + lane_incl;
-              const uint32_t hm = uint32_t(__ballot(hit) >> (grp * kGroup)) & kGroupMask;
-              // rounding can leave x past every lane's end: take the last lane with terms
-              const uint32_t pm = uint32_t(__ballot(lane_s > 0.0) >> (grp * kGroup)) & kGroupMask;
-              const int sel = hm ? __ffs(hm) - 1 : (pm ? 31 - __clz(pm) : 0);
-              const double excl = __shfl(lane_incl - lane_s, sel, kGroup);
-              const uint32_t pick = lane_walk(r, wh, K1, cbase + excl, x, bound);
-              topic = __shfl(pick, sel, kGroup);
-              found = true;
-            }
-            cbase += total;
-          }
-          if (!found) {
-            const double xq = x - cbase;
-            if (!(xq < qb[nb])) {
-              topic = (K1 == uint32_t(K - 1)) ? uint32_t(K - 2) : uint32_t(K - 1);  // last positive segment
-            } else {
-              int lo = 0, hi = nb - 1;
-              while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (qb[mid] <= xq) lo = mid;
-                else hi = mid - 1;
-              }
-              const int k = lo * kGroup + li;
-              const double term = k < K ? p.alpha * wh[k] : 0.0;
-              const double incl = row_incl_scan(term);
-              const bool hit = term > 0.0 && xq < qb[lo] + incl;
-              const uint32_t hm = uint32_t(__ballot(hit) >> (grp * kGroup)) & kGroupMask;
-              if (hm) {
-                topic = uint32_t(lo * kGroup + __ffs(hm) - 1);
-              } else {
-                const uint32_t pm = uint32_t(__ballot(term > 0.0) >> (grp * kGroup)) & kGroupMask;
-                topic = uint32_t(lo * kGroup + 31 - __clz(pm));
-              }
-            }
-          }
-        }
-        if (li == 0) {
-          d.z_w[base + uint32_t(src)] = uint16_t(topic);
-          n_sampled++;
-          nnz_sum += t_nnz;
-        }
-      }
+      // row-length classes: 16*C entries per group for C = 1, 2, 4, 8, 16, then longer rows
+      const uint32_t cls = bt.nnz <= 16 ? 0u : bt.nnz <= 32 ? 1u : bt.nnz <= 64 ? 2u : bt.nnz <= 128 ? 3u
+                                                                                   : bt.nnz <= 256 ? 4u : 5u;
+      uint16_t *zb = d.z_w + base;
+      draw_tokens<1>(__ballot(und && cls == 0u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
+      draw_tokens<2>(__ballot(und && cls == 1u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
+      draw_tokens<4>(__ballot(und && cls == 2u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
+      draw_tokens<8>(__ballot(und && cls == 3u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
+      draw_tokens<16>(__ballot(und && cls == 4u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
+      draw_tokens<0>(__ballot(und && cls == 5u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
     }
     __syncthreads();
   }
+  unsigned long long n_sampled = cnt.sampled, n_after_s = cnt.after_s, nnz_sum = cnt.nnz;
   n_sampled = group_sum_u64<kWave>(n_sampled);
   n_after_s = group_sum_u64<kWave>(n_after_s);
   nnz_sum = group_sum_u64<kWave>(nnz_sum);

@@ -19,7 +19,7 @@ constexpr uint16_t kUndecidedBit = 0x8000;
 constexpr uint16_t kC1Unknown = 0x7FFF;
 // Slack entries after the last D row: the sampler reads whole register
 // chunks past the end of a row and discards what lies beyond it.
-constexpr uint32_t kRowPad = 64;
+constexpr uint32_t kRowPad = 256;
 constexpr int kDefaultRegionTokens = 10000;  // Sec. 5.1
 constexpr int kBlock = 256;                  // threads per workgroup (4 wave64)
 
