@@ -82,6 +82,7 @@ def main():
     ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-docs", type=int, default=50000, help="documents in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dump-stats", default=None, help="write the per-iteration statistics (JSON lines) here")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -123,6 +124,10 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     log("timed %d steps in %.3f s" % (args.steps, elapsed))
+    if args.dump_stats:
+        with open(args.dump_stats, "w") as f:
+            for s in st:
+                f.write(json.dumps(s) + "\n")
     llpt = m.loglik()
 
     N = c.N

@@ -293,12 +293,18 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
 
 // Steps 2 and 3: per document, C1 = D[d][K1], C2 = D[d][K2], u, M, S_est and
 // the skip test (Eq. 7 and 9).  One wave per document; documents are handed
-// out in batches through an atomic counter.
+// out in batches through an atomic counter.  The document's D row is spread
+// into a per-wave topic -> count table in LDS, so each token's C1 and C2 are
+// two LDS reads; the table is cleared again from the row afterwards.
 constexpr uint32_t kDocBatch = 32;
 
 __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint32_t t,
                                                      unsigned long long *__restrict__ stats) {
-  const int lane = threadIdx.x & (kWave - 1);
+  extern __shared__ uint16_t cmap_all[];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int K = p.K;
+  uint16_t *cmap = cmap_all + size_t(wave) * size_t(K);
+  for (int k = lane; k < K; k += kWave) cmap[k] = 0;
   unsigned long long nskip = 0;
   const uint32_t M = uint32_t(p.M);
   for (;;) {
@@ -312,11 +318,16 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
       const uint32_t len = e - b;
       const uint32_t *row = d.d_ent + d.d_cap[dd];
       const uint32_t nnz = d.d_nnz[dd];
+      for (uint32_t q = lane; q < nnz; q += kWave) {
+        const uint32_t ent = row[q];
+        cmap[ent >> 16] = uint16_t(ent & 0xFFFFu);
+      }
+      __builtin_amdgcn_wave_barrier();
       for (uint32_t pp = b + lane; pp < e; pp += kWave) {
         const uint32_t v = d.dt_word[pp];
         const WordRec rec = d.wrec[v];
-        const uint32_t C1 = row_lookup(row, nnz, rec.k1);
-        const uint32_t C2 = row_lookup(row, nnz, rec.k2);
+        const uint32_t C1 = cmap[rec.k1];
+        const uint32_t C2 = cmap[rec.k2];
         const uint32_t key = p.key_identity ? pp : d.dt_key[pp];
         const double u = uniform_draw(p.seed, t, key);
         const double Mm = rec.a1 * (double(C1) + p.alpha);
@@ -326,6 +337,9 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
         d.z_w[d.dt_wpos[pp]] = skip ? uint16_t(rec.k1) : uint16_t(kUndecidedBit | min(C1, uint32_t(kC1Unknown)));
         nskip += skip ? 1ull : 0ull;
       }
+      __builtin_amdgcn_wave_barrier();
+      for (uint32_t q = lane; q < nnz; q += kWave) cmap[row[q] >> 16] = 0;
+      __builtin_amdgcn_wave_barrier();
     }
   }
   nskip = group_sum_u64<kWave>(nskip);
@@ -344,7 +358,8 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
 // sums S' per lane, scans the 16 lane sums, and finds the selected entry by a
 // walk inside a single lane.  Rows longer than kChunk are taken in chunks.
 static_assert(kGroup == 16, "the row scans use DPP rows of 16 lanes");
-constexpr uint32_t kChunk = 256;  // D entries one group holds in registers (16 per lane)
+constexpr int kMaxRun = 8;                            // D entries per lane in registers
+constexpr uint32_t kChunk = kGroup * kMaxRun;         // 128 entries per group per chunk
 
 // Per-lane data of one batch of 64 word-ordered tokens (lane = token).
 struct BatchTok {
@@ -387,47 +402,40 @@ __device__ __forceinline__ double run_sum(const uint32_t (&r)[C], const double *
   return s;
 }
 
-// x lies in [base, base + row total): find the lane whose run holds it, move
-// that lane's C entries onto lanes 0..C-1, scan their terms and return the
-// topic of the entry where x falls (the last positive entry if rounding
-// leaves x past them).
-template <int C>
-__device__ __forceinline__ uint32_t pick_in_row(const uint32_t (&r)[C], double s, double incl, double base, double x,
-                                                const double *__restrict__ wh, int grp, int li) {
+// Lane of the row whose run holds x: the first lane with terms whose
+// inclusive prefix passes x, else (rounding) the last lane with terms.
+__device__ __forceinline__ int run_lane(double s, double incl, double base, double x, int grp) {
   const uint32_t hm = uint32_t(__ballot(s > 0.0 && x < base + incl) >> (grp * kGroup)) & kGroupMask;
   const uint32_t pm = uint32_t(__ballot(s > 0.0) >> (grp * kGroup)) & kGroupMask;
-  const int sel = hm ? __ffs(hm) - 1 : (pm ? 31 - __clz(pm) : 0);
-  const double start = base + __shfl(incl - s, sel, kGroup);
-  uint32_t mine = 0u;
-#pragma unroll
-  for (int i = 0; i < C; ++i) {
-    const uint32_t vi = __shfl(r[i], sel, kGroup);
-    mine = li == i ? vi : mine;
-  }
-  const double term = double(mine & 0xFFFFu) * wh[mine >> 16];
-  const double in2 = row_incl_scan(term);
-  const uint32_t hm2 = uint32_t(__ballot(term > 0.0 && x < start + in2) >> (grp * kGroup)) & kGroupMask;
-  const uint32_t pm2 = uint32_t(__ballot(term > 0.0) >> (grp * kGroup)) & kGroupMask;
-  const int h = hm2 ? __ffs(hm2) - 1 : (pm2 ? 31 - __clz(pm2) : 0);
-  return __shfl(mine >> 16, h, kGroup);
+  return hm ? __ffs(hm) - 1 : (pm ? 31 - __clz(pm) : 0);
 }
 
-// Q' branch: xq measured from the start of the Q' segments.
-__device__ __forceinline__ uint32_t pick_in_q(double xq, const WordState &w, int grp, int li) {
-  if (!(xq < w.qb[w.nb])) return (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);
-  int lo = 0, hi = w.nb - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (w.qb[mid] <= xq) lo = mid;
-    else hi = mid - 1;
+// Block b of the Q' prefix holding xq: the largest b in [0, nb) with
+// qb[b] <= xq, found 16 candidates at a time.
+__device__ __forceinline__ int q_block(double xq, const WordState &w, int grp, int li) {
+  int lo = 0, span = w.nb;
+  while (span > 1) {
+    const int step = (span + kGroup - 1) / kGroup;
+    const int off = li * step;
+    const bool ok = off < span && w.qb[lo + off] <= xq;
+    const uint32_t bm = uint32_t(__ballot(ok) >> (grp * kGroup)) & kGroupMask;
+    const int best = bm ? 31 - __clz(bm) : 0;
+    lo += best * step;
+    span = min(step, span - best * step);
   }
-  const int k = lo * kGroup + li;
-  const double term = k < w.K ? w.alpha * w.wh[k] : 0.0;
-  const double incl = row_incl_scan(term);
-  const uint32_t hm = uint32_t(__ballot(term > 0.0 && xq < w.qb[lo] + incl) >> (grp * kGroup)) & kGroupMask;
-  if (hm) return uint32_t(lo * kGroup + __ffs(hm) - 1);
+  return lo;
+}
+
+// The last step of every draw: 16 candidate segments, one per lane (lane li
+// holds topic k_li with width term_li >= 0, in canonical order after
+// `start`); returns the topic of the first segment whose running sum passes
+// x (the last positive one if rounding leaves x past them all).
+__device__ __forceinline__ uint32_t pick_segment(uint32_t k, double term, double start, double x, int grp) {
+  const double in2 = row_incl_scan(term);
+  const uint32_t hm = uint32_t(__ballot(term > 0.0 && x < start + in2) >> (grp * kGroup)) & kGroupMask;
   const uint32_t pm = uint32_t(__ballot(term > 0.0) >> (grp * kGroup)) & kGroupMask;
-  return uint32_t(lo * kGroup + 31 - __clz(pm));
+  const int h = hm ? __ffs(hm) - 1 : (pm ? 31 - __clz(pm) : 0);
+  return __shfl(k, h, kGroup);
 }
 
 // Draw the tokens of `mask` whose D rows hold at most 16*C entries, four at a
@@ -438,6 +446,7 @@ template <int C>
 __device__ void draw_tokens(unsigned long long mask, const BatchTok &bt, const WordState &w,
                             const uint32_t *__restrict__ d_ent, uint16_t *__restrict__ z_out, int lane, int grp,
                             int li, SamplerCounts &cnt) {
+  constexpr int R = C > 0 ? C : kMaxRun;
   while (mask) {
     unsigned long long m = mask;
     for (int q = 0; q < grp; ++q) m &= m - 1ull;
@@ -452,48 +461,69 @@ __device__ void draw_tokens(unsigned long long mask, const BatchTok &bt, const W
     if (m == 0ull) continue;
     const uint32_t *row = d_ent + t_off;
     const double Mm = w.a1 * (double(t_c1) + w.alpha);
+    const uint32_t nch = C > 0 ? 1u : (t_nnz + kChunk - 1) / kChunk;
+    uint32_t r[R];
+    double s = 0.0, incl = 0.0, S = 0.0;
+    for (uint32_t ch = 0; ch < nch; ++ch) {
+      load_run<R>(row + ch * kChunk, t_nnz - ch * kChunk, li, r);
+      s = run_sum<R>(r, w.wh);
+      incl = row_incl_scan(s);
+      S += __shfl(incl, kGroup - 1, kGroup);
+    }
+    const double x = t_u * ((Mm + S) + w.qp);
     uint32_t topic = w.K1;
-    if constexpr (C > 0) {
-      uint32_t r[C];
-      load_run<C>(row, t_nnz, li, r);
-      const double s = run_sum<C>(r, w.wh);
-      const double incl = row_incl_scan(s);
-      const double S = __shfl(incl, kGroup - 1, kGroup);
-      const double x = t_u * ((Mm + S) + w.qp);
-      if (x < Mm) {
-        if (li == 0) cnt.after_s++;
-      } else if (x < Mm + S) {
-        topic = pick_in_row<C>(r, s, incl, Mm, x, w.wh, grp, li);
-      } else {
-        topic = pick_in_q(x - (Mm + S), w, grp, li);
-      }
+    if (x < Mm) {
+      if (li == 0) cnt.after_s++;
     } else {
-      const uint32_t nch = (t_nnz + kChunk - 1) / kChunk;
-      uint32_t r[16];
-      double S = 0.0;
-      for (uint32_t ch = 0; ch < nch; ++ch) {
-        load_run<16>(row + ch * kChunk, t_nnz - ch * kChunk, li, r);
-        S += __shfl(row_incl_scan(run_sum<16>(r, w.wh)), kGroup - 1, kGroup);
-      }
-      const double x = t_u * ((Mm + S) + w.qp);
-      if (x < Mm) {
-        if (li == 0) cnt.after_s++;
+      // locate the chunk (long rows only), then 16 candidate segments
+      double cbase = Mm;
+      bool in_s = false;
+      if (C > 0) {
+        in_s = x < Mm + S;
       } else {
-        double cbase = Mm;
-        bool found = false;
-        for (uint32_t ch = 0; ch < nch && !found; ++ch) {
-          load_run<16>(row + ch * kChunk, t_nnz - ch * kChunk, li, r);
-          const double s = run_sum<16>(r, w.wh);
-          const double incl = row_incl_scan(s);
-          const double total = __shfl(incl, kGroup - 1, kGroup);
-          if (x < cbase + total) {
-            topic = pick_in_row<16>(r, s, incl, cbase, x, w.wh, grp, li);
-            found = true;
+        for (uint32_t ch = 0; ch < nch && !in_s; ++ch) {
+          if (nch > 1) {
+            load_run<R>(row + ch * kChunk, t_nnz - ch * kChunk, li, r);
+            s = run_sum<R>(r, w.wh);
+            incl = row_incl_scan(s);
           }
-          cbase += total;
+          const double total = __shfl(incl, kGroup - 1, kGroup);
+          if (x < cbase + total) in_s = true;
+          else cbase += total;
         }
-        if (!found) topic = pick_in_q(x - cbase, w, grp, li);
       }
+      uint32_t k;
+      double term, start;
+      if (in_s) {
+        // S' run of one lane, moved across the group
+        const int sel = run_lane(s, incl, cbase, x, grp);
+        start = cbase + __shfl(incl - s, sel, kGroup);
+        uint32_t mine = 0u;
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+          const uint32_t vi = __shfl(r[i], sel, kGroup);
+          mine = li == i ? vi : mine;
+        }
+        k = mine >> 16;
+        term = double(mine & 0xFFFFu) * w.wh[k];
+      } else {
+        // Q' branch: boundaries (M + S') + Qcdf
+        const double qstart = C > 0 ? Mm + S : cbase;
+        const double xq = x - qstart;
+        if (!(xq < w.qb[w.nb])) {
+          k = (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);  // last positive segment
+          term = 0.0;
+          start = 0.0;
+        } else {
+          const int lo = q_block(xq, w, grp, li);
+          k = uint32_t(lo * kGroup + li);
+          term = int(k) < w.K ? w.alpha * w.wh[k] : 0.0;
+          start = qstart + w.qb[lo];
+        }
+      }
+      const bool fallback = !in_s && term == 0.0 && start == 0.0;
+      const uint32_t picked = pick_segment(k, term, start, x, grp);
+      topic = fallback ? k : picked;
     }
     if (li == 0) {
       z_out[src] = uint16_t(topic);
@@ -598,16 +628,14 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
         bt.nnz = d.d_nnz[doc];
         if (bt.c1 == kC1Unknown) bt.c1 = row_lookup(d.d_ent + bt.off, bt.nnz, K1);
       }
-      // row-length classes: 16*C entries per group for C = 1, 2, 4, 8, 16, then longer rows
-      const uint32_t cls = bt.nnz <= 16 ? 0u : bt.nnz <= 32 ? 1u : bt.nnz <= 64 ? 2u : bt.nnz <= 128 ? 3u
-                                                                                   : bt.nnz <= 256 ? 4u : 5u;
+      // row-length classes: 16*C entries per group for C = 1, 2, 4, 8, then longer rows
+      const uint32_t cls = bt.nnz <= 16 ? 0u : bt.nnz <= 32 ? 1u : bt.nnz <= 64 ? 2u : bt.nnz <= 128 ? 3u : 4u;
       uint16_t *zb = d.z_w + base;
       draw_tokens<1>(__ballot(und && cls == 0u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
       draw_tokens<2>(__ballot(und && cls == 1u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
       draw_tokens<4>(__ballot(und && cls == 2u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
       draw_tokens<8>(__ballot(und && cls == 3u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
-      draw_tokens<16>(__ballot(und && cls == 4u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
-      draw_tokens<0>(__ballot(und && cls == 5u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
+      draw_tokens<0>(__ballot(und && cls == 4u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
     }
     __syncthreads();
   }
@@ -863,7 +891,10 @@ hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s) {
 }
 
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
-  hipLaunchKernelGGL(k_doc_pass, dim3(uint32_t(p.grid_docs)), dim3(kBlock), 0, s, d, p, t, d.stats);
+  const size_t lds = sizeof(uint16_t) * size_t(p.K) * (kBlock / kWave);
+  hipError_t err = allow_lds(k_doc_pass, lds);
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_doc_pass, dim3(uint32_t(p.grid_docs)), dim3(kBlock), lds, s, d, p, t, d.stats);
   return hipGetLastError();
 }
 
