@@ -77,8 +77,8 @@ def cpu_baseline(c, n_docs):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--cpu-docs", type=int, default=50000, help="documents in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -316,8 +316,8 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
     for (uint32_t dd = d0; dd < d1; ++dd) {
       const uint32_t b = d.doc_off[dd], e = d.doc_off[dd + 1];
       const uint32_t len = e - b;
-      const uint32_t *row = d.d_ent + d.d_cap[dd];
-      const uint32_t nnz = d.d_nnz[dd];
+      const uint32_t *row = d.d_ent + d.d_cap[dd] + 1;
+      const uint32_t nnz = row[-1] & 0xFFFFu;
       for (uint32_t q = lane; q < nnz; q += kWave) {
         const uint32_t ent = row[q];
         cmap[ent >> 16] = uint16_t(ent & 0xFFFFu);
@@ -622,10 +622,9 @@ __global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32
       const bool und = (zz & kUndecidedBit) != 0u;
       BatchTok bt{0u, 0u, zz & 0x7FFFu, 0.0};
       if (und) {
-        const uint32_t doc = d.wt_doc[j];
+        bt.off = d.wt_rowoff[j] + 1;
         bt.u = uniform_draw(p.seed, t, d.wt_key[j]);
-        bt.off = d.d_cap[doc];
-        bt.nnz = d.d_nnz[doc];
+        bt.nnz = d.d_ent[bt.off - 1] & 0xFFFFu;
         if (bt.c1 == kC1Unknown) bt.c1 = row_lookup(d.d_ent + bt.off, bt.nnz, K1);
       }
       // row-length classes: 16*C entries per group for C = 1, 2, 4, 8, then longer rows
@@ -755,7 +754,7 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
         else bad++;
       }
       __threadfence_block();
-      uint32_t *out = d.d_ent + d.d_cap[dd];
+      uint32_t *out = d.d_ent + d.d_cap[dd] + 1;
       uint32_t base = 0;
       for (int q0 = 0; q0 < half; q0 += kWave) {
         const int q = q0 + lane;
@@ -771,7 +770,7 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
         if (hi) out[base + rank + (lo ? 1u : 0u)] = (uint32_t(2 * q + 1) << 16) | hi;
         base += uint32_t(__popcll(m0) + __popcll(m1));
       }
-      if (lane == 0) d.d_nnz[dd] = base;
+      if (lane == 0) out[-1] = ((e - b) << 16) | base;
       __threadfence_block();
     }
   }
@@ -829,16 +828,16 @@ __global__ __launch_bounds__(kBlock) void k_loglik(DevState d, Params p) {
     }
     double part = 0.0;
     for (uint32_t j = b + uint32_t(gid); j < e; j += kBlock / kGroup) {
-      const uint32_t doc = d.wt_doc[j];
-      const uint32_t *row = d.d_ent + d.d_cap[doc];
-      const uint32_t nnz = d.d_nnz[doc];
+      const uint32_t *row = d.d_ent + d.wt_rowoff[j] + 1;
+      const uint32_t hdr = row[-1];
+      const uint32_t nnz = hdr & 0xFFFFu;
       double acc = 0.0;
       for (uint32_t q = li; q < nnz; q += kGroup) {
         const uint32_t ent = row[q];
         acc += double(ent & 0xFFFFu) * wh[ent >> 16];
       }
       const double num = group_sum<kGroup>(acc) + p.alpha * sumw;
-      const double len = double(d.doc_off[doc + 1] - d.doc_off[doc]);
+      const double len = double(hdr >> 16);
       part += log2(num / (len + Kalpha));
     }
     if (li == 0) s_part[gid] = part;
@@ -859,6 +858,16 @@ __global__ __launch_bounds__(kBlock) void k_loglik_reduce(const double *__restri
   for (int64_t q = threadIdx.x; q < n; q += kBlock) s += part[q];
   s = block_sum(s, scratch);
   if (threadIdx.x == 0) out[0] = s;
+}
+
+// Total entries of D (for the size query of lda_get_counts).
+__global__ void k_sum_nnz(const uint32_t *__restrict__ d_ent, const uint32_t *__restrict__ d_cap, int32_t M,
+                          unsigned long long *__restrict__ out) {
+  unsigned long long s = 0;
+  for (int64_t dd = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; dd < M; dd += int64_t(gridDim.x) * blockDim.x)
+    s += d_ent[d_cap[dd]] & 0xFFFFu;
+  s = group_sum_u64<kWave>(s);
+  if ((threadIdx.x & (kWave - 1)) == 0 && s) atomicAdd(out, s);
 }
 
 }  // namespace
@@ -924,6 +933,13 @@ hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s) {
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kBlock),
                      sizeof(uint32_t) * half * (kBlock / kWave), s, d, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_nnz(const DevState &d, const Params &p, unsigned long long *out, hipStream_t s) {
+  const int64_t blocks = std::min<int64_t>((int64_t(p.M) + kBlock - 1) / kBlock, 4096);
+  hipLaunchKernelGGL(k_sum_nnz, dim3(uint32_t(std::max<int64_t>(blocks, 1))), dim3(kBlock), 0, s, d.d_ent, d.d_cap,
+                     p.M, out);
   return hipGetLastError();
 }
 

@@ -40,13 +40,15 @@ __global__ void k_boundaries(const uint32_t *__restrict__ keys, int64_t n, uint3
 }
 
 // Word-order slot of every token: its position in the caller-id sort, moved
-// with its whole word segment to the relabelled segment start.
+// with its whole word segment to the relabelled segment start.  Each
+// word-ordered token records the offset of its document's D row.
 __global__ void k_word_order(const uint32_t *__restrict__ wkey, const uint32_t *__restrict__ wpos, int64_t n,
                              const int32_t *__restrict__ relabel, const uint32_t *__restrict__ woff_orig,
                              const uint32_t *__restrict__ woff_new, const uint32_t *__restrict__ doc_sorted,
                              const int32_t *__restrict__ doc_in, const uint32_t *__restrict__ dt_key,
                              uint32_t *__restrict__ dt_word, uint32_t *__restrict__ dt_wpos,
-                             uint32_t *__restrict__ wt_doc, uint32_t *__restrict__ wt_key) {
+                             const uint32_t *__restrict__ d_cap, uint32_t *__restrict__ wt_rowoff,
+                             uint32_t *__restrict__ wt_key) {
   for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < n; q += int64_t(gridDim.x) * blockDim.x) {
     const uint32_t v = wkey[q];
     const uint32_t r = uint32_t(relabel[v]);
@@ -54,7 +56,7 @@ __global__ void k_word_order(const uint32_t *__restrict__ wkey, const uint32_t *
     const uint32_t p = wpos[q];
     dt_word[p] = r;
     dt_wpos[p] = j;
-    wt_doc[j] = doc_sorted ? doc_sorted[p] : uint32_t(doc_in[p]);
+    wt_rowoff[j] = d_cap[doc_sorted ? doc_sorted[p] : uint32_t(doc_in[p])];
     wt_key[j] = dt_key ? dt_key[p] : p;
   }
 }
@@ -109,9 +111,9 @@ hipError_t launch_boundaries(const uint32_t *keys, int64_t n, uint32_t nbins, ui
 hipError_t launch_word_order(const uint32_t *wkey, const uint32_t *wpos, int64_t n, const int32_t *relabel,
                              const uint32_t *woff_orig, const uint32_t *woff_new, const uint32_t *doc_sorted,
                              const int32_t *doc_in, const uint32_t *dt_key, uint32_t *dt_word, uint32_t *dt_wpos,
-                             uint32_t *wt_doc, uint32_t *wt_key, hipStream_t s) {
+                             const uint32_t *d_cap, uint32_t *wt_rowoff, uint32_t *wt_key, hipStream_t s) {
   hipLaunchKernelGGL(k_word_order, dim3(grid_for(n)), dim3(kThreads), 0, s, wkey, wpos, n, relabel, woff_orig,
-                     woff_new, doc_sorted, doc_in, dt_key, dt_word, dt_wpos, wt_doc, wt_key);
+                     woff_new, doc_sorted, doc_in, dt_key, dt_word, dt_wpos, d_cap, wt_rowoff, wt_key);
   return hipGetLastError();
 }
 

@@ -215,10 +215,12 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(upload(h, d.word_off, L.word_off));
   LDA_TRY(dalloc(h, &d.dt_word, n));
   LDA_TRY(dalloc(h, &d.dt_wpos, n));
-  LDA_TRY(dalloc(h, &d.wt_doc, n));
+  LDA_TRY(dalloc(h, &d.wt_rowoff, n));
   LDA_TRY(dalloc(h, &d.wt_key, n));
+  LDA_TRY(dalloc(h, &d.d_cap, L.d_cap.size()));
+  LDA_TRY(upload(h, d.d_cap, L.d_cap));
   HIP_TRY(h, launch_word_order(wkey, wpos, L.n, relabel_d, woff_orig, d.word_off, doc_sorted, doc_d, d.dt_key,
-                               d.dt_word, d.dt_wpos, d.wt_doc, d.wt_key, h->stream));
+                               d.dt_word, d.dt_wpos, d.d_cap, d.wt_rowoff, d.wt_key, h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   dfree(h, relabel_d);
   dfree(h, woff_orig);
@@ -232,8 +234,6 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.region, L.region.size()));
   LDA_TRY(dalloc(h, &d.split, L.split.size()));
   LDA_TRY(dalloc(h, &d.z_w, n));
-  LDA_TRY(dalloc(h, &d.d_cap, L.d_cap.size()));
-  LDA_TRY(dalloc(h, &d.d_nnz, size_t(L.M)));
   LDA_TRY(dalloc(h, &d.d_ent, size_t(L.d_cap.back()) + kRowPad));
   LDA_TRY(dalloc(h, &d.w_dense, size_t(L.n_dense) * size_t(L.K)));
   LDA_TRY(dalloc(h, &d.ws_cap, L.ws_cap.size()));
@@ -249,7 +249,6 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   d.stats = h->stats_base;
   LDA_TRY(upload(h, d.region, L.region));
   LDA_TRY(upload(h, d.split, L.split));
-  LDA_TRY(upload(h, d.d_cap, L.d_cap));
   LDA_TRY(upload(h, d.ws_cap, L.ws_cap));
   HIP_TRY(h, hipMemsetAsync(h->stats_base, 0, sizeof(unsigned long long) * kStatSlots * kStatsPerIter, h->stream));
   HIP_TRY(h, launch_init_topics(d, p, h->stream));
@@ -411,16 +410,21 @@ lda_status lda_get_counts(lda_handle *h, lda_counts *out) {
   const Layout &L = h->L;
   const size_t n = size_t(L.n);
   const int32_t K = L.K;
-  std::vector<uint32_t> d_nnz(static_cast<size_t>(L.M)), ws_nnz(L.ws_cap.size() - 1);
-  HIP_TRY(h, hipMemcpyAsync(d_nnz.data(), h->d.d_nnz, d_nnz.size() * 4, hipMemcpyDeviceToHost, h->stream));
+  std::vector<uint32_t> ws_nnz(L.ws_cap.size() - 1);
+  unsigned long long *nnz_dev = nullptr;
+  LDA_TRY(dalloc(h, &nnz_dev, 1));
+  HIP_TRY(h, hipMemsetAsync(nnz_dev, 0, sizeof(unsigned long long), h->stream));
+  HIP_TRY(h, launch_sum_nnz(h->d, h->p, nnz_dev, h->stream));
+  unsigned long long nnz_D_dev = 0;
+  HIP_TRY(h, hipMemcpyAsync(&nnz_D_dev, nnz_dev, sizeof(nnz_D_dev), hipMemcpyDeviceToHost, h->stream));
   if (!ws_nnz.empty())
     HIP_TRY(h, hipMemcpyAsync(ws_nnz.data(), h->d.ws_nnz, ws_nnz.size() * 4, hipMemcpyDeviceToHost, h->stream));
   std::vector<int32_t> wd(static_cast<size_t>(L.n_dense) * static_cast<size_t>(K));
   if (!wd.empty())
     HIP_TRY(h, hipMemcpyAsync(wd.data(), h->d.w_dense, wd.size() * 4, hipMemcpyDeviceToHost, h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
-  int64_t nnz_D = 0, nnz_W = 0;
-  for (uint32_t x : d_nnz) nnz_D += x;
+  dfree(h, nnz_dev);
+  int64_t nnz_D = int64_t(nnz_D_dev), nnz_W = 0;
   for (uint32_t x : ws_nnz) nnz_W += x;
   for (int32_t x : wd) nnz_W += x != 0;
   out->iteration = h->iteration;
@@ -453,8 +457,9 @@ lda_status lda_get_counts(lda_handle *h, lda_counts *out) {
     int64_t o = 0;
     for (int32_t dd = 0; dd < L.M; ++dd) {
       out->D_off[dd] = o;
-      for (uint32_t q = 0; q < d_nnz[size_t(dd)]; ++q) {
-        const uint32_t e = ent[size_t(L.d_cap[size_t(dd)]) + q];
+      const uint32_t hdr = ent[size_t(L.d_cap[size_t(dd)])];
+      for (uint32_t q = 0; q < (hdr & 0xFFFFu); ++q) {
+        const uint32_t e = ent[size_t(L.d_cap[size_t(dd)]) + 1 + q];
         out->D_topic[o] = int32_t(e >> 16);
         out->D_count[o] = int32_t(e & 0xFFFFu);
         ++o;

@@ -39,7 +39,7 @@ struct Layout {
   std::vector<uint32_t> doc_off;  // [M+1]
   std::vector<uint32_t> word_off; // [n_present+1]
   std::vector<uint32_t> wt_key;   // [n] input index of each word-ordered token (host reference only)
-  std::vector<uint32_t> d_cap;    // [M+1] offsets of D rows, capacity min(len, K)
+  std::vector<uint32_t> d_cap;    // [M+1] offsets of D rows: a header, then capacity min(len, K)
   std::vector<uint32_t> ws_cap;   // [n_present-n_dense+1] offsets of sparse W rows, capacity = count
   std::vector<uint32_t> region;   // [3*n_regions] (word, begin, end)
   std::vector<uint8_t> split;     // [n_dense] 1 if the dense word has more than one region
@@ -69,7 +69,7 @@ hipError_t launch_boundaries(const uint32_t *keys, int64_t n, uint32_t nbins, ui
 hipError_t launch_word_order(const uint32_t *wkey, const uint32_t *wpos, int64_t n, const int32_t *relabel,
                              const uint32_t *woff_orig, const uint32_t *woff_new, const uint32_t *doc_sorted,
                              const int32_t *doc_in, const uint32_t *dt_key, uint32_t *dt_word, uint32_t *dt_wpos,
-                             uint32_t *wt_doc, uint32_t *wt_key, hipStream_t s);
+                             const uint32_t *d_cap, uint32_t *wt_rowoff, uint32_t *wt_key, hipStream_t s);
 hipError_t launch_scatter_z(const uint16_t *z_w, const uint32_t *wt_key, int64_t n, int32_t *z_in, hipStream_t s);
 hipError_t launch_gather_z(const int32_t *z_in, const uint32_t *wt_key, int64_t n, int32_t K, uint16_t *z_w,
                            unsigned long long *bad, hipStream_t s);
@@ -84,13 +84,13 @@ struct WordRec {  // per relabelled word, refreshed every iteration (Sec. 3.2, s
 
 struct DevState {
   // layout
-  uint32_t *doc_off, *dt_word, *dt_key, *dt_wpos, *word_off, *wt_doc, *wt_key;
+  uint32_t *doc_off, *dt_word, *dt_key, *dt_wpos, *word_off, *wt_rowoff, *wt_key;
   uint32_t *region;   // 3 per region
   uint8_t *split;     // per dense word
   // assignment, word order
   uint16_t *z_w;
   // counts
-  uint32_t *d_cap, *d_nnz, *d_ent;
+  uint32_t *d_cap, *d_ent;  // D row of doc d at d_cap[d]: header (len << 16 | nnz), then entries
   int32_t *w_dense;
   uint32_t *ws_cap, *ws_nnz, *ws_ent;
   uint32_t *T;
@@ -128,5 +128,6 @@ hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipSt
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_sum_nnz(const DevState &d, const Params &p, unsigned long long *out, hipStream_t s);
 
 }  // namespace lda
