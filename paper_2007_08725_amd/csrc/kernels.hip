@@ -533,7 +533,7 @@ __device__ void draw_tokens(unsigned long long mask, const BatchTok &bt, const W
   }
 }
 
-__global__ __launch_bounds__(kBlock) void k_sampler(DevState d, Params p, uint32_t t,
+__global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uint32_t t,
                                                     unsigned long long *__restrict__ stats) {
   extern __shared__ double lds[];
   const int K = p.K;
