@@ -3,12 +3,14 @@
 // One synchronous iteration (Sec. 2.2, 3.2, 4.3):
 //   k_begin      den[k] = T[k] + V*beta; scheduler counters reset
 //   k_word_pre   per word: top-3 of W^[v] (K1, K2, a1..a3), Q' and sum W^   (step 1, Sec. 3.2)
+//   k_fill_undecided
+//                every word-ordered topic slot set to "undecided"
 //   k_doc_pass   per document: C1, C2 by lookup in the D row, u, M, S_est
-//                and the skip test; writes K1 or "undecided" into the
-//                word-ordered topic slot                                   (steps 2-3, Sec. 3.3)
+//                and the skip test; writes K1 into the word-ordered topic
+//                slot of every skipped token                               (steps 2-3, Sec. 3.3)
 //   k_sampler    per region of a word: W^ row and Q' block prefix in LDS,
-//                then for every undecided token S' over nz(D[d]) and the
-//                final draw over [K1 | S' | Q']                            (steps 4-6, Sec. 4.3)
+//                then for every undecided token C1 and S' over nz(D[d])
+//                and the final draw over [K1 | S' | Q']                    (steps 4-6, Sec. 4.3)
 //   k_zero_split, k_rebuild_w, k_rebuild_d
 //                count tables of the new assignment: dense rows of W by
 //                histogram (integer atomics for split words), sparse rows of
@@ -46,17 +48,6 @@ __device__ __forceinline__ double uniform_draw(uint64_t seed, uint32_t t, uint32
   const uint4 x = philox4x32_10(make_uint4(i, 0u, t, 0u), uint32_t(seed), uint32_t(seed >> 32));
   const uint64_t bits = (uint64_t(x.x) << 32) | uint64_t(x.y);
   return double(bits >> 11) * 0x1p-53;
-}
-
-// Count of topic k in a packed row with ascending topics (0 if absent).
-__device__ __forceinline__ uint32_t row_lookup(const uint32_t *__restrict__ row, uint32_t nnz, uint32_t k) {
-  uint32_t lo = 0, hi = nnz;
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if ((row[mid] >> 16) < k) lo = mid + 1;
-    else hi = mid;
-  }
-  return (lo < nnz && (row[lo] >> 16) == k) ? (row[lo] & 0xFFFFu) : 0u;
 }
 
 // W^[v][k] exactly as the paper defines it: an IEEE fp64 divide.
@@ -184,13 +175,21 @@ __device__ __forceinline__ uint32_t row_lower_bound(const uint32_t *__restrict__
 
 // ------------------------------------------------------------ kernels ----
 
+__device__ __forceinline__ uint16_t initial_topic(uint64_t seed, uint32_t i, int32_t K) {
+  const uint4 x = philox4x32_10(make_uint4(i, 0u, 0u, 1u), uint32_t(seed), uint32_t(seed >> 32));
+  return uint16_t((uint64_t(x.x) * uint64_t(uint32_t(K))) >> 32);
+}
+
 __global__ void k_init_topics(const uint32_t *__restrict__ wt_key, uint16_t *__restrict__ z_w, int64_t n, int32_t K,
                               uint64_t seed) {
-  for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < n; j += int64_t(gridDim.x) * blockDim.x) {
-    const uint32_t i = wt_key[j];
-    const uint4 x = philox4x32_10(make_uint4(i, 0u, 0u, 1u), uint32_t(seed), uint32_t(seed >> 32));
-    z_w[j] = uint16_t((uint64_t(x.x) * uint64_t(uint32_t(K))) >> 32);
-  }
+  for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < n; j += int64_t(gridDim.x) * blockDim.x)
+    z_w[j] = initial_topic(seed, wt_key[j], K);
+}
+
+// Every word-ordered topic slot starts the iteration undecided.
+__global__ void k_fill_undecided(uint32_t *__restrict__ z2, int64_t n2) {
+  for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < n2; q += int64_t(gridDim.x) * blockDim.x)
+    z2[q] = (uint32_t(kUndecided) << 16) | kUndecided;
 }
 
 __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, int32_t K, double vbeta,
@@ -288,6 +287,13 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
     rec.k1 = K1;
     rec.k2 = K2;
     d.wrec[r] = rec;
+    SkipRec sr;
+    sr.k12 = K1 | (K2 << 16);
+    sr.a1 = float(a1);
+    sr.a2 = float(a2);
+    sr.a3 = float(a3);
+    sr.qp = float(q);
+    d.wskip[r] = sr;
   }
 }
 
@@ -324,17 +330,20 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
       }
       __builtin_amdgcn_wave_barrier();
       for (uint32_t pp = b + lane; pp < e; pp += kWave) {
-        const uint32_t v = d.dt_word[pp];
-        const WordRec rec = d.wrec[v];
-        const uint32_t C1 = cmap[rec.k1];
-        const uint32_t C2 = cmap[rec.k2];
+        const SkipRec rec = d.wskip[d.dt_word[pp]];
+        const uint32_t K1 = rec.k12 & 0xFFFFu, K2 = rec.k12 >> 16;
+        const uint32_t C1 = cmap[K1], C2 = cmap[K2];
         const uint32_t key = p.key_identity ? pp : d.dt_key[pp];
-        const double u = uniform_draw(p.seed, t, key);
-        const double Mm = rec.a1 * (double(C1) + p.alpha);
-        const double Sest = p.g == 1 ? rec.a2 * double(len - C1)
-                                     : rec.a2 * double(C2) + rec.a3 * double(len - C1 - C2);
-        const bool skip = !p.no_skip && (u * (Mm + Sest + rec.qp) < Mm);
-        d.z_w[d.dt_wpos[pp]] = skip ? uint16_t(rec.k1) : uint16_t(kUndecidedBit | min(C1, uint32_t(kC1Unknown)));
+        // Step 3 in single precision with a relative margin of 2^-15, far
+        // above the fp32 rounding of these few operations (a few 2^-24): a
+        // token is skipped only if u*(M + S_est + Q') < M holds exactly, so
+        // its draw is K1 (S' <= S_est, Eq. 8-9).
+        const float u = float(uniform_draw(p.seed, t, key));
+        const float Mm = rec.a1 * (float(C1) + p.alpha_f);
+        const float Sest = p.g == 1 ? rec.a2 * float(len - C1)
+                                    : rec.a2 * float(C2) + rec.a3 * float(len - C1 - C2);
+        const bool skip = !p.no_skip && (u * ((Mm + Sest) + rec.qp) < Mm * (1.0f - 0x1p-15f));
+        if (skip) d.z_w[d.dt_wpos[pp]] = uint16_t(K1);
         nskip += skip ? 1ull : 0ull;
       }
       __builtin_amdgcn_wave_barrier();
@@ -351,20 +360,24 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
 // blocks of kGroup topics.
 //
 // Work split: a wave takes 64 consecutive word-ordered tokens; every lane
-// fetches its own token's document, key, D-row offset and length and draws its
-// own u, then the four 16-lane groups take the undecided tokens in turn.  A
-// group loads up to kChunk entries of the D row into registers at once (lane l
-// holds a contiguous run, so lane partial sums are in ascending topic order),
-// sums S' per lane, scans the 16 lane sums, and finds the selected entry by a
-// walk inside a single lane.  Rows longer than kChunk are taken in chunks.
+// fetches its own token's key, D-row offset and length, draws its own u and
+// stages them in the wave's slice of LDS, then the four 16-lane groups take
+// the undecided tokens in turn.  A group loads up to kChunk entries of the D
+// row into registers at once (lane l holds a contiguous run, so lane partial
+// sums are in ascending topic order), picks out C1 = D[d][K1] and sums S' per
+// lane, scans the 16 lane sums, and finds the selected entry by a walk inside
+// a single lane.  Rows longer than kChunk are taken in chunks.  The drawn
+// topics go back to LDS and leave in one coalesced store per batch.
 static_assert(kGroup == 16, "the row scans use DPP rows of 16 lanes");
 constexpr int kMaxRun = 8;                            // D entries per lane in registers
 constexpr uint32_t kChunk = kGroup * kMaxRun;         // 128 entries per group per chunk
 
-// Per-lane data of one batch of 64 word-ordered tokens (lane = token).
-struct BatchTok {
-  uint32_t off, nnz, c1;
-  double u;
+// One batch of 64 word-ordered tokens, staged in the wave's slice of LDS
+// (entry q = lane q's token): D-row offset, row length, u, and the drawn topic.
+struct BatchLds {
+  uint32_t *off, *nnz;
+  double *u;
+  uint16_t *top;
 };
 
 // The word of the current region: W^ row (with W^[K1] = 0) and Q' block
@@ -376,20 +389,19 @@ struct WordState {
   double a1, qp, alpha;
 };
 
-struct SamplerCounts {
-  unsigned long long sampled, after_s, nnz;
-};
 
 // Load C entries per lane from `row` (lane li gets entries [li*C, li*C + C),
-// topics ascending); entries at or past nn read as 0 (topic 0, count 0).
-// Reads may run past the row into the padding after the last row.
+// topics ascending); entries at or past nn read as `pad`, a count-0 entry of
+// a topic other than K1.  Reads may run past the row into the padding after
+// the last row.
 template <int C>
-__device__ __forceinline__ void load_run(const uint32_t *__restrict__ row, uint32_t nn, int li, uint32_t (&r)[C]) {
+__device__ __forceinline__ void load_run(const uint32_t *__restrict__ row, uint32_t nn, int li, uint32_t pad,
+                                         uint32_t (&r)[C]) {
   const uint32_t q0 = uint32_t(li) * C;
 #pragma unroll
   for (int i = 0; i < C; ++i) {
     const uint32_t v = row[q0 + i];
-    r[i] = (q0 + uint32_t(i) < nn) ? v : 0u;
+    r[i] = (q0 + uint32_t(i) < nn) ? v : pad;
   }
 }
 
@@ -400,6 +412,38 @@ __device__ __forceinline__ double run_sum(const uint32_t (&r)[C], const double *
 #pragma unroll
   for (int i = 0; i < C; ++i) s += double(r[i] & 0xFFFFu) * wh[r[i] >> 16];
   return s;
+}
+
+// min(c, D[d][K1]) if this lane's run holds topic K1, else c unchanged or
+// larger than 0xFFFF: an entry minus (K1 << 16) is its count when its topic
+// is K1 and at least 2^16 (modulo 2^32) for any other topic, since topics are
+// below 2^14.
+template <int C>
+__device__ __forceinline__ uint32_t run_count_of(const uint32_t (&r)[C], uint32_t K1, uint32_t c) {
+  const uint32_t key = K1 << 16;
+#pragma unroll
+  for (int i = 0; i < C; ++i) c = min(c, r[i] - key);
+  return c;
+}
+
+// Sum of a uint32 over each row of 16 lanes, in every lane of the row.
+__device__ __forceinline__ uint32_t row_sum_u32(uint32_t v) {
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x111, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x112, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x114, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x118, 0xF, 0xF, true));
+  return __shfl(v, kGroup - 1, kGroup);
+}
+
+// Sum of a uint32 over the wave (the total must fit in 32 bits), as a
+// wave-uniform value.
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x111, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x112, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x114, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x118, 0xF, 0xF, true));
+  return uint32_t(__builtin_amdgcn_readlane(int(v), 15)) + uint32_t(__builtin_amdgcn_readlane(int(v), 31)) +
+         uint32_t(__builtin_amdgcn_readlane(int(v), 47)) + uint32_t(__builtin_amdgcn_readlane(int(v), 63));
 }
 
 // Lane of the row whose run holds x: the first lane with terms whose
@@ -443,38 +487,38 @@ __device__ __forceinline__ uint32_t pick_segment(uint32_t k, double term, double
 // does the same amount of work.  C == 0 selects the long-row path, which
 // walks rows of any length in chunks of kChunk entries.
 template <int C>
-__device__ void draw_tokens(unsigned long long mask, const BatchTok &bt, const WordState &w,
-                            const uint32_t *__restrict__ d_ent, uint16_t *__restrict__ z_out, int lane, int grp,
-                            int li, SamplerCounts &cnt) {
+__device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const WordState &w,
+                            const uint32_t *__restrict__ d_ent, int grp, int li, unsigned long long &after_s) {
   constexpr int R = C > 0 ? C : kMaxRun;
   while (mask) {
     unsigned long long m = mask;
     for (int q = 0; q < grp; ++q) m &= m - 1ull;
     for (int q = 0; q < kWave / kGroup; ++q) mask &= mask - 1ull;
-    // every lane takes part in the permutes: a source lane may belong to a
-    // group that has no token in this round
-    const int src = m ? __ffsll(m) - 1 : lane;
-    const uint32_t t_off = __shfl(bt.off, src);
-    const uint32_t t_nnz = __shfl(bt.nnz, src);
-    const uint32_t t_c1 = __shfl(bt.c1, src);
-    const double t_u = __shfl(bt.u, src);
-    if (m == 0ull) continue;
+    bool in_m = false;
+    if (m) {
+    const int src = __ffsll(m) - 1;
+    const uint32_t t_off = bt.off[src];
+    const uint32_t t_nnz = bt.nnz[src];
+    const double t_u = bt.u[src];
     const uint32_t *row = d_ent + t_off;
-    const double Mm = w.a1 * (double(t_c1) + w.alpha);
     const uint32_t nch = C > 0 ? 1u : (t_nnz + kChunk - 1) / kChunk;
     uint32_t r[R];
     double s = 0.0, incl = 0.0, S = 0.0;
+    const uint32_t pad = uint32_t(w.K1 == 0u) << 16;
+    uint32_t c1 = 0xFFFFFFFFu;
     for (uint32_t ch = 0; ch < nch; ++ch) {
-      load_run<R>(row + ch * kChunk, t_nnz - ch * kChunk, li, r);
+      load_run<R>(row + ch * kChunk, t_nnz - ch * kChunk, li, pad, r);
+      c1 = run_count_of<R>(r, w.K1, c1);
       s = run_sum<R>(r, w.wh);
       incl = row_incl_scan(s);
       S += __shfl(incl, kGroup - 1, kGroup);
     }
+    // max-topic branch, Eq. 7: M = W^[v][K1] * (D[d][K1] + alpha)
+    const double Mm = w.a1 * (double(row_sum_u32(c1 <= 0xFFFFu ? c1 : 0u)) + w.alpha);
     const double x = t_u * ((Mm + S) + w.qp);
     uint32_t topic = w.K1;
-    if (x < Mm) {
-      if (li == 0) cnt.after_s++;
-    } else {
+    in_m = x < Mm;
+    if (!in_m) {
       // locate the chunk (long rows only), then 16 candidate segments
       double cbase = Mm;
       bool in_s = false;
@@ -483,7 +527,7 @@ __device__ void draw_tokens(unsigned long long mask, const BatchTok &bt, const W
       } else {
         for (uint32_t ch = 0; ch < nch && !in_s; ++ch) {
           if (nch > 1) {
-            load_run<R>(row + ch * kChunk, t_nnz - ch * kChunk, li, r);
+            load_run<R>(row + ch * kChunk, t_nnz - ch * kChunk, li, pad, r);
             s = run_sum<R>(r, w.wh);
             incl = row_incl_scan(s);
           }
@@ -525,15 +569,14 @@ __device__ void draw_tokens(unsigned long long mask, const BatchTok &bt, const W
       const uint32_t picked = pick_segment(k, term, start, x, grp);
       topic = fallback ? k : picked;
     }
-    if (li == 0) {
-      z_out[src] = uint16_t(topic);
-      cnt.sampled++;
-      cnt.nnz += t_nnz;
+    if (li == 0) bt.top[src] = uint16_t(topic);
     }
+    // outside the divergent part, so the count stays wave-uniform
+    after_s += uint32_t(__popcll(__ballot(in_m && li == 0)));
   }
 }
 
-__global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uint32_t t,
+__global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uint32_t t,
                                                     unsigned long long *__restrict__ stats) {
   extern __shared__ double lds[];
   const int K = p.K;
@@ -542,12 +585,18 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
   double *qb = lds + K;     // [nb + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup
   __shared__ uint32_t s_reg[3];
   __shared__ int s_valid;
+  __shared__ uint32_t s_off[kBlock], s_nnz[kBlock];
+  __shared__ double s_u[kBlock];
+  __shared__ uint16_t s_top[kBlock];
 
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int grp = lane / kGroup, li = lane % kGroup;
+  const BatchLds bt{s_off + wave * kWave, s_nnz + wave * kWave, s_u + wave * kWave, s_top + wave * kWave};
+  // region, word and count variables are uniform over the block (scalar registers)
   uint32_t cur = 0xFFFFFFFFu, K1 = 0;
   double a1 = 0.0, qp = 0.0;
-  SamplerCounts cnt{0ull, 0ull, 0ull};
+  unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0;
   unsigned long long n_reg = 0, n_dreg = 0, row_bytes = 0;
 
   for (;;) {
@@ -562,13 +611,13 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
     }
     __syncthreads();
     if (!s_valid) break;
-    const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2];
-    if (tid == 0) {
-      n_reg++;
-      if (int32_t(v) < p.n_dense) n_dreg++;
-      if (b == d.word_off[v])
-        row_bytes += int32_t(v) < p.n_dense ? 4ull * uint64_t(K) : 4ull * d.ws_nnz[int(v) - p.n_dense];
-    }
+    const uint32_t v = __builtin_amdgcn_readfirstlane(s_reg[0]);
+    const uint32_t b = __builtin_amdgcn_readfirstlane(s_reg[1]);
+    const uint32_t e = __builtin_amdgcn_readfirstlane(s_reg[2]);
+    n_reg++;
+    if (int32_t(v) < p.n_dense) n_dreg++;
+    if (b == d.word_off[v])
+      row_bytes += int32_t(v) < p.n_dense ? 4ull * uint64_t(K) : 4ull * d.ws_nnz[int(v) - p.n_dense];
     if (v != cur) {
       cur = v;
       const WordRec rec = d.wrec[v];
@@ -618,30 +667,30 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
     const WordState w{wh, qb, nb, K, K1, a1, qp, p.alpha};
     for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += kBlock) {
       const uint32_t j = base + uint32_t(lane);
-      const uint32_t zz = j < e ? uint32_t(d.z_w[j]) : 0u;
-      const bool und = (zz & kUndecidedBit) != 0u;
-      BatchTok bt{0u, 0u, zz & 0x7FFFu, 0.0};
+      const bool und = j < e && d.z_w[j] == kUndecided;
+      uint32_t nnz = 0;
       if (und) {
-        bt.off = d.wt_rowoff[j] + 1;
-        bt.u = uniform_draw(p.seed, t, d.wt_key[j]);
-        bt.nnz = d.d_ent[bt.off - 1] & 0xFFFFu;
-        if (bt.c1 == kC1Unknown) bt.c1 = row_lookup(d.d_ent + bt.off, bt.nnz, K1);
+        const uint32_t key = d.wt_key[j];
+        const uint32_t off = d.wt_rowoff[j] + 1;
+        nnz = d.d_ent[off - 1] & 0xFFFFu;
+        bt.off[lane] = off;
+        bt.nnz[lane] = nnz;
+        bt.u[lane] = uniform_draw(p.seed, t, key);
       }
+      n_sampled += uint32_t(__popcll(__ballot(und)));
+      nnz_sum += wave_sum_u32(nnz);
       // row-length classes: 16*C entries per group for C = 1, 2, 4, 8, then longer rows
-      const uint32_t cls = bt.nnz <= 16 ? 0u : bt.nnz <= 32 ? 1u : bt.nnz <= 64 ? 2u : bt.nnz <= 128 ? 3u : 4u;
-      uint16_t *zb = d.z_w + base;
-      draw_tokens<1>(__ballot(und && cls == 0u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
-      draw_tokens<2>(__ballot(und && cls == 1u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
-      draw_tokens<4>(__ballot(und && cls == 2u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
-      draw_tokens<8>(__ballot(und && cls == 3u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
-      draw_tokens<0>(__ballot(und && cls == 4u), bt, w, d.d_ent, zb, lane, grp, li, cnt);
+      const uint32_t cls = nnz <= 16 ? 0u : nnz <= 32 ? 1u : nnz <= 64 ? 2u : nnz <= 128 ? 3u : 4u;
+      draw_tokens<1>(__ballot(und && cls == 0u), bt, w, d.d_ent, grp, li, n_after_s);
+      draw_tokens<2>(__ballot(und && cls == 1u), bt, w, d.d_ent, grp, li, n_after_s);
+      draw_tokens<4>(__ballot(und && cls == 2u), bt, w, d.d_ent, grp, li, n_after_s);
+      draw_tokens<8>(__ballot(und && cls == 3u), bt, w, d.d_ent, grp, li, n_after_s);
+      draw_tokens<0>(__ballot(und && cls == 4u), bt, w, d.d_ent, grp, li, n_after_s);
+      // the batch's topics leave in one coalesced store
+      if (und) d.z_w[j] = bt.top[lane];
     }
     __syncthreads();
   }
-  unsigned long long n_sampled = cnt.sampled, n_after_s = cnt.after_s, nnz_sum = cnt.nnz;
-  n_sampled = group_sum_u64<kWave>(n_sampled);
-  n_after_s = group_sum_u64<kWave>(n_after_s);
-  nnz_sum = group_sum_u64<kWave>(nnz_sum);
   if (lane == 0) {
     if (n_sampled) atomicAdd(&stats[ST_SAMPLED], n_sampled);
     if (n_after_s) atomicAdd(&stats[ST_SKIP_AFTER_S], n_after_s);
@@ -885,6 +934,15 @@ hipError_t allow_lds(F *kernel, size_t bytes) {
 hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s) {
   const int64_t blocks = std::min<int64_t>((p.n + kBlock - 1) / kBlock, int64_t(p.grid_docs) * 8);
   hipLaunchKernelGGL(k_init_topics, dim3(uint32_t(blocks)), dim3(kBlock), 0, s, d.wt_key, d.z_w, p.n, p.K, p.seed);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_undecided(const DevState &d, const Params &p, hipStream_t s) {
+  // z_w is allocated with a whole number of 4-byte words (256-byte granules)
+  const int64_t n2 = (p.n + 1) / 2;
+  const int64_t blocks = std::min<int64_t>((n2 + kBlock - 1) / kBlock, int64_t(p.grid_docs) * 4);
+  hipLaunchKernelGGL(k_fill_undecided, dim3(uint32_t(blocks)), dim3(kBlock), 0, s,
+                     reinterpret_cast<uint32_t *>(d.z_w), n2);
   return hipGetLastError();
 }
 

@@ -242,6 +242,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.T, size_t(L.K)));
   LDA_TRY(dalloc(h, &d.den, size_t(L.K)));
   LDA_TRY(dalloc(h, &d.wrec, size_t(L.n_present)));
+  LDA_TRY(dalloc(h, &d.wskip, size_t(L.n_present)));
   LDA_TRY(dalloc(h, &d.counters, 8));
   LDA_TRY(dalloc(h, &h->stats_base, size_t(kStatSlots) * kStatsPerIter));
   LDA_TRY(dalloc(h, &d.ll_part, size_t(L.n_regions)));
@@ -324,6 +325,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   p.V = V;
   p.K = K;
   p.alpha = alpha;
+  p.alpha_f = float(alpha);
   p.beta = beta;
   p.vbeta = double(V) * beta;
   p.seed = seed;
@@ -361,6 +363,7 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       if (ev) HIP_TRY(h, hipEventRecord(ev[0], h->stream));
       HIP_TRY(h, launch_begin_iteration(d, h->p, h->stream));
       HIP_TRY(h, launch_word_pre(d, h->p, h->stream));
+      HIP_TRY(h, launch_fill_undecided(d, h->p, h->stream));
       if (ev) HIP_TRY(h, hipEventRecord(ev[1], h->stream));
       HIP_TRY(h, launch_doc_pass(d, h->p, t, h->stream));
       if (ev) HIP_TRY(h, hipEventRecord(ev[2], h->stream));

@@ -12,11 +12,9 @@
 
 namespace lda {
 
-// A 16-bit topic slot holds a topic (< K <= 16384) or, for a token the
-// step-3 test left undecided, kUndecidedBit | C1 with C1 = D[d][K1]
-// (kC1Unknown when C1 does not fit in 15 bits).
-constexpr uint16_t kUndecidedBit = 0x8000;
-constexpr uint16_t kC1Unknown = 0x7FFF;
+// A 16-bit topic slot holds a topic (< K <= 16384) or kUndecided for a token
+// the step-3 test has not decided.
+constexpr uint16_t kUndecided = 0x8000;
 // Slack entries after the last D row: the sampler reads whole register
 // chunks past the end of a row and discards what lies beyond it.
 constexpr uint32_t kRowPad = 256;
@@ -82,6 +80,13 @@ struct WordRec {  // per relabelled word, refreshed every iteration (Sec. 3.2, s
   uint32_t k1, k2;    // top-2 topic ids (lowest id on ties)
 };
 
+// Per-word record of the step-3 test in single precision (the test applies a
+// margin that covers the rounding, so a skip is always exact).
+struct SkipRec {
+  uint32_t k12;          // K1 | K2 << 16
+  float a1, a2, a3, qp;  // top-3 values of W^[v] and Q'
+};
+
 struct DevState {
   // layout
   uint32_t *doc_off, *dt_word, *dt_key, *dt_wpos, *word_off, *wt_rowoff, *wt_key;
@@ -96,6 +101,7 @@ struct DevState {
   uint32_t *T;
   double *den;
   WordRec *wrec;
+  SkipRec *wskip;
   // scheduler counters and statistics
   uint32_t *counters;           // [8]
   unsigned long long *stats;    // [8]
@@ -108,6 +114,7 @@ struct Params {
   int32_t M, V, K, n_present, n_dense;
   int64_t n_regions;
   double alpha, beta, vbeta;
+  float alpha_f;
   uint64_t seed;
   int32_t g;
   int32_t no_skip;
@@ -124,6 +131,7 @@ constexpr int kStatsPerIter = 8;
 hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_fill_undecided(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s);

@@ -55,7 +55,9 @@ def test_c1_every_iteration_from_oracle_snapshot(c1, c1_traj):
             check_counts_are_histograms(c1, cnt, c1.K)
             assert st["iteration"] == t and cnt["iteration"] == t + 1
             assert st["skip_step3"] + st["sampled"] == c1.N
-            assert abs(st["skip_step3"] - ost["skip3"]) <= ost["flagged"] + 2
+            # the GPU's step-3 test is conservative (single precision with a margin):
+            # it may skip a few tokens fewer than the oracle's fp64 test, never more
+            assert 0 <= ost["skip3"] - st["skip_step3"] <= max(2, 1e-3 * c1.N)
             assert st["ms_sampler"] > 0.0
 
 
