@@ -378,6 +378,7 @@ struct BatchLds {
   uint32_t *off, *nnz;
   double *u;
   uint16_t *top;
+  uint32_t *hand;  // kMaxRun slots per group: the selected lane's run
 };
 
 // The word of the current region: W^ row (with W^[K1] = 0) and Q' block
@@ -391,26 +392,24 @@ struct WordState {
 
 
 // Load C entries per lane from `row` (lane li gets entries [li*C, li*C + C),
-// topics ascending); entries at or past nn read as `pad`, a count-0 entry of
-// a topic other than K1.  Reads may run past the row into the padding after
-// the last row.
+// topics ascending).  The row is padded to its length class with count-0
+// entries of topic K, so all 16*C entries are in the row's slots.
 template <int C>
-__device__ __forceinline__ void load_run(const uint32_t *__restrict__ row, uint32_t nn, int li, uint32_t pad,
-                                         uint32_t (&r)[C]) {
+__device__ __forceinline__ void load_run(const uint32_t *__restrict__ row, int li, uint32_t (&r)[C]) {
   const uint32_t q0 = uint32_t(li) * C;
 #pragma unroll
-  for (int i = 0; i < C; ++i) {
-    const uint32_t v = row[q0 + i];
-    r[i] = (q0 + uint32_t(i) < nn) ? v : pad;
-  }
+  for (int i = 0; i < C; ++i) r[i] = row[q0 + i];
 }
 
-// This lane's S' terms in ascending topic order (W^[K1] = 0 in LDS).
+// This lane's S' terms in ascending topic order (W^[K1] = 0 in LDS).  The
+// lane sums are fused multiply-adds: S' is a sum in another association than
+// the sequential one anyway, so only draws within rounding distance of a
+// segment boundary can depend on it.
 template <int C>
 __device__ __forceinline__ double run_sum(const uint32_t (&r)[C], const double *__restrict__ wh) {
   double s = 0.0;
 #pragma unroll
-  for (int i = 0; i < C; ++i) s += double(r[i] & 0xFFFFu) * wh[r[i] >> 16];
+  for (int i = 0; i < C; ++i) s = __builtin_fma(double(r[i] & 0xFFFFu), wh[r[i] >> 16], s);
   return s;
 }
 
@@ -491,12 +490,15 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
                             const uint32_t *__restrict__ d_ent, int grp, int li, unsigned long long &after_s) {
   constexpr int R = C > 0 ? C : kMaxRun;
   while (mask) {
-    unsigned long long m = mask;
-    for (int q = 0; q < grp; ++q) m &= m - 1ull;
-    for (int q = 0; q < kWave / kGroup; ++q) mask &= mask - 1ull;
+    // the four lowest tokens of the mask, one per group (wave-uniform bit
+    // arithmetic; a group with none gets src = -1)
+    const unsigned long long m1 = mask & (mask - 1ull), m2 = m1 & (m1 - 1ull), m3 = m2 & (m2 - 1ull);
+    const int f0 = __ffsll((long long)mask) - 1, f1 = __ffsll((long long)m1) - 1;
+    const int f2 = __ffsll((long long)m2) - 1, f3 = __ffsll((long long)m3) - 1;
+    mask = m3 & (m3 - 1ull);
+    const int src = grp == 0 ? f0 : grp == 1 ? f1 : grp == 2 ? f2 : f3;
     bool in_m = false;
-    if (m) {
-    const int src = __ffsll(m) - 1;
+    if (src >= 0) {
     const uint32_t t_off = bt.off[src];
     const uint32_t t_nnz = bt.nnz[src];
     const double t_u = bt.u[src];
@@ -504,10 +506,9 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
     const uint32_t nch = C > 0 ? 1u : (t_nnz + kChunk - 1) / kChunk;
     uint32_t r[R];
     double s = 0.0, incl = 0.0, S = 0.0;
-    const uint32_t pad = uint32_t(w.K1 == 0u) << 16;
     uint32_t c1 = 0xFFFFFFFFu;
     for (uint32_t ch = 0; ch < nch; ++ch) {
-      load_run<R>(row + ch * kChunk, t_nnz - ch * kChunk, li, pad, r);
+      load_run<R>(row + ch * kChunk, li, r);
       c1 = run_count_of<R>(r, w.K1, c1);
       s = run_sum<R>(r, w.wh);
       incl = row_incl_scan(s);
@@ -527,7 +528,7 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
       } else {
         for (uint32_t ch = 0; ch < nch && !in_s; ++ch) {
           if (nch > 1) {
-            load_run<R>(row + ch * kChunk, t_nnz - ch * kChunk, li, pad, r);
+            load_run<R>(row + ch * kChunk, li, r);
             s = run_sum<R>(r, w.wh);
             incl = row_incl_scan(s);
           }
@@ -542,12 +543,13 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
         // S' run of one lane, moved across the group
         const int sel = run_lane(s, incl, cbase, x, grp);
         start = cbase + __shfl(incl - s, sel, kGroup);
-        uint32_t mine = 0u;
+        // lane li < R of the group takes entry li of the selected run
+        uint32_t *hand = bt.hand + grp * kMaxRun;
+        if (li == sel) {
 #pragma unroll
-        for (int i = 0; i < R; ++i) {
-          const uint32_t vi = __shfl(r[i], sel, kGroup);
-          mine = li == i ? vi : mine;
+          for (int i = 0; i < R; ++i) hand[i] = r[i];
         }
+        const uint32_t mine = li < R ? hand[li] : 0u;
         k = mine >> 16;
         term = double(mine & 0xFFFFu) * w.wh[k];
       } else {
@@ -582,17 +584,19 @@ __global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uin
   const int K = p.K;
   const int nb = (K + kGroup - 1) / kGroup;
   double *wh = lds;         // [K]
-  double *qb = lds + K;     // [nb + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup
+  double *qb = lds + K + 1; // [nb + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup
   __shared__ uint32_t s_reg[3];
   __shared__ int s_valid;
   __shared__ uint32_t s_off[kBlock], s_nnz[kBlock];
   __shared__ double s_u[kBlock];
   __shared__ uint16_t s_top[kBlock];
+  __shared__ uint32_t s_hand[kBlock / kGroup * kMaxRun];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int grp = lane / kGroup, li = lane % kGroup;
-  const BatchLds bt{s_off + wave * kWave, s_nnz + wave * kWave, s_u + wave * kWave, s_top + wave * kWave};
+  const BatchLds bt{s_off + wave * kWave, s_nnz + wave * kWave, s_u + wave * kWave, s_top + wave * kWave,
+                    s_hand + wave * (kWave / kGroup) * kMaxRun};
   // region, word and count variables are uniform over the block (scalar registers)
   uint32_t cur = 0xFFFFFFFFu, K1 = 0;
   double a1 = 0.0, qp = 0.0;
@@ -640,7 +644,10 @@ __global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uin
       }
       __syncthreads();
       // the max topic is its own branch: W^' has a 0 there (Eq. 5)
-      if (tid == 0) wh[K1] = 0.0;
+      if (tid == 0) {
+        wh[K1] = 0.0;
+        wh[K] = 0.0;  // topic of the padding entries of D rows
+      }
       __syncthreads();
       for (int blk = tid; blk < nb; blk += kBlock) {
         double s = 0.0;
@@ -819,6 +826,7 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
         if (hi) out[base + rank + (lo ? 1u : 0u)] = (uint32_t(2 * q + 1) << 16) | hi;
         base += uint32_t(__popcll(m0) + __popcll(m1));
       }
+      for (uint32_t q = base + lane; q < d_row_span(base); q += kWave) out[q] = uint32_t(K) << 16;
       if (lane == 0) out[-1] = ((e - b) << 16) | base;
       __threadfence_block();
     }
@@ -965,7 +973,7 @@ hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipSt
   return hipGetLastError();
 }
 
-size_t sampler_lds_bytes(int K) { return sizeof(double) * (size_t(K) + size_t((K + kGroup - 1) / kGroup) + 1); }
+size_t sampler_lds_bytes(int K) { return sizeof(double) * (size_t(K) + 1 + size_t((K + kGroup - 1) / kGroup) + 1); }
 
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
   hipError_t err = allow_lds(k_sampler, sampler_lds_bytes(p.K));
