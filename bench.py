@@ -33,12 +33,12 @@ def log(msg):
 
 
 def sampler_alg_bytes(st, N):
-    """Bytes the sampler must move per launch (see the design notes):
-    2 B topic slot per token; per sampled token its doc id and key (8 B), the
-    D-row offset and length (8 B), the D row (4 B per entry) and the new topic
-    (2 B); the W rows (4*K per dense word, 4*nnz per sparse word); the region
-    and word records (12 + 48 B per region)."""
-    return (2 * N + 18 * st["sampled"] + 4 * st["nnz_scanned"] + st["row_bytes"] + 60 * st["regions"])
+    """Bytes the sampler must move per launch: the 2 B topic slot of every
+    token (read to find the undecided ones); per sampled token its key (4 B),
+    D-row offset (4 B), row header (4 B), the nnz entries of its D row (4 B
+    each) and the new topic (2 B); the W rows (4*K B per dense word, 4*nnz B
+    per sparse word); the region and word records (12 + 48 B per region)."""
+    return (2 * N + 14 * st["sampled"] + 4 * st["nnz_scanned"] + st["row_bytes"] + 60 * st["regions"])
 
 
 def traffic_from_profile(alg_per_launch):
@@ -80,7 +80,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
-    ap.add_argument("--cpu-docs", type=int, default=50000, help="documents in the oracle's timed sample")
+    ap.add_argument("--cpu-docs", type=int, default=150000, help="documents in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dump-stats", default=None, help="write the per-iteration statistics (JSON lines) here")
     ap.add_argument("--calib-copy", action="store_true",
