@@ -379,6 +379,7 @@ struct BatchLds {
   double *u;
   uint16_t *top;
   uint32_t *hand;  // kMaxRun slots per group: the selected lane's run
+  uint8_t *list;   // the batch's lanes, sorted by row length, for the small-group draws
 };
 
 // The word of the current region: W^ row (with W^[K1] = 0) and Q' block
@@ -386,6 +387,7 @@ struct BatchLds {
 struct WordState {
   const double *wh, *qb;
   int nb, K;
+  int qsh;  // 4-ary search over qb: first level steps 4^(qsh/2) blocks (negative: a single block)
   uint32_t K1;
   double a1, qp, alpha;
 };
@@ -578,25 +580,282 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
   }
 }
 
+// Blocks of the Q' prefix rounded up to a power of 4 (the 4-ary search).
+__host__ __device__ inline int q_blocks_padded(int nb) {
+  int q = 1;
+  while (q < nb) q *= 4;
+  return q;
+}
+
+// ------------------------------------------------ small-group draws ----
+// Rows of at most 256 entries are drawn by groups of G = 4 lanes (rows of up
+// to 128 entries, 16 tokens per wave at a time) or G = 8 lanes (up to 256
+// entries, 8 tokens at a time), in chunks of G*kRun entries.  Group-wide sums
+// and scans are DPP moves inside quads (quad_perm) and half rows
+// (row_half_mirror); the selected entry is found by a walk inside one lane,
+// so all per-token work is spread over few lanes.
+constexpr int kRun = 8;
+constexpr int kDppXor1 = 0xB1;         // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;         // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // lane i <- lane 7-i inside each 8 lanes
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, 0xF, 0xF, true));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, 0xF, 0xF, true);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, 0xF, 0xF, true);
+  return __hiloint2double(hi, lo);
+}
+
+// Sum over a group of G (4 or 8) aligned lanes; every lane gets the same
+// bits (each step adds a pair in both orders, and IEEE addition commutes).
+template <int G>
+__device__ __forceinline__ double gsum(double v) {
+  v += dpp_f64<kDppXor1>(v);
+  v += dpp_f64<kDppXor2>(v);
+  if (G == 8) v += dpp_f64<kDppHalfMirror>(v);
+  return v;
+}
+template <int G>
+__device__ __forceinline__ uint32_t gsum_u32(uint32_t v) {
+  v += dpp_u32<kDppXor1>(v);
+  v += dpp_u32<kDppXor2>(v);
+  if (G == 8) v += dpp_u32<kDppHalfMirror>(v);
+  return v;
+}
+template <int G>
+__device__ __forceinline__ uint32_t gmin_u32(uint32_t v) {
+  v = min(v, dpp_u32<kDppXor1>(v));
+  v = min(v, dpp_u32<kDppXor2>(v));
+  if (G == 8) v = min(v, dpp_u32<kDppHalfMirror>(v));
+  return v;
+}
+template <int G>
+__device__ __forceinline__ uint32_t gmax_u32(uint32_t v) {
+  v = max(v, dpp_u32<kDppXor1>(v));
+  v = max(v, dpp_u32<kDppXor2>(v));
+  if (G == 8) v = max(v, dpp_u32<kDppHalfMirror>(v));
+  return v;
+}
+// Inclusive prefix sum over a group of G lanes (li = lane in the group).
+template <int G>
+__device__ __forceinline__ double gscan(double v, int li) {
+  { const double t = row_shr<1>(v); v += li >= 1 ? t : 0.0; }
+  { const double t = row_shr<2>(v); v += li >= 2 ? t : 0.0; }
+  if (G == 8) { const double t = row_shr<4>(v); v += li >= 4 ? t : 0.0; }
+  return v;
+}
+
+// Segment of a group's CDF that holds x: the group's lanes carry terms s >= 0
+// (in canonical order, lane by lane) whose inclusive scan is incl, starting at
+// base.  Returns the first lane whose range passes x, or, when rounding puts x
+// at or past the end, the last lane with a positive term.
+template <int G>
+__device__ __forceinline__ int pick_lane(double s, double incl, double base, double x, int li) {
+  const uint32_t n = gsum_u32<G>(x >= base + incl ? 1u : 0u);
+  if (n < uint32_t(G)) return int(n);
+  return int(gmax_u32<G>(s > 0.0 ? uint32_t(li) : 0u));
+}
+
+// First of kRun packed entries whose running S' sum (fused multiply-adds from
+// 0, as in run_sum) passes xs >= 0; the last entry with a positive term if
+// rounding leaves xs at or past the lane's total.  Such an entry always has
+// a positive term.
+__device__ __forceinline__ uint32_t walk_run(const uint32_t (&r)[kRun], const double *__restrict__ wh, double xs) {
+  double p = 0.0;
+  uint32_t ent = r[0];
+#pragma unroll
+  for (int i = 0; i < kRun; ++i) {
+    const bool open = p <= xs;
+    p = __builtin_fma(double(r[i] & 0xFFFFu), wh[r[i] >> 16], p);
+    ent = open ? r[i] : ent;
+  }
+  if (!(xs < p)) {
+#pragma unroll
+    for (int i = 0; i < kRun; ++i)
+      if ((r[i] & 0xFFFFu) != 0u && wh[r[i] >> 16] > 0.0) ent = r[i];
+  }
+  return ent;
+}
+
+// One round of small-group draws: group g of the wave draws the token in
+// list slot `slot` (if slot < n).  The row is read in chunks of G*kRun
+// entries, lane l holding entries [l*kRun, l*kRun + kRun) of each chunk (the
+// group's loads of a chunk share cache lines); NC is the largest chunk count
+// in the round, and a group whose row has fewer chunks skips the rest.
+template <int G, int NC>
+__device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState &w,
+                           const uint32_t *__restrict__ d_ent, int li, unsigned long long &after_s) {
+  constexpr uint32_t kSpan = uint32_t(G) * kRun;  // entries per chunk
+  bool in_m = false;
+  if (slot < n) {
+    const int src = bt.list[slot];
+    const uint32_t nc = (bt.nnz[src] + kSpan - 1) / kSpan;
+    const uint32_t *run = d_ent + bt.off[src] + uint32_t(li) * kRun;
+    const double u = bt.u[src];
+    // pass over the row: per lane and chunk the S' sum of kRun entries, and C1
+    double s[NC], T[NC];
+    uint32_t c1 = 0xFFFFFFFFu;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      s[c] = 0.0;
+      if (uint32_t(c) < nc) {
+        uint32_t r[kRun];
+        load_run<kRun>(run + c * kSpan, 0, r);
+        c1 = run_count_of<kRun>(r, w.K1, c1);
+        s[c] = run_sum<kRun>(r, w.wh);
+      }
+    }
+    // group totals, cumulative over the chunks (a missing chunk adds 0)
+    double S = 0.0;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      S += gsum<G>(s[c]);
+      T[c] = S;
+    }
+    c1 = gmin_u32<G>(c1);
+    // max-topic branch, Eq. 7: M = W^[v][K1] * (D[d][K1] + alpha)
+    const double Mm = w.a1 * (double(c1 <= 0xFFFFu ? c1 : 0u) + w.alpha);
+    const double x = u * ((Mm + S) + w.qp);
+    uint32_t topic = w.K1;
+    bool writer = li == 0;
+    in_m = x < Mm;
+    if (!in_m) {
+      if (x < Mm + S) {
+        // S': the chunk (the first whose cumulative total passes x; it has a
+        // positive total), the lane, then the entry
+        int cs = 0;
+        double base = Mm, sc = s[0];
+#pragma unroll
+        for (int c = 1; c < NC; ++c) {
+          if (uint32_t(c) < nc && x >= Mm + T[c - 1]) {
+            cs = c;
+            base = Mm + T[c - 1];
+            sc = s[c];
+          }
+        }
+        const double incl = gscan<G>(sc, li);
+        const int sel = pick_lane<G>(sc, incl, base, x, li);
+        uint32_t r[kRun];
+        load_run<kRun>(run + cs * kSpan, 0, r);
+        topic = walk_run(r, w.wh, fmax(x - (base + (incl - sc)), 0.0)) >> 16;
+        writer = li == sel;
+      } else {
+        // Q': the 16-topic block by a 4-ary search over the padded block
+        // prefix, then the topic; each quad of the group does it alone
+        const int q4 = li & 3;
+        const double qs = Mm + S;
+        const double xq = x - qs;
+        if (!(xq < w.qb[w.nb])) {
+          topic = (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);  // last positive segment
+        } else {
+          int lo = 0;
+          for (int sh = w.qsh; sh >= 0; sh -= 2) {
+            const bool ok = w.qb[lo + (q4 << sh)] <= xq;
+            lo += (int(gsum_u32<4>(ok ? 1u : 0u)) - 1) << sh;
+          }
+          const int k0 = lo * kGroup + q4 * 4;
+          double s4 = 0.0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) s4 += (k0 + i < w.K) ? w.alpha * w.wh[k0 + i] : 0.0;
+          const double start = qs + w.qb[lo];
+          const double incl = gscan<4>(s4, q4);
+          const int sel = pick_lane<4>(s4, incl, start, x, q4);
+          const double xs = fmax(x - (start + (incl - s4)), 0.0);
+          double pq = 0.0;
+          int kk = k0, last = k0;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const double t = (k0 + i < w.K) ? w.alpha * w.wh[k0 + i] : 0.0;
+            const bool open = pq <= xs;
+            pq += t;
+            kk = open ? k0 + i : kk;
+            last = t > 0.0 ? k0 + i : last;
+          }
+          topic = uint32_t(xs < pq ? kk : last);
+          writer = li == sel;
+        }
+      }
+    }
+    if (writer) bt.top[src] = uint16_t(topic);
+  }
+  // outside the divergent part, so the count stays wave-uniform
+  after_s += uint32_t(__popcll(__ballot(in_m && li == 0)));
+}
+
+// The small-group rounds of one batch: the undecided lanes with rows of
+// (lo_runs*G*kRun, hi_runs*G*kRun] entries are listed in order of their run
+// count, then drawn G-lane group per token, 64/G tokens per round.
+template <int G, int LO, int HI>
+__device__ void draw_small_batch(bool und, uint32_t nnz, const BatchLds &bt, const WordState &w,
+                                 const uint32_t *__restrict__ d_ent, int lane, unsigned long long &after_s) {
+  constexpr uint32_t kSpan = uint32_t(G) * kRun;
+  int n = 0, ends[HI + 1];
+#pragma unroll
+  for (int c = LO; c <= HI; ++c) {
+    const unsigned long long m = __ballot(und && nnz > uint32_t(c - 1) * kSpan && nnz <= uint32_t(c) * kSpan);
+    if ((m >> lane) & 1ull)
+      bt.list[n + int(__builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u)))] =
+          uint8_t(lane);
+    n += __popcll(m);
+    ends[c] = n;
+  }
+  const int g = lane / G, li = lane % G;
+  for (int base = 0; base < n; base += kWave / G) {
+    const int last = min(base + kWave / G, n) - 1;  // the round's largest run count is that of its last slot
+    int nc = LO;
+#pragma unroll
+    for (int c = LO; c < HI; ++c) nc = last >= ends[c] ? c + 1 : nc;
+    const int slot = base + g;
+    if constexpr (LO <= 1) {
+      if (nc <= 1) {
+        draw_small<G, 1>(bt, slot, n, w, d_ent, li, after_s);
+        continue;
+      }
+    }
+    if constexpr (LO <= 2) {
+      if (nc <= 2) {
+        draw_small<G, 2>(bt, slot, n, w, d_ent, li, after_s);
+        continue;
+      }
+    }
+    if constexpr (LO <= 3) {
+      if (nc <= 3) {
+        draw_small<G, 3>(bt, slot, n, w, d_ent, li, after_s);
+        continue;
+      }
+    }
+    draw_small<G, 4>(bt, slot, n, w, d_ent, li, after_s);
+  }
+}
+
 __global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uint32_t t,
                                                     unsigned long long *__restrict__ stats) {
   extern __shared__ double lds[];
   const int K = p.K;
   const int nb = (K + kGroup - 1) / kGroup;
-  double *wh = lds;         // [K]
-  double *qb = lds + K + 1; // [nb + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup
+  const int nbp = q_blocks_padded(nb);
+  double *wh = lds;          // [K + 1]
+  double *qb = lds + K + 1;  // [nbp + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup; +inf past nb
   __shared__ uint32_t s_reg[3];
   __shared__ int s_valid;
   __shared__ uint32_t s_off[kBlock], s_nnz[kBlock];
   __shared__ double s_u[kBlock];
   __shared__ uint16_t s_top[kBlock];
   __shared__ uint32_t s_hand[kBlock / kGroup * kMaxRun];
+  __shared__ uint8_t s_list[kBlock];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int grp = lane / kGroup, li = lane % kGroup;
   const BatchLds bt{s_off + wave * kWave, s_nnz + wave * kWave, s_u + wave * kWave, s_top + wave * kWave,
-                    s_hand + wave * (kWave / kGroup) * kMaxRun};
+                    s_hand + wave * (kWave / kGroup) * kMaxRun, s_list + wave * kWave};
+  int qsh = -2;
+  for (int q = 1; q < nbp; q *= 4) qsh += 2;
+  for (int q = nb + 1 + tid; q < nbp; q += kBlock) qb[q] = __builtin_inf();
   // region, word and count variables are uniform over the block (scalar registers)
   uint32_t cur = 0xFFFFFFFFu, K1 = 0;
   double a1 = 0.0, qp = 0.0;
@@ -671,7 +930,7 @@ __global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uin
       __syncthreads();
     }
 
-    const WordState w{wh, qb, nb, K, K1, a1, qp, p.alpha};
+    const WordState w{wh, qb, nb, K, qsh, K1, a1, qp, p.alpha};
     for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += kBlock) {
       const uint32_t j = base + uint32_t(lane);
       const bool und = j < e && d.z_w[j] == kUndecided;
@@ -686,13 +945,11 @@ __global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uin
       }
       n_sampled += uint32_t(__popcll(__ballot(und)));
       nnz_sum += wave_sum_u32(nnz);
-      // row-length classes: 16*C entries per group for C = 1, 2, 4, 8, then longer rows
-      const uint32_t cls = nnz <= 16 ? 0u : nnz <= 32 ? 1u : nnz <= 64 ? 2u : nnz <= 128 ? 3u : 4u;
-      draw_tokens<1>(__ballot(und && cls == 0u), bt, w, d.d_ent, grp, li, n_after_s);
-      draw_tokens<2>(__ballot(und && cls == 1u), bt, w, d.d_ent, grp, li, n_after_s);
-      draw_tokens<4>(__ballot(und && cls == 2u), bt, w, d.d_ent, grp, li, n_after_s);
-      draw_tokens<8>(__ballot(und && cls == 3u), bt, w, d.d_ent, grp, li, n_after_s);
-      draw_tokens<0>(__ballot(und && cls == 4u), bt, w, d.d_ent, grp, li, n_after_s);
+      // rows of up to 128 entries: 4 lanes per token; up to 256: 8 lanes;
+      // longer rows: 16 lanes, in chunks of kChunk entries
+      draw_small_batch<4, 1, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
+      draw_small_batch<8, 3, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
+      draw_tokens<0>(__ballot(und && nnz > 256u), bt, w, d.d_ent, grp, li, n_after_s);
       // the batch's topics leave in one coalesced store
       if (und) d.z_w[j] = bt.top[lane];
     }
@@ -973,7 +1230,9 @@ hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipSt
   return hipGetLastError();
 }
 
-size_t sampler_lds_bytes(int K) { return sizeof(double) * (size_t(K) + 1 + size_t((K + kGroup - 1) / kGroup) + 1); }
+size_t sampler_lds_bytes(int K) {
+  return sizeof(double) * (size_t(K) + 1 + size_t(q_blocks_padded((K + kGroup - 1) / kGroup)) + 1);
+}
 
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
   hipError_t err = allow_lds(k_sampler, sampler_lds_bytes(p.K));

@@ -142,6 +142,25 @@ def test_reduced_config_snapshots(name, over):
     assert ll == pytest.approx(oracle.llpt(c.word, c.doc, cnt["z"], **corpus_kw(c)), rel=1e-12)
 
 
+@pytest.mark.parametrize("name,over", REDUCED[:2], ids=[r[0] for r in REDUCED[:2]])
+def test_reduced_config_late_snapshot(name, over):
+    """Iteration 49 from the GPU's own state after 49 iterations (higher skip rates than at the start)."""
+    c = lda_synth.make_corpus(name, **over)
+    say("late snapshot %s N=%d" % (name, c.N))
+    with make_lda(c) as m:
+        m.iterate(49)
+        z = m.counts(D=False, W=False)["z"]
+        zo, flags, ost = oracle_step(c, z, 49)
+        st = m.iterate(1, stats=True)[0]
+        assert st["iteration"] == 49
+        cnt = m.counts()
+    compare_draws(cnt["z"], zo, flags, c.N)
+    check_counts_are_histograms(c, cnt, c.K)
+    assert st["skip_step3"] + st["sampled"] == c.N
+    assert 0 <= ost["skip3"] - st["skip_step3"] <= max(2, 1e-3 * c.N)
+    say("  skip3 gpu %d oracle %d of %d" % (st["skip_step3"], ost["skip3"], c.N))
+
+
 def test_shuffled_input_order():
     """Input not sorted by document: keys and z stay in the caller's order."""
     c = lda_synth.generate(lda_synth.SPECS["c1"], n_docs=300, shuffle=True)
