@@ -504,13 +504,15 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
     const uint32_t t_off = bt.off[src];
     const uint32_t t_nnz = bt.nnz[src];
     const double t_u = bt.u[src];
-    const uint32_t *row = d_ent + t_off;
-    const uint32_t nch = C > 0 ? 1u : (t_nnz + kChunk - 1) / kChunk;
+    const uint32_t *row = d_ent + t_off;  // slot 0 is the row header
+    const uint32_t pad = uint32_t(w.K) << 16;
+    const uint32_t nch = C > 0 ? 1u : (t_nnz + 1u + kChunk - 1) / kChunk;
     uint32_t r[R];
     double s = 0.0, incl = 0.0, S = 0.0;
     uint32_t c1 = 0xFFFFFFFFu;
     for (uint32_t ch = 0; ch < nch; ++ch) {
       load_run<R>(row + ch * kChunk, li, r);
+      if (ch == 0u && li == 0) r[0] = pad;
       c1 = run_count_of<R>(r, w.K1, c1);
       s = run_sum<R>(r, w.wh);
       incl = row_incl_scan(s);
@@ -531,6 +533,7 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
         for (uint32_t ch = 0; ch < nch && !in_s; ++ch) {
           if (nch > 1) {
             load_run<R>(row + ch * kChunk, li, r);
+            if (ch == 0u && li == 0) r[0] = pad;
             s = run_sum<R>(r, w.wh);
             incl = row_incl_scan(s);
           }
@@ -693,8 +696,9 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
   bool in_m = false;
   if (slot < n) {
     const int src = bt.list[slot];
-    const uint32_t nc = (bt.nnz[src] + kSpan - 1) / kSpan;
+    const uint32_t nc = (bt.nnz[src] + 1u + kSpan - 1) / kSpan;  // slots: header + entries
     const uint32_t *run = d_ent + bt.off[src] + uint32_t(li) * kRun;
+    const uint32_t pad = uint32_t(w.K) << 16;
     const double u = bt.u[src];
     // pass over the row: per lane and chunk the S' sum of kRun entries, and C1
     double s[NC], T[NC];
@@ -705,6 +709,7 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
       if (uint32_t(c) < nc) {
         uint32_t r[kRun];
         load_run<kRun>(run + c * kSpan, 0, r);
+        if (c == 0 && li == 0) r[0] = pad;  // the row header
         c1 = run_count_of<kRun>(r, w.K1, c1);
         s[c] = run_sum<kRun>(r, w.wh);
       }
@@ -741,6 +746,7 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
         const int sel = pick_lane<G>(sc, incl, base, x, li);
         uint32_t r[kRun];
         load_run<kRun>(run + cs * kSpan, 0, r);
+        if (cs == 0 && li == 0) r[0] = pad;
         topic = walk_run(r, w.wh, fmax(x - (base + (incl - sc)), 0.0)) >> 16;
         writer = li == sel;
       } else {
@@ -786,9 +792,9 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
   after_s += uint32_t(__popcll(__ballot(in_m && li == 0)));
 }
 
-// The small-group rounds of one batch: the undecided lanes with rows of
-// (lo_runs*G*kRun, hi_runs*G*kRun] entries are listed in order of their run
-// count, then drawn G-lane group per token, 64/G tokens per round.
+// The small-group rounds of one batch: the undecided lanes whose rows take
+// (LO-1, HI] chunks of G*kRun slots (header included) are listed in order of
+// their chunk count, then drawn with G lanes per token, 64/G tokens a round.
 template <int G, int LO, int HI>
 __device__ void draw_small_batch(bool und, uint32_t nnz, const BatchLds &bt, const WordState &w,
                                  const uint32_t *__restrict__ d_ent, int lane, unsigned long long &after_s) {
@@ -796,7 +802,7 @@ __device__ void draw_small_batch(bool und, uint32_t nnz, const BatchLds &bt, con
   int n = 0, ends[HI + 1];
 #pragma unroll
   for (int c = LO; c <= HI; ++c) {
-    const unsigned long long m = __ballot(und && nnz > uint32_t(c - 1) * kSpan && nnz <= uint32_t(c) * kSpan);
+    const unsigned long long m = __ballot(und && nnz + 1u > uint32_t(c - 1) * kSpan && nnz + 1u <= uint32_t(c) * kSpan);
     if ((m >> lane) & 1ull)
       bt.list[n + int(__builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u)))] =
           uint8_t(lane);
@@ -937,19 +943,19 @@ __global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uin
       uint32_t nnz = 0;
       if (und) {
         const uint32_t key = d.wt_key[j];
-        const uint32_t off = d.wt_rowoff[j] + 1;
-        nnz = d.d_ent[off - 1] & 0xFFFFu;
+        const uint32_t off = d.wt_rowoff[j];  // the row's first slot (its header)
+        nnz = d.d_ent[off] & 0xFFFFu;
         bt.off[lane] = off;
         bt.nnz[lane] = nnz;
         bt.u[lane] = uniform_draw(p.seed, t, key);
       }
       n_sampled += uint32_t(__popcll(__ballot(und)));
       nnz_sum += wave_sum_u32(nnz);
-      // rows of up to 128 entries: 4 lanes per token; up to 256: 8 lanes;
-      // longer rows: 16 lanes, in chunks of kChunk entries
+      // rows of up to 128 slots (header and entries): 4 lanes per token; up
+      // to 256: 8 lanes; longer rows: 16 lanes, in chunks of kChunk slots
       draw_small_batch<4, 1, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
       draw_small_batch<8, 3, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
-      draw_tokens<0>(__ballot(und && nnz > 256u), bt, w, d.d_ent, grp, li, n_after_s);
+      draw_tokens<0>(__ballot(und && nnz + 1u > 256u), bt, w, d.d_ent, grp, li, n_after_s);
       // the batch's topics leave in one coalesced store
       if (und) d.z_w[j] = bt.top[lane];
     }
@@ -1083,7 +1089,7 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
         if (hi) out[base + rank + (lo ? 1u : 0u)] = (uint32_t(2 * q + 1) << 16) | hi;
         base += uint32_t(__popcll(m0) + __popcll(m1));
       }
-      for (uint32_t q = base + lane; q < d_row_span(base); q += kWave) out[q] = uint32_t(K) << 16;
+      for (uint32_t q = base + lane; q + 1u < d_row_slots(base); q += kWave) out[q] = uint32_t(K) << 16;
       if (lane == 0) out[-1] = ((e - b) << 16) | base;
       __threadfence_block();
     }

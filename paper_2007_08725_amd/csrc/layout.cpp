@@ -85,14 +85,14 @@ lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t
   L.word_off.assign(size_t(np) + 1, 0);
   for (int32_t r = 0; r < np; r++) L.word_off[size_t(r) + 1] = L.word_off[size_t(r)] + L.count[size_t(r)];
 
-  // capacities: a D row is one header entry (len << 16 | nnz) followed by at
+  // capacities: a D row is one header slot (len << 16 | nnz) followed by at
   // most min(len, K) packed entries (Sec. 4.2), padded to the sampler's
-  // length class; sparse W rows = token count
+  // chunk (multiples of 32 slots); sparse W rows = token count
   L.d_cap.assign(size_t(M) + 1, 0);
   uint64_t total = 0;
   for (int32_t d = 0; d < M; d++) {
     const uint32_t len = L.doc_off[size_t(d) + 1] - L.doc_off[size_t(d)];
-    total += 1u + d_row_span(std::min<uint32_t>(len, uint32_t(K)));
+    total += d_row_slots(std::min<uint32_t>(len, uint32_t(K)));
     if (total + kRowPad >= (uint64_t(1) << 32)) {
       msg = "documents plus tokens exceed the 32-bit offsets of D";
       return LDA_E_RANGE;

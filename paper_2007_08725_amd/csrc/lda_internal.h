@@ -18,12 +18,15 @@ constexpr uint16_t kUndecided = 0x8000;
 // Slack entries after the last D row.
 constexpr uint32_t kRowPad = 256;
 
-// Slots a D row with nnz entries occupies: nnz rounded up to the unit the
-// sampler reads it in (32 entries up to 128, 64 up to 256, then 128).  The
-// slots past nnz hold count-0 entries of topic K (K << 16), whose W^ is 0,
-// so the sampler reads whole units without bounds checks.
-__host__ __device__ inline uint32_t d_row_span(uint32_t nnz) {
-  return nnz <= 128u ? (nnz + 31u) & ~31u : nnz <= 256u ? (nnz + 63u) & ~63u : (nnz + 127u) & ~127u;
+// Slots a D row with nnz entries occupies: its header and entries, rounded
+// up to the chunk the sampler reads it in (32 slots up to 128, 64 up to 256,
+// then 128).  Every row starts at a multiple of 32 slots (128 bytes), so
+// chunks are whole cache lines.  The slots past the entries hold count-0
+// entries of topic K (K << 16), whose W^ is 0, so the sampler reads whole
+// chunks without bounds checks.
+__host__ __device__ inline uint32_t d_row_slots(uint32_t nnz) {
+  const uint32_t n = nnz + 1u;
+  return n <= 128u ? (n + 31u) & ~31u : n <= 256u ? (n + 63u) & ~63u : (n + 127u) & ~127u;
 }
 constexpr int kDefaultRegionTokens = 10000;  // Sec. 5.1
 constexpr int kBlock = 256;                  // threads per workgroup (4 wave64)
