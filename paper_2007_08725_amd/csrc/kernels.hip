@@ -196,9 +196,9 @@ __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den
                         uint32_t *__restrict__ counters, unsigned long long *__restrict__ stats) {
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
   if (k < K) den[k] = double(T[k]) + vbeta;
-  if (blockIdx.x == 0 && threadIdx.x < 8) {
+  if (blockIdx.x == 0 && threadIdx.x < kCounters) {
     counters[threadIdx.x] = 0u;
-    if (stats) stats[threadIdx.x] = 0ull;
+    if (stats && threadIdx.x < kStatsPerIter) stats[threadIdx.x] = 0ull;
   }
 }
 
@@ -303,6 +303,32 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
 // into a per-wave topic -> count table in LDS, so each token's C1 and C2 are
 // two LDS reads; the table is cleared again from the row afterwards.
 constexpr uint32_t kDocBatch = 32;
+
+// Next batch [d0, d1) of documents for a wave of the D rebuild.  The
+// documents are split into kXcds ranges of equal token counts; workgroups are
+// dealt to the XCDs in turn, so blockIdx.x % kXcds names the wave's XCD, and
+// a wave takes batches from its own XCD's range first, then from the others
+// in turn.  Each XCD's L2 then sees a compact window of documents, and the
+// word-ordered topic slots that window gathers are fetched by one XCD
+// instead of all of them.
+__device__ __forceinline__ bool next_docs(uint32_t *__restrict__ cnt, const Params &p, int &part, int lane,
+                                          uint32_t &d0, uint32_t &d1) {
+  const int x = int(blockIdx.x % kXcds);
+  while (part < kXcds) {
+    const int r = (x + part) % kXcds;
+    uint32_t o = 0;
+    if (lane == 0) o = atomicAdd(&cnt[r], kDocBatch);
+    o = __shfl(o, 0);
+    const uint32_t b = p.xcd_doc[r] + o, e = p.xcd_doc[r + 1];
+    if (o < e - p.xcd_doc[r]) {
+      d0 = b;
+      d1 = min(b + kDocBatch, e);
+      return true;
+    }
+    ++part;
+  }
+  return false;
+}
 
 __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint32_t t,
                                                      unsigned long long *__restrict__ stats) {
@@ -1056,15 +1082,12 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   uint32_t *hist = ldsu + size_t(wave) * size_t(half);
   for (int q = lane; q < half; q += kWave) hist[q] = 0u;
-  const uint32_t M = uint32_t(p.M);
   const unsigned long long lt = (1ull << lane) - 1ull;
   uint32_t bad = 0;
+  int part = 0;
   for (;;) {
-    uint32_t d0 = 0;
-    if (lane == 0) d0 = atomicAdd(&d.counters[CNT_REBUILD_D], kDocBatch);
-    d0 = __shfl(d0, 0);
-    if (d0 >= M) break;
-    const uint32_t d1 = min(M, d0 + kDocBatch);
+    uint32_t d0 = 0, d1 = 0;
+    if (!next_docs(d.counters + CNT_REBUILD_D, p, part, lane, d0, d1)) break;
     for (uint32_t dd = d0; dd < d1; ++dd) {
       const uint32_t b = d.doc_off[dd], e = d.doc_off[dd + 1];
       for (uint32_t pp = b + lane; pp < e; pp += kWave) {

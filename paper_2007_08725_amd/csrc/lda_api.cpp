@@ -203,6 +203,14 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   std::string msg;
   lda_status st = plan_from_counts(cnt, L.K, R, L, msg);
   if (st != LDA_OK) return fail(h, st, msg);
+  // document ranges of equal token counts for the document kernels, one per XCD
+  p.xcd_doc[0] = 0;
+  for (int x = 1; x < kXcds; ++x) {
+    const uint64_t target = uint64_t(L.n) * uint64_t(x) / uint64_t(kXcds);
+    p.xcd_doc[x] = uint32_t(std::lower_bound(L.doc_off.begin(), L.doc_off.end(), uint32_t(target)) - L.doc_off.begin());
+    p.xcd_doc[x] = std::min<uint32_t>(std::max(p.xcd_doc[x], p.xcd_doc[x - 1]), uint32_t(L.M));
+  }
+  p.xcd_doc[kXcds] = uint32_t(L.M);
   p.n_present = L.n_present;
   p.n_dense = L.n_dense;
   p.n_regions = L.n_regions;
@@ -243,7 +251,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.den, size_t(L.K)));
   LDA_TRY(dalloc(h, &d.wrec, size_t(L.n_present)));
   LDA_TRY(dalloc(h, &d.wskip, size_t(L.n_present)));
-  LDA_TRY(dalloc(h, &d.counters, 8));
+  LDA_TRY(dalloc(h, &d.counters, kCounters));
   LDA_TRY(dalloc(h, &h->stats_base, size_t(kStatSlots) * kStatsPerIter));
   LDA_TRY(dalloc(h, &d.ll_part, size_t(L.n_regions)));
   LDA_TRY(dalloc(h, &d.ll_out, 1));

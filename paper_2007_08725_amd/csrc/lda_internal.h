@@ -30,6 +30,7 @@ __host__ __device__ inline uint32_t d_row_slots(uint32_t nnz) {
 }
 constexpr int kDefaultRegionTokens = 10000;  // Sec. 5.1
 constexpr int kBlock = 256;                  // threads per workgroup (4 wave64)
+constexpr int kXcds = 8;                     // accelerator dies (XCDs), each with its own L2
 
 // ----------------------------------------------------------------- layout --
 // Host-side token layout (Sec. 4.2-4.3 and 5.1).
@@ -131,9 +132,13 @@ struct Params {
   int32_t key_identity;
   int32_t grid_regions;  // persistent workgroups for region kernels
   int32_t grid_docs;     // persistent workgroups for doc kernels
+  uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
 
-enum { CNT_SAMPLER = 0, CNT_REBUILD_W = 1, CNT_DOCPASS = 2, CNT_REBUILD_D = 3, CNT_LOGLIK = 4 };
+// Scheduler counters: one each for the region kernels and the doc pass,
+// kXcds (one per document range) for the D rebuild.
+enum { CNT_SAMPLER = 0, CNT_REBUILD_W = 1, CNT_DOCPASS = 2, CNT_LOGLIK = 4, CNT_REBUILD_D = 16 };
+constexpr int kCounters = 32;
 enum { ST_SKIP3 = 0, ST_SKIP_AFTER_S = 1, ST_SAMPLED = 2, ST_NNZ = 3, ST_REGIONS = 4, ST_DENSE_REGIONS = 5, ST_ERRORS = 6, ST_ROW_BYTES = 7 };
 constexpr int kStatsPerIter = 8;
 
