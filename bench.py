@@ -80,7 +80,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5"])
-    ap.add_argument("--cpu-docs", type=int, default=150000, help="documents in the oracle's timed sample")
+    ap.add_argument("--cpu-docs", type=int, default=200000, help="documents in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dump-stats", default=None, help="write the per-iteration statistics (JSON lines) here")
     ap.add_argument("--calib-copy", action="store_true",
