@@ -617,16 +617,18 @@ __host__ __device__ inline int q_blocks_padded(int nb) {
 }
 
 // ------------------------------------------------ small-group draws ----
-// Rows of at most 256 entries are drawn by groups of G = 4 lanes (rows of up
-// to 128 entries, 16 tokens per wave at a time) or G = 8 lanes (up to 256
-// entries, 8 tokens at a time), in chunks of G*kRun entries.  Group-wide sums
-// and scans are DPP moves inside quads (quad_perm) and half rows
-// (row_half_mirror); the selected entry is found by a walk inside one lane,
-// so all per-token work is spread over few lanes.
+// Rows of at most 512 slots are drawn by groups of G = 4 lanes (rows of up
+// to 128 slots, 16 tokens per wave at a time), G = 8 lanes (up to 256 slots,
+// 8 tokens at a time) or G = 16 lanes (up to 512 slots, 4 tokens), in chunks
+// of G*kRun slots whose loads are all issued before the first is used.
+// Group-wide sums and scans are DPP moves inside quads (quad_perm), half
+// rows (row_half_mirror) and rows (row_mirror); the selected entry is found
+// by a walk inside one lane.
 constexpr int kRun = 8;
 constexpr int kDppXor1 = 0xB1;         // quad_perm [1,0,3,2]
 constexpr int kDppXor2 = 0x4E;         // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141;  // lane i <- lane 7-i inside each 8 lanes
+constexpr int kDppMirror = 0x140;      // lane i <- lane 15-i inside each 16 lanes
 
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
@@ -639,34 +641,39 @@ __device__ __forceinline__ double dpp_f64(double v) {
   return __hiloint2double(hi, lo);
 }
 
-// Sum over a group of G (4 or 8) aligned lanes; every lane gets the same
-// bits (each step adds a pair in both orders, and IEEE addition commutes).
+// Sum over a group of G (4, 8 or 16) aligned lanes; every lane gets the
+// same bits (each step adds a pair in both orders, and IEEE addition
+// commutes).
 template <int G>
 __device__ __forceinline__ double gsum(double v) {
   v += dpp_f64<kDppXor1>(v);
   v += dpp_f64<kDppXor2>(v);
-  if (G == 8) v += dpp_f64<kDppHalfMirror>(v);
+  if (G >= 8) v += dpp_f64<kDppHalfMirror>(v);
+  if (G >= 16) v += dpp_f64<kDppMirror>(v);
   return v;
 }
 template <int G>
 __device__ __forceinline__ uint32_t gsum_u32(uint32_t v) {
   v += dpp_u32<kDppXor1>(v);
   v += dpp_u32<kDppXor2>(v);
-  if (G == 8) v += dpp_u32<kDppHalfMirror>(v);
+  if (G >= 8) v += dpp_u32<kDppHalfMirror>(v);
+  if (G >= 16) v += dpp_u32<kDppMirror>(v);
   return v;
 }
 template <int G>
 __device__ __forceinline__ uint32_t gmin_u32(uint32_t v) {
   v = min(v, dpp_u32<kDppXor1>(v));
   v = min(v, dpp_u32<kDppXor2>(v));
-  if (G == 8) v = min(v, dpp_u32<kDppHalfMirror>(v));
+  if (G >= 8) v = min(v, dpp_u32<kDppHalfMirror>(v));
+  if (G >= 16) v = min(v, dpp_u32<kDppMirror>(v));
   return v;
 }
 template <int G>
 __device__ __forceinline__ uint32_t gmax_u32(uint32_t v) {
   v = max(v, dpp_u32<kDppXor1>(v));
   v = max(v, dpp_u32<kDppXor2>(v));
-  if (G == 8) v = max(v, dpp_u32<kDppHalfMirror>(v));
+  if (G >= 8) v = max(v, dpp_u32<kDppHalfMirror>(v));
+  if (G >= 16) v = max(v, dpp_u32<kDppMirror>(v));
   return v;
 }
 // Inclusive prefix sum over a group of G lanes (li = lane in the group).
@@ -674,7 +681,8 @@ template <int G>
 __device__ __forceinline__ double gscan(double v, int li) {
   { const double t = row_shr<1>(v); v += li >= 1 ? t : 0.0; }
   { const double t = row_shr<2>(v); v += li >= 2 ? t : 0.0; }
-  if (G == 8) { const double t = row_shr<4>(v); v += li >= 4 ? t : 0.0; }
+  if (G >= 8) { const double t = row_shr<4>(v); v += li >= 4 ? t : 0.0; }
+  if (G >= 16) { const double t = row_shr<8>(v); v += li >= 8 ? t : 0.0; }
   return v;
 }
 
@@ -726,18 +734,23 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
     const uint32_t *run = d_ent + bt.off[src] + uint32_t(li) * kRun;
     const uint32_t pad = uint32_t(w.K) << 16;
     const double u = bt.u[src];
-    // pass over the row: per lane and chunk the S' sum of kRun entries, and C1
+    // pass over the row: every chunk's loads are issued before the first is
+    // used (one memory latency per row, not one per chunk); then per lane
+    // and chunk the S' sum of kRun entries, and C1
+    uint32_t r[NC][kRun];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      if (uint32_t(c) < nc) load_run<kRun>(run + c * kSpan, 0, r[c]);
+    }
+    if (li == 0) r[0][0] = pad;  // the row header
     double s[NC], T[NC];
     uint32_t c1 = 0xFFFFFFFFu;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       s[c] = 0.0;
       if (uint32_t(c) < nc) {
-        uint32_t r[kRun];
-        load_run<kRun>(run + c * kSpan, 0, r);
-        if (c == 0 && li == 0) r[0] = pad;  // the row header
-        c1 = run_count_of<kRun>(r, w.K1, c1);
-        s[c] = run_sum<kRun>(r, w.wh);
+        c1 = run_count_of<kRun>(r[c], w.K1, c1);
+        s[c] = run_sum<kRun>(r[c], w.wh);
       }
     }
     // group totals, cumulative over the chunks (a missing chunk adds 0)
@@ -864,7 +877,7 @@ __device__ void draw_small_batch(bool und, uint32_t nnz, const BatchLds &bt, con
   }
 }
 
-__global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uint32_t t,
+__global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uint32_t t,
                                                     unsigned long long *__restrict__ stats) {
   extern __shared__ double lds[];
   const int K = p.K;
@@ -965,11 +978,17 @@ __global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uin
     const WordState w{wh, qb, nb, K, qsh, K1, a1, qp, p.alpha};
     for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += kBlock) {
       const uint32_t j = base + uint32_t(lane);
-      const bool und = j < e && d.z_w[j] == kUndecided;
+      // the slot, key and row offset are loaded together (one latency); the
+      // row header only for undecided tokens
+      uint32_t zj = 0, key = 0, off = 0;
+      if (j < e) {
+        zj = d.z_w[j];
+        key = d.wt_key[j];
+        off = d.wt_rowoff[j];  // the row's first slot (its header)
+      }
+      const bool und = j < e && zj == kUndecided;
       uint32_t nnz = 0;
       if (und) {
-        const uint32_t key = d.wt_key[j];
-        const uint32_t off = d.wt_rowoff[j];  // the row's first slot (its header)
         nnz = d.d_ent[off] & 0xFFFFu;
         bt.off[lane] = off;
         bt.nnz[lane] = nnz;
@@ -978,10 +997,12 @@ __global__ __launch_bounds__(kBlock, 8) void k_sampler(DevState d, Params p, uin
       n_sampled += uint32_t(__popcll(__ballot(und)));
       nnz_sum += wave_sum_u32(nnz);
       // rows of up to 128 slots (header and entries): 4 lanes per token; up
-      // to 256: 8 lanes; longer rows: 16 lanes, in chunks of kChunk slots
+      // to 256: 8 lanes; up to 512: 16 lanes; longer rows: 16 lanes, one
+      // chunk of kChunk slots at a time
       draw_small_batch<4, 1, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
       draw_small_batch<8, 3, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
-      draw_tokens<0>(__ballot(und && nnz + 1u > 256u), bt, w, d.d_ent, grp, li, n_after_s);
+      draw_small_batch<16, 3, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
+      draw_tokens<0>(__ballot(und && nnz + 1u > 512u), bt, w, d.d_ent, grp, li, n_after_s);
       // the batch's topics leave in one coalesced store
       if (und) d.z_w[j] = bt.top[lane];
     }
