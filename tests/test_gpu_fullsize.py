@@ -50,13 +50,13 @@ def _check_rows_sampled(c, cnt, rng):
         assert np.array_equal(got, hist[q]), v
 
 
-@pytest.mark.timeout(900)
 C5 = pytest.param("c5", marks=pytest.mark.skipif(
     not os.environ.get("LDA_FULLSIZE_C5"),
     reason="3.0e9-token corpus: about 7 minutes, mostly host-side generation and oracle counts; "
            "set LDA_FULLSIZE_C5=1 to run it"))
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["c2", "c3", "c4", C5])
 def test_full_size_first_iteration(name):
     c = lda_synth.make_corpus(name)
