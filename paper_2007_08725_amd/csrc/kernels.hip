@@ -342,21 +342,42 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
   for (;;) {
     uint32_t d0 = 0;
     if (lane == 0) d0 = atomicAdd(&d.counters[CNT_DOCPASS], kDocBatch);
-    d0 = __shfl(d0, 0);
+    d0 = __builtin_amdgcn_readfirstlane(__shfl(d0, 0));
     if (d0 >= M) break;
-    const uint32_t d1 = min(M, d0 + kDocBatch);
-    for (uint32_t dd = d0; dd < d1; ++dd) {
-      const uint32_t b = d.doc_off[dd], e = d.doc_off[dd + 1];
+    const int nd = int(min(M, d0 + kDocBatch) - d0);
+    // the batch's document offsets and row offsets, one per lane
+    const uint32_t offv = lane <= nd ? d.doc_off[d0 + uint32_t(lane)] : 0u;
+    const uint32_t capv = lane < nd ? d.d_cap[d0 + uint32_t(lane)] : 0u;
+    // the first 64 slots of a row (its header and first 63 entries) and the
+    // first 64 word ids of a document are loaded one document ahead
+    uint32_t nrow = 0, nw = 0;
+    {
+      const uint32_t b = uint32_t(__shfl(int(offv), 0)), e = uint32_t(__shfl(int(offv), 1));
+      nrow = d.d_ent[uint32_t(__shfl(int(capv), 0)) + uint32_t(lane)];
+      if (b + uint32_t(lane) < e) nw = d.dt_word[b + uint32_t(lane)];
+    }
+    for (int i = 0; i < nd; ++i) {
+      const uint32_t b = __builtin_amdgcn_readlane(offv, i), e = __builtin_amdgcn_readlane(offv, i + 1);
+      const uint32_t cap = __builtin_amdgcn_readlane(capv, i);
       const uint32_t len = e - b;
-      const uint32_t *row = d.d_ent + d.d_cap[dd] + 1;
-      const uint32_t nnz = row[-1] & 0xFFFFu;
-      for (uint32_t q = lane; q < nnz; q += kWave) {
+      const uint32_t rowv = nrow, wv = nw;
+      if (i + 1 < nd) {
+        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 1), en = __builtin_amdgcn_readlane(offv, i + 2);
+        nrow = d.d_ent[__builtin_amdgcn_readlane(capv, i + 1) + uint32_t(lane)];
+        if (bn + uint32_t(lane) < en) nw = d.dt_word[bn + uint32_t(lane)];
+      }
+      const uint32_t *row = d.d_ent + cap + 1;  // entries; slot 0 is the header
+      const uint32_t nnz = uint32_t(__builtin_amdgcn_readfirstlane(int(rowv))) & 0xFFFFu;
+      // spread the row into the topic -> count table
+      if (lane >= 1 && uint32_t(lane) <= nnz) cmap[rowv >> 16] = uint16_t(rowv & 0xFFFFu);
+      for (uint32_t q = 63u + uint32_t(lane); q < nnz; q += kWave) {
         const uint32_t ent = row[q];
         cmap[ent >> 16] = uint16_t(ent & 0xFFFFu);
       }
       __builtin_amdgcn_wave_barrier();
-      for (uint32_t pp = b + lane; pp < e; pp += kWave) {
-        const SkipRec rec = d.wskip[d.dt_word[pp]];
+      for (uint32_t pp = b + uint32_t(lane); pp < e; pp += kWave) {
+        const uint32_t v = pp < b + kWave ? wv : d.dt_word[pp];
+        const SkipRec rec = d.wskip[v];
         const uint32_t K1 = rec.k12 & 0xFFFFu, K2 = rec.k12 >> 16;
         const uint32_t C1 = cmap[K1], C2 = cmap[K2];
         const uint32_t key = p.key_identity ? pp : d.dt_key[pp];
@@ -373,7 +394,8 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
         nskip += skip ? 1ull : 0ull;
       }
       __builtin_amdgcn_wave_barrier();
-      for (uint32_t q = lane; q < nnz; q += kWave) cmap[row[q] >> 16] = 0;
+      if (lane >= 1 && uint32_t(lane) <= nnz) cmap[rowv >> 16] = 0;
+      for (uint32_t q = 63u + uint32_t(lane); q < nnz; q += kWave) cmap[row[q] >> 16] = 0;
       __builtin_amdgcn_wave_barrier();
     }
   }
