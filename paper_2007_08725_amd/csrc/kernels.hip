@@ -1115,6 +1115,8 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
 }
 
+constexpr int kPre = 2;  // chunks of 64 tokens per document gathered one document ahead
+
 // D rebuild: per document gather the new topics through the inverted index
 // (doc order -> word-order slot), histogram in a per-wave LDS table of
 // 16-bit counters, and emit ascending packed entries.
@@ -1131,15 +1133,61 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
   for (;;) {
     uint32_t d0 = 0, d1 = 0;
     if (!next_docs(d.counters + CNT_REBUILD_D, p, part, lane, d0, d1)) break;
-    for (uint32_t dd = d0; dd < d1; ++dd) {
-      const uint32_t b = d.doc_off[dd], e = d.doc_off[dd + 1];
-      for (uint32_t pp = b + lane; pp < e; pp += kWave) {
+    const int nd = int(d1 - d0);
+    // the batch's document offsets, one per lane
+    const uint32_t offv = lane <= nd ? d.doc_off[d0 + uint32_t(lane)] : 0u;
+    // two-stage pipeline over the first kPre*64 tokens of each document:
+    // the word-order slots of document i+1 are loaded while document i-1 is
+    // processed, and their topics are gathered while document i is
+    uint32_t wp1[kPre], z0[kPre];
+#pragma unroll
+    for (int c = 0; c < kPre; ++c) {
+      const uint32_t b = __builtin_amdgcn_readlane(offv, 0), e = __builtin_amdgcn_readlane(offv, 1);
+      const uint32_t pp = b + uint32_t(c * kWave + lane);
+      z0[c] = pp < e ? d.z_w[d.dt_wpos[pp]] : 0u;
+      wp1[c] = 0u;
+      if (nd > 1) {
+        const uint32_t bn = __builtin_amdgcn_readlane(offv, 1), en = __builtin_amdgcn_readlane(offv, 2);
+        const uint32_t pn = bn + uint32_t(c * kWave + lane);
+        if (pn < en) wp1[c] = d.dt_wpos[pn];
+      }
+    }
+    for (int i = 0; i < nd; ++i) {
+      const uint32_t b = __builtin_amdgcn_readlane(offv, i), e = __builtin_amdgcn_readlane(offv, i + 1);
+      uint32_t zv[kPre];
+#pragma unroll
+      for (int c = 0; c < kPre; ++c) zv[c] = z0[c];
+      if (i + 1 < nd) {
+        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 1), en = __builtin_amdgcn_readlane(offv, i + 2);
+#pragma unroll
+        for (int c = 0; c < kPre; ++c) {
+          const uint32_t pn = bn + uint32_t(c * kWave + lane);
+          z0[c] = pn < en ? d.z_w[wp1[c]] : 0u;
+        }
+      }
+      if (i + 2 < nd) {
+        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 2), en = __builtin_amdgcn_readlane(offv, i + 3);
+#pragma unroll
+        for (int c = 0; c < kPre; ++c) {
+          const uint32_t pn = bn + uint32_t(c * kWave + lane);
+          wp1[c] = pn < en ? d.dt_wpos[pn] : 0u;
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < kPre; ++c) {
+        if (b + uint32_t(c * kWave + lane) < e) {
+          const uint32_t z = zv[c];
+          if (z < uint32_t(K)) atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
+          else bad++;
+        }
+      }
+      for (uint32_t pp = b + uint32_t(kPre * kWave + lane); pp < e; pp += kWave) {
         const uint32_t z = d.z_w[d.dt_wpos[pp]];
         if (z < uint32_t(K)) atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
         else bad++;
       }
       __threadfence_block();
-      uint32_t *out = d.d_ent + d.d_cap[dd] + 1;
+      uint32_t *out = d.d_ent + d.d_cap[d0 + uint32_t(i)] + 1;
       uint32_t base = 0;
       for (int q0 = 0; q0 < half; q0 += kWave) {
         const int q = q0 + lane;
