@@ -71,7 +71,12 @@ typedef struct {
   /* Disable the step-3 skip test (every token scans its D row).  Ablation
    * switch; the draws are unchanged. */
   int32_t no_skip;
-  int32_t reserved[5];
+  /* Hybrid W cutoff, Sec. 4.2: a word is dense when its token count exceeds
+   * this (0 = default K; negative = every word dense).  Words with more than
+   * 65,535 tokens are always dense (16-bit sparse counts).  Ablation switch;
+   * the draws are unchanged. */
+  int32_t dense_cutoff;
+  int32_t reserved[4];
 } lda_options;
 
 /* Per-iteration statistics (filled by lda_iterate when requested). */
@@ -160,9 +165,10 @@ const char *lda_last_error(const lda_handle *h);
 /*
  * Layout description (host only; touches no device).  Relabels words by
  * descending token count (ties by ascending id), marks a word dense when its
- * count exceeds K (Sec. 4.2), and cuts every word into regions of at most
- * region_tokens consecutive word-ordered tokens (Sec. 5.1).  Arrays may be
- * NULL; sizes first via the scalar outputs.
+ * count exceeds the cutoff (dense_cutoff as in lda_options: 0 = K, Sec. 4.2),
+ * and cuts every dense word into regions of at most region_tokens
+ * consecutive word-ordered tokens (Sec. 5.1).  Arrays may be NULL; sizes
+ * first via the scalar outputs.
  *   relabel[V]      new id of each caller word id (absent words last)
  *   n_present, n_dense, n_regions, n_docs: scalar outputs
  *   word_off[n_present+1]  word-ordered offsets per new id
@@ -170,7 +176,8 @@ const char *lda_last_error(const lda_handle *h);
  *   region[3*n_regions]    (new word id, begin, end) per region
  */
 lda_status lda_describe_layout(const int32_t *word, const int32_t *doc, int64_t n_tokens, int32_t V, int32_t K,
-                               int32_t region_tokens, int32_t *relabel, int32_t *n_present, int32_t *n_dense,
+                               int32_t region_tokens, int32_t dense_cutoff, int32_t *relabel, int32_t *n_present,
+                               int32_t *n_dense,
                                int64_t *n_regions, int32_t *n_docs, uint32_t *word_off, uint32_t *wt_key,
                                uint32_t *region);
 

@@ -30,7 +30,7 @@ FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
 class Options(ctypes.Structure):
     _fields_ = [("stream", ctypes.c_void_p), ("dev_alloc", ALLOC_FN), ("dev_free", FREE_FN),
                 ("alloc_ctx", ctypes.c_void_p), ("g", ctypes.c_int32), ("region_tokens", ctypes.c_int32),
-                ("no_skip", ctypes.c_int32), ("reserved", ctypes.c_int32 * 5)]
+                ("no_skip", ctypes.c_int32), ("dense_cutoff", ctypes.c_int32), ("reserved", ctypes.c_int32 * 4)]
 
 
 class IterStats(ctypes.Structure):
@@ -87,7 +87,7 @@ def load_library():
     lib.lda_destroy.restype = None
     lib.lda_last_error.argtypes = [P]
     lib.lda_last_error.restype = ctypes.c_char_p
-    lib.lda_describe_layout.argtypes = [P, P, I64, I32, I32, I32, P, P, P, P, P, P, P, P]
+    lib.lda_describe_layout.argtypes = [P, P, I64, I32, I32, I32, I32, P, P, P, P, P, P, P, P]
     lib.lda_describe_layout.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -102,7 +102,7 @@ def _check(lib, handle, status):
         raise LDAError(status, lib.lda_last_error(handle).decode())
 
 
-def describe_layout(word, doc, V: int, K: int, region_tokens: int = 0) -> dict:
+def describe_layout(word, doc, V: int, K: int, region_tokens: int = 0, dense_cutoff: int = 0) -> dict:
     """Host-only layout of a token list: relabel, dense prefix, word order and regions (no device)."""
     lib = load_library()
     word = np.ascontiguousarray(word, np.int32)
@@ -110,15 +110,15 @@ def describe_layout(word, doc, V: int, K: int, region_tokens: int = 0) -> dict:
     n = word.shape[0]
     npres, nd, ndocs = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     nreg = ctypes.c_int64()
-    st = lib.lda_describe_layout(_p(word), _p(doc), n, V, K, region_tokens, None, ctypes.byref(npres),
+    st = lib.lda_describe_layout(_p(word), _p(doc), n, V, K, region_tokens, dense_cutoff, None, ctypes.byref(npres),
                                  ctypes.byref(nd), ctypes.byref(nreg), ctypes.byref(ndocs), None, None, None)
     _check(lib, None, st)
     relabel = np.empty(V, np.int32)
     word_off = np.empty(npres.value + 1, np.uint32)
     wt_key = np.empty(n, np.uint32)
     region = np.empty(3 * nreg.value, np.uint32)
-    st = lib.lda_describe_layout(_p(word), _p(doc), n, V, K, region_tokens, _p(relabel), None, None, None, None,
-                                 _p(word_off), _p(wt_key), _p(region))
+    st = lib.lda_describe_layout(_p(word), _p(doc), n, V, K, region_tokens, dense_cutoff, _p(relabel), None, None,
+                                 None, None, _p(word_off), _p(wt_key), _p(region))
     _check(lib, None, st)
     return dict(relabel=relabel, n_present=npres.value, n_dense=nd.value, n_docs=ndocs.value, word_off=word_off,
                 wt_key=wt_key, region=region.reshape(-1, 3))
@@ -129,12 +129,12 @@ class LDA:
 
     ``word``/``doc``: int32 token list (any order); ``V`` vocabulary size, ``K``
     topics, ``alpha``/``beta`` priors of Eq. 1, ``seed`` the Philox key.
-    ``g`` (1 or 2), ``region_tokens`` and ``no_skip`` are the options of
-    ``lda_options``; none of them changes the draws.
+    ``g`` (1 or 2), ``region_tokens``, ``no_skip`` and ``dense_cutoff`` are
+    the options of ``lda_options``; none of them changes the draws.
     """
 
     def __init__(self, word, doc, V: int, K: int, alpha: float, beta: float = 0.01, seed: int = 42, *, g: int = 2,
-                 region_tokens: int = 0, no_skip: bool = False, torch_stream: bool = True,
+                 region_tokens: int = 0, no_skip: bool = False, dense_cutoff: int = 0, torch_stream: bool = True,
                  torch_allocator: bool = True):
         self._lib = load_library()
         self._h = ctypes.c_void_p()
@@ -146,6 +146,7 @@ class LDA:
         opts.g = g
         opts.region_tokens = region_tokens
         opts.no_skip = 1 if no_skip else 0
+        opts.dense_cutoff = dense_cutoff
         self._keep = []
         if torch_stream or torch_allocator:
             import torch

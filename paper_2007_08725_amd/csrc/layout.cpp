@@ -54,7 +54,8 @@ lda_status scan_tokens(const int32_t *word, const int32_t *doc, int64_t n, int32
   return LDA_OK;
 }
 
-lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t R, Layout &L, std::string &msg) {
+lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t R, int32_t dense_cutoff, Layout &L,
+                            std::string &msg) {
   const int32_t V = int32_t(cnt.size());
   const int32_t M = int32_t(L.doc_off.size()) - 1;
   for (int32_t d = 0; d < M; d++) {
@@ -70,12 +71,14 @@ lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t
   L.relabel.assign(size_t(V), 0);
   for (int32_t r = 0; r < V; r++) L.relabel[size_t(order[size_t(r)])] = r;
   int32_t np = 0, nd = 0;
+  const uint32_t cutoff = dense_cutoff == 0 ? uint32_t(K) : dense_cutoff < 0 ? 0u : uint32_t(dense_cutoff);
   for (int32_t r = 0; r < V; r++) {
     const uint32_t c = cnt[size_t(order[size_t(r)])];
     if (c > 0) np++;
-    // dense iff the count exceeds K (Sec. 4.2); a count above 65535 cannot be
-    // packed in a 16-bit sparse entry, so such a word is dense as well
-    if (c > uint32_t(K) || c > 65535u) nd++;
+    // dense iff the count exceeds the cutoff, K by default (Sec. 4.2); a
+    // count above 65535 cannot be packed in a 16-bit sparse entry, so such a
+    // word is dense as well
+    if (c > 0 && (c > cutoff || c > 65535u)) nd++;
   }
   L.n_present = np;
   L.n_dense = nd;
@@ -125,7 +128,7 @@ lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t
 }
 
 lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t K, int32_t R,
-                        Layout &L, std::string &msg) {
+                        int32_t dense_cutoff, Layout &L, std::string &msg) {
   if (K < 2 || R <= 0) {
     msg = "build_layout: bad sizes";
     return LDA_E_ARG;
@@ -146,7 +149,7 @@ lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int3
   for (int32_t d = 0; d < M; d++) L.doc_off[size_t(d) + 1] += L.doc_off[size_t(d)];
   std::vector<uint32_t> cnt(static_cast<size_t>(V), 0u);
   for (int64_t i = 0; i < n; i++) cnt[size_t(word[i])]++;
-  st = plan_from_counts(cnt, K, R, L, msg);
+  st = plan_from_counts(cnt, K, R, dense_cutoff, L, msg);
   if (st != LDA_OK) return st;
 
   // doc order: stable counting sort by document

@@ -135,7 +135,8 @@ lda_status sort_pairs(lda_handle *h, const uint32_t *keys_in, uint32_t *keys_out
 
 // Device layout (Sec. 4.2-4.3, 5.1): both token orders are built with radix
 // sorts on the GPU; only per-word and per-document counts visit the host.
-lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *word, const int32_t *doc, int32_t R) {
+lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *word, const int32_t *doc, int32_t R,
+                         int32_t dense_cutoff) {
   Layout &L = h->L;
   HIP_TRY(h, hipGetDevice(&h->device));
   int cus = 0, lds_max = 0;
@@ -201,7 +202,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   std::vector<uint32_t> cnt(static_cast<size_t>(L.V));
   for (int32_t v = 0; v < L.V; ++v) cnt[size_t(v)] = woff_h[size_t(v) + 1] - woff_h[size_t(v)];
   std::string msg;
-  lda_status st = plan_from_counts(cnt, L.K, R, L, msg);
+  lda_status st = plan_from_counts(cnt, L.K, R, dense_cutoff, L, msg);
   if (st != LDA_OK) return fail(h, st, msg);
   // document ranges of equal token counts for the document kernels, one per XCD
   p.xcd_doc[0] = 0;
@@ -297,7 +298,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   if (K < 2 || K > LDA_MAX_TOPICS) return fail(nullptr, LDA_E_ARG, "K must be in [2, 16384]");
   if (!std::isfinite(alpha) || !(alpha > 0.0)) return fail(nullptr, LDA_E_ARG, "alpha must be finite and positive");
   if (!std::isfinite(beta) || !(beta > 0.0)) return fail(nullptr, LDA_E_ARG, "beta must be finite and positive");
-  int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0;
+  int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0;
   if (opts) {
     if (opts->g != 0 && opts->g != 1 && opts->g != 2) return fail(nullptr, LDA_E_ARG, "g must be 1 or 2");
     if (opts->g) g = opts->g;
@@ -306,6 +307,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
     if ((opts->dev_alloc == nullptr) != (opts->dev_free == nullptr))
       return fail(nullptr, LDA_E_ARG, "dev_alloc and dev_free must be given together");
     no_skip = opts->no_skip ? 1 : 0;
+    dense_cutoff = opts->dense_cutoff;
   }
   lda_handle *h = new (std::nothrow) lda_handle();
   if (!h) return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
@@ -341,7 +343,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   p.no_skip = no_skip;
   p.key_identity = sorted ? 1 : 0;
   try {
-    st = create_device(h, opts, word, doc, R);
+    st = create_device(h, opts, word, doc, R, dense_cutoff);
   } catch (const std::bad_alloc &) {
     st = fail(h, LDA_E_NOMEM, "host allocation failed");
   }
@@ -556,7 +558,8 @@ void lda_destroy(lda_handle *h) { release(h); }
 const char *lda_last_error(const lda_handle *h) { return h ? h->err.c_str() : g_create_error.c_str(); }
 
 lda_status lda_describe_layout(const int32_t *word, const int32_t *doc, int64_t n_tokens, int32_t V, int32_t K,
-                               int32_t region_tokens, int32_t *relabel, int32_t *n_present, int32_t *n_dense,
+                               int32_t region_tokens, int32_t dense_cutoff, int32_t *relabel, int32_t *n_present,
+                               int32_t *n_dense,
                                int64_t *n_regions, int32_t *n_docs, uint32_t *word_off, uint32_t *wt_key,
                                uint32_t *region) {
   if (!word || !doc || n_tokens <= 0 || V <= 0 || K < 2 || K > LDA_MAX_TOPICS || region_tokens < 0)
@@ -565,7 +568,8 @@ lda_status lda_describe_layout(const int32_t *word, const int32_t *doc, int64_t 
   std::string msg;
   lda_status st;
   try {
-    st = build_layout(word, doc, n_tokens, V, K, region_tokens ? region_tokens : kDefaultRegionTokens, L, msg);
+    st = build_layout(word, doc, n_tokens, V, K, region_tokens ? region_tokens : kDefaultRegionTokens, dense_cutoff, L,
+                      msg);
   } catch (const std::bad_alloc &) {
     return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
   }

@@ -64,10 +64,12 @@ lda_status scan_tokens(const int32_t *word, const int32_t *doc, int64_t n, int32
 // From the per-word token counts (caller ids) and L.doc_off: relabel, dense
 // prefix, relabelled word offsets, capacities and regions.  LDA_E_RANGE for a
 // document longer than LDA_MAX_DOC_LEN.
-lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t R, Layout &L, std::string &msg);
+// dense_cutoff as in lda_options (0 = K, negative = all words dense)
+lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t R, int32_t dense_cutoff, Layout &L,
+                            std::string &msg);
 // All-host reference of the layout (lda_describe_layout); fills L.wt_key.
 lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t K, int32_t R,
-                        Layout &L, std::string &msg);
+                        int32_t dense_cutoff, Layout &L, std::string &msg);
 
 // Device layout steps (layout_gpu.hip).
 unsigned bits_for(uint64_t max_value);

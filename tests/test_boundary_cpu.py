@@ -162,6 +162,25 @@ def test_layout_properties(lib, shuffle, R):
             assert rows.shape[0] == -(-(wo[r + 1] - wo[r]) // R)
 
 
+@pytest.mark.parametrize("cutoff", [-1, 3, 40, 1 << 30])
+def test_layout_dense_cutoff(lib, cutoff):
+    """The hybrid-W cutoff: dense iff count > cutoff (0 = K, negative = every present word)."""
+    rng = np.random.default_rng(5)
+    n, V, M, K = 5000, 300, 80, 16
+    word, doc = _layout_case(rng, n, V, M, K, False)
+    L = lda.describe_layout(word, doc, V, K, 100, cutoff)
+    cnt = np.bincount(word, minlength=V)
+    want = int((cnt > 0).sum()) if cutoff < 0 else int((cnt > cutoff).sum())
+    assert L["n_dense"] == want
+    # regions: dense words split into <= R tokens, sparse words whole
+    reg = L["region"].astype(np.int64)
+    wo = L["word_off"].astype(np.int64)
+    for r in range(L["n_present"]):
+        rows = reg[reg[:, 0] == r]
+        assert rows.shape[0] == (-(-(wo[r + 1] - wo[r]) // 100) if r < L["n_dense"] else 1)
+    assert lda.describe_layout(word, doc, V, K, 100, 0)["n_dense"] == int((cnt > K).sum())
+
+
 def test_layout_empty_documents_and_single_token(lib):
     word = np.array([3], np.int32)
     doc = np.array([5], np.int32)   # docs 0..4 are empty

@@ -82,9 +82,11 @@ def test_c1_free_running_trajectory_and_llpt(c1, c1_traj):
 
 
 @pytest.mark.parametrize("opts", [dict(region_tokens=7), dict(region_tokens=100), dict(g=1), dict(no_skip=True),
+                                  dict(dense_cutoff=-1), dict(dense_cutoff=1 << 30), dict(dense_cutoff=3),
                                   dict(torch_allocator=False, torch_stream=False)])
 def test_schedule_invariance(c1, opts):
-    """Region size, S_est depth, the skip test, allocator and stream never change the draws."""
+    """Region size, S_est depth, the skip test, the hybrid-W cutoff (all dense, all sparse),
+    allocator and stream never change the draws."""
     say("invariance %s" % opts)
     with make_lda(c1) as a:
         a.iterate(3)
