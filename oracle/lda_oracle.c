@@ -143,8 +143,8 @@ typedef struct {
   int64_t *T;
   double *den; /* den[k] = T[k] + V*beta */
   /* per-word quantities (sparse form) */
-  int32_t *K1, *K2;
-  double *a1, *a2, *a3, *Qp, *sumWh;
+  int32_t *K1, *K2, *K3;
+  double *a1, *a2, *a3, *a4, *Qp, *sumWh;
 } snap;
 
 static void snap_free(snap *s) {
@@ -157,9 +157,11 @@ static void snap_free(snap *s) {
   free(s->den);
   free(s->K1);
   free(s->K2);
+  free(s->K3);
   free(s->a1);
   free(s->a2);
   free(s->a3);
+  free(s->a4);
   free(s->Qp);
   free(s->sumWh);
   memset(s, 0, sizeof(*s));
@@ -203,19 +205,24 @@ static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *do
   if (!with_words) return 0;
   s->K1 = malloc(sizeof(int32_t) * (size_t)V);
   s->K2 = malloc(sizeof(int32_t) * (size_t)V);
+  s->K3 = malloc(sizeof(int32_t) * (size_t)V);
   s->a1 = malloc(sizeof(double) * (size_t)V);
   s->a2 = malloc(sizeof(double) * (size_t)V);
   s->a3 = malloc(sizeof(double) * (size_t)V);
+  s->a4 = malloc(sizeof(double) * (size_t)V);
   s->Qp = malloc(sizeof(double) * (size_t)V);
   s->sumWh = malloc(sizeof(double) * (size_t)V);
-  if (!s->K1 || !s->K2 || !s->a1 || !s->a2 || !s->a3 || !s->Qp || !s->sumWh) {
+  if (!s->K1 || !s->K2 || !s->K3 || !s->a1 || !s->a2 || !s->a3 || !s->a4 || !s->Qp || !s->sumWh) {
     snap_free(s);
     return 2;
   }
   for (int32_t v = 0; v < V; v++) {
     /* step 1 of the three-branch procedure: top topics of W^[v] (Sec. 3.2).
      * K1 = lowest topic id among the maxima; K2 = lowest id among the maxima
-     * over k != K1; a3 = largest value over k not in {K1, K2} (0 if K < 3). */
+     * over k != K1; K3 = lowest id among the maxima over k not in {K1, K2}
+     * (-1 if K < 3), a3 its value (0 if K < 3); a4 = largest value over k not
+     * in {K1, K2, K3} (0 if K < 4).  a1 >= a2 >= a3 >= a4 feed the S_est of
+     * Eq. 9 for g = 1, 2, 3. */
     int32_t k1 = 0;
     double m1 = what(s, v, 0);
     for (int32_t k = 1; k < K; k++) {
@@ -235,14 +242,24 @@ static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *do
         k2 = k;
       }
     }
+    int32_t k3 = -1;
     double m3 = 0.0;
-    int have3 = 0;
     for (int32_t k = 0; k < K; k++) {
       if (k == k1 || k == k2) continue;
       double w = what(s, v, k);
-      if (!have3 || w > m3) {
+      if (k3 < 0 || w > m3) {
         m3 = w;
-        have3 = 1;
+        k3 = k;
+      }
+    }
+    double m4 = 0.0;
+    int have4 = 0;
+    for (int32_t k = 0; k < K; k++) {
+      if (k == k1 || k == k2 || k == k3) continue;
+      double w = what(s, v, k);
+      if (!have4 || w > m4) {
+        m4 = w;
+        have4 = 1;
       }
     }
     /* Q' = sum over k != K1 of alpha*W^[v][k], ascending (Eq. 5, p_q). */
@@ -254,9 +271,11 @@ static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *do
     }
     s->K1[v] = k1;
     s->K2[v] = k2;
+    s->K3[v] = k3;
     s->a1[v] = m1;
     s->a2[v] = m2;
     s->a3[v] = m3;
+    s->a4[v] = m4;
     s->Qp[v] = q;
     s->sumWh[v] = sw;
   }
@@ -272,10 +291,13 @@ static int32_t dcount(const snap *s, int32_t d, int32_t k) {
 
 static const double BOUNDARY_REL = 1e-9;
 
-/* S_est of Eq. 9 for the depth g used by the statistics (g = 1 or 2). */
-static double s_est(int g, double a2, double a3, int32_t C1, int32_t C2, int64_t len) {
+/* S_est of Eq. 9 for the depth g used by the statistics (g = 1, 2 or 3):
+ * the counts of the top topics K2..Kg times their values, and all other
+ * tokens of the document times the next value a_{g+1}. */
+static double s_est(int g, double a2, double a3, double a4, int32_t C1, int32_t C2, int32_t C3, int64_t len) {
   if (g <= 1) return a2 * (double)(len - C1);
-  return a2 * (double)C2 + a3 * (double)(len - C1 - C2);
+  if (g == 2) return a2 * (double)C2 + a3 * (double)(len - C1 - C2);
+  return a2 * (double)C2 + a3 * (double)C3 + a4 * (double)(len - C1 - C2 - C3);
 }
 
 /* ------------------------------------------------------- sparse draw ---- */
@@ -287,6 +309,7 @@ static int32_t draw_sparse(const snap *s, int g, double u, int64_t i, double *Zo
   const double a1 = s->a1[v];
   const int64_t b = s->doff[d], e = s->doff[d + 1];
   const int32_t C1 = dcount(s, d, K1), C2 = dcount(s, d, s->K2[v]);
+  const int32_t C3 = s->K3[v] >= 0 ? dcount(s, d, s->K3[v]) : 0;
 
   /* max-topic branch, Eq. 7 */
   const double Mm = a1 * ((double)C1 + alpha);
@@ -303,7 +326,7 @@ static int32_t draw_sparse(const snap *s, int g, double u, int64_t i, double *Zo
   const double x = u * Z;
 
   /* step-3 statistics: S' <= S_est (Eq. 8-9) and the skip test */
-  const double Sest = s_est(g, s->a2[v], s->a3[v], C1, C2, s->len[d]);
+  const double Sest = s_est(g, s->a2[v], s->a3[v], s->a4[v], C1, C2, C3, s->len[d]);
   if (sprime > Sest * (1.0 + 1e-12)) st[ORA_ST_SEST_VIOL]++;
   const int skip3 = u * (Mm + Sest + s->Qp[v]) < Mm;
   if (skip3) st[ORA_ST_SKIP3]++;
@@ -379,20 +402,24 @@ static int32_t draw_dense(const snap *s, int g, double u, int64_t i, double *wh,
     wh[k] = what(s, v, k);
   }
   for (int64_t j = s->doff[d]; j < s->doff[d + 1]; j++) Dd[s->dtop[j]] = s->dcnt[j];
-  /* K1, K2, a3 recomputed from the dense row */
+  /* K1, K2, K3, a4 recomputed from the dense row */
   int32_t K1 = 0;
   for (int32_t k = 1; k < K; k++)
     if (wh[k] > wh[K1]) K1 = k;
   int32_t K2 = -1;
   for (int32_t k = 0; k < K; k++)
     if (k != K1 && (K2 < 0 || wh[k] > wh[K2])) K2 = k;
-  double a3 = 0.0;
-  int have3 = 0;
+  int32_t K3 = -1;
   for (int32_t k = 0; k < K; k++)
-    if (k != K1 && k != K2 && (!have3 || wh[k] > a3)) {
-      a3 = wh[k];
-      have3 = 1;
+    if (k != K1 && k != K2 && (K3 < 0 || wh[k] > wh[K3])) K3 = k;
+  double a4 = 0.0;
+  int have4 = 0;
+  for (int32_t k = 0; k < K; k++)
+    if (k != K1 && k != K2 && k != K3 && (!have4 || wh[k] > a4)) {
+      a4 = wh[k];
+      have4 = 1;
     }
+  const double a3 = K3 >= 0 ? wh[K3] : 0.0;
   const double Mm = wh[K1] * ((double)Dd[K1] + alpha);
   double S_end = Mm, sprime = 0.0;
   for (int32_t k = 0; k < K; k++) {
@@ -409,7 +436,7 @@ static int32_t draw_dense(const snap *s, int g, double u, int64_t i, double *wh,
 
   int64_t len = 0;
   for (int32_t k = 0; k < K; k++) len += Dd[k];
-  const double Sest = s_est(g, wh[K2], a3, Dd[K1], Dd[K2], len);
+  const double Sest = s_est(g, wh[K2], a3, a4, Dd[K1], Dd[K2], K3 >= 0 ? Dd[K3] : 0, len);
   if (sprime > Sest * (1.0 + 1e-12)) st[ORA_ST_SEST_VIOL]++;
   const int skip3 = u * (Mm + Sest + Q) < Mm;
   if (skip3) st[ORA_ST_SKIP3]++;
@@ -476,7 +503,7 @@ static int32_t draw_dense(const snap *s, int g, double u, int64_t i, double *wh,
 int ora_iterate(int mode, int g, int64_t n, const int32_t *word, const int32_t *doc, int32_t M, int32_t V, int32_t K,
                 double alpha, double beta, uint64_t seed, uint32_t t, const int32_t *z_in, int64_t n_sub,
                 const int64_t *idx, int32_t *z_out, uint8_t *flags, double *Zout, int64_t *stats) {
-  if ((mode != 0 && mode != 1) || (g != 1 && g != 2) || K < 2 || !(alpha > 0) || !(beta > 0)) return 1;
+  if ((mode != 0 && mode != 1) || g < 1 || g > 3 || K < 2 || !(alpha > 0) || !(beta > 0)) return 1;
   snap s;
   int rc = snap_build(&s, n, word, doc, z_in, M, V, K, alpha, beta, mode == 0);
   if (rc) return rc;

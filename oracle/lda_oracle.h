@@ -56,7 +56,7 @@ enum {
 /* One synchronous iteration from the snapshot of counts built from z_in.
  *   mode 0 = sparse decomposition (scans nz(D[d]), per-word Q' running sum)
  *   mode 1 = dense brute force (all K topics per token, recomputed per token)
- *   g      = depth of the S_est bound used for the skip statistics (1 or 2)
+ *   g      = depth of the S_est bound used for the skip statistics (1, 2 or 3)
  * If idx is NULL every token i in 0..n-1 is drawn into z_out[i]; otherwise
  * only tokens idx[0..n_sub-1], written to z_out[j], flags[j], Zout[j].
  * flags bit0 = near-boundary draw, bit1 = step-3 skip fired.

@@ -219,9 +219,10 @@ def test_dense_and_sparse_forms_bit_identical():
         word, doc, M, V, K = _random_corpus(rng)
         kw = dict(M=M, V=V, K=K, alpha=float(rng.choice([50.0 / K, 0.1, 1.0])), beta=0.01)
         z = ora.init_topics(len(word), K, seed)
+        g = 1 + seed % 3
         for t in range(20):
-            zs, fs, ss, Zs = ora.iterate(word, doc, z, seed=seed, t=t, mode="sparse", want_Z=True, **kw)
-            zd, fd, sd, Zd = ora.iterate(word, doc, z, seed=seed, t=t, mode="dense", want_Z=True, **kw)
+            zs, fs, ss, Zs = ora.iterate(word, doc, z, seed=seed, t=t, mode="sparse", g=g, want_Z=True, **kw)
+            zd, fd, sd, Zd = ora.iterate(word, doc, z, seed=seed, t=t, mode="dense", g=g, want_Z=True, **kw)
             assert np.array_equal(zs, zd) and np.array_equal(fs, fd)
             assert np.array_equal(Zs.view(np.uint64), Zd.view(np.uint64))
             assert ss == sd
@@ -273,20 +274,23 @@ def c1():
 
 
 def test_skip_bound_and_exactness_on_c1(c1):
-    """S' <= S_est on every token and 'skip => K1' on all 10 iterations of c1 (Eq. 8-9)."""
+    """S' <= S_est on every token and 'skip => K1' on all 10 iterations of c1 (Eq. 8-9), for
+    g = 1, 2, 3.  S_est(g+1) - S_est(g) = (a_{g+2} - a_{g+1}) * (the tokens outside K1..K_{g+1})
+    <= 0, so every token that skips at depth g also skips at depth g+1."""
     kw = dict(M=c1.n_docs, V=c1.V, K=c1.K, alpha=c1.alpha, beta=c1.beta)
     z = ora.init_topics(c1.N, c1.K, 42)
     skips = []
     for t in range(10):
-        z1, f1, st1 = ora.iterate(c1.word, c1.doc, z, seed=42, t=t, g=1, **kw)
-        z2, f2, st2 = ora.iterate(c1.word, c1.doc, z, seed=42, t=t, g=2, **kw)
-        assert np.array_equal(z1, z2)       # g changes statistics, never draws
-        for st in (st1, st2):
-            assert st["sest_violations"] == 0 and st["skip_not_k1"] == 0
-        assert st2["skip3"] >= st1["skip3"]  # a tighter bound skips at least as often
-        skips.append(st2["skip3"])
-        assert st2["flagged"] < 1e-3 * c1.N
-        z = z2
+        runs = [ora.iterate(c1.word, c1.doc, z, seed=42, t=t, g=g, **kw) for g in (1, 2, 3)]
+        for zg, fg, stg in runs:
+            assert np.array_equal(zg, runs[1][0])  # g changes statistics, never draws
+            assert stg["sest_violations"] == 0 and stg["skip_not_k1"] == 0
+        for (_, fa, sa), (_, fb, sb) in zip(runs, runs[1:]):
+            assert sb["skip3"] >= sa["skip3"]      # a tighter bound skips at least as often
+            assert np.all((fb & 2) >= (fa & 2))    # token by token
+        skips.append(runs[1][2]["skip3"])
+        assert runs[1][2]["flagged"] < 1e-3 * c1.N
+        z = runs[1][0]
     assert skips[-1] > skips[0]
 
 
