@@ -63,7 +63,7 @@ typedef struct {
   void *(*dev_alloc)(size_t bytes, void *ctx);
   void (*dev_free)(void *ptr, void *ctx);
   void *alloc_ctx;
-  /* Depth g of the S_est bound, Eq. 9: 1 or 2 (0 = default 2, Sec. 3.2
+  /* Depth g of the S_est bound, Eq. 9: 1, 2 or 3 (0 = default 2, Sec. 3.2
    * "Parameter tuning").  Changes which tokens skip the S' scan, never the draw. */
   int32_t g;
   /* Large-word split: tokens per region, Sec. 5.1 (0 = default 10,000). */

@@ -8,8 +8,10 @@ caching device allocator.  If the library is not built, constructing an
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import weakref
 
 import numpy as np
 
@@ -124,12 +126,22 @@ def describe_layout(word, doc, V: int, K: int, region_tokens: int = 0, dense_cut
                 wt_key=wt_key, region=region.reshape(-1, 3))
 
 
+_LIVE = weakref.WeakSet()
+
+
+@atexit.register
+def _close_all():
+    """Destroy the handles still open at exit, while torch's allocator can take their memory back."""
+    for m in list(_LIVE):
+        m.close()
+
+
 class LDA:
     """One sampler on the current HIP device.
 
     ``word``/``doc``: int32 token list (any order); ``V`` vocabulary size, ``K``
     topics, ``alpha``/``beta`` priors of Eq. 1, ``seed`` the Philox key.
-    ``g`` (1 or 2), ``region_tokens``, ``no_skip`` and ``dense_cutoff`` are
+    ``g`` (1, 2 or 3), ``region_tokens``, ``no_skip`` and ``dense_cutoff`` are
     the options of ``lda_options``; none of them changes the draws.
     """
 
@@ -164,7 +176,9 @@ class LDA:
                         return None
 
                 def _free(ptr, ctx):
-                    torch.cuda.caching_allocator_delete(ptr)
+                    cuda = getattr(torch, "cuda", None)  # None while the interpreter shuts down
+                    if cuda is not None:
+                        cuda.caching_allocator_delete(ptr)
 
                 fa, ff = ALLOC_FN(_alloc), FREE_FN(_free)
                 self._keep += [fa, ff]
@@ -172,6 +186,7 @@ class LDA:
         st = self._lib.lda_create(_p(word), _p(doc), self.N, self.V, self.K, self.alpha, self.beta, self.seed,
                                   ctypes.byref(opts), ctypes.byref(self._h))
         _check(self._lib, None, st)
+        _LIVE.add(self)
 
     # -- lifetime ---------------------------------------------------------
     def close(self):

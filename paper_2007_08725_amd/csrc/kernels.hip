@@ -103,28 +103,33 @@ __device__ __forceinline__ double row_incl_scan(double v) {
   return v;
 }
 
-struct Top3 {
-  double v[3];
-  uint32_t k[3];
+constexpr int kTop = 4;  // top values of W^[v] kept per word (a1..a4 of Eq. 9, g <= 3)
+
+struct TopN {
+  double v[kTop];
+  uint32_t k[kTop];
 };
 
 __device__ __forceinline__ bool better(double va, uint32_t ka, double vb, uint32_t kb) {
   return va > vb || (va == vb && ka < kb);
 }
 
-__device__ __forceinline__ void top3_insert(Top3 &t, double v, uint32_t k) {
-  if (!better(v, k, t.v[2], t.k[2])) return;
-  t.v[2] = v;
-  t.k[2] = k;
-  if (better(t.v[2], t.k[2], t.v[1], t.k[1])) {
-    double tv = t.v[1]; uint32_t tk = t.k[1];
-    t.v[1] = t.v[2]; t.k[1] = t.k[2];
-    t.v[2] = tv; t.k[2] = tk;
-  }
-  if (better(t.v[1], t.k[1], t.v[0], t.k[0])) {
-    double tv = t.v[0]; uint32_t tk = t.k[0];
-    t.v[0] = t.v[1]; t.k[0] = t.k[1];
-    t.v[1] = tv; t.k[1] = tk;
+// Insert (v, k) into a list kept in order of `better` (value descending,
+// lowest topic id first among equal values).
+__device__ __forceinline__ void top_insert(TopN &t, double v, uint32_t k) {
+  if (!better(v, k, t.v[kTop - 1], t.k[kTop - 1])) return;
+  t.v[kTop - 1] = v;
+  t.k[kTop - 1] = k;
+#pragma unroll
+  for (int q = kTop - 1; q > 0; --q) {
+    if (better(t.v[q], t.k[q], t.v[q - 1], t.k[q - 1])) {
+      const double tv = t.v[q - 1];
+      const uint32_t tk = t.k[q - 1];
+      t.v[q - 1] = t.v[q];
+      t.k[q - 1] = t.k[q];
+      t.v[q] = tv;
+      t.k[q] = tk;
+    }
   }
 }
 
@@ -206,8 +211,8 @@ __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den
 __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
   const int r = blockIdx.x, tid = threadIdx.x;
   const int K = p.K;
-  __shared__ double sv[kBlock * 3];
-  __shared__ uint32_t sk[kBlock * 3];
+  __shared__ double sv[kBlock * kTop];
+  __shared__ uint32_t sk[kBlock * kTop];
   __shared__ double scratch[kBlock / kWave];
   const bool dense = r < p.n_dense;
   const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
@@ -222,41 +227,41 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
   const int cs = (K + kBlock - 1) / kBlock;
   const int c0 = min(K, tid * cs), c1 = min(K, c0 + cs);
 
-  Top3 t;
-  for (int q = 0; q < 3; ++q) {
+  TopN t;
+  for (int q = 0; q < kTop; ++q) {
     t.v[q] = -1.0;
     t.k[q] = 0xFFFFFFFFu;
   }
   if (dense) {
-    for (int k = tid; k < K; k += kBlock) top3_insert(t, what(uint32_t(wrow[k]), p.beta, d.den[k]), uint32_t(k));
+    for (int k = tid; k < K; k += kBlock) top_insert(t, what(uint32_t(wrow[k]), p.beta, d.den[k]), uint32_t(k));
   } else {
     uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
     for (int k = c0; k < c1; ++k) {
       uint32_t c = 0;
       if (e < nnz && (ents[e] >> 16) == uint32_t(k)) c = ents[e++] & 0xFFFFu;
-      top3_insert(t, what(c, p.beta, d.den[k]), uint32_t(k));
+      top_insert(t, what(c, p.beta, d.den[k]), uint32_t(k));
     }
   }
-  for (int q = 0; q < 3; ++q) {
-    sv[tid * 3 + q] = t.v[q];
-    sk[tid * 3 + q] = t.k[q];
+  for (int q = 0; q < kTop; ++q) {
+    sv[tid * kTop + q] = t.v[q];
+    sk[tid * kTop + q] = t.k[q];
   }
   __syncthreads();
   for (int stride = kBlock / 2; stride > 0; stride >>= 1) {
     if (tid < stride) {
-      for (int q = 0; q < 3; ++q) top3_insert(t, sv[(tid + stride) * 3 + q], sk[(tid + stride) * 3 + q]);
+      for (int q = 0; q < kTop; ++q) top_insert(t, sv[(tid + stride) * kTop + q], sk[(tid + stride) * kTop + q]);
     }
     __syncthreads();
     if (tid < stride) {
-      for (int q = 0; q < 3; ++q) {
-        sv[tid * 3 + q] = t.v[q];
-        sk[tid * 3 + q] = t.k[q];
+      for (int q = 0; q < kTop; ++q) {
+        sv[tid * kTop + q] = t.v[q];
+        sk[tid * kTop + q] = t.k[q];
       }
     }
     __syncthreads();
   }
-  const uint32_t K1 = sk[0], K2 = sk[1];
-  const double a1 = sv[0], a2 = sv[1], a3 = K >= 3 ? sv[2] : 0.0;
+  const uint32_t K1 = sk[0], K2 = sk[1], K3 = K >= 3 ? sk[2] : 0xFFFFFFFFu;
+  const double a1 = sv[0], a2 = sv[1], a3 = K >= 3 ? sv[2] : 0.0, a4 = K >= 4 ? sv[3] : 0.0;
 
   double q = 0.0, sw = 0.0;
   if (dense) {
@@ -289,10 +294,13 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
     d.wrec[r] = rec;
     SkipRec sr;
     sr.k12 = K1 | (K2 << 16);
+    sr.k3 = K3;
     sr.a1 = float(a1);
     sr.a2 = float(a2);
     sr.a3 = float(a3);
+    sr.a4 = float(a4);
     sr.qp = float(q);
+    sr.pad = 0u;
     d.wskip[r] = sr;
   }
 }
@@ -387,8 +395,15 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
         // its draw is K1 (S' <= S_est, Eq. 8-9).
         const float u = float(uniform_draw(p.seed, t, key));
         const float Mm = rec.a1 * (float(C1) + p.alpha_f);
-        const float Sest = p.g == 1 ? rec.a2 * float(len - C1)
-                                    : rec.a2 * float(C2) + rec.a3 * float(len - C1 - C2);
+        float Sest;
+        if (p.g == 1) {
+          Sest = rec.a2 * float(len - C1);
+        } else if (p.g == 2) {
+          Sest = rec.a2 * float(C2) + rec.a3 * float(len - C1 - C2);
+        } else {
+          const uint32_t C3 = rec.k3 < uint32_t(K) ? uint32_t(cmap[rec.k3]) : 0u;
+          Sest = rec.a2 * float(C2) + rec.a3 * float(C3) + rec.a4 * float(len - C1 - C2 - C3);
+        }
         const bool skip = !p.no_skip && (u * ((Mm + Sest) + rec.qp) < Mm * (1.0f - 0x1p-15f));
         if (skip) d.z_w[d.dt_wpos[pp]] = uint16_t(K1);
         nskip += skip ? 1ull : 0ull;

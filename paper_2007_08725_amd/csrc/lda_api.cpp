@@ -300,7 +300,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   if (!std::isfinite(beta) || !(beta > 0.0)) return fail(nullptr, LDA_E_ARG, "beta must be finite and positive");
   int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0;
   if (opts) {
-    if (opts->g != 0 && opts->g != 1 && opts->g != 2) return fail(nullptr, LDA_E_ARG, "g must be 1 or 2");
+    if (opts->g < 0 || opts->g > 3) return fail(nullptr, LDA_E_ARG, "g must be 1, 2 or 3");
     if (opts->g) g = opts->g;
     if (opts->region_tokens < 0) return fail(nullptr, LDA_E_ARG, "region_tokens must be >= 0");
     if (opts->region_tokens) R = opts->region_tokens;

@@ -81,7 +81,7 @@ def test_c1_free_running_trajectory_and_llpt(c1, c1_traj):
     assert ll > ll0
 
 
-@pytest.mark.parametrize("opts", [dict(region_tokens=7), dict(region_tokens=100), dict(g=1), dict(no_skip=True),
+@pytest.mark.parametrize("opts", [dict(region_tokens=7), dict(region_tokens=100), dict(g=1), dict(g=3), dict(no_skip=True),
                                   dict(dense_cutoff=-1), dict(dense_cutoff=1 << 30), dict(dense_cutoff=3),
                                   dict(torch_allocator=False, torch_stream=False)])
 def test_schedule_invariance(c1, opts):
@@ -95,6 +95,21 @@ def test_schedule_invariance(c1, opts):
         b.iterate(3)
         zb = b.counts(D=False, W=False)["z"]
     assert np.array_equal(za, zb)
+
+
+@pytest.mark.parametrize("g", [1, 3])
+def test_skip_counts_follow_the_oracle_for_every_depth(c1, c1_traj, g):
+    """Step-3 skips at S_est depth g (Eq. 9) against the oracle's fp64 test on the same
+    snapshots: the GPU's single-precision test with its margin skips a few tokens fewer,
+    never more."""
+    with make_lda(c1, g=g) as m:
+        for t in range(3):
+            z = c1_traj[t][0]
+            zo, flags, ost = oracle_step(c1, z, t, g=g)
+            m.set_assignments(z, t)
+            st = m.iterate(1, stats=True)[0]
+            compare_draws(m.counts(D=False, W=False)["z"], zo, flags, c1.N)
+            assert 0 <= ost["skip3"] - st["skip_step3"] <= max(2, 1e-3 * c1.N)
 
 
 def test_determinism_and_resume(c1):
