@@ -111,8 +111,14 @@ def build_counts(word, doc, z, M: int, V: int, K: int) -> dict:
     return out
 
 
+def _mode(mode: str, branches: int) -> int:
+    if mode not in ("sparse", "dense") or branches not in (2, 3):
+        raise ValueError("mode must be 'sparse' or 'dense', branches 2 or 3")
+    return (1 if mode == "dense" else 0) | (2 if branches == 2 else 0)
+
+
 def iterate(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float, seed: int, t: int,
-            mode: str = "sparse", g: int = 2, idx=None, want_Z: bool = False):
+            mode: str = "sparse", g: int = 2, idx=None, want_Z: bool = False, branches: int = 3):
     """One synchronous iteration from the snapshot built from ``z``.
 
     Returns ``(z_new, flags, stats[, Z])``; with ``idx`` only those tokens are
@@ -131,7 +137,7 @@ def iterate(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float, 
     flags = np.empty(m, np.uint8)
     Z = np.empty(m, np.float64) if want_Z else None
     stats = np.zeros(8, np.int64)
-    rc = lib.ora_iterate(0 if mode == "sparse" else 1, g, n, _p(word), _p(doc), M, V, K, alpha, beta, seed, t, _p(z),
+    rc = lib.ora_iterate(_mode(mode, branches), g, n, _p(word), _p(doc), M, V, K, alpha, beta, seed, t, _p(z),
                          m if idx is not None else 0, _p(idx), _p(z_out), _p(flags), _p(Z), _p(stats))
     if rc:
         raise ValueError("ora_iterate failed (%d)" % rc)
@@ -171,12 +177,12 @@ def run(word, doc, *, M: int, V: int, K: int, alpha: float, beta: float, seed: i
 
 
 def draw_given_u(word, doc, z, i: int, u: float, *, M: int, V: int, K: int, alpha: float, beta: float,
-                 mode: str = "sparse"):
+                 mode: str = "sparse", branches: int = 3):
     """Draw token ``i`` of the snapshot built from ``z`` with the uniform ``u``.  Returns (topic, Z, flag)."""
     word, doc, z = _i32(word), _i32(doc), _i32(z)
     Z = ctypes.c_double(0.0)
     f = ctypes.c_uint8(0)
-    k = _load().ora_draw_given_u(0 if mode == "sparse" else 1, word.shape[0], _p(word), _p(doc), _p(z), M, V, K,
+    k = _load().ora_draw_given_u(_mode(mode, branches), word.shape[0], _p(word), _p(doc), _p(z), M, V, K,
                                  alpha, beta, i, u, ctypes.byref(Z), ctypes.byref(f))
     if k < 0:
         raise ValueError("ora_draw_given_u: bad argument")

@@ -144,7 +144,7 @@ typedef struct {
   double *den; /* den[k] = T[k] + V*beta */
   /* per-word quantities (sparse form) */
   int32_t *K1, *K2, *K3;
-  double *a1, *a2, *a3, *a4, *Qp, *sumWh;
+  double *a1, *a2, *a3, *a4, *Qp, *Qall, *sumWh;
 } snap;
 
 static void snap_free(snap *s) {
@@ -163,6 +163,7 @@ static void snap_free(snap *s) {
   free(s->a3);
   free(s->a4);
   free(s->Qp);
+  free(s->Qall);
   free(s->sumWh);
   memset(s, 0, sizeof(*s));
 }
@@ -211,8 +212,9 @@ static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *do
   s->a3 = malloc(sizeof(double) * (size_t)V);
   s->a4 = malloc(sizeof(double) * (size_t)V);
   s->Qp = malloc(sizeof(double) * (size_t)V);
+  s->Qall = malloc(sizeof(double) * (size_t)V);
   s->sumWh = malloc(sizeof(double) * (size_t)V);
-  if (!s->K1 || !s->K2 || !s->K3 || !s->a1 || !s->a2 || !s->a3 || !s->a4 || !s->Qp || !s->sumWh) {
+  if (!s->K1 || !s->K2 || !s->K3 || !s->a1 || !s->a2 || !s->a3 || !s->a4 || !s->Qp || !s->Qall || !s->sumWh) {
     snap_free(s);
     return 2;
   }
@@ -262,11 +264,13 @@ static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *do
         have4 = 1;
       }
     }
-    /* Q' = sum over k != K1 of alpha*W^[v][k], ascending (Eq. 5, p_q). */
-    double q = 0.0, sw = 0.0;
+    /* Q' = sum over k != K1 of alpha*W^[v][k], ascending (Eq. 5, p_q); the
+     * two-branch Q sums every k (Sec. 2.2). */
+    double q = 0.0, qa = 0.0, sw = 0.0;
     for (int32_t k = 0; k < K; k++) {
       double w = what(s, v, k);
       sw += w;
+      qa += alpha * w;
       if (k != k1) q += alpha * w;
     }
     s->K1[v] = k1;
@@ -277,6 +281,7 @@ static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *do
     s->a3[v] = m3;
     s->a4[v] = m4;
     s->Qp[v] = q;
+    s->Qall[v] = qa;
     s->sumWh[v] = sw;
   }
   return 0;
@@ -498,20 +503,129 @@ static int32_t draw_dense(const snap *s, int g, double u, int64_t i, double *wh,
   return pick;
 }
 
+/* ---------------------------------------------------- two-branch draw ---- */
+/* The two-branch form of Eq. 1 (Sec. 2.2): p = D o W^ (the S part, over
+ * nz(D[d])) + alpha o W^ (the Q part, over every topic), drawn by one
+ * forward inverse CDF over [S terms, topics ascending | Q terms, topics
+ * ascending] with a strict "x < running sum" test.  There is no max-topic
+ * branch and no skip test; this is the ablation of the three-branch split. */
+
+static uint8_t boundary_flag(double x, double lo, double hi, double Z) {
+  return fmin(x - lo, hi - x) < BOUNDARY_REL * Z ? 1 : 0;
+}
+
+static int32_t draw2_sparse(const snap *s, double u, int64_t i, double *Zo, uint8_t *flag, int64_t *st) {
+  const int32_t v = s->word[i], d = s->doc[i], K = s->K;
+  const double alpha = s->alpha;
+  const int64_t b = s->doff[d], e = s->doff[d + 1];
+  double S = 0.0;
+  for (int64_t j = b; j < e; j++) S += (double)s->dcnt[j] * what(s, v, s->dtop[j]);
+  const double Z = S + s->Qall[v];
+  const double x = u * Z;
+  st[ORA_ST_NNZ_SCANNED] += e - b;
+  int32_t pick = -1;
+  double lo = 0.0, hi = 0.0, prev = 0.0;
+  for (int64_t j = b; j < e && pick < 0; j++) {
+    const double cur = prev + (double)s->dcnt[j] * what(s, v, s->dtop[j]);
+    if (x < cur) {
+      pick = s->dtop[j];
+      lo = prev;
+      hi = cur;
+    }
+    prev = cur;
+  }
+  if (pick < 0) {
+    double q = 0.0;
+    for (int32_t k = 0; k < K && pick < 0; k++) {
+      const double qb = q;
+      q += alpha * what(s, v, k);
+      if (x < S + q) {
+        pick = k;
+        lo = S + qb;
+        hi = S + q;
+      }
+    }
+    if (pick < 0) {
+      /* x >= Z after rounding: the last segment (Q terms are all positive) */
+      pick = K - 1;
+      lo = S + (q - alpha * what(s, v, K - 1));
+      hi = Z;
+      st[ORA_ST_FALLBACK]++;
+    }
+  }
+  const uint8_t f = boundary_flag(x, lo, hi, Z);
+  if (f) st[ORA_ST_FLAGGED]++;
+  *Zo = Z;
+  *flag = f;
+  return pick;
+}
+
+static int32_t draw2_dense(const snap *s, double u, int64_t i, double *wh, int32_t *Dd, double *Zo, uint8_t *flag,
+                           int64_t *st) {
+  const int32_t v = s->word[i], d = s->doc[i], K = s->K;
+  const double alpha = s->alpha;
+  for (int32_t k = 0; k < K; k++) {
+    Dd[k] = 0;
+    wh[k] = what(s, v, k);
+  }
+  for (int64_t j = s->doff[d]; j < s->doff[d + 1]; j++) Dd[s->dtop[j]] = s->dcnt[j];
+  double S = 0.0, Q = 0.0;
+  for (int32_t k = 0; k < K; k++) S += (double)Dd[k] * wh[k];
+  for (int32_t k = 0; k < K; k++) Q += alpha * wh[k];
+  const double Z = S + Q;
+  const double x = u * Z;
+  st[ORA_ST_NNZ_SCANNED] += s->doff[d + 1] - s->doff[d];
+  int32_t pick = -1;
+  double lo = 0.0, hi = 0.0, prev = 0.0;
+  for (int32_t k = 0; k < K && pick < 0; k++) {
+    const double cur = prev + (double)Dd[k] * wh[k];
+    if (x < cur) {
+      pick = k;
+      lo = prev;
+      hi = cur;
+    }
+    prev = cur;
+  }
+  if (pick < 0) {
+    double q = 0.0;
+    for (int32_t k = 0; k < K && pick < 0; k++) {
+      const double qb = q;
+      q += alpha * wh[k];
+      if (x < S + q) {
+        pick = k;
+        lo = S + qb;
+        hi = S + q;
+      }
+    }
+    if (pick < 0) {
+      pick = K - 1;
+      lo = S + (q - alpha * wh[K - 1]);
+      hi = Z;
+      st[ORA_ST_FALLBACK]++;
+    }
+  }
+  const uint8_t f = boundary_flag(x, lo, hi, Z);
+  if (f) st[ORA_ST_FLAGGED]++;
+  *Zo = Z;
+  *flag = f;
+  return pick;
+}
+
 /* ---------------------------------------------------------- iterate ---- */
 
 int ora_iterate(int mode, int g, int64_t n, const int32_t *word, const int32_t *doc, int32_t M, int32_t V, int32_t K,
                 double alpha, double beta, uint64_t seed, uint32_t t, const int32_t *z_in, int64_t n_sub,
                 const int64_t *idx, int32_t *z_out, uint8_t *flags, double *Zout, int64_t *stats) {
-  if ((mode != 0 && mode != 1) || g < 1 || g > 3 || K < 2 || !(alpha > 0) || !(beta > 0)) return 1;
+  if (mode < 0 || mode > 3 || g < 1 || g > 3 || K < 2 || !(alpha > 0) || !(beta > 0)) return 1;
+  const int dense = mode & 1, two = mode & 2;
   snap s;
-  int rc = snap_build(&s, n, word, doc, z_in, M, V, K, alpha, beta, mode == 0);
+  int rc = snap_build(&s, n, word, doc, z_in, M, V, K, alpha, beta, !dense);
   if (rc) return rc;
   int64_t st[ORA_N_STATS];
   memset(st, 0, sizeof(st));
   double *wh = NULL;
   int32_t *Dd = NULL;
-  if (mode == 1) {
+  if (dense) {
     wh = malloc(sizeof(double) * (size_t)K);
     Dd = malloc(sizeof(int32_t) * (size_t)K);
     if (!wh || !Dd) {
@@ -531,7 +645,9 @@ int ora_iterate(int mode, int g, int64_t n, const int32_t *word, const int32_t *
     double Z;
     uint8_t f;
     const double u = ora_uniform(seed, t, (uint64_t)i);
-    int32_t k = mode == 0 ? draw_sparse(&s, g, u, i, &Z, &f, st) : draw_dense(&s, g, u, i, wh, Dd, &Z, &f, st);
+    int32_t k;
+    if (two) k = dense ? draw2_dense(&s, u, i, wh, Dd, &Z, &f, st) : draw2_sparse(&s, u, i, &Z, &f, st);
+    else k = dense ? draw_dense(&s, g, u, i, wh, Dd, &Z, &f, st) : draw_sparse(&s, g, u, i, &Z, &f, st);
     z_out[j] = k;
     if (flags) flags[j] = f;
     if (Zout) Zout[j] = Z;
@@ -597,18 +713,20 @@ int ora_word_stats(int64_t n, const int32_t *word, const int32_t *doc, const int
 int32_t ora_draw_given_u(int mode, int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M,
                          int32_t V, int32_t K, double alpha, double beta, int64_t i, double u, double *Z,
                          uint8_t *flag) {
-  if ((mode != 0 && mode != 1) || K < 2 || i < 0 || i >= n || !(u >= 0.0 && u < 1.0)) return -1;
+  if (mode < 0 || mode > 3 || K < 2 || i < 0 || i >= n || !(u >= 0.0 && u < 1.0)) return -1;
+  const int dense = mode & 1, two = mode & 2;
   snap s;
-  if (snap_build(&s, n, word, doc, z, M, V, K, alpha, beta, mode == 0)) return -1;
+  if (snap_build(&s, n, word, doc, z, M, V, K, alpha, beta, !dense)) return -1;
   int64_t st[ORA_N_STATS];
   memset(st, 0, sizeof(st));
   int32_t k;
-  if (mode == 0) {
-    k = draw_sparse(&s, 2, u, i, Z, flag, st);
+  if (!dense) {
+    k = two ? draw2_sparse(&s, u, i, Z, flag, st) : draw_sparse(&s, 2, u, i, Z, flag, st);
   } else {
     double *wh = malloc(sizeof(double) * (size_t)K);
     int32_t *Dd = malloc(sizeof(int32_t) * (size_t)K);
-    k = (wh && Dd) ? draw_dense(&s, 2, u, i, wh, Dd, Z, flag, st) : -1;
+    k = (wh && Dd) ? (two ? draw2_dense(&s, u, i, wh, Dd, Z, flag, st) : draw_dense(&s, 2, u, i, wh, Dd, Z, flag, st))
+                   : -1;
     free(wh);
     free(Dd);
   }

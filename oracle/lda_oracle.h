@@ -54,8 +54,11 @@ enum {
 };
 
 /* One synchronous iteration from the snapshot of counts built from z_in.
- *   mode 0 = sparse decomposition (scans nz(D[d]), per-word Q' running sum)
- *   mode 1 = dense brute force (all K topics per token, recomputed per token)
+ *   mode bit 0: 0 = sparse decomposition (scans nz(D[d]), per-word Q' running
+ *               sum), 1 = dense brute force (all K topics per token)
+ *   mode bit 1: 0 = three-branch canonical order [K1 | S' | Q'] (Eq. 5),
+ *               1 = two-branch order [S | Q] of Sec. 2.2 (no max-topic
+ *               branch, no skip statistics; the ablation)
  *   g      = depth of the S_est bound used for the skip statistics (1, 2 or 3)
  * If idx is NULL every token i in 0..n-1 is drawn into z_out[i]; otherwise
  * only tokens idx[0..n_sub-1], written to z_out[j], flags[j], Zout[j].

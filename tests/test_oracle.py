@@ -30,15 +30,20 @@ def _counts_np(word, doc, z, M, V, K):
     return D, W, W.sum(axis=0)
 
 
-def _eq1_layout(word, doc, z, M, V, K, alpha, beta, i):
-    """Canonical segments [K1 | S' asc | Q' asc] written from Eq. 1 and Eq. 5 with numpy."""
+def _eq1_layout(word, doc, z, M, V, K, alpha, beta, i, branches=3):
+    """Canonical segments written from Eq. 1 with numpy: [K1 | S' asc | Q' asc] of Eq. 5, or the
+    two-branch [S asc | Q asc] of Sec. 2.2."""
     D, W, T = _counts_np(word, doc, z, M, V, K)
     wh = (W[word[i]] + beta) / (T + V * beta)
     d = doc[i]
-    k1 = int(np.argmax(wh))  # first maximum = lowest topic id
-    segs = [(k1, (D[d, k1] + alpha) * wh[k1])]
-    segs += [(k, D[d, k] * wh[k]) for k in range(K) if k != k1 and D[d, k] > 0]
-    segs += [(k, alpha * wh[k]) for k in range(K) if k != k1]
+    if branches == 3:
+        k1 = int(np.argmax(wh))  # first maximum = lowest topic id
+        segs = [(k1, (D[d, k1] + alpha) * wh[k1])]
+        segs += [(k, D[d, k] * wh[k]) for k in range(K) if k != k1 and D[d, k] > 0]
+        segs += [(k, alpha * wh[k]) for k in range(K) if k != k1]
+    else:
+        segs = [(k, D[d, k] * wh[k]) for k in range(K) if D[d, k] > 0]
+        segs += [(k, alpha * wh[k]) for k in range(K)]
     p = (D[d] + alpha) * wh  # Eq. 1 numerator
     return segs, p / p.sum()
 
@@ -107,6 +112,12 @@ def test_worked_example_what_and_two_branch(wex):
     assert k == pr["new_topic"]
     kd, Zd, flagd = ora.draw_given_u(word, doc, z, wex["token_index"], u, mode="dense", **kw)
     assert (kd, Zd, flagd) == (k, Z, flag)
+    # the two-branch form, drawn forward over [S | Q]: x = u*(S+Q) lies past S and falls into
+    # Q at the same topic, with the same total
+    k2, Z2, _ = ora.draw_given_u(word, doc, z, wex["token_index"], u, branches=2, **kw)
+    assert k2 == pr["new_topic"]
+    assert Z2 == pytest.approx(S + Q, rel=1e-12) and Z2 == pytest.approx(Z, rel=1e-12)
+    assert u * Z2 > S and u * Z2 - S < q[pr["new_topic"]] and u * Z2 - S >= q[pr["new_topic"] - 1]
 
 
 def test_worked_example_three_branch(wex):
@@ -164,9 +175,11 @@ def test_uniform_and_init_are_uniform():
 
 # --------------------------------------------------------- closed form, Eq. 1
 
+@pytest.mark.parametrize("branches", [3, 2])
 @pytest.mark.parametrize("mode", ["sparse", "dense"])
-def test_canonical_layout_from_eq1(mode):
-    """Every segment of [K1 | S' | Q'] built from Eq. 1/5 maps to its topic; edges are flagged."""
+def test_canonical_layout_from_eq1(mode, branches):
+    """Every segment of [K1 | S' | Q'] (or the two-branch [S | Q]) built from Eq. 1 maps to its
+    topic; edges are flagged."""
     cases = [_tiny_case()]
     rng = np.random.default_rng(17)
     for _ in range(6):
@@ -175,31 +188,33 @@ def test_canonical_layout_from_eq1(mode):
         cases.append((word, doc, z, dict(M=M, V=V, K=K, alpha=float(rng.uniform(0.05, 3)), beta=0.01)))
     for word, doc, z, kw in cases:
         for i in range(len(word)):
-            segs, _ = _eq1_layout(word, doc, z, kw["M"], kw["V"], kw["K"], kw["alpha"], kw["beta"], i)
+            segs, _ = _eq1_layout(word, doc, z, kw["M"], kw["V"], kw["K"], kw["alpha"], kw["beta"], i, branches)
             w = np.array([s[1] for s in segs])
             cum = np.concatenate([[0.0], np.cumsum(w)])
             Z = cum[-1]
             for j, (k, width) in enumerate(segs):
                 if width <= 1e-6 * Z:
                     continue
-                got, Zo, flag = ora.draw_given_u(word, doc, z, i, 0.5 * (cum[j] + cum[j + 1]) / Z, mode=mode, **kw)
+                got, Zo, flag = ora.draw_given_u(word, doc, z, i, 0.5 * (cum[j] + cum[j + 1]) / Z, mode=mode,
+                                                 branches=branches, **kw)
                 assert got == k and not (flag & 1)
                 assert Zo == pytest.approx(Z, rel=1e-12)
             # a draw exactly on an inner edge is flagged as near-boundary
             j = 1
             if cum[j] / Z < 1.0:
-                _, _, flag = ora.draw_given_u(word, doc, z, i, cum[j] / Z, mode=mode, **kw)
+                _, _, flag = ora.draw_given_u(word, doc, z, i, cum[j] / Z, mode=mode, branches=branches, **kw)
                 assert flag & 1
 
 
-def test_chi2_against_closed_form():
+@pytest.mark.parametrize("branches", [3, 2])
+def test_chi2_against_closed_form(branches):
     """10^6 Philox-driven draws on the 3-doc/5-word/4-topic case vs Eq. 1 (chi-square, p = 0.001)."""
     word, doc, z, kw = _tiny_case()
     n = len(word)
     iters = 1_000_000 // n + 1
     hist = np.zeros((n, kw["K"]), np.int64)
     for t in range(iters):
-        zn, _, _ = ora.iterate(word, doc, z, seed=2024, t=t, **kw)
+        zn, _, _ = ora.iterate(word, doc, z, seed=2024, t=t, branches=branches, **kw)
         hist[np.arange(n), zn] += 1
     total = 0.0
     for i in range(n):
@@ -220,9 +235,12 @@ def test_dense_and_sparse_forms_bit_identical():
         kw = dict(M=M, V=V, K=K, alpha=float(rng.choice([50.0 / K, 0.1, 1.0])), beta=0.01)
         z = ora.init_topics(len(word), K, seed)
         g = 1 + seed % 3
+        br = 2 if seed % 4 == 3 else 3
         for t in range(20):
-            zs, fs, ss, Zs = ora.iterate(word, doc, z, seed=seed, t=t, mode="sparse", g=g, want_Z=True, **kw)
-            zd, fd, sd, Zd = ora.iterate(word, doc, z, seed=seed, t=t, mode="dense", g=g, want_Z=True, **kw)
+            zs, fs, ss, Zs = ora.iterate(word, doc, z, seed=seed, t=t, mode="sparse", g=g, want_Z=True, branches=br,
+                                         **kw)
+            zd, fd, sd, Zd = ora.iterate(word, doc, z, seed=seed, t=t, mode="dense", g=g, want_Z=True, branches=br,
+                                         **kw)
             assert np.array_equal(zs, zd) and np.array_equal(fs, fd)
             assert np.array_equal(Zs.view(np.uint64), Zd.view(np.uint64))
             assert ss == sd
