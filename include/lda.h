@@ -76,7 +76,11 @@ typedef struct {
    * 65,535 tokens are always dense (16-bit sparse counts).  Ablation switch;
    * the draws are unchanged. */
   int32_t dense_cutoff;
-  int32_t reserved[4];
+  /* Two-branch sampling, Sec. 2.2: draw over [S | Q] with no max-topic branch
+   * and no skip test (the ablation of Eq. 5).  Same distribution, different
+   * canonical order, so different draws for the same u. */
+  int32_t two_branch;
+  int32_t reserved[3];
 } lda_options;
 
 /* Per-iteration statistics (filled by lda_iterate when requested). */

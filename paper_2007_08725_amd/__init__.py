@@ -32,7 +32,8 @@ FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
 class Options(ctypes.Structure):
     _fields_ = [("stream", ctypes.c_void_p), ("dev_alloc", ALLOC_FN), ("dev_free", FREE_FN),
                 ("alloc_ctx", ctypes.c_void_p), ("g", ctypes.c_int32), ("region_tokens", ctypes.c_int32),
-                ("no_skip", ctypes.c_int32), ("dense_cutoff", ctypes.c_int32), ("reserved", ctypes.c_int32 * 4)]
+                ("no_skip", ctypes.c_int32), ("dense_cutoff", ctypes.c_int32), ("two_branch", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 3)]
 
 
 class IterStats(ctypes.Structure):
@@ -143,11 +144,13 @@ class LDA:
     topics, ``alpha``/``beta`` priors of Eq. 1, ``seed`` the Philox key.
     ``g`` (1, 2 or 3), ``region_tokens``, ``no_skip`` and ``dense_cutoff`` are
     the options of ``lda_options``; none of them changes the draws.
+    ``two_branch`` samples over [S | Q] (Sec. 2.2): same distribution, other
+    canonical order.
     """
 
     def __init__(self, word, doc, V: int, K: int, alpha: float, beta: float = 0.01, seed: int = 42, *, g: int = 2,
-                 region_tokens: int = 0, no_skip: bool = False, dense_cutoff: int = 0, torch_stream: bool = True,
-                 torch_allocator: bool = True):
+                 region_tokens: int = 0, no_skip: bool = False, dense_cutoff: int = 0, two_branch: bool = False,
+                 torch_stream: bool = True, torch_allocator: bool = True):
         self._lib = load_library()
         self._h = ctypes.c_void_p()
         word = np.ascontiguousarray(word, np.int32)
@@ -159,6 +162,7 @@ class LDA:
         opts.region_tokens = region_tokens
         opts.no_skip = 1 if no_skip else 0
         opts.dense_cutoff = dense_cutoff
+        opts.two_branch = 1 if two_branch else 0
         self._keep = []
         if torch_stream or torch_allocator:
             import torch

@@ -268,7 +268,7 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
     for (int k = tid; k < K; k += kBlock) {
       const double w = what(uint32_t(wrow[k]), p.beta, d.den[k]);
       sw += w;
-      if (uint32_t(k) != K1) q += p.alpha * w;
+      if (p.two_branch || uint32_t(k) != K1) q += p.alpha * w;
     }
   } else {
     uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
@@ -277,19 +277,22 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
       if (e < nnz && (ents[e] >> 16) == uint32_t(k)) c = ents[e++] & 0xFFFFu;
       const double w = what(c, p.beta, d.den[k]);
       sw += w;
-      if (uint32_t(k) != K1) q += p.alpha * w;
+      if (p.two_branch || uint32_t(k) != K1) q += p.alpha * w;
     }
   }
   q = block_sum(q, scratch);
   sw = block_sum(sw, scratch);
   if (tid == 0) {
+    // the sampler's record; in two-branch mode (Sec. 2.2) the max-topic
+    // branch is empty (a1 = 0, K1 = K, a topic no row holds with a count)
+    // and Q' is the full Q
     WordRec rec;
-    rec.a1 = a1;
+    rec.a1 = p.two_branch ? 0.0 : a1;
     rec.a2 = a2;
     rec.a3 = a3;
     rec.qp = q;
     rec.sumw = sw;
-    rec.k1 = K1;
+    rec.k1 = p.two_branch ? uint32_t(K) : K1;
     rec.k2 = K2;
     d.wrec[r] = rec;
     SkipRec sr;

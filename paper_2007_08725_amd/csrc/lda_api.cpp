@@ -298,7 +298,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   if (K < 2 || K > LDA_MAX_TOPICS) return fail(nullptr, LDA_E_ARG, "K must be in [2, 16384]");
   if (!std::isfinite(alpha) || !(alpha > 0.0)) return fail(nullptr, LDA_E_ARG, "alpha must be finite and positive");
   if (!std::isfinite(beta) || !(beta > 0.0)) return fail(nullptr, LDA_E_ARG, "beta must be finite and positive");
-  int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0;
+  int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0, two_branch = 0;
   if (opts) {
     if (opts->g < 0 || opts->g > 3) return fail(nullptr, LDA_E_ARG, "g must be 1, 2 or 3");
     if (opts->g) g = opts->g;
@@ -308,6 +308,8 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
       return fail(nullptr, LDA_E_ARG, "dev_alloc and dev_free must be given together");
     no_skip = opts->no_skip ? 1 : 0;
     dense_cutoff = opts->dense_cutoff;
+    two_branch = opts->two_branch ? 1 : 0;
+    if (two_branch) no_skip = 1;  // the skip test needs the max-topic branch
   }
   lda_handle *h = new (std::nothrow) lda_handle();
   if (!h) return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
@@ -341,6 +343,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   p.seed = seed;
   p.g = g;
   p.no_skip = no_skip;
+  p.two_branch = two_branch;
   p.key_identity = sorted ? 1 : 0;
   try {
     st = create_device(h, opts, word, doc, R, dense_cutoff);
@@ -375,7 +378,7 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       HIP_TRY(h, launch_word_pre(d, h->p, h->stream));
       HIP_TRY(h, launch_fill_undecided(d, h->p, h->stream));
       if (ev) HIP_TRY(h, hipEventRecord(ev[1], h->stream));
-      HIP_TRY(h, launch_doc_pass(d, h->p, t, h->stream));
+      if (!h->p.no_skip) HIP_TRY(h, launch_doc_pass(d, h->p, t, h->stream));  // steps 2-3 only decide skips
       if (ev) HIP_TRY(h, hipEventRecord(ev[2], h->stream));
       HIP_TRY(h, launch_sampler(d, h->p, t, h->stream));
       if (ev) HIP_TRY(h, hipEventRecord(ev[3], h->stream));

@@ -133,6 +133,7 @@ struct Params {
   uint64_t seed;
   int32_t g;
   int32_t no_skip;
+  int32_t two_branch;  // Sec. 2.2 sampling over [S | Q]: no max-topic branch, no skip test
   int32_t key_identity;
   int32_t grid_regions;  // persistent workgroups for region kernels
   int32_t grid_docs;     // persistent workgroups for doc kernels

@@ -112,6 +112,25 @@ def test_skip_counts_follow_the_oracle_for_every_depth(c1, c1_traj, g):
             assert 0 <= ost["skip3"] - st["skip_step3"] <= max(2, 1e-3 * c1.N)
 
 
+def test_two_branch_mode_follows_the_oracle(c1, c1_traj):
+    """The two-branch ablation (Sec. 2.2, draws over [S | Q]) against the oracle's two-branch
+    form on c1 snapshots: same draws except flagged boundary cases, counts the histograms of z,
+    and no token skipped."""
+    with make_lda(c1, two_branch=True) as m:
+        for t in range(3):
+            z = c1_traj[t][0]
+            zo, flags, ost = oracle_step(c1, z, t, branches=2)
+            m.set_assignments(z, t)
+            st = m.iterate(1, stats=True)[0]
+            cnt = m.counts()
+            compare_draws(cnt["z"], zo, flags, c1.N)
+            check_counts_are_histograms(c1, cnt, c1.K)
+            assert st["skip_step3"] == 0 and st["skip_after_s"] == 0 and st["sampled"] == c1.N
+        z3 = m.counts(D=False, W=False)["z"]
+    # a different canonical order: the same u gives other topics for some tokens
+    assert not np.array_equal(z3, c1_traj[3][0])
+
+
 def test_determinism_and_resume(c1):
     with make_lda(c1) as a:
         a.iterate(10)
