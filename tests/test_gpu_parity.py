@@ -197,6 +197,28 @@ def test_reduced_config_late_snapshot(name, over):
     say("  skip3 gpu %d oracle %d of %d" % (st["skip_step3"], ost["skip3"], c.N))
 
 
+@pytest.mark.timeout(600)
+def test_llpt_after_fifty_iterations_reduced_c2():
+    """Free-running GPU and oracle trajectories from the same initial topics diverge token by
+    token, but after 50 iterations their per-token log-likelihoods agree within 1e-3 relative;
+    the GPU's LLPT of its own state equals the oracle's LLPT of that state to 1e-12."""
+    c = lda_synth.make_corpus("c2", n_docs=2500)
+    kw = corpus_kw(c)
+    say("LLPT-50 c2 reduced N=%d" % c.N)
+    z = oracle.init_topics(c.N, c.K, SEED)
+    for t in range(50):
+        z, _, _ = oracle_step(c, z, t)
+    lo = oracle.llpt(c.word, c.doc, z, **kw)
+    with make_lda(c) as m:
+        m.iterate(50)
+        lg = m.loglik()
+        zg = m.counts(D=False, W=False)["z"]
+    say("  LLPT gpu %.6f oracle %.6f" % (lg, lo))
+    assert lg == pytest.approx(lo, rel=1e-3)
+    assert lg == pytest.approx(oracle.llpt(c.word, c.doc, zg, **kw), rel=1e-12)
+    assert lg > oracle.llpt(c.word, c.doc, oracle.init_topics(c.N, c.K, SEED), **kw)
+
+
 def test_shuffled_input_order():
     """Input not sorted by document: keys and z stay in the caller's order."""
     c = lda_synth.generate(lda_synth.SPECS["c1"], n_docs=300, shuffle=True)
