@@ -80,7 +80,12 @@ typedef struct {
    * and no skip test (the ablation of Eq. 5).  Same distribution, different
    * canonical order, so different draws for the same u. */
   int32_t two_branch;
-  int32_t reserved[3];
+  /* Threads per sampler workgroup: 256, 512 or 1024 (0 = the size with the
+   * most resident waves per CU for this K; the W^ row of K fp64 values in LDS
+   * limits how many workgroups a CU holds).  LDA_E_RANGE if the size asked
+   * for does not fit.  Performance switch; the draws are unchanged. */
+  int32_t sampler_block;
+  int32_t reserved[2];
 } lda_options;
 
 /* Per-iteration statistics (filled by lda_iterate when requested). */
@@ -98,6 +103,7 @@ typedef struct {
   int64_t regions;       /* regions handed out by the scheduler */
   int64_t dense_regions; /* of which regions of dense (full-row) words */
   int64_t row_bytes;     /* bytes of W rows the sampler needs: 4*K per dense word, 4*nnz per sparse word */
+  int64_t sampler_block; /* threads per sampler workgroup */
 } lda_iter_stats;
 
 /* Count tables in the caller's ids.  Caller-allocated; a call with every array

@@ -33,7 +33,7 @@ class Options(ctypes.Structure):
     _fields_ = [("stream", ctypes.c_void_p), ("dev_alloc", ALLOC_FN), ("dev_free", FREE_FN),
                 ("alloc_ctx", ctypes.c_void_p), ("g", ctypes.c_int32), ("region_tokens", ctypes.c_int32),
                 ("no_skip", ctypes.c_int32), ("dense_cutoff", ctypes.c_int32), ("two_branch", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 3)]
+                ("sampler_block", ctypes.c_int32), ("reserved", ctypes.c_int32 * 2)]
 
 
 class IterStats(ctypes.Structure):
@@ -41,7 +41,7 @@ class IterStats(ctypes.Structure):
                 ("ms_docpass", ctypes.c_double), ("ms_rebuild", ctypes.c_double), ("ms_precompute", ctypes.c_double),
                 ("skip_step3", ctypes.c_int64), ("skip_after_s", ctypes.c_int64), ("sampled", ctypes.c_int64),
                 ("nnz_scanned", ctypes.c_int64), ("regions", ctypes.c_int64), ("dense_regions", ctypes.c_int64),
-                ("row_bytes", ctypes.c_int64)]
+                ("row_bytes", ctypes.c_int64), ("sampler_block", ctypes.c_int64)]
 
 
 class Counts(ctypes.Structure):
@@ -145,12 +145,13 @@ class LDA:
     ``g`` (1, 2 or 3), ``region_tokens``, ``no_skip`` and ``dense_cutoff`` are
     the options of ``lda_options``; none of them changes the draws.
     ``two_branch`` samples over [S | Q] (Sec. 2.2): same distribution, other
-    canonical order.
+    canonical order.  ``sampler_block`` (256, 512, 1024; 0 = by occupancy)
+    sets the sampler's workgroup size.
     """
 
     def __init__(self, word, doc, V: int, K: int, alpha: float, beta: float = 0.01, seed: int = 42, *, g: int = 2,
                  region_tokens: int = 0, no_skip: bool = False, dense_cutoff: int = 0, two_branch: bool = False,
-                 torch_stream: bool = True, torch_allocator: bool = True):
+                 sampler_block: int = 0, torch_stream: bool = True, torch_allocator: bool = True):
         self._lib = load_library()
         self._h = ctypes.c_void_p()
         word = np.ascontiguousarray(word, np.int32)
@@ -163,6 +164,7 @@ class LDA:
         opts.no_skip = 1 if no_skip else 0
         opts.dense_cutoff = dense_cutoff
         opts.two_branch = 1 if two_branch else 0
+        opts.sampler_block = sampler_block
         self._keep = []
         if torch_stream or torch_allocator:
             import torch

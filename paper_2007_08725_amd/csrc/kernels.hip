@@ -917,8 +917,11 @@ __device__ void draw_small_batch(bool und, uint32_t nnz, const BatchLds &bt, con
   }
 }
 
-__global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uint32_t t,
-                                                    unsigned long long *__restrict__ stats) {
+// The sampler for workgroups of NB threads (NB / 64 waves); every wave works
+// on its own batches, so NB only changes how many waves share a region's W^
+// row in LDS (larger workgroups for large K, where LDS bounds the residency).
+template <int NB>
+__device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, unsigned long long *__restrict__ stats) {
   extern __shared__ double lds[];
   const int K = p.K;
   const int nb = (K + kGroup - 1) / kGroup;
@@ -927,11 +930,11 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
   double *qb = lds + K + 1;  // [nbp + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup; +inf past nb
   __shared__ uint32_t s_reg[3];
   __shared__ int s_valid;
-  __shared__ uint32_t s_off[kBlock], s_nnz[kBlock];
-  __shared__ double s_u[kBlock];
-  __shared__ uint16_t s_top[kBlock];
-  __shared__ uint32_t s_hand[kBlock / kGroup * kMaxRun];
-  __shared__ uint8_t s_list[kBlock];
+  __shared__ uint32_t s_off[NB], s_nnz[NB];
+  __shared__ double s_u[NB];
+  __shared__ uint16_t s_top[NB];
+  __shared__ uint32_t s_hand[NB / kGroup * kMaxRun];
+  __shared__ uint8_t s_list[NB];
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -940,7 +943,7 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
                     s_hand + wave * (kWave / kGroup) * kMaxRun, s_list + wave * kWave};
   int qsh = -2;
   for (int q = 1; q < nbp; q *= 4) qsh += 2;
-  for (int q = nb + 1 + tid; q < nbp; q += kBlock) qb[q] = __builtin_inf();
+  for (int q = nb + 1 + tid; q < nbp; q += NB) qb[q] = __builtin_inf();
   // region, word and count variables are uniform over the block (scalar registers)
   uint32_t cur = 0xFFFFFFFFu, K1 = 0;
   double a1 = 0.0, qp = 0.0;
@@ -974,14 +977,14 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
       qp = rec.qp;
       if (int32_t(v) < p.n_dense) {
         const int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
-        for (int k = tid; k < K; k += kBlock) wh[k] = what(uint32_t(wrow[k]), p.beta, d.den[k]);
+        for (int k = tid; k < K; k += NB) wh[k] = what(uint32_t(wrow[k]), p.beta, d.den[k]);
       } else {
         const int s = int(v) - p.n_dense;
         const uint32_t *ents = d.ws_ent + d.ws_cap[s];
         const uint32_t nnz = d.ws_nnz[s];
-        for (int k = tid; k < K; k += kBlock) wh[k] = what(0u, p.beta, d.den[k]);
+        for (int k = tid; k < K; k += NB) wh[k] = what(0u, p.beta, d.den[k]);
         __syncthreads();
-        for (uint32_t q = tid; q < nnz; q += kBlock) {
+        for (uint32_t q = tid; q < nnz; q += NB) {
           const uint32_t ent = ents[q];
           wh[ent >> 16] = what(ent & 0xFFFFu, p.beta, d.den[ent >> 16]);
         }
@@ -993,7 +996,7 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
         wh[K] = 0.0;  // topic of the padding entries of D rows
       }
       __syncthreads();
-      for (int blk = tid; blk < nb; blk += kBlock) {
+      for (int blk = tid; blk < nb; blk += NB) {
         double s = 0.0;
         const int k1 = min(K, (blk + 1) * kGroup);
         for (int k = blk * kGroup; k < k1; ++k) s += p.alpha * wh[k];
@@ -1016,7 +1019,7 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
     }
 
     const WordState w{wh, qb, nb, K, qsh, K1, a1, qp, p.alpha};
-    for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += kBlock) {
+    for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += NB) {
       const uint32_t j = base + uint32_t(lane);
       // the slot, key and row offset are loaded together (one latency); the
       // row header only for undecided tokens
@@ -1058,6 +1061,20 @@ __global__ __launch_bounds__(kBlock, 7) void k_sampler(DevState d, Params p, uin
     if (n_dreg) atomicAdd(&stats[ST_DENSE_REGIONS], n_dreg);
     if (row_bytes) atomicAdd(&stats[ST_ROW_BYTES], row_bytes);
   }
+}
+
+
+__global__ __launch_bounds__(256, 7) void k_sampler(DevState d, Params p, uint32_t t,
+                                                 unsigned long long *__restrict__ stats) {
+  sampler_body<256>(d, p, t, stats);
+}
+__global__ __launch_bounds__(512, 4) void k_sampler_512(DevState d, Params p, uint32_t t,
+                                                     unsigned long long *__restrict__ stats) {
+  sampler_body<512>(d, p, t, stats);
+}
+__global__ __launch_bounds__(1024, 4) void k_sampler_1024(DevState d, Params p, uint32_t t,
+                                                       unsigned long long *__restrict__ stats) {
+  sampler_body<1024>(d, p, t, stats);
 }
 
 // Rows of split dense words are accumulated with atomics; clear them and T.
@@ -1372,11 +1389,52 @@ size_t sampler_lds_bytes(int K) {
   return sizeof(double) * (size_t(K) + 1 + size_t(q_blocks_padded((K + kGroup - 1) / kGroup)) + 1);
 }
 
+// Threads per sampler workgroup for this K: `want` when nonzero, else the
+// size with the most resident waves per CU (ties to the smaller).  LDS holds
+// the W^ row, so a large K leaves room for few workgroups and larger ones
+// keep more waves busy.  0 when the size asked for (or none) fits.
+int sampler_block(int K, int want) {
+  const size_t lds = sampler_lds_bytes(K);
+  int best = 0, best_waves = 0;
+  const int sizes[3] = {256, 512, 1024};
+  for (int q = 0; q < 3; ++q) {
+    const int nb = sizes[q];
+    if (want && nb != want) continue;
+    hipError_t err = nb == 256 ? allow_lds(k_sampler, lds) : nb == 512 ? allow_lds(k_sampler_512, lds)
+                                                                        : allow_lds(k_sampler_1024, lds);
+    int blocks = 0;
+    if (err == hipSuccess)
+      err = nb == 256 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler, nb, lds)
+          : nb == 512 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler_512, nb, lds)
+                      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler_1024, nb, lds);
+    const int waves = err == hipSuccess ? blocks * nb / kWave : 0;
+    if (waves > best_waves) {
+      best = nb;
+      best_waves = waves;
+    }
+  }
+  (void)hipGetLastError();
+  return best;
+}
+
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
-  hipError_t err = allow_lds(k_sampler, sampler_lds_bytes(p.K));
-  if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_sampler, dim3(uint32_t(p.grid_regions)), dim3(kBlock), sampler_lds_bytes(p.K), s, d, p, t,
-                     d.stats);
+  const size_t lds = sampler_lds_bytes(p.K);
+  const int nb = p.sampler_block;
+  const uint32_t grid = uint32_t(std::max<int64_t>(1, int64_t(p.grid_regions) * kBlock / nb));
+  hipError_t err;
+  if (nb == 1024) {
+    err = allow_lds(k_sampler_1024, lds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_sampler_1024, dim3(grid), dim3(1024), lds, s, d, p, t, d.stats);
+  } else if (nb == 512) {
+    err = allow_lds(k_sampler_512, lds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_sampler_512, dim3(grid), dim3(512), lds, s, d, p, t, d.stats);
+  } else {
+    err = allow_lds(k_sampler, lds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_sampler, dim3(grid), dim3(256), lds, s, d, p, t, d.stats);
+  }
   return hipGetLastError();
 }
 

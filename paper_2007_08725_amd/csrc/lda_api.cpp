@@ -154,6 +154,10 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   }
   Params &p = h->p;
   p.grid_regions = std::max(1, cus * 8);
+  p.sampler_block = sampler_block(p.K, o ? o->sampler_block : 0);
+  if (!p.sampler_block)
+    return fail(h, LDA_E_RANGE, "no sampler workgroup of " + std::string(o && o->sampler_block ? std::to_string(o->sampler_block) + " threads" : "any size") +
+                                    " fits the LDS of K = " + std::to_string(L.K));
   p.grid_docs = std::max(1, cus * 8);
   const size_t n = size_t(L.n);
   const bool identity = L.key_identity;
@@ -310,6 +314,9 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
     dense_cutoff = opts->dense_cutoff;
     two_branch = opts->two_branch ? 1 : 0;
     if (two_branch) no_skip = 1;  // the skip test needs the max-topic branch
+    const int32_t sb = opts->sampler_block;
+    if (sb != 0 && sb != 256 && sb != 512 && sb != 1024)
+      return fail(nullptr, LDA_E_ARG, "sampler_block must be 0, 256, 512 or 1024");
   }
   lda_handle *h = new (std::nothrow) lda_handle();
   if (!h) return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
@@ -414,6 +421,7 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       o.regions = int64_t(s[ST_REGIONS]);
       o.dense_regions = int64_t(s[ST_DENSE_REGIONS]);
       o.row_bytes = int64_t(s[ST_ROW_BYTES]);
+      o.sampler_block = h->p.sampler_block;
     }
     done += chunk;
   }

@@ -136,6 +136,7 @@ struct Params {
   int32_t two_branch;  // Sec. 2.2 sampling over [S | Q]: no max-topic branch, no skip test
   int32_t key_identity;
   int32_t grid_regions;  // persistent workgroups for region kernels
+  int32_t sampler_block; // threads per sampler workgroup: 256, 512 or 1024
   int32_t grid_docs;     // persistent workgroups for doc kernels
   uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
@@ -154,6 +155,7 @@ hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_fill_undecided(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
+int sampler_block(int K, int want);
 hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_sum_nnz(const DevState &d, const Params &p, unsigned long long *out, hipStream_t s);

@@ -83,10 +83,11 @@ def test_c1_free_running_trajectory_and_llpt(c1, c1_traj):
 
 @pytest.mark.parametrize("opts", [dict(region_tokens=7), dict(region_tokens=100), dict(g=1), dict(g=3), dict(no_skip=True),
                                   dict(dense_cutoff=-1), dict(dense_cutoff=1 << 30), dict(dense_cutoff=3),
+                                  dict(sampler_block=256), dict(sampler_block=512), dict(sampler_block=1024),
                                   dict(torch_allocator=False, torch_stream=False)])
 def test_schedule_invariance(c1, opts):
     """Region size, S_est depth, the skip test, the hybrid-W cutoff (all dense, all sparse),
-    allocator and stream never change the draws."""
+    the sampler's workgroup size, allocator and stream never change the draws."""
     say("invariance %s" % opts)
     with make_lda(c1) as a:
         a.iterate(3)
@@ -270,6 +271,26 @@ def test_edge_cases(name, c):
         ll = m.loglik()
     assert ll == pytest.approx(oracle.llpt(c.word, c.doc, cnt["z"], **kw), rel=1e-12, abs=1e-14)
 
+
+
+@pytest.mark.parametrize("K", [16384, 5000])
+@pytest.mark.parametrize("block", [0, 256, 512, 1024])
+def test_sampler_block_sizes_at_large_K(K, block):
+    """Every sampler workgroup size the LDS allows draws what the oracle draws at a
+    large K (the W^ row of K fp64 values fills most of the LDS); the default picks
+    one of them."""
+    rng = np.random.default_rng(5)
+    c = _Tiny(rng.integers(0, 60, 6000), np.sort(rng.integers(0, 40, 6000)), 60, K, 0.01)
+    say("sampler block %d K=%d" % (block, K))
+    kw = dict(M=c.n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta)
+    z = oracle.init_topics(c.N, c.K, SEED)
+    zo, flags, _ = oracle.iterate(c.word, c.doc, z, seed=SEED, t=0, **kw)
+    with lda_make(c, sampler_block=block) as m:
+        st = m.iterate(1, stats=True)[0]
+        cnt = m.counts()
+    assert st["sampler_block"] == (block or st["sampler_block"]) and st["sampler_block"] in (256, 512, 1024)
+    compare_draws(cnt["z"], zo, flags, c.N)
+    check_counts_are_histograms(c, cnt, c.K)
 
 def lda_make(c, **kw):
     import paper_2007_08725_amd as lda
