@@ -44,8 +44,13 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1
 }
 
 // u in [0,1) for token i (input order) at iteration t: counter (i, 0, t, 0).
+// The key and t pass through an empty asm so that the compiler computes the
+// key schedule where the draw is made instead of keeping twenty hoisted
+// round keys live (in the sampler they would spill).
 __device__ __forceinline__ double uniform_draw(uint64_t seed, uint32_t t, uint32_t i) {
-  const uint4 x = philox4x32_10(make_uint4(i, 0u, t, 0u), uint32_t(seed), uint32_t(seed >> 32));
+  uint32_t k0 = uint32_t(seed), k1 = uint32_t(seed >> 32);
+  asm volatile("" : "+s"(k0), "+s"(k1), "+s"(t));
+  const uint4 x = philox4x32_10(make_uint4(i, 0u, t, 0u), k0, k1);
   const uint64_t bits = (uint64_t(x.x) << 32) | uint64_t(x.y);
   return double(bits >> 11) * 0x1p-53;
 }
@@ -758,6 +763,61 @@ __device__ __forceinline__ uint32_t walk_run(const uint32_t (&r)[kRun], const do
   return ent;
 }
 
+// The lane's index in the wave, computed where it is used: an opaque value
+// keeps the compiler from hoisting the many lane-derived offsets and masks of
+// the rounds out of the loops, where they would all stay live and spill.
+__device__ __forceinline__ int lane_here() {
+  int v;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(v));
+  return v;
+}
+
+// Codes left in a token's topic slot by the small-group rounds: the draw
+// fell in S' (the entry is found by a walk over the recorded run) or in Q'
+// (a search of the word's Q' prefix).  Topics are below 2^14.
+constexpr uint16_t kDrawS = 0xFFFF;
+constexpr uint16_t kDrawQ = 0xFFFE;
+
+// Topic of x in [0, Q') by the word's Q' prefix: the block by a binary
+// search of qb (blocks of kGroup topics, +inf past the last), then a walk
+// over the block's alpha * W^' terms.  A rounding that leaves x at or past
+// the end selects the last positive term.
+__device__ __forceinline__ uint32_t q_draw(double xq, const WordState &w) {
+  if (!(xq < w.qb[w.nb])) return (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);
+  int lo = 0;  // the largest block with qb[lo] <= xq; qb holds 4 << qsh entries before its +inf tail ends
+  for (int step = w.qsh >= 0 ? 2 << w.qsh : 0; step > 0; step >>= 1) lo = w.qb[lo + step] <= xq ? lo + step : lo;
+  const double xs = xq - w.qb[lo];
+  const int k0 = lo * kGroup;
+  double p = 0.0;
+  int kk = k0, last = k0;
+#pragma unroll
+  for (int i = 0; i < kGroup; ++i) {
+    const int k = k0 + i;
+    const double t = k < w.K ? w.alpha * w.wh[k] : 0.0;
+    const bool open = p <= xs;
+    p += t;
+    kk = open ? k : kk;
+    last = t > 0.0 ? k : last;
+  }
+  return uint32_t(xs < p ? kk : last);
+}
+
+// The drawn topic of a batch token, one lane per token: the topic itself,
+// or the end of an S' or Q' draw recorded by the rounds.
+__device__ __forceinline__ uint32_t finish_draw(int q, const BatchLds &bt, const WordState &w,
+                                                const uint32_t *__restrict__ d_ent) {
+  const uint32_t code = bt.top[q];
+  if (code == kDrawS) {
+    const uint32_t a = bt.off[q];
+    uint32_t r[kRun];
+    load_run<kRun>(d_ent + (a & ~uint32_t(kRun - 1)), 0, r);
+    if (a & 1u) r[0] = uint32_t(w.K) << 16;  // the run starts with the row header
+    return walk_run(r, w.wh, bt.u[q]) >> 16;
+  }
+  if (code == kDrawQ) return q_draw(bt.u[q], w);
+  return code;
+}
+
 // One round of small-group draws: group g of the wave draws the token in
 // list slot `slot` (if slot < n).  The row is read in chunks of G*kRun
 // entries, lane l holding entries [l*kRun, l*kRun + kRun) of each chunk (the
@@ -771,7 +831,8 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
   if (slot < n) {
     const int src = bt.list[slot];
     const uint32_t nc = (bt.nnz[src] + 1u + kSpan - 1) / kSpan;  // slots: header + entries
-    const uint32_t *run = d_ent + bt.off[src] + uint32_t(li) * kRun;
+    const uint32_t off0 = bt.off[src];
+    const uint32_t *run = d_ent + off0 + uint32_t(li) * kRun;
     const uint32_t pad = uint32_t(w.K) << 16;
     const double u = bt.u[src];
     // pass over the row: every chunk's loads are issued before the first is
@@ -804,8 +865,6 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
     // max-topic branch, Eq. 7: M = W^[v][K1] * (D[d][K1] + alpha)
     const double Mm = w.a1 * (double(c1 <= 0xFFFFu ? c1 : 0u) + w.alpha);
     const double x = u * ((Mm + S) + w.qp);
-    uint32_t topic = w.K1;
-    bool writer = li == 0;
     in_m = x < Mm;
     if (!in_m) {
       if (x < Mm + S) {
@@ -823,73 +882,45 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
         }
         const double incl = gscan<G>(sc, li);
         const int sel = pick_lane<G>(sc, incl, base, x, li);
-        uint32_t r[kRun];
-        load_run<kRun>(run + cs * kSpan, 0, r);
-        if (cs == 0 && li == 0) r[0] = pad;
-        topic = walk_run(r, w.wh, fmax(x - (base + (incl - sc)), 0.0)) >> 16;
-        writer = li == sel;
-      } else {
-        // Q': the 16-topic block by a 4-ary search over the padded block
-        // prefix, then the topic; each quad of the group does it alone
-        const int q4 = li & 3;
-        const double qs = Mm + S;
-        const double xq = x - qs;
-        if (!(xq < w.qb[w.nb])) {
-          topic = (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);  // last positive segment
-        } else {
-          int lo = 0;
-          for (int sh = w.qsh; sh >= 0; sh -= 2) {
-            const bool ok = w.qb[lo + (q4 << sh)] <= xq;
-            lo += (int(gsum_u32<4>(ok ? 1u : 0u)) - 1) << sh;
-          }
-          const int k0 = lo * kGroup + q4 * 4;
-          double s4 = 0.0;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) s4 += (k0 + i < w.K) ? w.alpha * w.wh[k0 + i] : 0.0;
-          const double start = qs + w.qb[lo];
-          const double incl = gscan<4>(s4, q4);
-          const int sel = pick_lane<4>(s4, incl, start, x, q4);
-          const double xs = fmax(x - (start + (incl - s4)), 0.0);
-          double pq = 0.0;
-          int kk = k0, last = k0;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const double t = (k0 + i < w.K) ? w.alpha * w.wh[k0 + i] : 0.0;
-            const bool open = pq <= xs;
-            pq += t;
-            kk = open ? k0 + i : kk;
-            last = t > 0.0 ? k0 + i : last;
-          }
-          topic = uint32_t(xs < pq ? kk : last);
-          writer = li == sel;
+        if (li == sel) {
+          // the selected lane's run and x inside it, for the walk after the rounds
+          bt.off[src] = (off0 + uint32_t(cs) * kSpan + uint32_t(li) * kRun) | (cs == 0 && li == 0 ? 1u : 0u);
+          bt.u[src] = fmax(x - (base + (incl - sc)), 0.0);
+          bt.top[src] = kDrawS;
         }
+      } else if (li == 0) {
+        // Q': x past M + S', searched after the rounds
+        bt.u[src] = x - (Mm + S);
+        bt.top[src] = kDrawQ;
       }
     }
-    if (writer) bt.top[src] = uint16_t(topic);
+    if (in_m && li == 0) bt.top[src] = uint16_t(w.K1);
   }
   // outside the divergent part, so the count stays wave-uniform
   after_s += uint32_t(__popcll(__ballot(in_m && li == 0)));
 }
 
 // The small-group rounds of one batch: the undecided lanes whose rows take
-// (LO-1, HI] chunks of G*kRun slots (header included) are listed in order of
-// their chunk count, then drawn with G lanes per token, 64/G tokens a round.
-template <int G, int LO, int HI>
+// (LO-1, HI] chunks of G*kRun slots (header included), and more than
+// MIN_SLOTS slots, are listed in order of their chunk count, then drawn with
+// G lanes per token, 64/G tokens a round.
+template <int G, int LO, int HI, uint32_t MIN_SLOTS>
 __device__ void draw_small_batch(bool und, uint32_t nnz, const BatchLds &bt, const WordState &w,
                                  const uint32_t *__restrict__ d_ent, int lane, unsigned long long &after_s) {
   constexpr uint32_t kSpan = uint32_t(G) * kRun;
   int n = 0, ends[HI + 1];
 #pragma unroll
   for (int c = LO; c <= HI; ++c) {
-    const unsigned long long m = __ballot(und && nnz + 1u > uint32_t(c - 1) * kSpan && nnz + 1u <= uint32_t(c) * kSpan);
+    const uint32_t lo_slots = uint32_t(c - 1) * kSpan > MIN_SLOTS ? uint32_t(c - 1) * kSpan : MIN_SLOTS;
+    const unsigned long long m = __ballot(und && nnz + 1u > lo_slots && nnz + 1u <= uint32_t(c) * kSpan);
     if ((m >> lane) & 1ull)
       bt.list[n + int(__builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u)))] =
           uint8_t(lane);
     n += __popcll(m);
     ends[c] = n;
   }
-  const int g = lane / G, li = lane % G;
   for (int base = 0; base < n; base += kWave / G) {
+    const int ln = lane_here(), g = ln / G, li = ln % G;
     const int last = min(base + kWave / G, n) - 1;  // the round's largest run count is that of its last slot
     int nc = LO;
 #pragma unroll
@@ -913,7 +944,7 @@ __device__ void draw_small_batch(bool und, uint32_t nnz, const BatchLds &bt, con
         continue;
       }
     }
-    draw_small<G, 4>(bt, slot, n, w, d_ent, li, after_s);
+    if constexpr (HI >= 4) draw_small<G, 4>(bt, slot, n, w, d_ent, li, after_s);
   }
 }
 
@@ -1020,7 +1051,8 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
 
     const WordState w{wh, qb, nb, K, qsh, K1, a1, qp, p.alpha};
     for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += NB) {
-      const uint32_t j = base + uint32_t(lane);
+      const int ln = lane_here();  // the lane, recomputed per batch
+      const uint32_t j = base + uint32_t(ln);
       // the slot, key and row offset are loaded together (one latency); the
       // row header only for undecided tokens
       uint32_t zj = 0, key = 0, off = 0;
@@ -1033,21 +1065,22 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       uint32_t nnz = 0;
       if (und) {
         nnz = d.d_ent[off] & 0xFFFFu;
-        bt.off[lane] = off;
-        bt.nnz[lane] = nnz;
-        bt.u[lane] = uniform_draw(p.seed, t, key);
+        bt.off[ln] = off;
+        bt.nnz[ln] = nnz;
+        bt.u[ln] = uniform_draw(p.seed, t, key);
       }
       n_sampled += uint32_t(__popcll(__ballot(und)));
       nnz_sum += wave_sum_u32(nnz);
       // rows of up to 128 slots (header and entries): 4 lanes per token; up
       // to 256: 8 lanes; up to 512: 16 lanes; longer rows: 16 lanes, one
       // chunk of kChunk slots at a time
-      draw_small_batch<4, 1, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
-      draw_small_batch<8, 3, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
-      draw_small_batch<16, 3, 4>(und, nnz, bt, w, d.d_ent, lane, n_after_s);
-      draw_tokens<0>(__ballot(und && nnz + 1u > 512u), bt, w, d.d_ent, grp, li, n_after_s);
-      // the batch's topics leave in one coalesced store
-      if (und) d.z_w[j] = bt.top[lane];
+      draw_small_batch<4, 1, 4, 0>(und, nnz, bt, w, d.d_ent, ln, n_after_s);
+      draw_small_batch<8, 3, 4, 128>(und, nnz, bt, w, d.d_ent, ln, n_after_s);
+      draw_small_batch<16, 3, 4, 256>(und, nnz, bt, w, d.d_ent, ln, n_after_s);
+      draw_tokens<0>(__ballot(und && nnz + 1u > 512u), bt, w, d.d_ent, ln / kGroup, ln % kGroup, n_after_s);
+      // the S' walks and Q' searches, one lane per token; the batch's topics
+      // leave in one coalesced store
+      if (und) d.z_w[j] = uint16_t(finish_draw(ln, bt, w, d.d_ent));
     }
     __syncthreads();
   }
