@@ -34,8 +34,9 @@ constexpr uint32_t kGroupMask = (1u << kGroup) - 1u;
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int round = 0; round < 10; ++round) {
-    const uint32_t lo0 = 0xD2511F53u * c.x, hi0 = __umulhi(0xD2511F53u, c.x);
-    const uint32_t lo1 = 0xCD9E8D57u * c.z, hi1 = __umulhi(0xCD9E8D57u, c.z);
+    const uint64_t p0 = uint64_t(0xD2511F53u) * c.x, p1 = uint64_t(0xCD9E8D57u) * c.z;  // one 32x32->64 product each
+    const uint32_t lo0 = uint32_t(p0), hi0 = uint32_t(p0 >> 32);
+    const uint32_t lo1 = uint32_t(p1), hi1 = uint32_t(p1 >> 32);
     c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
@@ -464,6 +465,18 @@ struct WordState {
 };
 
 
+// W^' of a packed D entry's topic (entry = topic << 16 | count) from the
+// row in LDS: the address, topic * 8 + the row's LDS offset, is one
+// v_mad_u32_u16 on the entry's high half (op_sel), read as an LDS pointer.
+typedef const __attribute__((address_space(3))) double lds_f64;
+__device__ __forceinline__ double wh_of(const double *__restrict__ wh, uint32_t e) {
+  uint32_t a;
+  asm("v_mad_u32_u16 %0, %1, 8, %2 op_sel:[1,0,0,0]"
+      : "=v"(a)
+      : "v"(e), "s"(uint32_t(reinterpret_cast<uintptr_t>(wh))));
+  return *(lds_f64 *)(size_t)a;
+}
+
 // Load C entries per lane from `row` (lane li gets entries [li*C, li*C + C),
 // topics ascending).  The row is padded to its length class with count-0
 // entries of topic K, so all 16*C entries are in the row's slots.
@@ -482,7 +495,7 @@ template <int C>
 __device__ __forceinline__ double run_sum(const uint32_t (&r)[C], const double *__restrict__ wh) {
   double s = 0.0;
 #pragma unroll
-  for (int i = 0; i < C; ++i) s = __builtin_fma(double(r[i] & 0xFFFFu), wh[r[i] >> 16], s);
+  for (int i = 0; i < C; ++i) s = __builtin_fma(double(r[i] & 0xFFFFu), wh_of(wh, r[i]), s);
   return s;
 }
 
@@ -654,6 +667,10 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
   }
 }
 
+// Entries of the sampler's W^' row in LDS: K + 1 (topic K is the padding of
+// D rows) rounded up to whole blocks of kGroup topics, zeros past K.
+__host__ __device__ inline int wh_entries(int K) { return (K + 1 + kGroup - 1) / kGroup * kGroup; }
+
 // Blocks of the Q' prefix rounded up to a power of 4 (the 4-ary search).
 __host__ __device__ inline int q_blocks_padded(int nb) {
   int q = 1;
@@ -752,13 +769,13 @@ __device__ __forceinline__ uint32_t walk_run(const uint32_t (&r)[kRun], const do
 #pragma unroll
   for (int i = 0; i < kRun; ++i) {
     const bool open = p <= xs;
-    p = __builtin_fma(double(r[i] & 0xFFFFu), wh[r[i] >> 16], p);
+    p = __builtin_fma(double(r[i] & 0xFFFFu), wh_of(wh, r[i]), p);
     ent = open ? r[i] : ent;
   }
   if (!(xs < p)) {
 #pragma unroll
     for (int i = 0; i < kRun; ++i)
-      if ((r[i] & 0xFFFFu) != 0u && wh[r[i] >> 16] > 0.0) ent = r[i];
+      if ((r[i] & 0xFFFFu) != 0u && wh_of(wh, r[i]) > 0.0) ent = r[i];
   }
   return ent;
 }
@@ -780,7 +797,7 @@ constexpr uint16_t kDrawQ = 0xFFFE;
 
 // Topic of x in [0, Q') by the word's Q' prefix: the block by a binary
 // search of qb (blocks of kGroup topics, +inf past the last), then a walk
-// over the block's alpha * W^' terms.  A rounding that leaves x at or past
+// over the block's alpha * W^' terms (W^' is 0 from K up to the block end).  A rounding that leaves x at or past
 // the end selects the last positive term.
 __device__ __forceinline__ uint32_t q_draw(double xq, const WordState &w) {
   if (!(xq < w.qb[w.nb])) return (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);
@@ -793,7 +810,7 @@ __device__ __forceinline__ uint32_t q_draw(double xq, const WordState &w) {
 #pragma unroll
   for (int i = 0; i < kGroup; ++i) {
     const int k = k0 + i;
-    const double t = k < w.K ? w.alpha * w.wh[k] : 0.0;
+    const double t = w.alpha * w.wh[k];  // zeros past K (the row is padded to whole blocks)
     const bool open = p <= xs;
     p += t;
     kk = open ? k : kk;
@@ -900,52 +917,63 @@ __device__ void draw_small(const BatchLds &bt, int slot, int n, const WordState 
   after_s += uint32_t(__popcll(__ballot(in_m && li == 0)));
 }
 
-// The small-group rounds of one batch: the undecided lanes whose rows take
-// (LO-1, HI] chunks of G*kRun slots (header included), and more than
-// MIN_SLOTS slots, are listed in order of their chunk count, then drawn with
-// G lanes per token, 64/G tokens a round.
-template <int G, int LO, int HI, uint32_t MIN_SLOTS>
-__device__ void draw_small_batch(bool und, uint32_t nnz, const BatchLds &bt, const WordState &w,
-                                 const uint32_t *__restrict__ d_ent, int lane, unsigned long long &after_s) {
+// Row-length buckets of a batch (slots, header included): upper bounds.
+// Buckets 0-3 are rows padded to 32-slot multiples, 4-5 to 64, 6-7 to 128.
+__device__ constexpr uint32_t kBucketEnd[8] = {32, 64, 96, 128, 192, 256, 384, 512};
+
+// The small-group rounds over list places [from, to) (rows in ascending
+// bucket order), G lanes per token and 64/G tokens a round.  A round reads
+// as many chunks of G*kRun slots as its last (longest) row needs.
+template <int G>
+__device__ void draw_rounds(int from, int to, const int (&ends)[8], const BatchLds &bt, const WordState &w,
+                            const uint32_t *__restrict__ d_ent, unsigned long long &after_s) {
   constexpr uint32_t kSpan = uint32_t(G) * kRun;
-  int n = 0, ends[HI + 1];
+  for (int base = from; base < to; base += kWave / G) {
+    const int ln = lane_here(), g = ln / G, li = ln % G;
+    const int last = min(base + kWave / G, to) - 1;
+    uint32_t upper = kBucketEnd[7];
 #pragma unroll
-  for (int c = LO; c <= HI; ++c) {
-    const uint32_t lo_slots = uint32_t(c - 1) * kSpan > MIN_SLOTS ? uint32_t(c - 1) * kSpan : MIN_SLOTS;
-    const unsigned long long m = __ballot(und && nnz + 1u > lo_slots && nnz + 1u <= uint32_t(c) * kSpan);
+    for (int k = 6; k >= 0; --k) upper = last < ends[k] ? kBucketEnd[k] : upper;
+    const uint32_t nc = (upper + kSpan - 1) / kSpan;
+    const int slot = base + g;
+    if (nc <= 1) {
+      draw_small<G, 1>(bt, slot, to, w, d_ent, li, after_s);
+    } else if (nc == 2) {
+      draw_small<G, 2>(bt, slot, to, w, d_ent, li, after_s);
+    } else if (nc == 3) {
+      draw_small<G, 3>(bt, slot, to, w, d_ent, li, after_s);
+    } else {
+      draw_small<G, 4>(bt, slot, to, w, d_ent, li, after_s);
+    }
+  }
+}
+
+// The small-group draws of one batch.  The undecided lanes are listed in
+// ascending bucket order; rows of up to 128 slots are drawn by groups of 4
+// lanes (16 a round), up to 256 by 8 lanes, up to 512 by 16 lanes.  When the
+// 4-lane rounds would end with a partial round of at most 8 rows, all of
+// 97-128 slots (two whole 64-slot chunks), those rows join the 8-lane
+// rounds instead: they fill free places there, or make a round that reads
+// half as many entries per lane as the partial 4-lane round would.
+__device__ void draw_batch_small(bool und, uint32_t nnz, const BatchLds &bt, const WordState &w,
+                                 const uint32_t *__restrict__ d_ent, int lane, unsigned long long &after_s) {
+  int n = 0, ends[8];
+  const uint32_t slots = nnz + 1u;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t lo = k ? kBucketEnd[k - 1] : 0u;
+    const unsigned long long m = __ballot(und && slots > lo && slots <= kBucketEnd[k]);
     if ((m >> lane) & 1ull)
       bt.list[n + int(__builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u)))] =
           uint8_t(lane);
     n += __popcll(m);
-    ends[c] = n;
+    ends[k] = n;
   }
-  for (int base = 0; base < n; base += kWave / G) {
-    const int ln = lane_here(), g = ln / G, li = ln % G;
-    const int last = min(base + kWave / G, n) - 1;  // the round's largest run count is that of its last slot
-    int nc = LO;
-#pragma unroll
-    for (int c = LO; c < HI; ++c) nc = last >= ends[c] ? c + 1 : nc;
-    const int slot = base + g;
-    if constexpr (LO <= 1) {
-      if (nc <= 1) {
-        draw_small<G, 1>(bt, slot, n, w, d_ent, li, after_s);
-        continue;
-      }
-    }
-    if constexpr (LO <= 2) {
-      if (nc <= 2) {
-        draw_small<G, 2>(bt, slot, n, w, d_ent, li, after_s);
-        continue;
-      }
-    }
-    if constexpr (LO <= 3) {
-      if (nc <= 3) {
-        draw_small<G, 3>(bt, slot, n, w, d_ent, li, after_s);
-        continue;
-      }
-    }
-    if constexpr (HI >= 4) draw_small<G, 4>(bt, slot, n, w, d_ent, li, after_s);
-  }
+  const int left = ends[3] % 16;
+  const int a = left > 0 && left <= 8 && ends[3] - ends[2] >= left ? ends[3] - left : ends[3];
+  draw_rounds<4>(0, a, ends, bt, w, d_ent, after_s);
+  draw_rounds<8>(a, ends[5], ends, bt, w, d_ent, after_s);
+  draw_rounds<16>(ends[5], ends[7], ends, bt, w, d_ent, after_s);
 }
 
 // The sampler for workgroups of NB threads (NB / 64 waves); every wave works
@@ -957,15 +985,16 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
   const int K = p.K;
   const int nb = (K + kGroup - 1) / kGroup;
   const int nbp = q_blocks_padded(nb);
-  double *wh = lds;          // [K + 1]
-  double *qb = lds + K + 1;  // [nbp + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup; +inf past nb
-  __shared__ uint32_t s_reg[3];
-  __shared__ int s_valid;
-  __shared__ uint32_t s_off[NB], s_nnz[NB];
-  __shared__ double s_u[NB];
-  __shared__ uint16_t s_top[NB];
-  __shared__ uint32_t s_hand[NB / kGroup * kMaxRun];
-  __shared__ uint8_t s_list[NB];
+  // dynamic LDS only (sampler_lds_bytes)
+  double *wh = lds;                  // [wh_entries(K)]: W^' of the region's word, zeros past K
+  double *qb = lds + wh_entries(K);  // [nbp + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup; +inf past nb
+  double *s_u = qb + nbp + 1;        // [NB]: the batch slices of the waves
+  uint32_t *s_off = reinterpret_cast<uint32_t *>(s_u + NB);  // [NB]
+  uint32_t *s_nnz = s_off + NB;                              // [NB]
+  uint32_t *s_hand = s_nnz + NB;                             // [NB / kGroup * kMaxRun]
+  uint32_t *s_reg = s_hand + NB / kGroup * kMaxRun;          // [4]: the region (word, begin, end) and a valid flag
+  uint16_t *s_top = reinterpret_cast<uint16_t *>(s_reg + 4); // [NB]
+  uint8_t *s_list = reinterpret_cast<uint8_t *>(s_top + NB); // [NB]
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -975,6 +1004,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
   int qsh = -2;
   for (int q = 1; q < nbp; q *= 4) qsh += 2;
   for (int q = nb + 1 + tid; q < nbp; q += NB) qb[q] = __builtin_inf();
+  for (int k = K + 1 + tid; k < wh_entries(K); k += NB) wh[k] = 0.0;
   // region, word and count variables are uniform over the block (scalar registers)
   uint32_t cur = 0xFFFFFFFFu, K1 = 0;
   double a1 = 0.0, qp = 0.0;
@@ -984,15 +1014,15 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
   for (;;) {
     if (tid == 0) {
       const uint32_t r = atomicAdd(&d.counters[CNT_SAMPLER], 1u);
-      s_valid = int64_t(r) < p.n_regions;
-      if (s_valid) {
+      s_reg[3] = int64_t(r) < p.n_regions ? 1u : 0u;
+      if (s_reg[3]) {
         s_reg[0] = d.region[3 * size_t(r)];
         s_reg[1] = d.region[3 * size_t(r) + 1];
         s_reg[2] = d.region[3 * size_t(r) + 2];
       }
     }
     __syncthreads();
-    if (!s_valid) break;
+    if (!s_reg[3]) break;
     const uint32_t v = __builtin_amdgcn_readfirstlane(s_reg[0]);
     const uint32_t b = __builtin_amdgcn_readfirstlane(s_reg[1]);
     const uint32_t e = __builtin_amdgcn_readfirstlane(s_reg[2]);
@@ -1074,9 +1104,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       // rows of up to 128 slots (header and entries): 4 lanes per token; up
       // to 256: 8 lanes; up to 512: 16 lanes; longer rows: 16 lanes, one
       // chunk of kChunk slots at a time
-      draw_small_batch<4, 1, 4, 0>(und, nnz, bt, w, d.d_ent, ln, n_after_s);
-      draw_small_batch<8, 3, 4, 128>(und, nnz, bt, w, d.d_ent, ln, n_after_s);
-      draw_small_batch<16, 3, 4, 256>(und, nnz, bt, w, d.d_ent, ln, n_after_s);
+      draw_batch_small(und, nnz, bt, w, d.d_ent, ln, n_after_s);
       draw_tokens<0>(__ballot(und && nnz + 1u > 512u), bt, w, d.d_ent, ln / kGroup, ln % kGroup, n_after_s);
       // the S' walks and Q' searches, one lane per token; the batch's topics
       // leave in one coalesced store
@@ -1418,8 +1446,13 @@ hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipSt
   return hipGetLastError();
 }
 
-size_t sampler_lds_bytes(int K) {
-  return sizeof(double) * (size_t(K) + 1 + size_t(q_blocks_padded((K + kGroup - 1) / kGroup)) + 1);
+// The sampler's dynamic LDS for K topics and workgroups of nb threads: the
+// W^' row, the Q' block prefix, the per-wave batch slices (u, row offset,
+// length, drawn topic, list place; the long-row hand-off) and the region.
+size_t sampler_lds_bytes(int K, int nb) {
+  const size_t words = size_t(wh_entries(K)) + size_t(q_blocks_padded((K + kGroup - 1) / kGroup)) + 1;
+  return sizeof(double) * words + size_t(nb) * (sizeof(double) + 2 * sizeof(uint32_t) + sizeof(uint16_t) + 1) +
+         sizeof(uint32_t) * (size_t(nb) / kGroup * kMaxRun + 4);
 }
 
 // Threads per sampler workgroup for this K: `want` when nonzero, else the
@@ -1427,11 +1460,11 @@ size_t sampler_lds_bytes(int K) {
 // the W^ row, so a large K leaves room for few workgroups and larger ones
 // keep more waves busy.  0 when the size asked for (or none) fits.
 int sampler_block(int K, int want) {
-  const size_t lds = sampler_lds_bytes(K);
   int best = 0, best_waves = 0;
   const int sizes[3] = {256, 512, 1024};
   for (int q = 0; q < 3; ++q) {
     const int nb = sizes[q];
+    const size_t lds = sampler_lds_bytes(K, nb);
     if (want && nb != want) continue;
     hipError_t err = nb == 256 ? allow_lds(k_sampler, lds) : nb == 512 ? allow_lds(k_sampler_512, lds)
                                                                         : allow_lds(k_sampler_1024, lds);
@@ -1451,8 +1484,8 @@ int sampler_block(int K, int want) {
 }
 
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
-  const size_t lds = sampler_lds_bytes(p.K);
   const int nb = p.sampler_block;
+  const size_t lds = sampler_lds_bytes(p.K, nb);
   const uint32_t grid = uint32_t(std::max<int64_t>(1, int64_t(p.grid_regions) * kBlock / nb));
   hipError_t err;
   if (nb == 1024) {

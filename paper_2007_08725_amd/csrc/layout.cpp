@@ -9,7 +9,9 @@
 //             slot, i.e. the inverted index between the two orders.
 //   Sec. 5.1: every word is cut into regions of at most R consecutive
 //             word-ordered tokens (large-word dissection); the regions are
-//             the units the atomic scheduler hands out.
+//             the units the atomic scheduler hands out, in an order that
+//             keeps the documents of concurrent regions close (see the end
+//             of plan_from_counts).
 //
 // scan_tokens and plan_from_counts are shared by the device builder (the
 // sorts run on the GPU, see layout_gpu.hip) and by build_layout, the
@@ -122,6 +124,35 @@ lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t
       L.region.push_back(b + uint32_t(uint64_t(c) * (q + 1) / nreg));
       if (r < nd) L.n_dense_regions++;
     }
+  }
+  // Hand-out order (a choice of this implementation, not the paper's): the
+  // regions of split words by the middle of their span of the word's
+  // document-sorted tokens, which tracks the document ids they touch, so the
+  // regions that run at the same time read the D rows of nearby documents and
+  // the device's last-level cache serves the repeated reads; then the
+  // unsplit words in word order (the small regions last, filling the tail).
+  {
+    const size_t nr = L.region.size() / 3;
+    std::vector<size_t> split_idx, rest_idx;
+    for (size_t i = 0; i < nr; ++i) {
+      const uint32_t r = L.region[3 * i];
+      (int32_t(r) < nd && L.split[r] ? split_idx : rest_idx).push_back(i);
+    }
+    // middle of region i as a fraction of its word: (b + e - 2 wb) / (2 c), compared exactly
+    auto mid_num = [&](size_t i) {
+      const uint32_t r = L.region[3 * i];
+      return uint64_t(L.region[3 * i + 1] - L.word_off[r]) + uint64_t(L.region[3 * i + 2] - L.word_off[r]);
+    };
+    std::stable_sort(split_idx.begin(), split_idx.end(), [&](size_t x, size_t y) {
+      const unsigned __int128 lhs = (unsigned __int128)mid_num(x) * L.count[L.region[3 * y]];
+      const unsigned __int128 rhs = (unsigned __int128)mid_num(y) * L.count[L.region[3 * x]];
+      return lhs < rhs;
+    });
+    std::vector<uint32_t> ordered;
+    ordered.reserve(L.region.size());
+    for (const std::vector<size_t> *part : {&split_idx, &rest_idx})
+      for (size_t i : *part) ordered.insert(ordered.end(), L.region.begin() + 3 * i, L.region.begin() + 3 * i + 3);
+    L.region.swap(ordered);
   }
   L.n_regions = int64_t(L.region.size() / 3);
   return LDA_OK;

@@ -149,10 +149,20 @@ def test_layout_properties(lib, shuffle, R):
     same = np.diff(new_word) == 0
     assert np.all(np.diff(rank[key])[same] > 0)
     # regions tile every word exactly; only dense words are split; each region <= R
-    reg = L["region"].astype(np.int64)
+    reg_order = L["region"].astype(np.int64)
+    reg = reg_order[np.argsort(reg_order[:, 1], kind="stable")]
     assert reg[0, 1] == 0 and reg[-1, 2] == n
     assert np.all(reg[1:, 1] == reg[:-1, 2])
     assert np.all(reg[:, 2] > reg[:, 1])
+    # hand-out order: regions of split words by the middle of their span of
+    # the word (ascending), then the unsplit words in word order
+    cnt_new = np.diff(wo)
+    split = np.array([cnt_new[w] > R and w < L["n_dense"] for w in reg_order[:, 0]])
+    ns = int(split.sum())
+    assert np.all(split[:ns]) and not np.any(split[ns:])
+    mid = (reg_order[:ns, 1] + reg_order[:ns, 2] - 2 * wo[reg_order[:ns, 0]]) / (2.0 * cnt_new[reg_order[:ns, 0]])
+    assert np.all(np.diff(mid) >= 0)
+    assert np.all(np.diff(reg_order[ns:, 0]) > 0)
     for r in range(L["n_present"]):
         rows = reg[reg[:, 0] == r]
         assert rows[0, 1] == wo[r] and rows[-1, 2] == wo[r + 1]
