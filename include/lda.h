@@ -48,10 +48,12 @@ typedef enum {
   LDA_E_STATE = 5   /* the handle was poisoned by an earlier device error */
 } lda_status;
 
-/* Largest topic count: the packed (topic << 16 | count) entries of D and of
- * the sparse rows of W (Sec. 4.2) keep 16 bits per field; one code is
- * reserved, and a word-topic row of K fp64 values must fit in 128 KB of LDS. */
-#define LDA_MAX_TOPICS 16384
+/* Largest topic count (the paper's largest, Sec. 6): the packed
+ * (topic << 16 | count) entries of D and of the sparse rows of W (Sec. 4.2)
+ * keep 16 bits per field, and one topic code marks an undrawn token.  Above
+ * about 17,000 topics the fp64 word-topic row no longer fits one
+ * workgroup's LDS, and the sampler walks it in two tiles. */
+#define LDA_MAX_TOPICS 32768
 /* Longest document: its per-topic counts must fit 16 bits (Sec. 4.2). */
 #define LDA_MAX_DOC_LEN 65535
 

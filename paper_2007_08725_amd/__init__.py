@@ -22,7 +22,7 @@ _lib = None
 LDA_OK, LDA_E_ARG, LDA_E_RANGE, LDA_E_NOMEM, LDA_E_DEVICE, LDA_E_STATE = range(6)
 STATUS_NAMES = {0: "LDA_OK", 1: "LDA_E_ARG", 2: "LDA_E_RANGE", 3: "LDA_E_NOMEM", 4: "LDA_E_DEVICE",
                 5: "LDA_E_STATE"}
-MAX_TOPICS = 16384
+MAX_TOPICS = 32768
 MAX_DOC_LEN = 65535
 
 ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)

@@ -1138,6 +1138,325 @@ __global__ __launch_bounds__(1024, 4) void k_sampler_1024(DevState d, Params p, 
   sampler_body<1024>(d, p, t, stats);
 }
 
+// ---------------------------------------------------------- large K ----
+// When the fp64 W^' row does not fit in LDS (K above about 17,000 topics,
+// up to 32,768), the topics are split in two tiles, [0, KT) and [KT, K]
+// (topic K is the padding of D rows), and a region is walked three times:
+//   pass 0, tile 0: per token the S' terms of topics below KT and C1;
+//   pass 1, tile 1: the S' terms of the other topics, then the draw (Eq. 5);
+//                   draws in M, in the tile-1 part of S' or in a tile-1 Q'
+//                   block finish here, the others are recorded;
+//   pass 2, tile 0: the recorded draws finish.
+// The canonical order [K1 | S' ascending | Q' ascending] is unchanged: the
+// tile-0 part of S' precedes the tile-1 part.  A 16-lane group draws one
+// token at a time and reads its D row in chunks of kChunk slots; entries of
+// the other tile read a zero.  Per-token results between passes live in a
+// per-workgroup slice of global scratch.
+struct TileState {
+  const double *wt;  // the tile: W^' of topics [base, base + KT), zeros past the tile's end
+  uint32_t base, kt;
+};
+
+// W^' of a packed D entry's topic if it lies in the tile, else 0 (wt[kt] is 0).
+__device__ __forceinline__ double wt_of(const TileState &ts, uint32_t e) {
+  return ts.wt[min((e >> 16) - ts.base, ts.kt)];
+}
+
+// This lane's run of chunk ch of a row of `slots` padded slots; runs past
+// the row read the padding entry, and the header (slot 0) is padding too.
+__device__ __forceinline__ void load_run_masked(const uint32_t *__restrict__ row, uint32_t ch, uint32_t slots, int li,
+                                                uint32_t pad, uint32_t (&r)[kMaxRun]) {
+  const uint32_t q0 = ch * kChunk + uint32_t(li) * kMaxRun;
+  if (q0 < slots) {
+#pragma unroll
+    for (int i = 0; i < kMaxRun; ++i) r[i] = row[q0 + i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < kMaxRun; ++i) r[i] = pad;
+  }
+  if (q0 == 0u) r[0] = pad;
+}
+
+__device__ __forceinline__ double run_sum_tile(const uint32_t (&r)[kMaxRun], const TileState &ts) {
+  double s = 0.0;
+#pragma unroll
+  for (int i = 0; i < kMaxRun; ++i) s = __builtin_fma(double(r[i] & 0xFFFFu), wt_of(ts, r[i]), s);
+  return s;
+}
+
+// The S' draw inside one tile: the entry whose segment holds x, the tile's
+// terms starting at `base`; the chunks are walked again in order.  When
+// rounding leaves x past the tile's terms, the last positive term is taken.
+__device__ uint32_t tile_walk(const uint32_t *__restrict__ row, uint32_t slots, const TileState &ts, double base,
+                              double x, uint32_t pad, int grp, int li, uint32_t *__restrict__ hand) {
+  const uint32_t nch = (slots + kChunk - 1) / kChunk;
+  uint32_t r[kMaxRun];
+  int last_pos = -1;
+  double last_base = base;
+  uint32_t pick = nch;
+  double s = 0.0, incl = 0.0;
+  for (uint32_t ch = 0; ch < nch; ++ch) {
+    load_run_masked(row, ch, slots, li, pad, r);
+    s = run_sum_tile(r, ts);
+    incl = row_incl_scan(s);
+    const double total = __shfl(incl, kGroup - 1, kGroup);
+    if (total > 0.0) {
+      last_pos = int(ch);
+      last_base = base;
+    }
+    if (x < base + total) {
+      pick = ch;
+      break;
+    }
+    base += total;
+  }
+  if (pick == nch) {
+    // rounding: x at or past the end of the tile's terms
+    if (last_pos < 0) return uint32_t(-1);
+    pick = uint32_t(last_pos);
+    base = last_base;
+    load_run_masked(row, pick, slots, li, pad, r);
+    s = run_sum_tile(r, ts);
+    incl = row_incl_scan(s);
+  }
+  const int sel = run_lane(s, incl, base, x, grp);
+  const double start = base + __shfl(incl - s, sel, kGroup);
+  if (li == sel) {
+#pragma unroll
+    for (int i = 0; i < kMaxRun; ++i) hand[i] = r[i];
+  }
+  __builtin_amdgcn_wave_barrier();
+  const uint32_t mine = li < kMaxRun ? hand[li] : 0u;
+  const double term = li < kMaxRun ? double(mine & 0xFFFFu) * wt_of(ts, mine) : 0.0;
+  return pick_segment(mine >> 16, term, start, x, grp);
+}
+
+// Fills the tile [base, base + len) of the region's word (zeros elsewhere,
+// at K1 and at the padding topic K).
+__device__ void fill_tile(const DevState &d, const Params &p, uint32_t v, uint32_t K1, uint32_t base, uint32_t len,
+                          uint32_t kt, double *__restrict__ wt, int tid, int nthreads) {
+  const int K = p.K;
+  if (int32_t(v) < p.n_dense) {
+    const int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
+    for (uint32_t q = uint32_t(tid); q < kt + uint32_t(kGroup); q += uint32_t(nthreads)) {
+      const uint32_t k = base + q;
+      wt[q] = q < len && k < uint32_t(K) && k != K1 ? what(uint32_t(wrow[k]), p.beta, d.den[k]) : 0.0;
+    }
+  } else {
+    const int s = int(v) - p.n_dense;
+    const uint32_t *ents = d.ws_ent + d.ws_cap[s];
+    const uint32_t nnz = d.ws_nnz[s];
+    for (uint32_t q = uint32_t(tid); q < kt + uint32_t(kGroup); q += uint32_t(nthreads)) {
+      const uint32_t k = base + q;
+      wt[q] = q < len && k < uint32_t(K) && k != K1 ? what(0u, p.beta, d.den[k]) : 0.0;
+    }
+    __syncthreads();
+    for (uint32_t q = uint32_t(tid); q < nnz; q += uint32_t(nthreads)) {
+      const uint32_t ent = ents[q], k = ent >> 16;
+      if (k >= base && k < base + len && k < uint32_t(K) && k != K1) wt[k - base] = what(ent & 0xFFFFu, p.beta, d.den[k]);
+    }
+  }
+  __syncthreads();
+}
+
+constexpr int kTiledBlock = kTiledThreads;  // threads per workgroup of the tiled sampler (8 waves)
+
+__global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Params p, uint32_t t,
+                                                               unsigned long long *__restrict__ stats) {
+  extern __shared__ double lds[];
+  const int K = p.K;
+  const uint32_t kt = uint32_t(p.tile_topics);  // topics per tile, a multiple of kGroup
+  const int nb = (K + kGroup - 1) / kGroup;
+  double *wt = lds;                                  // [kt + kGroup]
+  double *qb = lds + kt + kGroup;                    // [nb + 1]: prefix of alpha*W^' over blocks of kGroup topics
+  uint32_t *s_hand = reinterpret_cast<uint32_t *>(qb + nb + 1);  // [kTiledBlock / kGroup * kMaxRun]
+  uint32_t *s_reg = s_hand + kTiledBlock / kGroup * kMaxRun;     // [4]
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int wave = tid / kWave, grp = lane / kGroup, li = lane % kGroup;
+  uint32_t *hand = s_hand + (tid / kGroup) * kMaxRun;
+  const uint32_t pad = uint32_t(K) << 16;
+  // per-workgroup scratch slices, indexed by the token's place in its region
+  double *sc_s = d.ts_s + size_t(blockIdx.x) * size_t(p.max_region);
+  double *sc_x = d.ts_x + size_t(blockIdx.x) * size_t(p.max_region);
+  uint32_t *sc_c1 = d.ts_c1 + size_t(blockIdx.x) * size_t(p.max_region);
+  uint32_t *sc_code = d.ts_code + size_t(blockIdx.x) * size_t(p.max_region);
+  unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0, n_reg = 0, n_dreg = 0, row_bytes = 0;
+  const int waves = kTiledBlock / kWave;
+  for (;;) {
+    if (tid == 0) {
+      const uint32_t r = atomicAdd(&d.counters[CNT_SAMPLER], 1u);
+      s_reg[3] = int64_t(r) < p.n_regions ? 1u : 0u;
+      if (s_reg[3]) {
+        s_reg[0] = d.region[3 * size_t(r)];
+        s_reg[1] = d.region[3 * size_t(r) + 1];
+        s_reg[2] = d.region[3 * size_t(r) + 2];
+      }
+    }
+    __syncthreads();
+    if (!s_reg[3]) break;
+    const uint32_t v = __builtin_amdgcn_readfirstlane(s_reg[0]);
+    const uint32_t b = __builtin_amdgcn_readfirstlane(s_reg[1]);
+    const uint32_t e = __builtin_amdgcn_readfirstlane(s_reg[2]);
+    __syncthreads();  // s_reg is rewritten by the next region's fetch
+    n_reg++;
+    if (int32_t(v) < p.n_dense) n_dreg++;
+    if (b == d.word_off[v])
+      row_bytes += int32_t(v) < p.n_dense ? 4ull * uint64_t(K) : 4ull * d.ws_nnz[int(v) - p.n_dense];
+    const WordRec rec = d.wrec[v];
+    const uint32_t K1 = rec.k1;
+    for (int pass = 0; pass < 3; ++pass) {
+      const uint32_t tbase = pass == 1 ? kt : 0u;
+      const uint32_t tlen = pass == 1 ? uint32_t(K) + 1u - kt : kt;
+      fill_tile(d, p, v, K1, tbase, tlen, kt, wt, tid, kTiledBlock);
+      const TileState ts{wt, tbase, kt};
+      if (pass < 2) {
+        // this tile's blocks of the Q' prefix, continuing the previous tile's
+        const int b0 = int(tbase) / kGroup, b1 = min(nb, int(tbase + tlen + kGroup - 1) / kGroup);
+        for (int blk = b0 + tid; blk < b1; blk += kTiledBlock) {
+          double sum = 0.0;
+          for (int i = 0; i < kGroup; ++i) sum += p.alpha * wt[(blk - b0) * kGroup + i];
+          qb[blk + 1] = sum;
+        }
+        __syncthreads();
+        if (wave == 0) {
+          const int n = b1 - b0;
+          const int per = (n + kWave - 1) / kWave;
+          const int q0 = min(n, lane * per), q1 = min(n, q0 + per);
+          double sum = 0.0;
+          for (int q = q0; q < q1; ++q) sum += qb[b0 + q + 1];
+          const double carry = pass == 0 ? 0.0 : qb[b0];
+          double run = carry + (group_incl_scan<kWave>(sum, lane) - sum);
+          for (int q = q0; q < q1; ++q) {
+            run += qb[b0 + q + 1];
+            qb[b0 + q + 1] = run;
+          }
+          if (pass == 0 && lane == 0) qb[0] = 0.0;
+        }
+        __syncthreads();
+      }
+      // four tokens per wave at a time, one per 16-lane group
+      for (uint32_t j0 = b + uint32_t(wave) * 4u; j0 < e; j0 += uint32_t(waves) * 4u) {
+        const uint32_t j = j0 + uint32_t(grp);
+        const uint32_t q = j - b;  // place in the region
+        bool live = j < e && d.z_w[j] == kUndecided;
+        if (pass == 2) live = live && sc_code[q] != 0u;
+        if (!live) continue;
+        const uint32_t off = d.wt_rowoff[j];
+        const uint32_t *row = d.d_ent + off;
+        const uint32_t nnz = row[0] & 0xFFFFu;
+        const uint32_t slots = d_row_slots(nnz);
+        const uint32_t nch = (slots + kChunk - 1) / kChunk;
+        if (pass == 0) {
+          // S' over the tile-0 topics, and C1 over the whole row
+          uint32_t r[kMaxRun];
+          double S0 = 0.0;
+          uint32_t c1 = 0xFFFFFFFFu;
+          for (uint32_t ch = 0; ch < nch; ++ch) {
+            load_run_masked(row, ch, slots, li, pad, r);
+            c1 = run_count_of<kMaxRun>(r, K1, c1);
+            S0 += group_sum<kGroup>(run_sum_tile(r, ts));
+          }
+          c1 = row_sum_u32(c1 <= 0xFFFFu ? c1 : 0u);
+          if (li == 0) {
+            sc_s[q] = S0;
+            sc_c1[q] = c1;
+            sc_code[q] = 0u;
+          }
+        } else if (pass == 1) {
+          uint32_t r[kMaxRun];
+          double S1 = 0.0;
+          for (uint32_t ch = 0; ch < nch; ++ch) {
+            load_run_masked(row, ch, slots, li, pad, r);
+            S1 += group_sum<kGroup>(run_sum_tile(r, ts));
+          }
+          const double S0 = sc_s[q];
+          const uint32_t c1 = sc_c1[q];
+          const double Mm = rec.a1 * (double(c1) + p.alpha);  // Eq. 7
+          const double S = S0 + S1;
+          const double u = uniform_draw(p.seed, t, d.wt_key[j]);
+          const double x = u * ((Mm + S) + rec.qp);
+          uint32_t topic = K1, code = 0u;
+          double keep = 0.0;
+          if (x < Mm) {
+            if (li == 0) n_after_s++;
+          } else if (x < Mm + S) {
+            if (x < Mm + S0) {
+              code = 1u;  // S' draw in tile 0
+            } else {
+              const uint32_t k = tile_walk(row, slots, ts, Mm + S0, x, pad, grp, li, hand);
+              if (k == uint32_t(-1)) code = 1u;  // nothing positive in tile 1: rounding at the tile edge
+              else topic = k;
+            }
+          } else {
+            const double qs = Mm + S;
+            const double xq = x - qs;
+            if (!(xq < qb[nb])) {
+              topic = (K1 == uint32_t(K - 1)) ? uint32_t(K - 2) : uint32_t(K - 1);  // last positive segment
+            } else {
+              // the largest block lo < nb with qb[lo] <= xq
+              int lo = 0, hi = nb;
+              while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (qb[mid] <= xq) lo = mid;
+                else hi = mid;
+              }
+              const uint32_t k = uint32_t(lo * kGroup + li);
+              if (uint32_t(lo * kGroup) >= kt) {
+                const double term = p.alpha * wt[k - kt];
+                topic = pick_segment(k, term, qs + qb[lo], x, grp);
+              } else {
+                code = 2u | (uint32_t(lo) << 2);  // Q' draw in a tile-0 block
+                keep = qs;
+              }
+            }
+          }
+          if (li == 0) {
+            n_sampled++;
+            nnz_sum += nnz;
+            if (code) {
+              sc_code[q] = code;
+              sc_x[q] = x;
+              sc_s[q] = keep;
+            } else {
+              d.z_w[j] = uint16_t(topic);
+            }
+          }
+        } else {
+          const uint32_t code = sc_code[q];
+          const double x = sc_x[q];
+          uint32_t topic;
+          if (code == 1u) {
+            const double Mm = rec.a1 * (double(sc_c1[q]) + p.alpha);
+            topic = tile_walk(row, slots, ts, Mm, x, pad, grp, li, hand);
+            if (topic == uint32_t(-1)) topic = K1;  // no positive S' term below KT: cannot happen for x in S'
+          } else {
+            const int lo = int(code >> 2);
+            const uint32_t k = uint32_t(lo * kGroup + li);
+            const double term = p.alpha * wt[k];
+            topic = pick_segment(k, term, sc_s[q] + qb[lo], x, grp);
+          }
+          if (li == 0) d.z_w[j] = uint16_t(topic);
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // per-lane counts of group leaders, summed over the wave
+  n_sampled = group_sum_u64<kWave>(n_sampled);
+  n_after_s = group_sum_u64<kWave>(n_after_s);
+  nnz_sum = group_sum_u64<kWave>(nnz_sum);
+  if (lane == 0) {
+    if (n_sampled) atomicAdd(&stats[ST_SAMPLED], n_sampled);
+    if (n_after_s) atomicAdd(&stats[ST_SKIP_AFTER_S], n_after_s);
+    if (nnz_sum) atomicAdd(&stats[ST_NNZ], nnz_sum);
+  }
+  if (tid == 0) {
+    if (n_reg) atomicAdd(&stats[ST_REGIONS], n_reg);
+    if (n_dreg) atomicAdd(&stats[ST_DENSE_REGIONS], n_dreg);
+    if (row_bytes) atomicAdd(&stats[ST_ROW_BYTES], row_bytes);
+  }
+}
+
 // Rows of split dense words are accumulated with atomics; clear them and T.
 __global__ void k_zero_split(DevState d, Params p) {
   const int64_t total = int64_t(p.n_dense) * p.K;
@@ -1154,14 +1473,15 @@ __global__ void k_zero_split(DevState d, Params p) {
 __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
-  uint32_t *hist = ldsu;      // [K]
-  uint32_t *tloc = ldsu + K;  // [K]
+  uint32_t *hist = ldsu;                           // [K]
+  uint32_t *tloc = p.big_k ? nullptr : ldsu + K;  // [K]; large K: T is added per region instead
   __shared__ uint32_t s_reg[3];
   __shared__ int s_valid;
   __shared__ uint32_t s_scan[kBlock / kWave];
   const int tid = threadIdx.x;
   uint32_t bad = 0;
-  for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
+  if (tloc)
+    for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
   for (;;) {
     if (tid == 0) {
       const uint32_t r = atomicAdd(&d.counters[CNT_REBUILD_W], 1u);
@@ -1203,11 +1523,17 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
         if (hist[k]) out[off++] = (uint32_t(k) << 16) | hist[k];
       if (tid == 0) d.ws_nnz[s] = total;
     }
-    for (int k = tid; k < K; k += kBlock) tloc[k] += hist[k];
+    if (tloc) {
+      for (int k = tid; k < K; k += kBlock) tloc[k] += hist[k];
+    } else {
+      for (int k = tid; k < K; k += kBlock)
+        if (hist[k]) atomicAdd(&d.T[k], hist[k]);
+    }
     __syncthreads();
   }
-  for (int k = tid; k < K; k += kBlock)
-    if (tloc[k]) atomicAdd(&d.T[k], tloc[k]);
+  if (tloc)
+    for (int k = tid; k < K; k += kBlock)
+      if (tloc[k]) atomicAdd(&d.T[k], tloc[k]);
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
 }
 
@@ -1313,7 +1639,8 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
 __global__ __launch_bounds__(kBlock) void k_loglik(DevState d, Params p) {
   extern __shared__ double lds[];
   const int K = p.K;
-  double *wh = lds;
+  // large K: the row lives in the workgroup's slice of global scratch
+  double *wh = p.big_k ? d.wscratch + size_t(blockIdx.x) * size_t(K) : lds;
   __shared__ uint32_t s_reg[3];
   __shared__ int s_valid;
   __shared__ uint32_t s_r;
@@ -1439,10 +1766,10 @@ hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s) {
 }
 
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
-  const size_t lds = sizeof(uint16_t) * size_t(p.K) * (kBlock / kWave);
+  const size_t lds = sizeof(uint16_t) * size_t(p.K) * size_t(p.doc_waves);
   hipError_t err = allow_lds(k_doc_pass, lds);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_doc_pass, dim3(uint32_t(p.grid_docs)), dim3(kBlock), lds, s, d, p, t, d.stats);
+  hipLaunchKernelGGL(k_doc_pass, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), lds, s, d, p, t, d.stats);
   return hipGetLastError();
 }
 
@@ -1483,7 +1810,19 @@ int sampler_block(int K, int want) {
   return best;
 }
 
+int tiled_topics(int K) { return ((K + 2) / 2 + kGroup - 1) / kGroup * kGroup; }
+size_t tiled_lds_bytes(int K, int kt) {
+  const size_t nb = size_t((K + kGroup - 1) / kGroup);
+  return sizeof(double) * (size_t(kt) + kGroup + nb + 1) + sizeof(uint32_t) * (kTiledBlock / kGroup * kMaxRun + 4);
+}
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
+  if (p.big_k) {
+    const size_t lds = tiled_lds_bytes(p.K, p.tile_topics);
+    hipError_t err = allow_lds(k_sampler_tiled, lds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_sampler_tiled, dim3(uint32_t(tiled_grid(p))), dim3(kTiledBlock), lds, s, d, p, t, d.stats);
+    return hipGetLastError();
+  }
   const int nb = p.sampler_block;
   const size_t lds = sampler_lds_bytes(p.K, nb);
   const uint32_t grid = uint32_t(std::max<int64_t>(1, int64_t(p.grid_regions) * kBlock / nb));
@@ -1509,17 +1848,17 @@ hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s) {
   hipLaunchKernelGGL(k_zero_split, dim3(uint32_t(zb)), dim3(kBlock), 0, s, d, p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  err = allow_lds(k_rebuild_w, sizeof(uint32_t) * 2 * size_t(p.K));
+  const size_t wlds = sizeof(uint32_t) * (p.big_k ? 1 : 2) * size_t(p.K);
+  err = allow_lds(k_rebuild_w, wlds);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_rebuild_w, dim3(uint32_t(p.grid_regions)), dim3(kBlock), sizeof(uint32_t) * 2 * size_t(p.K),
-                     s, d, p);
+  hipLaunchKernelGGL(k_rebuild_w, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   const size_t half = size_t((p.K + 1) / 2);
-  err = allow_lds(k_rebuild_d, sizeof(uint32_t) * half * (kBlock / kWave));
+  err = allow_lds(k_rebuild_d, sizeof(uint32_t) * half * size_t(p.doc_waves));
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kBlock),
-                     sizeof(uint32_t) * half * (kBlock / kWave), s, d, p);
+  hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves),
+                     sizeof(uint32_t) * half * size_t(p.doc_waves), s, d, p);
   return hipGetLastError();
 }
 
@@ -1531,9 +1870,12 @@ hipError_t launch_sum_nnz(const DevState &d, const Params &p, unsigned long long
 }
 
 hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s) {
-  hipError_t err0 = allow_lds(k_loglik, sizeof(double) * size_t(p.K));
+  const size_t lds = p.big_k ? 0 : sizeof(double) * size_t(p.K);
+  hipError_t err0 = allow_lds(k_loglik, lds);
   if (err0 != hipSuccess) return err0;
-  hipLaunchKernelGGL(k_loglik, dim3(uint32_t(p.grid_regions)), dim3(kBlock), sizeof(double) * size_t(p.K), s, d, p);
+  // large K: one workgroup per slice of the W^' scratch
+  const uint32_t grid = uint32_t(p.big_k ? loglik_grid_big_k(p) : p.grid_regions);
+  hipLaunchKernelGGL(k_loglik, dim3(grid), dim3(kBlock), lds, s, d, p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(k_loglik_reduce, dim3(1), dim3(kBlock), 0, s, d.ll_part, p.n_regions, d.ll_out);

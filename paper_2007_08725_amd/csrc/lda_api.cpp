@@ -142,10 +142,6 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   int cus = 0, lds_max = 0;
   HIP_TRY(h, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device));
   HIP_TRY(h, hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device));
-  const size_t need = sizeof(double) * (size_t(L.K) + size_t(L.K) / 16 + 2) + 256;
-  if (need > size_t(lds_max))
-    return fail(h, LDA_E_RANGE, "K = " + std::to_string(L.K) + " needs " + std::to_string(need) +
-                                    " bytes of LDS per workgroup; the device allows " + std::to_string(lds_max));
   if (o && o->stream) {
     h->stream = static_cast<hipStream_t>(o->stream);
   } else {
@@ -154,10 +150,24 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   }
   Params &p = h->p;
   p.grid_regions = std::max(1, cus * 8);
-  p.sampler_block = sampler_block(p.K, o ? o->sampler_block : 0);
-  if (!p.sampler_block)
-    return fail(h, LDA_E_RANGE, "no sampler workgroup of " + std::string(o && o->sampler_block ? std::to_string(o->sampler_block) + " threads" : "any size") +
-                                    " fits the LDS of K = " + std::to_string(L.K));
+  const int want = o ? o->sampler_block : 0;
+  p.sampler_block = sampler_block(p.K, want);
+  if (!p.sampler_block && want)
+    return fail(h, LDA_E_RANGE, "no sampler workgroup of " + std::to_string(want) + " threads fits the LDS of K = " +
+                                    std::to_string(L.K));
+  if (!p.sampler_block) {
+    // the W^' row does not fit one workgroup's LDS: the tiled sampler
+    p.big_k = 1;
+    p.tile_topics = tiled_topics(p.K);
+    p.sampler_block = kTiledThreads;
+    if (tiled_lds_bytes(p.K, p.tile_topics) > size_t(lds_max))
+      return fail(h, LDA_E_RANGE, "K = " + std::to_string(L.K) + " needs " +
+                                      std::to_string(tiled_lds_bytes(p.K, p.tile_topics)) +
+                                      " bytes of LDS per workgroup even in tiles; the device allows " +
+                                      std::to_string(lds_max));
+  }
+  // the doc pass and the D rebuild keep a table of K 16-bit counts per wave
+  p.doc_waves = std::max(1, std::min(kBlock / 64, int(size_t(lds_max) / (sizeof(uint32_t) * size_t((p.K + 1) / 2)))));
   p.grid_docs = std::max(1, cus * 8);
   const size_t n = size_t(L.n);
   const bool identity = L.key_identity;
@@ -259,6 +269,17 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.counters, kCounters));
   LDA_TRY(dalloc(h, &h->stats_base, size_t(kStatSlots) * kStatsPerIter));
   LDA_TRY(dalloc(h, &d.ll_part, size_t(L.n_regions)));
+  if (p.big_k) {
+    uint32_t max_region = 1;
+    for (size_t r = 0; r < L.region.size(); r += 3) max_region = std::max(max_region, L.region[r + 2] - L.region[r + 1]);
+    p.max_region = int32_t(max_region);
+    const size_t slots = size_t(tiled_grid(p)) * size_t(max_region);
+    LDA_TRY(dalloc(h, &d.ts_s, slots));
+    LDA_TRY(dalloc(h, &d.ts_x, slots));
+    LDA_TRY(dalloc(h, &d.ts_c1, slots));
+    LDA_TRY(dalloc(h, &d.ts_code, slots));
+    LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(L.K)));
+  }
   LDA_TRY(dalloc(h, &d.ll_out, 1));
   d.stats = h->stats_base;
   LDA_TRY(upload(h, d.region, L.region));
@@ -299,7 +320,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   if (!word || !doc) return fail(nullptr, LDA_E_ARG, "word or doc is NULL");
   if (n_tokens <= 0) return fail(nullptr, LDA_E_ARG, "n_tokens must be positive");
   if (V <= 0) return fail(nullptr, LDA_E_ARG, "V must be positive");
-  if (K < 2 || K > LDA_MAX_TOPICS) return fail(nullptr, LDA_E_ARG, "K must be in [2, 16384]");
+  if (K < 2 || K > LDA_MAX_TOPICS) return fail(nullptr, LDA_E_ARG, "K must be in [2, 32768]");
   if (!std::isfinite(alpha) || !(alpha > 0.0)) return fail(nullptr, LDA_E_ARG, "alpha must be finite and positive");
   if (!std::isfinite(beta) || !(beta > 0.0)) return fail(nullptr, LDA_E_ARG, "beta must be finite and positive");
   int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0, two_branch = 0;

@@ -12,7 +12,7 @@
 
 namespace lda {
 
-// A 16-bit topic slot holds a topic (< K <= 16384) or kUndecided for a token
+// A 16-bit topic slot holds a topic (< K <= 32768) or kUndecided for a token
 // the step-3 test has not decided.
 constexpr uint16_t kUndecided = 0x8000;
 // Slack entries after the last D row.
@@ -122,6 +122,12 @@ struct DevState {
   unsigned long long *stats;    // [8]
   double *ll_part;              // [n_regions]
   double *ll_out;               // [1]
+  // large K only (the tiled sampler): per-workgroup slices of max_region
+  // entries carrying a token's S' part, C1 and recorded draw between passes,
+  // and the LLPT kernel's W^' rows
+  double *ts_s, *ts_x;
+  uint32_t *ts_c1, *ts_code;
+  double *wscratch;
 };
 
 struct Params {
@@ -138,6 +144,10 @@ struct Params {
   int32_t grid_regions;  // persistent workgroups for region kernels
   int32_t sampler_block; // threads per sampler workgroup: 256, 512 or 1024
   int32_t grid_docs;     // persistent workgroups for doc kernels
+  int32_t big_k;         // the W^' row does not fit LDS: tiled sampler, LDS-light rebuilds (K <= 32768)
+  int32_t tile_topics;   // topics per tile of the tiled sampler (a multiple of 16)
+  int32_t max_region;    // tokens of the largest region
+  int32_t doc_waves;     // waves per workgroup of the doc pass and the D rebuild (LDS tables of K entries per wave)
   uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
 
@@ -156,6 +166,14 @@ hipError_t launch_fill_undecided(const DevState &d, const Params &p, hipStream_t
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 int sampler_block(int K, int want);
+// Large K: topics per tile and the tiled sampler's dynamic LDS.
+int tiled_topics(int K);
+size_t tiled_lds_bytes(int K, int kt);
+constexpr int kTiledThreads = 512;
+// Workgroups of the tiled sampler (one per CU: its LDS fills a CU) and of the
+// large-K LLPT kernel; the scratch slices are sized for these grids.
+inline int tiled_grid(const Params &p) { return p.grid_regions / 8 > 0 ? p.grid_regions / 8 : 1; }
+inline int loglik_grid_big_k(const Params &p) { return tiled_grid(p); }
 hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_sum_nnz(const DevState &d, const Params &p, unsigned long long *out, hipStream_t s);

@@ -252,6 +252,7 @@ def _edge_cases():
     yield "longest_doc", _Tiny(rng.integers(0, 50, 65535), np.zeros(65535, np.int32), 50, 16, 0.2)
     yield "max_topics", _Tiny(rng.integers(0, 40, 3000), np.sort(rng.integers(0, 30, 3000)), 40, 16384, 0.01)
     yield "ragged_K", _Tiny(rng.integers(0, 300, 20000), np.sort(rng.integers(0, 200, 20000)), 300, 1013, 0.05)
+    yield "max_topics_tiled", _Tiny(rng.integers(0, 40, 3000), np.sort(rng.integers(0, 30, 3000)), 40, 32768, 0.01)
 
 
 @pytest.mark.parametrize("name,c", list(_edge_cases()), ids=[e[0] for e in _edge_cases()])
@@ -291,6 +292,55 @@ def test_sampler_block_sizes_at_large_K(K, block):
     assert st["sampler_block"] == (block or st["sampler_block"]) and st["sampler_block"] in (256, 512, 1024)
     compare_draws(cnt["z"], zo, flags, c.N)
     check_counts_are_histograms(c, cnt, c.K)
+
+
+def _large_k_corpus(K):
+    """About 100K tokens over 40 words: the top word holds more than K tokens,
+    so it is dense and split into regions; the rest are sparse."""
+    rng = np.random.default_rng(11)
+    n_docs, V = 1000, 40
+    lens = rng.integers(60, 140, n_docs)
+    p = 1.0 / np.arange(1, V + 1) ** 1.5
+    word = rng.choice(V, size=int(lens.sum()), p=p / p.sum()).astype(np.int32)
+    doc = np.repeat(np.arange(n_docs), lens).astype(np.int32)
+    return _Tiny(word, doc, V, K, 0.05)
+
+
+@pytest.mark.parametrize("K", [32768, 20000])
+def test_large_k_tiled_sampler_follows_the_oracle(K):
+    """K above what one workgroup's LDS holds as an fp64 row: the tiled sampler
+    (two topic tiles, three passes per region) draws what the oracle draws, over
+    three snapshots, with dense split words and sparse words; counts and LLPT too."""
+    c = _large_k_corpus(K)
+    cnt_w = np.bincount(c.word, minlength=c.V)
+    assert (cnt_w > K).sum() >= 1  # a dense word, split into regions of 10,000
+    say("large K=%d N=%d" % (K, c.N))
+    kw = dict(M=c.n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta)
+    z = oracle.init_topics(c.N, c.K, SEED)
+    with lda_make(c) as m:
+        for t in range(3):
+            zo, flags, _ = oracle.iterate(c.word, c.doc, z, seed=SEED, t=t, **kw)
+            m.set_assignments(z, t)
+            st = m.iterate(1, stats=True)[0]
+            assert st["sampler_block"] == 512 and st["sampled"] + st["skip_step3"] == c.N
+            cnt = m.counts()
+            compare_draws(cnt["z"], zo, flags, c.N)
+            check_counts_are_histograms(c, cnt, c.K)
+            z = zo
+        ll = m.loglik()
+    assert ll == pytest.approx(oracle.llpt(c.word, c.doc, cnt["z"], **kw), rel=1e-12, abs=1e-14)
+
+
+def test_large_k_schedule_invariance():
+    """The tiled sampler's draws do not depend on the region size."""
+    c = _large_k_corpus(32768)
+    with lda_make(c) as a:
+        a.iterate(2)
+        za = a.counts(D=False, W=False)["z"]
+    with lda_make(c, region_tokens=777) as b:
+        b.iterate(2)
+        zb = b.counts(D=False, W=False)["z"]
+    assert np.array_equal(za, zb)
 
 def lda_make(c, **kw):
     import paper_2007_08725_amd as lda
