@@ -76,7 +76,8 @@ class CorpusSpec:
     theta_conc: float = 0.1
 
 
-# The five workloads.  c4 reuses c2's corpus (same seed) with K = 10,000.
+# The five workloads, plus c6 for the largest topic count.  c4 and c6 reuse
+# c2's corpus (same seed) with K = 10,000 and K = 32,768.
 SPECS = {
     "c1": CorpusSpec("c1", 1_000, ("poisson", 50.0), 2_000, 1.0, 20, 16, 50.0 / 16, iters=10, seed=1001),
     "c2": CorpusSpec("c2", 300_000, ("poisson", 330.0), 102_000, 1.07, 200, 1000, 0.05, seed=1002),
@@ -84,6 +85,7 @@ SPECS = {
     "c4": CorpusSpec("c4", 300_000, ("poisson", 330.0), 102_000, 1.07, 200, 10_000, 0.1, seed=1002),
     "c5": CorpusSpec("c5", 20_000_000, ("lognormal", 150.0, 1.5, 50_000), 1_000_000, 1.2, 1000, 1000, 0.05,
                      seed=1005),
+    "c6": CorpusSpec("c6", 300_000, ("poisson", 330.0), 102_000, 1.07, 200, 32_768, 0.05, seed=1002),
 }
 
 SAMPLER_SEED = 42

@@ -214,40 +214,13 @@ __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den
 }
 
 // Step 1 of Sec. 3.2 and the per-word Q' of Sec. 2.2 ("Q tree once per word").
-__global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
-  const int r = blockIdx.x, tid = threadIdx.x;
-  const int K = p.K;
-  __shared__ double sv[kBlock * kTop];
-  __shared__ uint32_t sk[kBlock * kTop];
-  __shared__ double scratch[kBlock / kWave];
-  const bool dense = r < p.n_dense;
-  const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
-  const uint32_t *ents = nullptr;
-  uint32_t nnz = 0;
-  if (!dense) {
-    const int s = r - p.n_dense;
-    ents = d.ws_ent + d.ws_cap[s];
-    nnz = d.ws_nnz[s];
-  }
-  // sparse rows: each thread walks a contiguous chunk of topics
-  const int cs = (K + kBlock - 1) / kBlock;
-  const int c0 = min(K, tid * cs), c1 = min(K, c0 + cs);
+struct WordTop {
+  uint32_t k1, k2, k3;
+  double a1, a2, a3, a4;
+};
 
-  TopN t;
-  for (int q = 0; q < kTop; ++q) {
-    t.v[q] = -1.0;
-    t.k[q] = 0xFFFFFFFFu;
-  }
-  if (dense) {
-    for (int k = tid; k < K; k += kBlock) top_insert(t, what(uint32_t(wrow[k]), p.beta, d.den[k]), uint32_t(k));
-  } else {
-    uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
-    for (int k = c0; k < c1; ++k) {
-      uint32_t c = 0;
-      if (e < nnz && (ents[e] >> 16) == uint32_t(k)) c = ents[e++] & 0xFFFFu;
-      top_insert(t, what(c, p.beta, d.den[k]), uint32_t(k));
-    }
-  }
+// Block-wide top kTop of the threads' lists (sv, sk: kBlock * kTop slots).
+__device__ void block_top(TopN &t, double *__restrict__ sv, uint32_t *__restrict__ sk, int tid, WordTop &out) {
   for (int q = 0; q < kTop; ++q) {
     sv[tid * kTop + q] = t.v[q];
     sk[tid * kTop + q] = t.k[q];
@@ -266,8 +239,136 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
     }
     __syncthreads();
   }
-  const uint32_t K1 = sk[0], K2 = sk[1], K3 = K >= 3 ? sk[2] : 0xFFFFFFFFu;
-  const double a1 = sv[0], a2 = sv[1], a3 = K >= 3 ? sv[2] : 0.0, a4 = K >= 4 ? sv[3] : 0.0;
+  out.k1 = sk[0];
+  out.k2 = sk[1];
+  out.k3 = sk[2];
+  out.a1 = sv[0];
+  out.a2 = sv[1];
+  out.a3 = sv[2] > 0.0 ? sv[2] : 0.0;
+  out.a4 = sv[3] > 0.0 ? sv[3] : 0.0;
+}
+
+// The sampler's and the skip test's per-word records.  In two-branch mode
+// (Sec. 2.2) the max-topic branch is empty (a1 = 0, K1 = K, a topic no row
+// holds with a count) and Q' is the full Q.
+__device__ void write_word_records(const DevState &d, const Params &p, int r, const WordTop &top, double q, double sw) {
+  const int K = p.K;
+  const uint32_t K3 = K >= 3 ? top.k3 : 0xFFFFFFFFu;
+  WordRec rec;
+  rec.a1 = p.two_branch ? 0.0 : top.a1;
+  rec.a2 = top.a2;
+  rec.a3 = K >= 3 ? top.a3 : 0.0;
+  rec.qp = q;
+  rec.sumw = sw;
+  rec.k1 = p.two_branch ? uint32_t(K) : top.k1;
+  rec.k2 = top.k2;
+  d.wrec[r] = rec;
+  SkipRec sr;
+  sr.k12 = top.k1 | (top.k2 << 16);
+  sr.k3 = K3;
+  sr.a1 = float(top.a1);
+  sr.a2 = float(top.a2);
+  sr.a3 = float(K >= 3 ? top.a3 : 0.0);
+  sr.a4 = float(K >= 4 ? top.a4 : 0.0);
+  sr.qp = float(q);
+  sr.pad = 0u;
+  d.wskip[r] = sr;
+}
+
+// Large K: the sum over all topics of beta/den[k] (one workgroup, a fixed
+// order), for the sparse words' sums in k_word_pre.
+__global__ __launch_bounds__(kBlock) void k_beta_sum(DevState d, Params p) {
+  __shared__ double scratch[kBlock / kWave];
+  const int K = p.K;
+  const int cs = (K + kBlock - 1) / kBlock;
+  const int c0 = min(K, int(threadIdx.x) * cs), c1 = min(K, c0 + cs);
+  double s = 0.0;
+  for (int k = c0; k < c1; ++k) s += what(0u, p.beta, d.den[k]);
+  s = block_sum(s, scratch);
+  if (threadIdx.x == 0) d.beta_sum[0] = s;
+}
+
+__global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const int K = p.K;
+  __shared__ double sv[kBlock * kTop];
+  __shared__ uint32_t sk[kBlock * kTop];
+  __shared__ double scratch[kBlock / kWave];
+  const bool dense = r < p.n_dense;
+  const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
+  const uint32_t *ents = nullptr;
+  uint32_t nnz = 0;
+  if (!dense) {
+    const int s = r - p.n_dense;
+    ents = d.ws_ent + d.ws_cap[s];
+    nnz = d.ws_nnz[s];
+  }
+  // sparse rows: each thread walks a contiguous chunk of topics
+  const int cs = (K + kBlock - 1) / kBlock;
+  const int c0 = min(K, tid * cs), c1 = min(K, c0 + cs);
+  __shared__ int s_full;
+
+  TopN t;
+  for (int q = 0; q < kTop; ++q) {
+    t.v[q] = -1.0;
+    t.k[q] = 0xFFFFFFFFu;
+  }
+  if (!dense && p.sparse_pre) {
+    // Large K, sparse word: W^ = beta/den[k] on every topic outside the row.
+    // The top values come from the row's topics and from the first topics
+    // outside the row in the list of all topics by ascending T (descending
+    // beta/den[k], lowest id first on ties); the sums use the sum of
+    // beta/den[k] over all topics, corrected on the row's topics.
+    double snz = 0.0, sb = 0.0;
+    for (uint32_t q = uint32_t(tid); q < nnz; q += kBlock) {
+      const uint32_t ent = ents[q], k = ent >> 16;
+      const double w = what(ent & 0xFFFFu, p.beta, d.den[k]);
+      top_insert(t, w, k);
+      snz += w;
+      sb += what(0u, p.beta, d.den[k]);
+    }
+    if (tid == 0) {
+      int found = 0;
+      const int want = min(kTop, K - int(nnz));
+      for (int i = 0; i < p.top_list && found < want; ++i) {
+        const uint32_t k = d.topic_order[i];
+        const uint32_t lb = row_lower_bound(ents, nnz, k);
+        if (lb < nnz && (ents[lb] >> 16) == k) continue;
+        top_insert(t, what(0u, p.beta, d.den[k]), k);
+        found++;
+      }
+      s_full = found < want;  // the list ran out: scan every topic instead
+    }
+    snz = block_sum(snz, scratch);
+    sb = block_sum(sb, scratch);
+    __syncthreads();
+    if (!s_full) {
+      WordTop top;
+      block_top(t, sv, sk, tid, top);
+      if (tid == 0) {
+        const double sw = (d.beta_sum[0] - sb) + snz;
+        write_word_records(d, p, r, top, p.two_branch ? p.alpha * sw : p.alpha * (sw - top.a1), sw);
+      }
+      return;
+    }
+    for (int q = 0; q < kTop; ++q) {
+      t.v[q] = -1.0;
+      t.k[q] = 0xFFFFFFFFu;
+    }
+  }
+  if (dense) {
+    for (int k = tid; k < K; k += kBlock) top_insert(t, what(uint32_t(wrow[k]), p.beta, d.den[k]), uint32_t(k));
+  } else {
+    uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
+    for (int k = c0; k < c1; ++k) {
+      uint32_t c = 0;
+      if (e < nnz && (ents[e] >> 16) == uint32_t(k)) c = ents[e++] & 0xFFFFu;
+      top_insert(t, what(c, p.beta, d.den[k]), uint32_t(k));
+    }
+  }
+  WordTop top;
+  block_top(t, sv, sk, tid, top);
+  const uint32_t K1 = top.k1;
 
   double q = 0.0, sw = 0.0;
   if (dense) {
@@ -288,30 +389,7 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
   }
   q = block_sum(q, scratch);
   sw = block_sum(sw, scratch);
-  if (tid == 0) {
-    // the sampler's record; in two-branch mode (Sec. 2.2) the max-topic
-    // branch is empty (a1 = 0, K1 = K, a topic no row holds with a count)
-    // and Q' is the full Q
-    WordRec rec;
-    rec.a1 = p.two_branch ? 0.0 : a1;
-    rec.a2 = a2;
-    rec.a3 = a3;
-    rec.qp = q;
-    rec.sumw = sw;
-    rec.k1 = p.two_branch ? uint32_t(K) : K1;
-    rec.k2 = K2;
-    d.wrec[r] = rec;
-    SkipRec sr;
-    sr.k12 = K1 | (K2 << 16);
-    sr.k3 = K3;
-    sr.a1 = float(a1);
-    sr.a2 = float(a2);
-    sr.a3 = float(a3);
-    sr.a4 = float(a4);
-    sr.qp = float(q);
-    sr.pad = 0u;
-    d.wskip[r] = sr;
-  }
+  if (tid == 0) write_word_records(d, p, r, top, q, sw);
 }
 
 // Steps 2 and 3: per document, C1 = D[d][K1], C2 = D[d][K2], u, M, S_est and
@@ -1195,8 +1273,12 @@ __device__ uint32_t tile_walk(const uint32_t *__restrict__ row, uint32_t slots, 
   double last_base = base;
   uint32_t pick = nch;
   double s = 0.0, incl = 0.0;
+  uint32_t rn[kMaxRun];
+  load_run_masked(row, 0, slots, li, pad, rn);
   for (uint32_t ch = 0; ch < nch; ++ch) {
-    load_run_masked(row, ch, slots, li, pad, r);
+#pragma unroll
+    for (int i = 0; i < kMaxRun; ++i) r[i] = rn[i];
+    if (ch + 1 < nch) load_run_masked(row, ch + 1, slots, li, pad, rn);  // the next chunk's loads, in flight meanwhile
     s = run_sum_tile(r, ts);
     incl = row_incl_scan(s);
     const double total = __shfl(incl, kGroup - 1, kGroup);
@@ -1260,6 +1342,7 @@ __device__ void fill_tile(const DevState &d, const Params &p, uint32_t v, uint32
 }
 
 constexpr int kTiledBlock = kTiledThreads;  // threads per workgroup of the tiled sampler (8 waves)
+constexpr int kTiledAhead = 4;              // chunks whose loads a group issues together
 
 __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Params p, uint32_t t,
                                                                unsigned long long *__restrict__ stats) {
@@ -1347,15 +1430,21 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
         const uint32_t slots = d_row_slots(nnz);
         const uint32_t nch = (slots + kChunk - 1) / kChunk;
         if (pass == 0) {
-          // S' over the tile-0 topics, and C1 over the whole row
-          uint32_t r[kMaxRun];
-          double S0 = 0.0;
+          // S' over the tile-0 topics, and C1 over the whole row; the
+          // loads of up to kTiledAhead chunks are issued together
+          double s0 = 0.0;
           uint32_t c1 = 0xFFFFFFFFu;
-          for (uint32_t ch = 0; ch < nch; ++ch) {
-            load_run_masked(row, ch, slots, li, pad, r);
-            c1 = run_count_of<kMaxRun>(r, K1, c1);
-            S0 += group_sum<kGroup>(run_sum_tile(r, ts));
+          for (uint32_t c0 = 0; c0 < nch; c0 += kTiledAhead) {
+            uint32_t r[kTiledAhead][kMaxRun];
+#pragma unroll
+            for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
+#pragma unroll
+            for (int c = 0; c < kTiledAhead; ++c) {
+              c1 = run_count_of<kMaxRun>(r[c], K1, c1);
+              s0 += run_sum_tile(r[c], ts);
+            }
           }
+          const double S0 = group_sum<kGroup>(s0);
           c1 = row_sum_u32(c1 <= 0xFFFFu ? c1 : 0u);
           if (li == 0) {
             sc_s[q] = S0;
@@ -1363,12 +1452,15 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
             sc_code[q] = 0u;
           }
         } else if (pass == 1) {
-          uint32_t r[kMaxRun];
-          double S1 = 0.0;
-          for (uint32_t ch = 0; ch < nch; ++ch) {
-            load_run_masked(row, ch, slots, li, pad, r);
-            S1 += group_sum<kGroup>(run_sum_tile(r, ts));
+          double s1 = 0.0;
+          for (uint32_t c0 = 0; c0 < nch; c0 += kTiledAhead) {
+            uint32_t r[kTiledAhead][kMaxRun];
+#pragma unroll
+            for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
+#pragma unroll
+            for (int c = 0; c < kTiledAhead; ++c) s1 += run_sum_tile(r[c], ts);
           }
+          const double S1 = group_sum<kGroup>(s1);
           const double S0 = sc_s[q];
           const uint32_t c1 = sc_c1[q];
           const double Mm = rec.a1 * (double(c1) + p.alpha);  // Eq. 7
@@ -1470,6 +1562,7 @@ __global__ void k_zero_split(DevState d, Params p) {
 // W rebuild from the word-ordered topics: LDS histogram per region; dense
 // rows written whole (or added with atomics when the word is split), sparse
 // rows compacted to ascending packed entries; T accumulated per workgroup.
+// W rebuild for moderate K: per region a K-entry histogram, scanned in full.
 __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
@@ -1537,11 +1630,100 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
 }
 
+// W rebuild for large K: the touched topics of a region are marked in a
+// bitmap, so the work per region follows its tokens, not K.
+__global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p) {
+  extern __shared__ uint32_t ldsu[];
+  const int K = p.K;
+  const int nw = (K + 31) / 32;
+  uint32_t *hist = ldsu;                              // [K]: the region's topic counts
+  uint32_t *bits = ldsu + K;                          // [nw]: topics with a nonzero count
+  uint32_t *tloc = p.big_k ? nullptr : bits + nw;     // [K]; large K: T is added per region instead
+  __shared__ uint32_t s_reg[3];
+  __shared__ int s_valid;
+  __shared__ uint32_t s_scan[kBlock / kWave];
+  const int tid = threadIdx.x;
+  uint32_t bad = 0;
+  for (int k = tid; k < K; k += kBlock) hist[k] = 0u;
+  for (int q = tid; q < nw; q += kBlock) bits[q] = 0u;
+  if (tloc)
+    for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
+  __syncthreads();
+  for (;;) {
+    if (tid == 0) {
+      const uint32_t r = atomicAdd(&d.counters[CNT_REBUILD_W], 1u);
+      s_valid = int64_t(r) < p.n_regions;
+      if (s_valid) {
+        s_reg[0] = d.region[3 * size_t(r)];
+        s_reg[1] = d.region[3 * size_t(r) + 1];
+        s_reg[2] = d.region[3 * size_t(r) + 2];
+      }
+    }
+    __syncthreads();
+    if (!s_valid) break;
+    const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2];
+    for (uint32_t j = b + tid; j < e; j += kBlock) {
+      const uint32_t z = d.z_w[j];
+      if (z < uint32_t(K)) {
+        atomicAdd(&hist[z], 1u);
+        atomicOr(&bits[z >> 5], 1u << (z & 31u));
+      } else {
+        bad++;
+      }
+    }
+    __syncthreads();
+    // the touched topics, each thread a contiguous run of bitmap words (ascending)
+    const int per = (nw + kBlock - 1) / kBlock;
+    const int q0 = min(nw, tid * per), q1 = min(nw, q0 + per);
+    if (int32_t(v) < p.n_dense) {
+      int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
+      if (d.split[v]) {
+        for (int q = q0; q < q1; ++q)
+          for (uint32_t m = bits[q]; m; m &= m - 1u) {
+            const int k = q * 32 + __ffs(m) - 1;
+            atomicAdd(&wrow[k], int32_t(hist[k]));
+          }
+      } else {
+        for (int k = tid; k < K; k += kBlock) wrow[k] = int32_t(hist[k]);
+      }
+    } else {
+      const int s = int(v) - p.n_dense;
+      uint32_t cnt = 0;
+      for (int q = q0; q < q1; ++q) cnt += uint32_t(__popc(bits[q]));
+      uint32_t total = 0;
+      uint32_t off = block_exclusive_u32(cnt, s_scan, &total);
+      uint32_t *out = d.ws_ent + d.ws_cap[s];
+      for (int q = q0; q < q1; ++q)
+        for (uint32_t m = bits[q]; m; m &= m - 1u) {
+          const int k = q * 32 + __ffs(m) - 1;
+          out[off++] = (uint32_t(k) << 16) | hist[k];
+        }
+      if (tid == 0) d.ws_nnz[s] = total;
+    }
+    __syncthreads();  // the non-split dense row reads every hist entry
+    for (int q = q0; q < q1; ++q) {
+      for (uint32_t m = bits[q]; m; m &= m - 1u) {
+        const int k = q * 32 + __ffs(m) - 1;
+        if (tloc) tloc[k] += hist[k];
+        else atomicAdd(&d.T[k], hist[k]);
+        hist[k] = 0u;
+      }
+      bits[q] = 0u;
+    }
+    __syncthreads();
+  }
+  if (tloc)
+    for (int k = tid; k < K; k += kBlock)
+      if (tloc[k]) atomicAdd(&d.T[k], tloc[k]);
+  if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
+}
+
 constexpr int kPre = 2;  // chunks of 64 tokens per document gathered one document ahead
 
-// D rebuild: per document gather the new topics through the inverted index
-// (doc order -> word-order slot), histogram in a per-wave LDS table of
-// 16-bit counters, and emit ascending packed entries.
+// D rebuild for moderate K: per document gather the new topics through the
+// inverted index (doc order -> word-order slot), histogram in a per-wave
+// LDS table of 16-bit counters, and emit ascending packed entries by a scan
+// of the whole table.
 __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
@@ -1624,6 +1806,124 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
         if (lo) out[base + rank] = (uint32_t(2 * q) << 16) | lo;
         if (hi) out[base + rank + (lo ? 1u : 0u)] = (uint32_t(2 * q + 1) << 16) | hi;
         base += uint32_t(__popcll(m0) + __popcll(m1));
+      }
+      for (uint32_t q = base + lane; q + 1u < d_row_slots(base); q += kWave) out[q] = uint32_t(K) << 16;
+      if (lane == 0) out[-1] = ((e - b) << 16) | base;
+      __threadfence_block();
+    }
+  }
+  if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
+}
+
+// D rebuild: per document gather the new topics through the inverted index
+// (doc order -> word-order slot), histogram in a per-wave LDS table of
+// 16-bit counters with a bitmap of the touched topics, and emit ascending
+// packed entries by walking the bitmap (work per document: K/2048 wave
+// steps plus one per entry).
+__global__ __launch_bounds__(kBlock) void k_rebuild_d_bits(DevState d, Params p) {
+  extern __shared__ uint32_t ldsu[];
+  const int K = p.K;
+  const int half = (K + 1) / 2, nw = (K + 31) / 32;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  uint32_t *hist = ldsu + size_t(wave) * size_t(half + nw);
+  uint32_t *bits = hist + half;
+  for (int q = lane; q < half; q += kWave) hist[q] = 0u;
+  for (int q = lane; q < nw; q += kWave) bits[q] = 0u;
+  uint32_t bad = 0;
+  int part = 0;
+  for (;;) {
+    uint32_t d0 = 0, d1 = 0;
+    if (!next_docs(d.counters + CNT_REBUILD_D, p, part, lane, d0, d1)) break;
+    const int nd = int(d1 - d0);
+    // the batch's document offsets, one per lane
+    const uint32_t offv = lane <= nd ? d.doc_off[d0 + uint32_t(lane)] : 0u;
+    // two-stage pipeline over the first kPre*64 tokens of each document:
+    // the word-order slots of document i+1 are loaded while document i-1 is
+    // processed, and their topics are gathered while document i is
+    uint32_t wp1[kPre], z0[kPre];
+#pragma unroll
+    for (int c = 0; c < kPre; ++c) {
+      const uint32_t b = __builtin_amdgcn_readlane(offv, 0), e = __builtin_amdgcn_readlane(offv, 1);
+      const uint32_t pp = b + uint32_t(c * kWave + lane);
+      z0[c] = pp < e ? d.z_w[d.dt_wpos[pp]] : 0u;
+      wp1[c] = 0u;
+      if (nd > 1) {
+        const uint32_t bn = __builtin_amdgcn_readlane(offv, 1), en = __builtin_amdgcn_readlane(offv, 2);
+        const uint32_t pn = bn + uint32_t(c * kWave + lane);
+        if (pn < en) wp1[c] = d.dt_wpos[pn];
+      }
+    }
+    for (int i = 0; i < nd; ++i) {
+      const uint32_t b = __builtin_amdgcn_readlane(offv, i), e = __builtin_amdgcn_readlane(offv, i + 1);
+      uint32_t zv[kPre];
+#pragma unroll
+      for (int c = 0; c < kPre; ++c) zv[c] = z0[c];
+      if (i + 1 < nd) {
+        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 1), en = __builtin_amdgcn_readlane(offv, i + 2);
+#pragma unroll
+        for (int c = 0; c < kPre; ++c) {
+          const uint32_t pn = bn + uint32_t(c * kWave + lane);
+          z0[c] = pn < en ? d.z_w[wp1[c]] : 0u;
+        }
+      }
+      if (i + 2 < nd) {
+        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 2), en = __builtin_amdgcn_readlane(offv, i + 3);
+#pragma unroll
+        for (int c = 0; c < kPre; ++c) {
+          const uint32_t pn = bn + uint32_t(c * kWave + lane);
+          wp1[c] = pn < en ? d.dt_wpos[pn] : 0u;
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < kPre; ++c) {
+        if (b + uint32_t(c * kWave + lane) < e) {
+          const uint32_t z = zv[c];
+          if (z < uint32_t(K)) {
+            atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
+            atomicOr(&bits[z >> 5], 1u << (z & 31u));
+          } else {
+            bad++;
+          }
+        }
+      }
+      for (uint32_t pp = b + uint32_t(kPre * kWave + lane); pp < e; pp += kWave) {
+        const uint32_t z = d.z_w[d.dt_wpos[pp]];
+        if (z < uint32_t(K)) {
+          atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
+          atomicOr(&bits[z >> 5], 1u << (z & 31u));
+        } else {
+          bad++;
+        }
+      }
+      __threadfence_block();
+      uint32_t *out = d.d_ent + d.d_cap[d0 + uint32_t(i)] + 1;
+      uint32_t base = 0;
+      for (int q0 = 0; q0 < nw; q0 += kWave) {
+        const int q = q0 + lane;
+        uint32_t m = 0;
+        if (q < nw) {
+          m = bits[q];
+          bits[q] = 0u;
+        }
+        // this lane's entries go after those of the lower lanes
+        const uint32_t cnt = uint32_t(__popc(m));
+        uint32_t incl = cnt;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+          const uint32_t y = __shfl_up(incl, o, kWave);
+          if (lane >= o) incl += y;
+        }
+        uint32_t o = base + incl - cnt;
+        while (m) {
+          const int bit = __ffs(m) - 1;
+          m &= m - 1u;
+          const uint32_t z = uint32_t(q) * 32u + uint32_t(bit);
+          const uint32_t w = hist[z >> 1];
+          out[o++] = (z << 16) | ((z & 1u) ? (w >> 16) : (w & 0xFFFFu));
+          // a word holds topics 2h and 2h+1: clear it after its last touched topic
+          if ((z & 1u) || !((m >> (bit + 1)) & 1u)) hist[z >> 1] = 0u;
+        }
+        base += uint32_t(__shfl(int(incl), kWave - 1, kWave));
       }
       for (uint32_t q = base + lane; q + 1u < d_row_slots(base); q += kWave) out[q] = uint32_t(K) << 16;
       if (lane == 0) out[-1] = ((e - b) << 16) | base;
@@ -1760,7 +2060,19 @@ hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_
   return hipGetLastError();
 }
 
+hipError_t launch_beta_sum(const DevState &d, const Params &p, hipStream_t s) {
+  hipLaunchKernelGGL(k_beta_sum, dim3(1), dim3(kBlock), 0, s, d, p);
+  return hipGetLastError();
+}
 hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s) {
+  if (p.sparse_pre) {
+    // the topic list and the sum of beta/den[k] follow the current T
+    size_t bytes = d.topic_tmp_bytes;
+    hipError_t err = sort_pairs_u32(d.topic_tmp, bytes, d.T, d.topic_keys, d.topic_iota, d.topic_order, p.K, 32, s);
+    if (err != hipSuccess) return err;
+    err = launch_beta_sum(d, p, s);
+    if (err != hipSuccess) return err;
+  }
   hipLaunchKernelGGL(k_word_pre, dim3(uint32_t(p.n_present)), dim3(kBlock), 0, s, d, p);
   return hipGetLastError();
 }
@@ -1848,17 +2160,32 @@ hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s) {
   hipLaunchKernelGGL(k_zero_split, dim3(uint32_t(zb)), dim3(kBlock), 0, s, d, p);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  const size_t wlds = sizeof(uint32_t) * (p.big_k ? 1 : 2) * size_t(p.K);
-  err = allow_lds(k_rebuild_w, wlds);
-  if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_rebuild_w, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
+  // large K: the bitmap variants, whose work follows the tokens instead of K
+  const size_t nwords = size_t((p.K + 31) / 32);
+  if (p.big_k) {
+    const size_t wlds = sizeof(uint32_t) * (size_t(p.K) + nwords);
+    err = allow_lds(k_rebuild_w_bits, wlds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_rebuild_w_bits, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
+  } else {
+    const size_t wlds = sizeof(uint32_t) * 2 * size_t(p.K);
+    err = allow_lds(k_rebuild_w, wlds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_rebuild_w, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
+  }
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  const size_t half = size_t((p.K + 1) / 2);
-  err = allow_lds(k_rebuild_d, sizeof(uint32_t) * half * size_t(p.doc_waves));
-  if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves),
-                     sizeof(uint32_t) * half * size_t(p.doc_waves), s, d, p);
+  if (p.big_k) {
+    const size_t dlds = sizeof(uint32_t) * (size_t((p.K + 1) / 2) + nwords) * size_t(p.doc_waves);
+    err = allow_lds(k_rebuild_d_bits, dlds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_rebuild_d_bits, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), dlds, s, d, p);
+  } else {
+    const size_t dlds = sizeof(uint32_t) * size_t((p.K + 1) / 2) * size_t(p.doc_waves);
+    err = allow_lds(k_rebuild_d, dlds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), dlds, s, d, p);
+  }
   return hipGetLastError();
 }
 

@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstring>
 #include <new>
+#include <numeric>
 #include <string>
 #include <vector>
 
@@ -167,7 +168,9 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
                                       std::to_string(lds_max));
   }
   // the doc pass and the D rebuild keep a table of K 16-bit counts per wave
-  p.doc_waves = std::max(1, std::min(kBlock / 64, int(size_t(lds_max) / (sizeof(uint32_t) * size_t((p.K + 1) / 2)))));
+  // (and the D rebuild a bitmap of K bits)
+  p.doc_waves = std::max(1, std::min(kBlock / 64, int(size_t(lds_max) / (sizeof(uint32_t) *
+                                                                             size_t((p.K + 1) / 2 + (p.K + 31) / 32)))));
   p.grid_docs = std::max(1, cus * 8);
   const size_t n = size_t(L.n);
   const bool identity = L.key_identity;
@@ -269,6 +272,24 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.counters, kCounters));
   LDA_TRY(dalloc(h, &h->stats_base, size_t(kStatSlots) * kStatsPerIter));
   LDA_TRY(dalloc(h, &d.ll_part, size_t(L.n_regions)));
+  // large K: sparse words' per-word records from their rows and a list of
+  // the topics with the largest beta/den[k] (sorted each iteration)
+  p.sparse_pre = L.K >= 4096 ? 1 : 0;
+  p.top_list = std::min(L.K, 512);
+  if (p.sparse_pre) {
+    LDA_TRY(dalloc(h, &d.topic_order, size_t(L.K)));
+    LDA_TRY(dalloc(h, &d.topic_keys, size_t(L.K)));
+    LDA_TRY(dalloc(h, &d.topic_iota, size_t(L.K)));
+    LDA_TRY(dalloc(h, &d.beta_sum, 1));
+    std::vector<uint32_t> iota(static_cast<size_t>(L.K));
+    std::iota(iota.begin(), iota.end(), 0u);
+    LDA_TRY(upload(h, d.topic_iota, iota));
+    HIP_TRY(h, sort_pairs_u32(nullptr, d.topic_tmp_bytes, d.T, d.topic_keys, d.topic_iota, d.topic_order,
+                              L.K, 32, h->stream));
+    uint8_t *tmp = nullptr;
+    LDA_TRY(dalloc(h, &tmp, d.topic_tmp_bytes));
+    d.topic_tmp = tmp;
+  }
   if (p.big_k) {
     uint32_t max_region = 1;
     for (size_t r = 0; r < L.region.size(); r += 3) max_region = std::max(max_region, L.region[r + 2] - L.region[r + 1]);

@@ -128,6 +128,12 @@ struct DevState {
   double *ts_s, *ts_x;
   uint32_t *ts_c1, *ts_code;
   double *wscratch;
+  // large K (p.sparse_pre): topics by ascending T (descending beta/den[k]),
+  // their sort buffers, and the sum of beta/den[k] over all topics
+  uint32_t *topic_order, *topic_keys, *topic_iota;
+  void *topic_tmp;
+  size_t topic_tmp_bytes;
+  double *beta_sum;
 };
 
 struct Params {
@@ -148,6 +154,8 @@ struct Params {
   int32_t tile_topics;   // topics per tile of the tiled sampler (a multiple of 16)
   int32_t max_region;    // tokens of the largest region
   int32_t doc_waves;     // waves per workgroup of the doc pass and the D rebuild (LDS tables of K entries per wave)
+  int32_t sparse_pre;    // per-word precompute of sparse words from their row and a topic list (large K)
+  int32_t top_list;      // length of that topic list
   uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
 
@@ -162,6 +170,7 @@ constexpr int kStatsPerIter = 8;
 hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_beta_sum(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_fill_undecided(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);

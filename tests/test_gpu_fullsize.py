@@ -57,7 +57,7 @@ C5 = pytest.param("c5", marks=pytest.mark.skipif(
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", ["c2", "c3", "c4", C5])
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c6", C5])
 def test_full_size_first_iteration(name):
     c = lda_synth.make_corpus(name)
     say("full-size %s N=%d V=%d K=%d" % (name, c.N, c.V, c.K))
