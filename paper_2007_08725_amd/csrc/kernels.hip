@@ -1341,8 +1341,8 @@ __device__ void fill_tile(const DevState &d, const Params &p, uint32_t v, uint32
   __syncthreads();
 }
 
-constexpr int kTiledBlock = kTiledThreads;  // threads per workgroup of the tiled sampler (8 waves)
-constexpr int kTiledAhead = 4;              // chunks whose loads a group issues together
+constexpr int kTiledBlock = kTiledThreads;  // threads per workgroup of the tiled sampler (16 waves)
+constexpr int kTiledAhead = 2;              // chunks whose loads a group issues together
 
 __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Params p, uint32_t t,
                                                                unsigned long long *__restrict__ stats) {

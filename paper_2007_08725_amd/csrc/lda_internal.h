@@ -178,7 +178,7 @@ int sampler_block(int K, int want);
 // Large K: topics per tile and the tiled sampler's dynamic LDS.
 int tiled_topics(int K);
 size_t tiled_lds_bytes(int K, int kt);
-constexpr int kTiledThreads = 512;
+constexpr int kTiledThreads = 1024;
 // Workgroups of the tiled sampler (one per CU: its LDS fills a CU) and of the
 // large-K LLPT kernel; the scratch slices are sized for these grids.
 inline int tiled_grid(const Params &p) { return p.grid_regions / 8 > 0 ? p.grid_regions / 8 : 1; }

@@ -322,7 +322,7 @@ def test_large_k_tiled_sampler_follows_the_oracle(K):
             zo, flags, _ = oracle.iterate(c.word, c.doc, z, seed=SEED, t=t, **kw)
             m.set_assignments(z, t)
             st = m.iterate(1, stats=True)[0]
-            assert st["sampler_block"] == 512 and st["sampled"] + st["skip_step3"] == c.N
+            assert st["sampler_block"] == 1024 and st["sampled"] + st["skip_step3"] == c.N
             cnt = m.counts()
             compare_draws(cnt["z"], zo, flags, c.N)
             check_counts_are_histograms(c, cnt, c.K)
