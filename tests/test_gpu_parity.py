@@ -342,6 +342,40 @@ def test_large_k_schedule_invariance():
         zb = b.counts(D=False, W=False)["z"]
     assert np.array_equal(za, zb)
 
+
+def test_large_k_two_branch_follows_the_oracle():
+    """The two-branch ablation through the tiled sampler and the large-K precompute
+    (K = 32,768) against the oracle's two-branch form."""
+    c = _large_k_corpus(32768)
+    kw = dict(M=c.n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta)
+    z = oracle.init_topics(c.N, c.K, SEED)
+    zo, flags, _ = oracle.iterate(c.word, c.doc, z, seed=SEED, t=0, branches=2, **kw)
+    with lda_make(c, two_branch=True) as m:
+        st = m.iterate(1, stats=True)[0]
+        cnt = m.counts()
+    compare_draws(cnt["z"], zo, flags, c.N)
+    check_counts_are_histograms(c, cnt, c.K)
+    assert st["skip_step3"] == 0 and st["skip_after_s"] == 0 and st["sampled"] == c.N
+
+
+@pytest.mark.parametrize("opts", [dict(g=1), dict(g=3), dict(no_skip=True), dict(dense_cutoff=-1),
+                                  dict(dense_cutoff=1 << 30)])
+def test_large_k_options_leave_the_draws_unchanged(opts):
+    """S_est depth, the skip test and the hybrid-W cutoff at K = 32,768 (tiled sampler,
+    bitmap rebuilds, sparse-word precompute or its dense fallback)."""
+    c = _large_k_corpus(32768)
+    say("large K options %s" % opts)
+    with lda_make(c) as a:
+        a.iterate(2)
+        za = a.counts(D=False, W=False)["z"]
+        lla = a.loglik()
+    with lda_make(c, **opts) as b:
+        b.iterate(2)
+        zb = b.counts(D=False, W=False)["z"]
+        llb = b.loglik()
+    assert np.array_equal(za, zb)
+    assert llb == pytest.approx(lla, rel=1e-12)
+
 def lda_make(c, **kw):
     import paper_2007_08725_amd as lda
     return lda.LDA(c.word, c.doc, c.V, c.K, c.alpha, c.beta, SEED, **kw)
