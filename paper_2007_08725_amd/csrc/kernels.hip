@@ -537,7 +537,7 @@ struct BatchLds {
 struct WordState {
   const double *wh, *qb;
   int nb, K;
-  int qsh;  // 4-ary search over qb: first level steps 4^(qsh/2) blocks (negative: a single block)
+  int qhalf;  // half the padded block count of qb (0 for a single block): the binary search's first step
   uint32_t K1;
   double a1, qp, alpha;
 };
@@ -645,14 +645,12 @@ __device__ __forceinline__ uint32_t pick_segment(uint32_t k, double term, double
   return __shfl(k, h, kGroup);
 }
 
-// Draw the tokens of `mask` whose D rows hold at most 16*C entries, four at a
-// time (one per 16-lane group); C is fixed per call so every group of a round
-// does the same amount of work.  C == 0 selects the long-row path, which
-// walks rows of any length in chunks of kChunk entries.
-template <int C>
-__device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const WordState &w,
-                            const uint32_t *__restrict__ d_ent, int grp, int li, unsigned long long &after_s) {
-  constexpr int R = C > 0 ? C : kMaxRun;
+// Draw the tokens of `mask` (rows longer than the small-group rounds take),
+// four at a time, one per 16-lane group, walking each row in chunks of
+// kChunk entries.
+__device__ void draw_long(unsigned long long mask, const BatchLds &bt, const WordState &w,
+                          const uint32_t *__restrict__ d_ent, int grp, int li, unsigned long long &after_s) {
+  constexpr int R = kMaxRun;
   while (mask) {
     // the four lowest tokens of the mask, one per group (wave-uniform bit
     // arithmetic; a group with none gets src = -1)
@@ -668,7 +666,7 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
     const double t_u = bt.u[src];
     const uint32_t *row = d_ent + t_off;  // slot 0 is the row header
     const uint32_t pad = uint32_t(w.K) << 16;
-    const uint32_t nch = C > 0 ? 1u : (t_nnz + 1u + kChunk - 1) / kChunk;
+    const uint32_t nch = (t_nnz + 1u + kChunk - 1) / kChunk;
     uint32_t r[R];
     double s = 0.0, incl = 0.0, S = 0.0;
     uint32_t c1 = 0xFFFFFFFFu;
@@ -686,23 +684,19 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
     uint32_t topic = w.K1;
     in_m = x < Mm;
     if (!in_m) {
-      // locate the chunk (long rows only), then 16 candidate segments
+      // locate the chunk, then 16 candidate segments
       double cbase = Mm;
       bool in_s = false;
-      if (C > 0) {
-        in_s = x < Mm + S;
-      } else {
-        for (uint32_t ch = 0; ch < nch && !in_s; ++ch) {
-          if (nch > 1) {
-            load_run<R>(row + ch * kChunk, li, r);
-            if (ch == 0u && li == 0) r[0] = pad;
-            s = run_sum<R>(r, w.wh);
-            incl = row_incl_scan(s);
-          }
-          const double total = __shfl(incl, kGroup - 1, kGroup);
-          if (x < cbase + total) in_s = true;
-          else cbase += total;
+      for (uint32_t ch = 0; ch < nch && !in_s; ++ch) {
+        if (nch > 1) {
+          load_run<R>(row + ch * kChunk, li, r);
+          if (ch == 0u && li == 0) r[0] = pad;
+          s = run_sum<R>(r, w.wh);
+          incl = row_incl_scan(s);
         }
+        const double total = __shfl(incl, kGroup - 1, kGroup);
+        if (x < cbase + total) in_s = true;
+        else cbase += total;
       }
       uint32_t k;
       double term, start;
@@ -721,7 +715,7 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
         term = double(mine & 0xFFFFu) * w.wh[k];
       } else {
         // Q' branch: boundaries (M + S') + Qcdf
-        const double qstart = C > 0 ? Mm + S : cbase;
+        const double qstart = cbase;
         const double xq = x - qstart;
         if (!(xq < w.qb[w.nb])) {
           k = (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);  // last positive segment
@@ -749,10 +743,10 @@ __device__ void draw_tokens(unsigned long long mask, const BatchLds &bt, const W
 // D rows) rounded up to whole blocks of kGroup topics, zeros past K.
 __host__ __device__ inline int wh_entries(int K) { return (K + 1 + kGroup - 1) / kGroup * kGroup; }
 
-// Blocks of the Q' prefix rounded up to a power of 4 (the 4-ary search).
+// Blocks of the Q' prefix rounded up to a power of 2 (its binary search).
 __host__ __device__ inline int q_blocks_padded(int nb) {
   int q = 1;
-  while (q < nb) q *= 4;
+  while (q < nb) q *= 2;
   return q;
 }
 
@@ -879,8 +873,8 @@ constexpr uint16_t kDrawQ = 0xFFFE;
 // the end selects the last positive term.
 __device__ __forceinline__ uint32_t q_draw(double xq, const WordState &w) {
   if (!(xq < w.qb[w.nb])) return (w.K1 == uint32_t(w.K - 1)) ? uint32_t(w.K - 2) : uint32_t(w.K - 1);
-  int lo = 0;  // the largest block with qb[lo] <= xq; qb holds 4 << qsh entries before its +inf tail ends
-  for (int step = w.qsh >= 0 ? 2 << w.qsh : 0; step > 0; step >>= 1) lo = w.qb[lo + step] <= xq ? lo + step : lo;
+  int lo = 0;  // the largest block with qb[lo] <= xq (qb is +inf from nb + 1 up to 2 * qhalf)
+  for (int step = w.qhalf; step > 0; step >>= 1) lo = w.qb[lo + step] <= xq ? lo + step : lo;
   const double xs = xq - w.qb[lo];
   const int k0 = lo * kGroup;
   double p = 0.0;
@@ -1076,11 +1070,9 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const int grp = lane / kGroup, li = lane % kGroup;
   const BatchLds bt{s_off + wave * kWave, s_nnz + wave * kWave, s_u + wave * kWave, s_top + wave * kWave,
                     s_hand + wave * (kWave / kGroup) * kMaxRun, s_list + wave * kWave};
-  int qsh = -2;
-  for (int q = 1; q < nbp; q *= 4) qsh += 2;
+  const int qhalf = nbp / 2;
   for (int q = nb + 1 + tid; q < nbp; q += NB) qb[q] = __builtin_inf();
   for (int k = K + 1 + tid; k < wh_entries(K); k += NB) wh[k] = 0.0;
   // region, word and count variables are uniform over the block (scalar registers)
@@ -1157,7 +1149,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       __syncthreads();
     }
 
-    const WordState w{wh, qb, nb, K, qsh, K1, a1, qp, p.alpha};
+    const WordState w{wh, qb, nb, K, qhalf, K1, a1, qp, p.alpha};
     for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += NB) {
       const int ln = lane_here();  // the lane, recomputed per batch
       const uint32_t j = base + uint32_t(ln);
@@ -1183,7 +1175,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       // to 256: 8 lanes; up to 512: 16 lanes; longer rows: 16 lanes, one
       // chunk of kChunk slots at a time
       draw_batch_small(und, nnz, bt, w, d.d_ent, ln, n_after_s);
-      draw_tokens<0>(__ballot(und && nnz + 1u > 512u), bt, w, d.d_ent, ln / kGroup, ln % kGroup, n_after_s);
+      draw_long(__ballot(und && nnz + 1u > 512u), bt, w, d.d_ent, ln / kGroup, ln % kGroup, n_after_s);
       // the S' walks and Q' searches, one lane per token; the batch's topics
       // leave in one coalesced store
       if (und) d.z_w[j] = uint16_t(finish_draw(ln, bt, w, d.d_ent));
