@@ -64,16 +64,20 @@ def test_full_size_first_iteration(name):
     rng = np.random.default_rng(2024)
     idx = np.sort(rng.choice(c.N, SAMPLE, replace=False))
     z0 = oracle.init_topics(c.N, c.K, SEED)
+    say("  oracle initial topics drawn")
     with make_lda(c) as m:
+        say("  library created")
         cnt0 = m.counts()
         assert np.array_equal(cnt0["z"], z0)
         _check_rows_sampled(c, cnt0, rng)
         del cnt0
+        say("  initial counts checked")
         st = m.iterate(1, stats=True)[0]
         say("  gpu iteration %.1f ms (sampler %.1f ms)" % (st["ms_iter"], st["ms_sampler"]))
         cnt1 = m.counts()
     assert st["skip_step3"] + st["sampled"] == c.N
     _check_rows_sampled(c, cnt1, rng)
+    say("  new counts checked")
     say("  oracle on %d sampled tokens" % SAMPLE)
     zo, flags, ost = oracle.iterate(c.word, c.doc, z0, seed=SEED, t=0, idx=idx, **corpus_kw(c))
     n_bad = compare_draws(cnt1["z"][idx], zo, flags, c.N)
