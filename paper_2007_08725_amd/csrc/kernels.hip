@@ -1712,113 +1712,37 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
 
 constexpr int kPre = 2;  // chunks of 64 tokens per document gathered one document ahead
 
-// D rebuild for moderate K: per document gather the new topics through the
-// inverted index (doc order -> word-order slot), histogram in a per-wave
-// LDS table of 16-bit counters, and emit ascending packed entries by a scan
-// of the whole table.
-__global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
-  extern __shared__ uint32_t ldsu[];
-  const int K = p.K;
-  const int half = (K + 1) / 2;
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  uint32_t *hist = ldsu + size_t(wave) * size_t(half);
-  for (int q = lane; q < half; q += kWave) hist[q] = 0u;
-  const unsigned long long lt = (1ull << lane) - 1ull;
-  uint32_t bad = 0;
-  int part = 0;
-  for (;;) {
-    uint32_t d0 = 0, d1 = 0;
-    if (!next_docs(d.counters + CNT_REBUILD_D, p, part, lane, d0, d1)) break;
-    const int nd = int(d1 - d0);
-    // the batch's document offsets, one per lane
-    const uint32_t offv = lane <= nd ? d.doc_off[d0 + uint32_t(lane)] : 0u;
-    // two-stage pipeline over the first kPre*64 tokens of each document:
-    // the word-order slots of document i+1 are loaded while document i-1 is
-    // processed, and their topics are gathered while document i is
-    uint32_t wp1[kPre], z0[kPre];
-#pragma unroll
-    for (int c = 0; c < kPre; ++c) {
-      const uint32_t b = __builtin_amdgcn_readlane(offv, 0), e = __builtin_amdgcn_readlane(offv, 1);
-      const uint32_t pp = b + uint32_t(c * kWave + lane);
-      z0[c] = pp < e ? d.z_w[d.dt_wpos[pp]] : 0u;
-      wp1[c] = 0u;
-      if (nd > 1) {
-        const uint32_t bn = __builtin_amdgcn_readlane(offv, 1), en = __builtin_amdgcn_readlane(offv, 2);
-        const uint32_t pn = bn + uint32_t(c * kWave + lane);
-        if (pn < en) wp1[c] = d.dt_wpos[pn];
-      }
-    }
-    for (int i = 0; i < nd; ++i) {
-      const uint32_t b = __builtin_amdgcn_readlane(offv, i), e = __builtin_amdgcn_readlane(offv, i + 1);
-      uint32_t zv[kPre];
-#pragma unroll
-      for (int c = 0; c < kPre; ++c) zv[c] = z0[c];
-      if (i + 1 < nd) {
-        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 1), en = __builtin_amdgcn_readlane(offv, i + 2);
-#pragma unroll
-        for (int c = 0; c < kPre; ++c) {
-          const uint32_t pn = bn + uint32_t(c * kWave + lane);
-          z0[c] = pn < en ? d.z_w[wp1[c]] : 0u;
-        }
-      }
-      if (i + 2 < nd) {
-        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 2), en = __builtin_amdgcn_readlane(offv, i + 3);
-#pragma unroll
-        for (int c = 0; c < kPre; ++c) {
-          const uint32_t pn = bn + uint32_t(c * kWave + lane);
-          wp1[c] = pn < en ? d.dt_wpos[pn] : 0u;
-        }
-      }
-#pragma unroll
-      for (int c = 0; c < kPre; ++c) {
-        if (b + uint32_t(c * kWave + lane) < e) {
-          const uint32_t z = zv[c];
-          if (z < uint32_t(K)) atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
-          else bad++;
-        }
-      }
-      for (uint32_t pp = b + uint32_t(kPre * kWave + lane); pp < e; pp += kWave) {
-        const uint32_t z = d.z_w[d.dt_wpos[pp]];
-        if (z < uint32_t(K)) atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
-        else bad++;
-      }
-      __threadfence_block();
-      uint32_t *out = d.d_ent + d.d_cap[d0 + uint32_t(i)] + 1;
-      uint32_t base = 0;
-      for (int q0 = 0; q0 < half; q0 += kWave) {
-        const int q = q0 + lane;
-        uint32_t w = 0;
-        if (q < half) {
-          w = hist[q];
-          hist[q] = 0u;
-        }
-        const uint32_t lo = w & 0xFFFFu, hi = w >> 16;
-        const unsigned long long m0 = __ballot(lo != 0u), m1 = __ballot(hi != 0u);
-        const uint32_t rank = uint32_t(__popcll(m0 & lt) + __popcll(m1 & lt));
-        if (lo) out[base + rank] = (uint32_t(2 * q) << 16) | lo;
-        if (hi) out[base + rank + (lo ? 1u : 0u)] = (uint32_t(2 * q + 1) << 16) | hi;
-        base += uint32_t(__popcll(m0) + __popcll(m1));
-      }
-      for (uint32_t q = base + lane; q + 1u < d_row_slots(base); q += kWave) out[q] = uint32_t(K) << 16;
-      if (lane == 0) out[-1] = ((e - b) << 16) | base;
-      __threadfence_block();
-    }
-  }
-  if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
+// Inclusive prefix sum of a u32 over the 64 lanes of a wave: DPP shifts
+// inside each row of 16 lanes (lanes below the shift read 0), then the row
+// totals carried across rows.
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x111, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x112, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x114, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x118, 0xF, 0xF, true));
+  const uint32_t r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31),
+                 r2 = __builtin_amdgcn_readlane(v, 47);
+  v += lane >= 16 ? r0 : 0u;
+  v += lane >= 32 ? r1 : 0u;
+  v += lane >= 48 ? r2 : 0u;
+  return v;
 }
 
-// D rebuild: per document gather the new topics through the inverted index
-// (doc order -> word-order slot), histogram in a per-wave LDS table of
-// 16-bit counters with a bitmap of the touched topics, and emit ascending
-// packed entries by walking the bitmap (work per document: K/2048 wave
-// steps plus one per entry).
-__global__ __launch_bounds__(kBlock) void k_rebuild_d_bits(DevState d, Params p) {
+// D rebuild (Sec. 5.2): per document gather the new topics through the
+// inverted index (doc order -> word-order slot) into a per-wave LDS table of
+// 16-bit counts, marking each touched topic in a bitmap.  The row is then
+// emitted in ascending topic order: each lane expands one bitmap word into a
+// list of topics at its prefix-sum offset, and one lane per listed topic
+// writes the packed entry.  The work per document is K/2048 wave steps plus
+// about one per 32 touched topics, so it follows the tokens, not K.
+__global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
   const int half = (K + 1) / 2, nw = (K + 31) / 32;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  uint32_t *hist = ldsu + size_t(wave) * size_t(half + nw);
+  uint32_t *hist = ldsu + size_t(wave) * d_rebuild_lds_words(K);
   uint32_t *bits = hist + half;
+  uint16_t *list = reinterpret_cast<uint16_t *>(bits + nw);
   for (int q = lane; q < half; q += kWave) hist[q] = 0u;
   for (int q = lane; q < nw; q += kWave) bits[q] = 0u;
   uint32_t bad = 0;
@@ -1827,8 +1751,10 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d_bits(DevState d, Params p)
     uint32_t d0 = 0, d1 = 0;
     if (!next_docs(d.counters + CNT_REBUILD_D, p, part, lane, d0, d1)) break;
     const int nd = int(d1 - d0);
-    // the batch's document offsets, one per lane
+    // the batch's document offsets and D-row offsets, one per lane (loaded
+    // here so that no later wait for them also waits for the prefetches)
     const uint32_t offv = lane <= nd ? d.doc_off[d0 + uint32_t(lane)] : 0u;
+    const uint32_t capv = lane < nd ? d.d_cap[d0 + uint32_t(lane)] : 0u;
     // two-stage pipeline over the first kPre*64 tokens of each document:
     // the word-order slots of document i+1 are loaded while document i-1 is
     // processed, and their topics are gathered while document i is
@@ -1888,8 +1814,11 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d_bits(DevState d, Params p)
         }
       }
       __threadfence_block();
-      uint32_t *out = d.d_ent + d.d_cap[d0 + uint32_t(i)] + 1;
+      uint32_t *out = d.d_ent + __builtin_amdgcn_readlane(capv, i) + 1;
       uint32_t base = 0;
+      // 64 bitmap words (2048 topics) per step, one per lane; the two
+      // topics of a count word share a bitmap word, so both are listed in
+      // the same step
       for (int q0 = 0; q0 < nw; q0 += kWave) {
         const int q = q0 + lane;
         uint32_t m = 0;
@@ -1897,25 +1826,27 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d_bits(DevState d, Params p)
           m = bits[q];
           bits[q] = 0u;
         }
-        // this lane's entries go after those of the lower lanes
         const uint32_t cnt = uint32_t(__popc(m));
-        uint32_t incl = cnt;
-#pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-          const uint32_t y = __shfl_up(incl, o, kWave);
-          if (lane >= o) incl += y;
-        }
-        uint32_t o = base + incl - cnt;
+        const uint32_t incl = wave_incl_scan_u32(cnt, lane);
+        const uint32_t n = __builtin_amdgcn_readlane(incl, kWave - 1);
+        if (n == 0u) continue;
+        uint32_t o = incl - cnt;
         while (m) {
-          const int bit = __ffs(m) - 1;
+          const uint32_t bit = uint32_t(__ffs(m) - 1);
           m &= m - 1u;
-          const uint32_t z = uint32_t(q) * 32u + uint32_t(bit);
-          const uint32_t w = hist[z >> 1];
-          out[o++] = (z << 16) | ((z & 1u) ? (w >> 16) : (w & 0xFFFFu));
-          // a word holds topics 2h and 2h+1: clear it after its last touched topic
-          if ((z & 1u) || !((m >> (bit + 1)) & 1u)) hist[z >> 1] = 0u;
+          list[o++] = uint16_t(uint32_t(q) * 32u + bit);
         }
-        base += uint32_t(__shfl(int(incl), kWave - 1, kWave));
+        __threadfence_block();
+        for (uint32_t j = uint32_t(lane); j < n; j += kWave) {
+          const uint32_t z = list[j];
+          const uint32_t zn = j + 1u < n ? uint32_t(list[j + 1u]) : 0xFFFFFFFFu;
+          const uint32_t w = hist[z >> 1];
+          out[base + j] = (z << 16) | ((z & 1u) ? (w >> 16) : (w & 0xFFFFu));
+          // clear a count word after its last listed topic has been read
+          if ((z & 1u) || zn != z + 1u) hist[z >> 1] = 0u;
+        }
+        __threadfence_block();
+        base += n;
       }
       for (uint32_t q = base + lane; q + 1u < d_row_slots(base); q += kWave) out[q] = uint32_t(K) << 16;
       if (lane == 0) out[-1] = ((e - b) << 16) | base;
@@ -2167,17 +2098,10 @@ hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s) {
   }
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  if (p.big_k) {
-    const size_t dlds = sizeof(uint32_t) * (size_t((p.K + 1) / 2) + nwords) * size_t(p.doc_waves);
-    err = allow_lds(k_rebuild_d_bits, dlds);
-    if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(k_rebuild_d_bits, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), dlds, s, d, p);
-  } else {
-    const size_t dlds = sizeof(uint32_t) * size_t((p.K + 1) / 2) * size_t(p.doc_waves);
-    err = allow_lds(k_rebuild_d, dlds);
-    if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), dlds, s, d, p);
-  }
+  const size_t dlds = sizeof(uint32_t) * d_rebuild_lds_words(p.K) * size_t(p.doc_waves);
+  err = allow_lds(k_rebuild_d, dlds);
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), dlds, s, d, p);
   return hipGetLastError();
 }
 

@@ -167,10 +167,9 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
                                       " bytes of LDS per workgroup even in tiles; the device allows " +
                                       std::to_string(lds_max));
   }
-  // the doc pass and the D rebuild keep a table of K 16-bit counts per wave
-  // (and the D rebuild a bitmap of K bits)
-  p.doc_waves = std::max(1, std::min(kBlock / 64, int(size_t(lds_max) / (sizeof(uint32_t) *
-                                                                             size_t((p.K + 1) / 2 + (p.K + 31) / 32)))));
+  // the doc pass keeps a table of K 16-bit counts per wave; the D rebuild
+  // the same table plus a bitmap of the touched topics and a list of them
+  p.doc_waves = std::max(1, std::min(kBlock / 64, int(size_t(lds_max) / (sizeof(uint32_t) * d_rebuild_lds_words(p.K)))));
   p.grid_docs = std::max(1, cus * 8);
   const size_t n = size_t(L.n);
   const bool identity = L.key_identity;

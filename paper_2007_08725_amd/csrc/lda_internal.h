@@ -28,6 +28,12 @@ __host__ __device__ inline uint32_t d_row_slots(uint32_t nnz) {
   const uint32_t n = nnz + 1u;
   return n <= 128u ? (n + 31u) & ~31u : n <= 256u ? (n + 63u) & ~63u : (n + 127u) & ~127u;
 }
+// LDS words (u32) per wave of the D rebuild: K 16-bit counts, a bitmap of K
+// bits and a list of up to min(K, 2048) 16-bit topics
+__host__ __device__ inline size_t d_rebuild_lds_words(int K) {
+  const size_t half = size_t(K + 1) / 2;
+  return half + size_t(K + 31) / 32 + (half < 1024 ? half : 1024);
+}
 constexpr int kDefaultRegionTokens = 10000;  // Sec. 5.1
 constexpr int kBlock = 256;                  // threads per workgroup (4 wave64)
 constexpr int kXcds = 8;                     // accelerator dies (XCDs), each with its own L2
