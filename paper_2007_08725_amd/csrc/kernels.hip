@@ -3,14 +3,14 @@
 // One synchronous iteration (Sec. 2.2, 3.2, 4.3):
 //   k_begin      den[k] = T[k] + V*beta; scheduler counters reset
 //   k_word_pre   per word: top-3 of W^[v] (K1, K2, a1..a3), Q' and sum W^   (step 1, Sec. 3.2)
-//   k_fill_undecided
-//                every word-ordered topic slot set to "undecided"
+//   k_clear_skips
+//                the skip bitmap (one bit per word-ordered token) cleared
 //   k_doc_pass   per document: C1, C2 by lookup in the D row, u, M, S_est
-//                and the skip test; writes K1 into the word-ordered topic
-//                slot of every skipped token                               (steps 2-3, Sec. 3.3)
+//                and the skip test; sets the bit of every skipped token    (steps 2-3, Sec. 3.3)
 //   k_sampler    per region of a word: W^ row and Q' block prefix in LDS,
-//                then for every undecided token C1 and S' over nz(D[d])
-//                and the final draw over [K1 | S' | Q']                    (steps 4-6, Sec. 4.3)
+//                then for every token whose bit is clear C1 and S' over
+//                nz(D[d]) and the final draw over [K1 | S' | Q']; every
+//                topic slot of the region written (K1 for the skipped)     (steps 4-6, Sec. 4.3)
 //   k_zero_split, k_rebuild_w, k_rebuild_d
 //                count tables of the new assignment: dense rows of W by
 //                histogram (integer atomics for split words), sparse rows of
@@ -197,10 +197,10 @@ __global__ void k_init_topics(const uint32_t *__restrict__ wt_key, uint16_t *__r
     z_w[j] = initial_topic(seed, wt_key[j], K);
 }
 
-// Every word-ordered topic slot starts the iteration undecided.
-__global__ void k_fill_undecided(uint32_t *__restrict__ z2, int64_t n2) {
-  for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < n2; q += int64_t(gridDim.x) * blockDim.x)
-    z2[q] = (uint32_t(kUndecided) << 16) | kUndecided;
+// The skip bitmap starts every iteration clear.
+__global__ void k_clear_skips(uint32_t *__restrict__ bits, int64_t n) {
+  for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < n; q += int64_t(gridDim.x) * blockDim.x)
+    bits[q] = 0u;
 }
 
 __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, int32_t K, double vbeta,
@@ -470,30 +470,51 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
         cmap[ent >> 16] = uint16_t(ent & 0xFFFFu);
       }
       __builtin_amdgcn_wave_barrier();
-      for (uint32_t pp = b + uint32_t(lane); pp < e; pp += kWave) {
-        const uint32_t v = pp < b + kWave ? wv : d.dt_word[pp];
-        const SkipRec rec = d.wskip[v];
-        const uint32_t K1 = rec.k12 & 0xFFFFu, K2 = rec.k12 >> 16;
-        const uint32_t C1 = cmap[K1], C2 = cmap[K2];
-        const uint32_t key = p.key_identity ? pp : d.dt_key[pp];
-        // Step 3 in single precision with a relative margin of 2^-15, far
-        // above the fp32 rounding of these few operations (a few 2^-24): a
-        // token is skipped only if u*(M + S_est + Q') < M holds exactly, so
-        // its draw is K1 (S' <= S_est, Eq. 8-9).
-        const float u = float(uniform_draw(p.seed, t, key));
-        const float Mm = rec.a1 * (float(C1) + p.alpha_f);
-        float Sest;
-        if (p.g == 1) {
-          Sest = rec.a2 * float(len - C1);
-        } else if (p.g == 2) {
-          Sest = rec.a2 * float(C2) + rec.a3 * float(len - C1 - C2);
-        } else {
-          const uint32_t C3 = rec.k3 < uint32_t(K) ? uint32_t(cmap[rec.k3]) : 0u;
-          Sest = rec.a2 * float(C2) + rec.a3 * float(C3) + rec.a4 * float(len - C1 - C2 - C3);
+      // two chunks of 64 tokens per step, so that the word-id loads and the
+      // skip-record gathers of both are in flight together
+      for (uint32_t p0 = b; p0 < e; p0 += 2u * kWave) {
+        uint32_t v[2];
+        SkipRec rec[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const uint32_t pp = p0 + uint32_t(c * kWave + lane);
+          v[c] = pp < e ? (pp < b + kWave ? wv : d.dt_word[pp]) : 0u;
         }
-        const bool skip = !p.no_skip && (u * ((Mm + Sest) + rec.qp) < Mm * (1.0f - 0x1p-15f));
-        if (skip) d.z_w[d.dt_wpos[pp]] = uint16_t(K1);
-        nskip += skip ? 1ull : 0ull;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          rec[c] = SkipRec{};
+          if (p0 + uint32_t(c * kWave + lane) < e) rec[c] = d.wskip[v[c]];
+        }
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const uint32_t pp = p0 + uint32_t(c * kWave + lane);
+          if (pp >= e) continue;
+          const uint32_t K1 = rec[c].k12 & 0xFFFFu, K2 = rec[c].k12 >> 16;
+          const uint32_t C1 = cmap[K1], C2 = cmap[K2];
+          const uint32_t key = p.key_identity ? pp : d.dt_key[pp];
+          // Step 3 in single precision with a relative margin of 2^-15, far
+          // above the fp32 rounding of these few operations (a few 2^-24): a
+          // token is skipped only if u*(M + S_est + Q') < M holds exactly, so
+          // its draw is K1 (S' <= S_est, Eq. 8-9).
+          const float u = float(uniform_draw(p.seed, t, key));
+          const float Mm = rec[c].a1 * (float(C1) + p.alpha_f);
+          float Sest;
+          if (p.g == 1) {
+            Sest = rec[c].a2 * float(len - C1);
+          } else if (p.g == 2) {
+            Sest = rec[c].a2 * float(C2) + rec[c].a3 * float(len - C1 - C2);
+          } else {
+            const uint32_t C3 = rec[c].k3 < uint32_t(K) ? uint32_t(cmap[rec[c].k3]) : 0u;
+            Sest = rec[c].a2 * float(C2) + rec[c].a3 * float(C3) + rec[c].a4 * float(len - C1 - C2 - C3);
+          }
+          const bool skip = !p.no_skip && (u * ((Mm + Sest) + rec[c].qp) < Mm * (1.0f - 0x1p-15f));
+          if (skip) {
+            // the sampler writes K1 into the slot with the rest of its batch
+            const uint32_t slot = d.dt_wpos[pp];
+            atomicOr(&d.skip_bits[slot >> 5], 1u << (slot & 31u));
+          }
+          nskip += skip ? 1ull : 0ull;
+        }
       }
       __builtin_amdgcn_wave_barrier();
       if (lane >= 1 && uint32_t(lane) <= nnz) cmap[rowv >> 16] = 0;
@@ -1155,13 +1176,13 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       const uint32_t j = base + uint32_t(ln);
       // the slot, key and row offset are loaded together (one latency); the
       // row header only for undecided tokens
-      uint32_t zj = 0, key = 0, off = 0;
+      uint32_t sk = 0, key = 0, off = 0;
       if (j < e) {
-        zj = d.z_w[j];
+        sk = d.skip_bits[j >> 5];
         key = d.wt_key[j];
         off = d.wt_rowoff[j];  // the row's first slot (its header)
       }
-      const bool und = j < e && zj == kUndecided;
+      const bool und = j < e && !((sk >> (j & 31u)) & 1u);
       uint32_t nnz = 0;
       if (und) {
         nnz = d.d_ent[off] & 0xFFFFu;
@@ -1177,8 +1198,10 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       draw_batch_small(und, nnz, bt, w, d.d_ent, ln, n_after_s);
       draw_long(__ballot(und && nnz + 1u > 512u), bt, w, d.d_ent, ln / kGroup, ln % kGroup, n_after_s);
       // the S' walks and Q' searches, one lane per token; the batch's topics
-      // leave in one coalesced store
-      if (und) d.z_w[j] = uint16_t(finish_draw(ln, bt, w, d.d_ent));
+      // (K1 for the tokens the step-3 test decided) leave in one coalesced store
+      uint32_t topic = K1;
+      if (und) topic = finish_draw(ln, bt, w, d.d_ent);
+      if (j < e) d.z_w[j] = uint16_t(topic);
     }
     __syncthreads();
   }
@@ -1413,7 +1436,9 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
       for (uint32_t j0 = b + uint32_t(wave) * 4u; j0 < e; j0 += uint32_t(waves) * 4u) {
         const uint32_t j = j0 + uint32_t(grp);
         const uint32_t q = j - b;  // place in the region
-        bool live = j < e && d.z_w[j] == kUndecided;
+        const bool skipped = j < e && ((d.skip_bits[j >> 5] >> (j & 31u)) & 1u);
+        if (pass == 0 && skipped && li == 0) d.z_w[j] = uint16_t(K1);  // decided by the step-3 test
+        bool live = j < e && !skipped;
         if (pass == 2) live = live && sc_code[q] != 0u;
         if (!live) continue;
         const uint32_t off = d.wt_rowoff[j];
@@ -1710,7 +1735,8 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
 }
 
-constexpr int kPre = 2;  // chunks of 64 tokens per document gathered one document ahead
+constexpr int kPre = 2;   // chunks of 64 tokens per document gathered one document ahead
+constexpr int kTail = 4;  // chunks of 64 tokens gathered together past the first kPre
 
 // Inclusive prefix sum of a u32 over the 64 lanes of a wave: DPP shifts
 // inside each row of 16 lanes (lanes below the shift read 0), then the row
@@ -1804,13 +1830,31 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
           }
         }
       }
-      for (uint32_t pp = b + uint32_t(kPre * kWave + lane); pp < e; pp += kWave) {
-        const uint32_t z = d.z_w[d.dt_wpos[pp]];
-        if (z < uint32_t(K)) {
-          atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
-          atomicOr(&bits[z >> 5], 1u << (z & 31u));
-        } else {
-          bad++;
+      // the rest of a long document, kTail chunks at a time: all their slot
+      // loads, then all their topic gathers, are in flight together
+      for (uint32_t p0 = b + uint32_t(kPre * kWave); p0 < e; p0 += uint32_t(kTail * kWave)) {
+        uint32_t zt[kTail];
+#pragma unroll
+        for (int c = 0; c < kTail; ++c) {
+          const uint32_t pp = p0 + uint32_t(c * kWave + lane);
+          zt[c] = pp < e ? d.dt_wpos[pp] : 0u;
+        }
+#pragma unroll
+        for (int c = 0; c < kTail; ++c) {
+          const uint32_t pp = p0 + uint32_t(c * kWave + lane);
+          if (pp < e) zt[c] = d.z_w[zt[c]];
+        }
+#pragma unroll
+        for (int c = 0; c < kTail; ++c) {
+          if (p0 + uint32_t(c * kWave + lane) < e) {
+            const uint32_t z = zt[c];
+            if (z < uint32_t(K)) {
+              atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
+              atomicOr(&bits[z >> 5], 1u << (z & 31u));
+            } else {
+              bad++;
+            }
+          }
         }
       }
       __threadfence_block();
@@ -1968,12 +2012,10 @@ hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s)
   return hipGetLastError();
 }
 
-hipError_t launch_fill_undecided(const DevState &d, const Params &p, hipStream_t s) {
-  // z_w is allocated with a whole number of 4-byte words (256-byte granules)
-  const int64_t n2 = (p.n + 1) / 2;
-  const int64_t blocks = std::min<int64_t>((n2 + kBlock - 1) / kBlock, int64_t(p.grid_docs) * 4);
-  hipLaunchKernelGGL(k_fill_undecided, dim3(uint32_t(blocks)), dim3(kBlock), 0, s,
-                     reinterpret_cast<uint32_t *>(d.z_w), n2);
+hipError_t launch_clear_skips(const DevState &d, const Params &p, hipStream_t s) {
+  const int64_t n = skip_words(p.n);
+  const int64_t blocks = std::min<int64_t>((n + kBlock - 1) / kBlock, int64_t(p.grid_docs) * 4);
+  hipLaunchKernelGGL(k_clear_skips, dim3(uint32_t(std::max<int64_t>(blocks, 1))), dim3(kBlock), 0, s, d.skip_bits, n);
   return hipGetLastError();
 }
 

@@ -259,6 +259,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.region, L.region.size()));
   LDA_TRY(dalloc(h, &d.split, L.split.size()));
   LDA_TRY(dalloc(h, &d.z_w, n));
+  LDA_TRY(dalloc(h, &d.skip_bits, skip_words(int64_t(n))));
   LDA_TRY(dalloc(h, &d.d_ent, size_t(L.d_cap.back()) + kRowPad));
   LDA_TRY(dalloc(h, &d.w_dense, size_t(L.n_dense) * size_t(L.K)));
   LDA_TRY(dalloc(h, &d.ws_cap, L.ws_cap.size()));
@@ -424,7 +425,7 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       if (ev) HIP_TRY(h, hipEventRecord(ev[0], h->stream));
       HIP_TRY(h, launch_begin_iteration(d, h->p, h->stream));
       HIP_TRY(h, launch_word_pre(d, h->p, h->stream));
-      HIP_TRY(h, launch_fill_undecided(d, h->p, h->stream));
+      HIP_TRY(h, launch_clear_skips(d, h->p, h->stream));
       if (ev) HIP_TRY(h, hipEventRecord(ev[1], h->stream));
       if (!h->p.no_skip) HIP_TRY(h, launch_doc_pass(d, h->p, t, h->stream));  // steps 2-3 only decide skips
       if (ev) HIP_TRY(h, hipEventRecord(ev[2], h->stream));

@@ -12,9 +12,6 @@
 
 namespace lda {
 
-// A 16-bit topic slot holds a topic (< K <= 32768) or kUndecided for a token
-// the step-3 test has not decided.
-constexpr uint16_t kUndecided = 0x8000;
 // Slack entries after the last D row.
 constexpr uint32_t kRowPad = 256;
 
@@ -28,6 +25,9 @@ __host__ __device__ inline uint32_t d_row_slots(uint32_t nnz) {
   const uint32_t n = nnz + 1u;
   return n <= 128u ? (n + 31u) & ~31u : n <= 256u ? (n + 63u) & ~63u : (n + 127u) & ~127u;
 }
+// Words of the per-iteration skip bitmap (one bit per token, a whole number
+// of 64-word blocks).
+__host__ __device__ inline int64_t skip_words(int64_t n) { return (n + 2047) / 2048 * 64; }
 // LDS words (u32) per wave of the D rebuild: K 16-bit counts, a bitmap of K
 // bits and a list of up to min(K, 2048) 16-bit topics
 __host__ __device__ inline size_t d_rebuild_lds_words(int K) {
@@ -115,6 +115,7 @@ struct DevState {
   uint8_t *split;     // per dense word
   // assignment, word order
   uint16_t *z_w;
+  uint32_t *skip_bits;  // one bit per word-ordered token: the step-3 test drew K1
   // counts
   uint32_t *d_cap, *d_ent;  // D row of doc d at d_cap[d]: header (len << 16 | nnz), then entries
   int32_t *w_dense;
@@ -177,7 +178,7 @@ hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s)
 hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_beta_sum(const DevState &d, const Params &p, hipStream_t s);
-hipError_t launch_fill_undecided(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_clear_skips(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 int sampler_block(int K, int want);
