@@ -425,6 +425,25 @@ __device__ __forceinline__ bool next_docs(uint32_t *__restrict__ cnt, const Para
   return false;
 }
 
+// The fields of a skip record that the test needs at g <= 2 (the first 20
+// bytes of the record: one 16-byte and one 4-byte load).
+struct SkipHead {
+  uint32_t k12;
+  float a1, a2, a3, qp;
+};
+__device__ __forceinline__ SkipHead skip_head(const SkipRec *__restrict__ r) {
+  return SkipHead{r->k12, r->a1, r->a2, r->a3, r->qp};
+}
+
+constexpr int kDocAhead = 2;  // chunks of 64 tokens per document loaded one document ahead
+
+// Steps 2-3 per document (Sec. 3.3): the D row spread into a per-wave
+// topic -> count table in LDS, then for every token C1 and C2 by lookup, u,
+// M, S_est and the skip test.  A skipped token's bit is set in the
+// word-ordered skip bitmap; the sampler writes K1 into its slot with the rest
+// of its batch.  KeyId: the input is sorted by document, so a token's key
+// (its input index) is its document-order position.
+template <bool KeyId>
 __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint32_t t,
                                                      unsigned long long *__restrict__ stats) {
   extern __shared__ uint16_t cmap_all[];
@@ -434,6 +453,31 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
   for (int k = lane; k < K; k += kWave) cmap[k] = 0;
   unsigned long long nskip = 0;
   const uint32_t M = uint32_t(p.M);
+  const uint32_t last = uint32_t(p.n - 1);
+  // Step 3 for token pp of a document of length len, in single precision
+  // with a relative margin of 2^-15, far above the fp32 rounding of these
+  // few operations (a few 2^-24): a token is skipped only if
+  // u*(M + S_est + Q') < M holds exactly, so its draw is K1 (S' <= S_est,
+  // Eq. 8-9).
+  auto test = [&](uint32_t pp, uint32_t len, const SkipHead &h, uint32_t v) -> bool {
+    const uint32_t K1 = h.k12 & 0xFFFFu, K2 = h.k12 >> 16;
+    const uint32_t C1 = cmap[K1], C2 = cmap[K2];
+    const uint32_t key = KeyId ? pp : d.dt_key[pp];
+    const float u = float(uniform_draw(p.seed, t, key));
+    const float Mm = h.a1 * (float(C1) + p.alpha_f);
+    float Sest;
+    if (p.g == 1) {
+      Sest = h.a2 * float(len - C1);
+    } else if (p.g == 2) {
+      Sest = h.a2 * float(C2) + h.a3 * float(len - C1 - C2);
+    } else {
+      const SkipRec &r = d.wskip[v];
+      const uint32_t C3 = r.k3 < uint32_t(K) ? uint32_t(cmap[r.k3]) : 0u;
+      Sest = h.a2 * float(C2) + h.a3 * float(C3) + r.a4 * float(len - C1 - C2 - C3);
+    }
+    return !p.no_skip && (u * ((Mm + Sest) + h.qp) < Mm * (1.0f - 0x1p-15f));
+  };
+  auto mark = [&](uint32_t slot) { atomicOr(&d.skip_bits[slot >> 5], 1u << (slot & 31u)); };
   for (;;) {
     uint32_t d0 = 0;
     if (lane == 0) d0 = atomicAdd(&d.counters[CNT_DOCPASS], kDocBatch);
@@ -443,84 +487,116 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
     // the batch's document offsets and row offsets, one per lane
     const uint32_t offv = lane <= nd ? d.doc_off[d0 + uint32_t(lane)] : 0u;
     const uint32_t capv = lane < nd ? d.d_cap[d0 + uint32_t(lane)] : 0u;
-    // the first 64 slots of a row (its header and first 63 entries) and the
-    // first 64 word ids of a document are loaded one document ahead
-    uint32_t nrow = 0, nw = 0;
-    {
-      const uint32_t b = uint32_t(__shfl(int(offv), 0)), e = uint32_t(__shfl(int(offv), 1));
-      nrow = d.d_ent[uint32_t(__shfl(int(capv), 0)) + uint32_t(lane)];
-      if (b + uint32_t(lane) < e) nw = d.dt_word[b + uint32_t(lane)];
+    // Pipeline over the first kDocAhead*64 tokens and row slots of each
+    // document: while document i is processed, the first row slots of
+    // document i+1 (its header and entries), the skip records of the words
+    // of document i+1 and the word ids of document i+2 are loaded.  Every
+    // load is issued (indexes past the batch are clamped; lanes past a
+    // document's end read word 0's record), and the skip marks of document
+    // i are set at document i+1, after its loads have been issued: the
+    // memory counter that the waits use counts in issue order, so that no
+    // wait drains the pipeline.
+    auto rows_of = [&](int doc, uint32_t (&r)[kDocAhead]) {
+      const uint32_t cap = __builtin_amdgcn_readlane(capv, doc);  // 0 past the batch; kRowPad covers the reach
+#pragma unroll
+      for (int c = 0; c < kDocAhead; ++c) r[c] = d.d_ent[cap + uint32_t(c * kWave + lane)];
+    };
+    auto words_of = [&](int doc, uint32_t (&w)[kDocAhead]) {
+      const uint32_t bn = __builtin_amdgcn_readlane(offv, doc);
+#pragma unroll
+      for (int c = 0; c < kDocAhead; ++c) w[c] = d.dt_word[min(bn + uint32_t(c * kWave + lane), last)];
+    };
+    auto heads_of = [&](int doc, const uint32_t (&w)[kDocAhead], SkipHead (&h)[kDocAhead]) {
+      const uint32_t bn = __builtin_amdgcn_readlane(offv, doc), en = __builtin_amdgcn_readlane(offv, doc + 1);
+#pragma unroll
+      for (int c = 0; c < kDocAhead; ++c) {
+        const uint32_t pn = bn + uint32_t(c * kWave + lane);
+        h[c] = skip_head(d.wskip + (pn < en ? w[c] : 0u));
+      }
+    };
+    uint32_t rowA[kDocAhead], wA[kDocAhead], wB[kDocAhead];
+    SkipHead hA[kDocAhead];
+    rows_of(0, rowA);
+    words_of(0, wA);
+    words_of(1, wB);
+    heads_of(0, wA, hA);
+    // the previous document's skipped tokens (lane masks) and their slots
+    unsigned long long pmask[kDocAhead];
+    uint32_t pslot[kDocAhead];
+#pragma unroll
+    for (int c = 0; c < kDocAhead; ++c) {
+      pmask[c] = 0ull;
+      pslot[c] = 0u;
     }
     for (int i = 0; i < nd; ++i) {
       const uint32_t b = __builtin_amdgcn_readlane(offv, i), e = __builtin_amdgcn_readlane(offv, i + 1);
       const uint32_t cap = __builtin_amdgcn_readlane(capv, i);
       const uint32_t len = e - b;
-      const uint32_t rowv = nrow, wv = nw;
-      if (i + 1 < nd) {
-        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 1), en = __builtin_amdgcn_readlane(offv, i + 2);
-        nrow = d.d_ent[__builtin_amdgcn_readlane(capv, i + 1) + uint32_t(lane)];
-        if (bn + uint32_t(lane) < en) nw = d.dt_word[bn + uint32_t(lane)];
+      uint32_t rowv[kDocAhead], wv[kDocAhead];
+      SkipHead hv[kDocAhead];
+#pragma unroll
+      for (int c = 0; c < kDocAhead; ++c) {
+        rowv[c] = rowA[c];
+        hv[c] = hA[c];
+        wv[c] = wA[c];
+        wA[c] = wB[c];
       }
+      rows_of(i + 1, rowA);
+      words_of(i + 2, wB);
+      heads_of(i + 1, wA, hA);
+#pragma unroll
+      for (int c = 0; c < kDocAhead; ++c)
+        if (pmask[c] && ((pmask[c] >> lane) & 1ull)) mark(pslot[c]);
       const uint32_t *row = d.d_ent + cap + 1;  // entries; slot 0 is the header
-      const uint32_t nnz = uint32_t(__builtin_amdgcn_readfirstlane(int(rowv))) & 0xFFFFu;
+      const uint32_t nnz = uint32_t(__builtin_amdgcn_readfirstlane(int(rowv[0]))) & 0xFFFFu;
       // spread the row into the topic -> count table
-      if (lane >= 1 && uint32_t(lane) <= nnz) cmap[rowv >> 16] = uint16_t(rowv & 0xFFFFu);
-      for (uint32_t q = 63u + uint32_t(lane); q < nnz; q += kWave) {
+#pragma unroll
+      for (int c = 0; c < kDocAhead; ++c) {
+        const uint32_t q = uint32_t(c * kWave + lane);  // slot; entry q - 1
+        if (q >= 1u && q <= nnz) cmap[rowv[c] >> 16] = uint16_t(rowv[c] & 0xFFFFu);
+      }
+      for (uint32_t q = uint32_t(kDocAhead * kWave - 1 + lane); q < nnz; q += kWave) {
         const uint32_t ent = row[q];
         cmap[ent >> 16] = uint16_t(ent & 0xFFFFu);
       }
       __builtin_amdgcn_wave_barrier();
-      // two chunks of 64 tokens per step, so that the word-id loads and the
-      // skip-record gathers of both are in flight together
-      for (uint32_t p0 = b; p0 < e; p0 += 2u * kWave) {
+#pragma unroll
+      for (int c = 0; c < kDocAhead; ++c) {
+        const uint32_t pp = b + uint32_t(c * kWave + lane);
+        const bool skip = pp < e && test(pp, len, hv[c], wv[c]);
+        nskip += skip ? 1ull : 0ull;
+        pmask[c] = __ballot(skip);
+        if (pmask[c]) pslot[c] = d.dt_wpos[min(pp, last)];
+      }
+      // the rest of a long document, two chunks per step, marked at once
+      for (uint32_t p0 = b + uint32_t(kDocAhead * kWave); p0 < e; p0 += 2u * kWave) {
         uint32_t v[2];
-        SkipRec rec[2];
+        SkipHead h[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) v[c] = d.dt_word[min(p0 + uint32_t(c * kWave + lane), last)];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) h[c] = skip_head(d.wskip + (p0 + uint32_t(c * kWave + lane) < e ? v[c] : 0u));
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           const uint32_t pp = p0 + uint32_t(c * kWave + lane);
-          v[c] = pp < e ? (pp < b + kWave ? wv : d.dt_word[pp]) : 0u;
-        }
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          rec[c] = SkipRec{};
-          if (p0 + uint32_t(c * kWave + lane) < e) rec[c] = d.wskip[v[c]];
-        }
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const uint32_t pp = p0 + uint32_t(c * kWave + lane);
-          if (pp >= e) continue;
-          const uint32_t K1 = rec[c].k12 & 0xFFFFu, K2 = rec[c].k12 >> 16;
-          const uint32_t C1 = cmap[K1], C2 = cmap[K2];
-          const uint32_t key = p.key_identity ? pp : d.dt_key[pp];
-          // Step 3 in single precision with a relative margin of 2^-15, far
-          // above the fp32 rounding of these few operations (a few 2^-24): a
-          // token is skipped only if u*(M + S_est + Q') < M holds exactly, so
-          // its draw is K1 (S' <= S_est, Eq. 8-9).
-          const float u = float(uniform_draw(p.seed, t, key));
-          const float Mm = rec[c].a1 * (float(C1) + p.alpha_f);
-          float Sest;
-          if (p.g == 1) {
-            Sest = rec[c].a2 * float(len - C1);
-          } else if (p.g == 2) {
-            Sest = rec[c].a2 * float(C2) + rec[c].a3 * float(len - C1 - C2);
-          } else {
-            const uint32_t C3 = rec[c].k3 < uint32_t(K) ? uint32_t(cmap[rec[c].k3]) : 0u;
-            Sest = rec[c].a2 * float(C2) + rec[c].a3 * float(C3) + rec[c].a4 * float(len - C1 - C2 - C3);
+          if (pp < e && test(pp, len, h[c], v[c])) {
+            nskip++;
+            mark(d.dt_wpos[pp]);
           }
-          const bool skip = !p.no_skip && (u * ((Mm + Sest) + rec[c].qp) < Mm * (1.0f - 0x1p-15f));
-          if (skip) {
-            // the sampler writes K1 into the slot with the rest of its batch
-            const uint32_t slot = d.dt_wpos[pp];
-            atomicOr(&d.skip_bits[slot >> 5], 1u << (slot & 31u));
-          }
-          nskip += skip ? 1ull : 0ull;
         }
       }
       __builtin_amdgcn_wave_barrier();
-      if (lane >= 1 && uint32_t(lane) <= nnz) cmap[rowv >> 16] = 0;
-      for (uint32_t q = 63u + uint32_t(lane); q < nnz; q += kWave) cmap[row[q] >> 16] = 0;
+#pragma unroll
+      for (int c = 0; c < kDocAhead; ++c) {
+        const uint32_t q = uint32_t(c * kWave + lane);
+        if (q >= 1u && q <= nnz) cmap[rowv[c] >> 16] = 0;
+      }
+      for (uint32_t q = uint32_t(kDocAhead * kWave - 1 + lane); q < nnz; q += kWave) cmap[row[q] >> 16] = 0;
       __builtin_amdgcn_wave_barrier();
     }
+#pragma unroll
+    for (int c = 0; c < kDocAhead; ++c)
+      if (pmask[c] && ((pmask[c] >> lane) & 1ull)) mark(pslot[c]);
   }
   nskip = group_sum_u64<kWave>(nskip);
   if (lane == 0 && nskip) atomicAdd(&stats[ST_SKIP3], nskip);
@@ -1781,43 +1857,41 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
     // here so that no later wait for them also waits for the prefetches)
     const uint32_t offv = lane <= nd ? d.doc_off[d0 + uint32_t(lane)] : 0u;
     const uint32_t capv = lane < nd ? d.d_cap[d0 + uint32_t(lane)] : 0u;
-    // two-stage pipeline over the first kPre*64 tokens of each document:
-    // the word-order slots of document i+1 are loaded while document i-1 is
-    // processed, and their topics are gathered while document i is
-    uint32_t wp1[kPre], z0[kPre];
+    // pipeline over the first kPre*64 tokens of each document: the
+    // word-order slots of document i+3 and the topics of document i+2 are
+    // loaded while document i is processed.  Every load is issued (slot
+    // indexes past the batch are clamped; lanes past a document's end read
+    // slot 0's topic), so the waits count a fixed number of loads and do not
+    // drain the pipeline.
+    const uint32_t last = uint32_t(p.n - 1);
+    auto slots_of = [&](int doc, uint32_t (&w)[kPre]) {
+      const uint32_t bn = __builtin_amdgcn_readlane(offv, doc);
 #pragma unroll
-    for (int c = 0; c < kPre; ++c) {
-      const uint32_t b = __builtin_amdgcn_readlane(offv, 0), e = __builtin_amdgcn_readlane(offv, 1);
-      const uint32_t pp = b + uint32_t(c * kWave + lane);
-      z0[c] = pp < e ? d.z_w[d.dt_wpos[pp]] : 0u;
-      wp1[c] = 0u;
-      if (nd > 1) {
-        const uint32_t bn = __builtin_amdgcn_readlane(offv, 1), en = __builtin_amdgcn_readlane(offv, 2);
-        const uint32_t pn = bn + uint32_t(c * kWave + lane);
-        if (pn < en) wp1[c] = d.dt_wpos[pn];
-      }
-    }
+      for (int c = 0; c < kPre; ++c) w[c] = d.dt_wpos[min(bn + uint32_t(c * kWave + lane), last)];
+    };
+    auto topics_of = [&](int doc, const uint32_t (&w)[kPre], uint32_t (&z)[kPre]) {
+      const uint32_t bn = __builtin_amdgcn_readlane(offv, doc), en = __builtin_amdgcn_readlane(offv, doc + 1);
+#pragma unroll
+      for (int c = 0; c < kPre; ++c) z[c] = d.z_w[bn + uint32_t(c * kWave + lane) < en ? w[c] : 0u];
+    };
+    uint32_t zA[kPre], zB[kPre], wC[kPre], wD[kPre];
+    slots_of(0, wD);
+    topics_of(0, wD, zA);
+    slots_of(1, wD);
+    topics_of(1, wD, zB);
+    slots_of(2, wC);
     for (int i = 0; i < nd; ++i) {
       const uint32_t b = __builtin_amdgcn_readlane(offv, i), e = __builtin_amdgcn_readlane(offv, i + 1);
       uint32_t zv[kPre];
 #pragma unroll
-      for (int c = 0; c < kPre; ++c) zv[c] = z0[c];
-      if (i + 1 < nd) {
-        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 1), en = __builtin_amdgcn_readlane(offv, i + 2);
-#pragma unroll
-        for (int c = 0; c < kPre; ++c) {
-          const uint32_t pn = bn + uint32_t(c * kWave + lane);
-          z0[c] = pn < en ? d.z_w[wp1[c]] : 0u;
-        }
+      for (int c = 0; c < kPre; ++c) {
+        zv[c] = zA[c];
+        zA[c] = zB[c];
       }
-      if (i + 2 < nd) {
-        const uint32_t bn = __builtin_amdgcn_readlane(offv, i + 2), en = __builtin_amdgcn_readlane(offv, i + 3);
+      slots_of(i + 3, wD);
+      topics_of(i + 2, wC, zB);
 #pragma unroll
-        for (int c = 0; c < kPre; ++c) {
-          const uint32_t pn = bn + uint32_t(c * kWave + lane);
-          wp1[c] = pn < en ? d.dt_wpos[pn] : 0u;
-        }
-      }
+      for (int c = 0; c < kPre; ++c) wC[c] = wD[c];
 #pragma unroll
       for (int c = 0; c < kPre; ++c) {
         if (b + uint32_t(c * kWave + lane) < e) {
@@ -2044,9 +2118,10 @@ hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s) {
 
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
   const size_t lds = sizeof(uint16_t) * size_t(p.K) * size_t(p.doc_waves);
-  hipError_t err = allow_lds(k_doc_pass, lds);
+  const auto kernel = p.key_identity ? k_doc_pass<true> : k_doc_pass<false>;
+  hipError_t err = allow_lds(kernel, lds);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_doc_pass, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), lds, s, d, p, t, d.stats);
+  hipLaunchKernelGGL(kernel, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), lds, s, d, p, t, d.stats);
   return hipGetLastError();
 }
 

@@ -102,9 +102,10 @@ struct WordRec {  // per relabelled word, refreshed every iteration (Sec. 3.2, s
 // Per-word record of the step-3 test in single precision (the test applies a
 // margin that covers the rounding, so a skip is always exact).
 struct SkipRec {
-  uint32_t k12;              // K1 | K2 << 16
-  uint32_t k3;               // third top topic (>= K when K < 3)
-  float a1, a2, a3, a4, qp;  // top-4 values of W^[v] and Q'
+  uint32_t k12;          // K1 | K2 << 16
+  float a1, a2, a3, qp;  // top-3 values of W^[v] and Q' (what the test needs at g <= 2)
+  uint32_t k3;           // third top topic (>= K when K < 3)
+  float a4;              // fourth top value (g = 3)
   uint32_t pad;
 };
 
