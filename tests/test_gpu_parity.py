@@ -253,6 +253,16 @@ def _edge_cases():
     yield "max_topics", _Tiny(rng.integers(0, 40, 3000), np.sort(rng.integers(0, 30, 3000)), 40, 16384, 0.01)
     yield "ragged_K", _Tiny(rng.integers(0, 300, 20000), np.sort(rng.integers(0, 200, 20000)), 300, 1013, 0.05)
     yield "max_topics_tiled", _Tiny(rng.integers(0, 40, 3000), np.sort(rng.integers(0, 30, 3000)), 40, 32768, 0.01)
+    # document lengths on both sides of every chunk edge of the document-major kernels (64-token
+    # chunks, 128 tokens and row slots loaded one document ahead, 32 documents per batch), with
+    # empty documents in between, and rows of more than 128 entries
+    lens = [0, 1, 63, 64, 65, 127, 128, 129, 191, 192, 193, 255, 256, 257, 383, 384, 385, 511, 512, 513]
+    lens = [lens[(7 * i) % len(lens)] for i in range(85)]
+    doc = np.repeat(np.arange(len(lens), dtype=np.int32), lens)
+    word = rng.zipf(1.3, doc.shape[0]) % 400
+    yield "chunk_edges", _Tiny(word, doc, 400, 301, 0.05)
+    perm = rng.permutation(doc.shape[0])  # the same corpus in shuffled input order (keys are not positions)
+    yield "chunk_edges_shuffled", _Tiny(word[perm], doc[perm], 400, 301, 0.05)
 
 
 @pytest.mark.parametrize("name,c", list(_edge_cases()), ids=[e[0] for e in _edge_cases()])
