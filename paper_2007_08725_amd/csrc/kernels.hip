@@ -203,10 +203,15 @@ __global__ void k_clear_skips(uint32_t *__restrict__ bits, int64_t n) {
     bits[q] = 0u;
 }
 
-__global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, int32_t K, double vbeta,
-                        uint32_t *__restrict__ counters, unsigned long long *__restrict__ stats) {
+__global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, double *__restrict__ bden, int32_t K,
+                        double beta, double vbeta, uint32_t *__restrict__ counters,
+                        unsigned long long *__restrict__ stats) {
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
-  if (k < K) den[k] = double(T[k]) + vbeta;
+  if (k < K) {
+    const double dk = double(T[k]) + vbeta;
+    den[k] = dk;
+    bden[k] = what(0u, beta, dk);  // W^[v][k] of every topic that word v does not hold
+  }
   if (blockIdx.x == 0 && threadIdx.x < kCounters) {
     counters[threadIdx.x] = 0u;
     if (stats && threadIdx.x < kStatsPerIter) stats[threadIdx.x] = 0ull;
@@ -283,7 +288,7 @@ __global__ __launch_bounds__(kBlock) void k_beta_sum(DevState d, Params p) {
   const int cs = (K + kBlock - 1) / kBlock;
   const int c0 = min(K, int(threadIdx.x) * cs), c1 = min(K, c0 + cs);
   double s = 0.0;
-  for (int k = c0; k < c1; ++k) s += what(0u, p.beta, d.den[k]);
+  for (int k = c0; k < c1; ++k) s += d.bden[k];
   s = block_sum(s, scratch);
   if (threadIdx.x == 0) d.beta_sum[0] = s;
 }
@@ -325,7 +330,7 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
       const double w = what(ent & 0xFFFFu, p.beta, d.den[k]);
       top_insert(t, w, k);
       snz += w;
-      sb += what(0u, p.beta, d.den[k]);
+      sb += d.bden[k];
     }
     if (tid == 0) {
       int found = 0;
@@ -334,7 +339,7 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
         const uint32_t k = d.topic_order[i];
         const uint32_t lb = row_lower_bound(ents, nnz, k);
         if (lb < nnz && (ents[lb] >> 16) == k) continue;
-        top_insert(t, what(0u, p.beta, d.den[k]), k);
+        top_insert(t, d.bden[k], k);
         found++;
       }
       s_full = found < want;  // the list ran out: scan every topic instead
@@ -1210,7 +1215,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
         const int s = int(v) - p.n_dense;
         const uint32_t *ents = d.ws_ent + d.ws_cap[s];
         const uint32_t nnz = d.ws_nnz[s];
-        for (int k = tid; k < K; k += NB) wh[k] = what(0u, p.beta, d.den[k]);
+        for (int k = tid; k < K; k += NB) wh[k] = d.bden[k];
         __syncthreads();
         for (uint32_t q = tid; q < nnz; q += NB) {
           const uint32_t ent = ents[q];
@@ -1421,7 +1426,7 @@ __device__ void fill_tile(const DevState &d, const Params &p, uint32_t v, uint32
     const uint32_t nnz = d.ws_nnz[s];
     for (uint32_t q = uint32_t(tid); q < kt + uint32_t(kGroup); q += uint32_t(nthreads)) {
       const uint32_t k = base + q;
-      wt[q] = q < len && k < uint32_t(K) && k != K1 ? what(0u, p.beta, d.den[k]) : 0.0;
+      wt[q] = q < len && k < uint32_t(K) && k != K1 ? d.bden[k] : 0.0;
     }
     __syncthreads();
     for (uint32_t q = uint32_t(tid); q < nnz; q += uint32_t(nthreads)) {
@@ -1508,26 +1513,46 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
         }
         __syncthreads();
       }
-      // four tokens per wave at a time, one per 16-lane group
+      // four tokens per wave at a time, one per 16-lane group.  A token's
+      // skip word, row offset and pass-2 code are loaded together, then its
+      // row header and first chunk together (the header is slot 0)
       for (uint32_t j0 = b + uint32_t(wave) * 4u; j0 < e; j0 += uint32_t(waves) * 4u) {
         const uint32_t j = j0 + uint32_t(grp);
         const uint32_t q = j - b;  // place in the region
-        const bool skipped = j < e && ((d.skip_bits[j >> 5] >> (j & 31u)) & 1u);
+        const uint32_t jj = min(j, e - 1u);
+        const uint32_t sk = d.skip_bits[jj >> 5], off = d.wt_rowoff[jj];
+        const uint32_t code0 = pass == 2 ? sc_code[jj - b] : 0u;
+        const bool skipped = j < e && ((sk >> (j & 31u)) & 1u);
         if (pass == 0 && skipped && li == 0) d.z_w[j] = uint16_t(K1);  // decided by the step-3 test
         bool live = j < e && !skipped;
-        if (pass == 2) live = live && sc_code[q] != 0u;
+        if (pass == 2) live = live && code0 != 0u;
         if (!live) continue;
-        const uint32_t off = d.wt_rowoff[j];
         const uint32_t *row = d.d_ent + off;
-        const uint32_t nnz = row[0] & 0xFFFFu;
+        // the first chunk in full (a row start plus kChunk slots stays
+        // inside the kRowPad slots past the last row), masked below
+        uint32_t r0[kMaxRun];
+        if (pass < 2) {
+#pragma unroll
+          for (int i = 0; i < kMaxRun; ++i) r0[i] = row[uint32_t(li) * kMaxRun + uint32_t(i)];
+        }
+        const uint32_t nnz = uint32_t(__shfl(int(pass < 2 ? r0[0] : row[0]), 0, kGroup)) & 0xFFFFu;
         const uint32_t slots = d_row_slots(nnz);
         const uint32_t nch = (slots + kChunk - 1) / kChunk;
+        if (pass < 2) {
+#pragma unroll
+          for (int i = 0; i < kMaxRun; ++i) {
+            const uint32_t qs = uint32_t(li) * kMaxRun + uint32_t(i);
+            if (qs == 0u || qs >= slots) r0[i] = pad;
+          }
+        }
         if (pass == 0) {
           // S' over the tile-0 topics, and C1 over the whole row; the
           // loads of up to kTiledAhead chunks are issued together
           double s0 = 0.0;
           uint32_t c1 = 0xFFFFFFFFu;
-          for (uint32_t c0 = 0; c0 < nch; c0 += kTiledAhead) {
+          c1 = run_count_of<kMaxRun>(r0, K1, c1);
+          s0 += run_sum_tile(r0, ts);
+          for (uint32_t c0 = 1; c0 < nch; c0 += kTiledAhead) {
             uint32_t r[kTiledAhead][kMaxRun];
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
@@ -1546,7 +1571,8 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
           }
         } else if (pass == 1) {
           double s1 = 0.0;
-          for (uint32_t c0 = 0; c0 < nch; c0 += kTiledAhead) {
+          s1 += run_sum_tile(r0, ts);
+          for (uint32_t c0 = 1; c0 < nch; c0 += kTiledAhead) {
             uint32_t r[kTiledAhead][kMaxRun];
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
@@ -1607,7 +1633,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
             }
           }
         } else {
-          const uint32_t code = sc_code[q];
+          const uint32_t code = code0;
           const double x = sc_x[q];
           uint32_t topic;
           if (code == 1u) {
@@ -2015,7 +2041,7 @@ __global__ __launch_bounds__(kBlock) void k_loglik(DevState d, Params p) {
         const int s = int(v) - p.n_dense;
         const uint32_t *ents = d.ws_ent + d.ws_cap[s];
         const uint32_t nnz = d.ws_nnz[s];
-        for (int k = tid; k < K; k += kBlock) wh[k] = what(0u, p.beta, d.den[k]);
+        for (int k = tid; k < K; k += kBlock) wh[k] = d.bden[k];
         __syncthreads();
         for (uint32_t q = tid; q < nnz; q += kBlock) {
           const uint32_t ent = ents[q];
@@ -2094,8 +2120,8 @@ hipError_t launch_clear_skips(const DevState &d, const Params &p, hipStream_t s)
 }
 
 hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_t s) {
-  hipLaunchKernelGGL(k_begin, dim3((p.K + kBlock - 1) / kBlock), dim3(kBlock), 0, s, d.T, d.den, p.K, p.vbeta,
-                     d.counters, d.stats);
+  hipLaunchKernelGGL(k_begin, dim3((p.K + kBlock - 1) / kBlock), dim3(kBlock), 0, s, d.T, d.den, d.bden, p.K, p.beta,
+                     p.vbeta, d.counters, d.stats);
   return hipGetLastError();
 }
 

@@ -267,6 +267,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.ws_ent, size_t(L.ws_cap.back())));
   LDA_TRY(dalloc(h, &d.T, size_t(L.K)));
   LDA_TRY(dalloc(h, &d.den, size_t(L.K)));
+  LDA_TRY(dalloc(h, &d.bden, size_t(L.K)));
   LDA_TRY(dalloc(h, &d.wrec, size_t(L.n_present)));
   LDA_TRY(dalloc(h, &d.wskip, size_t(L.n_present)));
   LDA_TRY(dalloc(h, &d.counters, kCounters));

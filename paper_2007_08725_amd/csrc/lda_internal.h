@@ -123,6 +123,7 @@ struct DevState {
   uint32_t *ws_cap, *ws_nnz, *ws_ent;
   uint32_t *T;
   double *den;
+  double *bden;  // beta / den[k]: W^[v][k] where W[v][k] = 0
   WordRec *wrec;
   SkipRec *wskip;
   // scheduler counters and statistics
