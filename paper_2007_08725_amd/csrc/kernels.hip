@@ -1958,7 +1958,9 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
         }
       }
       __threadfence_block();
-      uint32_t *out = d.d_ent + __builtin_amdgcn_readlane(capv, i) + 1;
+      // (readlane returns a signed int: the offset is taken back to unsigned,
+      // since D has more than 2^31 slots on the largest corpora)
+      uint32_t *out = d.d_ent + uint32_t(__builtin_amdgcn_readlane(capv, i)) + 1u;
       uint32_t base = 0;
       // 64 bitmap words (2048 topics) per step, one per lane; the two
       // topics of a count word share a bitmap word, so both are listed in
