@@ -82,3 +82,48 @@ def test_full_size_first_iteration(name):
     zo, flags, ost = oracle.iterate(c.word, c.doc, z0, seed=SEED, t=0, idx=idx, **corpus_kw(c))
     n_bad = compare_draws(cnt1["z"][idx], zo, flags, c.N)
     say("  %d flagged mismatches; oracle skip3 %d of %d" % (n_bad, ost["skip3"], SAMPLE))
+
+
+class _ManyDocs:
+    """70M one-token documents: every D row takes its minimum of 32 slots, so D
+    holds 2.24e9 slots and the rows of the last 2.2M documents start past 2^31
+    (the 32-bit unsigned offsets that address them must never pass through a
+    signed int)."""
+
+    def __init__(self, n=70_000_000, V=1000, K=1000):
+        rng = np.random.default_rng(31)
+        self.word = ((rng.zipf(1.2, n) - 1) % V).astype(np.int32)
+        self.doc = np.arange(n, dtype=np.int32)
+        self.N, self.n_docs, self.V, self.K, self.alpha, self.beta = n, n, V, K, 0.05, 0.01
+
+
+@pytest.mark.timeout(900)
+def test_d_row_offsets_past_2_31():
+    c = _ManyDocs()
+    say("many one-token documents: N=M=%d, D slots %.3g" % (c.N, 32.0 * c.N))
+    assert 32 * c.N > 2 ** 31
+    rng = np.random.default_rng(7)
+    # sampled tokens from the whole range and from the documents whose rows start past 2^31
+    idx = np.unique(np.concatenate([rng.choice(c.N, 4000, replace=False),
+                                    rng.choice(np.arange(c.N - 2_000_000, c.N), 4000, replace=False)]))
+    z0 = oracle.init_topics(c.N, c.K, SEED)
+    with make_lda(c) as m:
+        say("  library created")
+        st = m.iterate(1, stats=True)[0]
+        say("  gpu iteration %.1f ms" % st["ms_iter"])
+        cnt = m.counts()
+    z = cnt["z"]
+    assert st["skip_step3"] + st["sampled"] == c.N
+    # a one-token document's row is its token's topic with count 1
+    assert np.array_equal(cnt["D_off"], np.arange(c.N + 1))
+    assert np.array_equal(cnt["D_topic"], z) and np.all(cnt["D_count"] == 1)
+    assert np.array_equal(cnt["T"], np.bincount(z, minlength=c.K))
+    W = np.bincount(c.word.astype(np.int64) * c.K + z, minlength=c.V * c.K)
+    got = np.zeros(c.V * c.K, np.int64)
+    rows = np.repeat(np.arange(c.V, dtype=np.int64), np.diff(cnt["W_off"]))
+    got[rows * c.K + cnt["W_topic"]] = cnt["W_count"]
+    assert np.array_equal(got, W)
+    say("  counts checked; oracle on %d sampled tokens" % idx.size)
+    zo, flags, _ = oracle.iterate(c.word, c.doc, z0, seed=SEED, t=0, idx=idx, **corpus_kw(c))
+    n_bad = compare_draws(z[idx], zo, flags, c.N)
+    say("  %d flagged mismatches" % n_bad)
