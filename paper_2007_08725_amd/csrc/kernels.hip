@@ -607,19 +607,21 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
   if (lane == 0 && nskip) atomicAdd(&stats[ST_SKIP3], nskip);
 }
 
-// Steps 4-6 for the undecided tokens of one region; the W^ row of the word
+// Steps 4-6 for the tokens of one region that step 3 left to draw; the W^ row of the word
 // sits in LDS (Sec. 4.3, last paragraph) together with the Q' prefix over
 // blocks of kGroup topics.
 //
-// Work split: a wave takes 64 consecutive word-ordered tokens; every lane
-// fetches its own token's key, D-row offset and length, draws its own u and
-// stages them in the wave's slice of LDS, then the four 16-lane groups take
-// the undecided tokens in turn.  A group loads up to kChunk entries of the D
-// row into registers at once (lane l holds a contiguous run, so lane partial
-// sums are in ascending topic order), picks out C1 = D[d][K1] and sums S' per
-// lane, scans the 16 lane sums, and finds the selected entry by a walk inside
-// a single lane.  Rows longer than kChunk are taken in chunks.  The drawn
-// topics go back to LDS and leave in one coalesced store per batch.
+// Work split: a wave takes 64 consecutive word-ordered tokens.  Each lane
+// loads its token's skip bit, key and D-row offset, and for a token left to
+// draw its row header and u, staged in the wave's slice of LDS.  Those
+// tokens are listed by row length and drawn in rounds by groups of 4, 8 or
+// 16 lanes (draw_batch_small); rows over 512 slots by 16-lane groups in
+// chunks (draw_long).  A group holds the row in registers (lane l a
+// contiguous run, so lane partial sums are in ascending topic order), picks
+// out C1 = D[d][K1], sums S', splits x between M, S' and Q', and records the
+// selected run (S') or the remainder (Q'); one lane per token then finishes
+// the draw (finish_draw).  The batch's topics, K1 for the skipped tokens,
+// leave in one coalesced store.
 static_assert(kGroup == 16, "the row scans use DPP rows of 16 lanes");
 constexpr int kMaxRun = 8;                            // D entries per lane in registers
 constexpr uint32_t kChunk = kGroup * kMaxRun;         // 128 entries per group per chunk
@@ -1122,7 +1124,7 @@ __device__ void draw_rounds(int from, int to, const int (&ends)[8], const BatchL
   }
 }
 
-// The small-group draws of one batch.  The undecided lanes are listed in
+// The small-group draws of one batch.  The lanes left to draw are listed in
 // ascending bucket order; rows of up to 128 slots are drawn by groups of 4
 // lanes (16 a round), up to 256 by 8 lanes, up to 512 by 16 lanes.  When the
 // 4-lane rounds would end with a partial round of at most 8 rows, all of
@@ -1256,7 +1258,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       const int ln = lane_here();  // the lane, recomputed per batch
       const uint32_t j = base + uint32_t(ln);
       // the slot, key and row offset are loaded together (one latency); the
-      // row header only for undecided tokens
+      // row header only for the tokens left to draw
       uint32_t sk = 0, key = 0, off = 0;
       if (j < e) {
         sk = d.skip_bits[j >> 5];

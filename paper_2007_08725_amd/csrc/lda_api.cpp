@@ -98,7 +98,7 @@ lda_status check_handle(lda_handle *h) {
 }
 
 lda_status check_errors(lda_handle *h, const unsigned long long *st) {
-  if (st[ST_ERRORS]) return fail(h, LDA_E_DEVICE, "kernel found " + std::to_string(st[ST_ERRORS]) + " undecided topic slots");
+  if (st[ST_ERRORS]) return fail(h, LDA_E_DEVICE, "kernel found " + std::to_string(st[ST_ERRORS]) + " topic slots outside [0, K)");
   return LDA_OK;
 }
 
