@@ -1564,8 +1564,8 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
               s0 += run_sum_tile(r[c], ts);
             }
           }
-          const double S0 = group_sum<kGroup>(s0);
-          c1 = row_sum_u32(c1 <= 0xFFFFu ? c1 : 0u);
+          const double S0 = gsum<kGroup>(s0);
+          c1 = gsum_u32<kGroup>(c1 <= 0xFFFFu ? c1 : 0u);
           if (li == 0) {
             sc_s[q] = S0;
             sc_c1[q] = c1;
@@ -1581,7 +1581,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) s1 += run_sum_tile(r[c], ts);
           }
-          const double S1 = group_sum<kGroup>(s1);
+          const double S1 = gsum<kGroup>(s1);
           const double S0 = sc_s[q];
           const uint32_t c1 = sc_c1[q];
           const double Mm = rec.a1 * (double(c1) + p.alpha);  // Eq. 7
