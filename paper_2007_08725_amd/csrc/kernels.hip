@@ -683,8 +683,8 @@ __device__ __forceinline__ double run_sum(const uint32_t (&r)[C], const double *
 
 // min(c, D[d][K1]) if this lane's run holds topic K1, else c unchanged or
 // larger than 0xFFFF: an entry minus (K1 << 16) is its count when its topic
-// is K1 and at least 2^16 (modulo 2^32) for any other topic, since topics are
-// below 2^14.
+// is K1 and at least 2^16 (modulo 2^32) for any other topic, since topics
+// (and the padding topic K) are below 2^16.
 template <int C>
 __device__ __forceinline__ uint32_t run_count_of(const uint32_t (&r)[C], uint32_t K1, uint32_t c) {
   const uint32_t key = K1 << 16;
@@ -967,7 +967,7 @@ __device__ __forceinline__ int lane_here() {
 
 // Codes left in a token's topic slot by the small-group rounds: the draw
 // fell in S' (the entry is found by a walk over the recorded run) or in Q'
-// (a search of the word's Q' prefix).  Topics are below 2^14.
+// (a search of the word's Q' prefix).  Topics are below 2^15.
 constexpr uint16_t kDrawS = 0xFFFF;
 constexpr uint16_t kDrawQ = 0xFFFE;
 
