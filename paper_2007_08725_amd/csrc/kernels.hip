@@ -497,10 +497,8 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
     // document i+1 (its header and entries), the skip records of the words
     // of document i+1 and the word ids of document i+2 are loaded.  Every
     // load is issued (indexes past the batch are clamped; lanes past a
-    // document's end read word 0's record), and the skip marks of document
-    // i are set at document i+1, after its loads have been issued: the
-    // memory counter that the waits use counts in issue order, so that no
-    // wait drains the pipeline.
+    // document's end read word 0's record), so that the waits count a fixed
+    // number of loads.
     auto rows_of = [&](int doc, uint32_t (&r)[kDocAhead]) {
       const uint32_t cap = __builtin_amdgcn_readlane(capv, doc);  // 0 past the batch; kRowPad covers the reach
 #pragma unroll
@@ -525,14 +523,6 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
     words_of(0, wA);
     words_of(1, wB);
     heads_of(0, wA, hA);
-    // the previous document's skipped tokens (lane masks) and their slots
-    unsigned long long pmask[kDocAhead];
-    uint32_t pslot[kDocAhead];
-#pragma unroll
-    for (int c = 0; c < kDocAhead; ++c) {
-      pmask[c] = 0ull;
-      pslot[c] = 0u;
-    }
     for (int i = 0; i < nd; ++i) {
       const uint32_t b = __builtin_amdgcn_readlane(offv, i), e = __builtin_amdgcn_readlane(offv, i + 1);
       const uint32_t cap = __builtin_amdgcn_readlane(capv, i);
@@ -549,9 +539,6 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
       rows_of(i + 1, rowA);
       words_of(i + 2, wB);
       heads_of(i + 1, wA, hA);
-#pragma unroll
-      for (int c = 0; c < kDocAhead; ++c)
-        if (pmask[c] && ((pmask[c] >> lane) & 1ull)) mark(pslot[c]);
       const uint32_t *row = d.d_ent + cap + 1;  // entries; slot 0 is the header
       const uint32_t nnz = uint32_t(__builtin_amdgcn_readfirstlane(int(rowv[0]))) & 0xFFFFu;
       // spread the row into the topic -> count table
@@ -568,12 +555,12 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
 #pragma unroll
       for (int c = 0; c < kDocAhead; ++c) {
         const uint32_t pp = b + uint32_t(c * kWave + lane);
-        const bool skip = pp < e && test(pp, len, hv[c], wv[c]);
-        nskip += skip ? 1ull : 0ull;
-        pmask[c] = __ballot(skip);
-        if (pmask[c]) pslot[c] = d.dt_wpos[min(pp, last)];
+        if (pp < e && test(pp, len, hv[c], wv[c])) {
+          nskip++;
+          mark(d.dt_wpos[pp]);
+        }
       }
-      // the rest of a long document, two chunks per step, marked at once
+      // the rest of a long document, two chunks per step
       for (uint32_t p0 = b + uint32_t(kDocAhead * kWave); p0 < e; p0 += 2u * kWave) {
         uint32_t v[2];
         SkipHead h[2];
@@ -599,9 +586,6 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
       for (uint32_t q = uint32_t(kDocAhead * kWave - 1 + lane); q < nnz; q += kWave) cmap[row[q] >> 16] = 0;
       __builtin_amdgcn_wave_barrier();
     }
-#pragma unroll
-    for (int c = 0; c < kDocAhead; ++c)
-      if (pmask[c] && ((pmask[c] >> lane) & 1ull)) mark(pslot[c]);
   }
   nskip = group_sum_u64<kWave>(nskip);
   if (lane == 0 && nskip) atomicAdd(&stats[ST_SKIP3], nskip);
