@@ -88,8 +88,8 @@ def main():
                     help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported "
-              "(the multi-GPU design is described but not built)" % args.gpus, file=sys.stderr)
+        print("bench.py: the library runs on exactly one GPU; --gpus %d is not supported "
+              "(sharding across GPUs is designed, not implemented)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
