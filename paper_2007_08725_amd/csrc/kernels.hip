@@ -1668,6 +1668,8 @@ __global__ void k_zero_split(DevState d, Params p) {
 // rows written whole (or added with atomics when the word is split), sparse
 // rows compacted to ascending packed entries; T accumulated per workgroup.
 // W rebuild for moderate K: per region a K-entry histogram, scanned in full.
+constexpr int kHistAhead = 8;  // word-ordered topic loads per thread issued together in the W rebuild
+
 __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
@@ -1694,10 +1696,18 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
     __syncthreads();
     if (!s_valid) break;
     const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2];
-    for (uint32_t j = b + tid; j < e; j += kBlock) {
-      const uint32_t z = d.z_w[j];
-      if (z < uint32_t(K)) atomicAdd(&hist[z], 1u);
-      else bad++;
+    // kHistAhead topic loads per thread in flight at once
+    for (uint32_t j0 = b + tid; j0 < e; j0 += uint32_t(kHistAhead * kBlock)) {
+      uint32_t zz[kHistAhead];
+#pragma unroll
+      for (int u = 0; u < kHistAhead; ++u) zz[u] = uint32_t(u * kBlock) < e - j0 ? uint32_t(d.z_w[j0 + u * kBlock]) : 0u;
+#pragma unroll
+      for (int u = 0; u < kHistAhead; ++u) {
+        if (uint32_t(u * kBlock) < e - j0) {
+          if (zz[u] < uint32_t(K)) atomicAdd(&hist[zz[u]], 1u);
+          else bad++;
+        }
+      }
     }
     __syncthreads();
     if (int32_t(v) < p.n_dense) {
@@ -1767,13 +1777,22 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
     __syncthreads();
     if (!s_valid) break;
     const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2];
-    for (uint32_t j = b + tid; j < e; j += kBlock) {
-      const uint32_t z = d.z_w[j];
-      if (z < uint32_t(K)) {
-        atomicAdd(&hist[z], 1u);
-        atomicOr(&bits[z >> 5], 1u << (z & 31u));
-      } else {
-        bad++;
+    // kHistAhead topic loads per thread in flight at once
+    for (uint32_t j0 = b + tid; j0 < e; j0 += uint32_t(kHistAhead * kBlock)) {
+      uint32_t zz[kHistAhead];
+#pragma unroll
+      for (int u = 0; u < kHistAhead; ++u) zz[u] = uint32_t(u * kBlock) < e - j0 ? uint32_t(d.z_w[j0 + u * kBlock]) : 0u;
+#pragma unroll
+      for (int u = 0; u < kHistAhead; ++u) {
+        if (uint32_t(u * kBlock) < e - j0) {
+          const uint32_t z = zz[u];
+          if (z < uint32_t(K)) {
+            atomicAdd(&hist[z], 1u);
+            atomicOr(&bits[z >> 5], 1u << (z & 31u));
+          } else {
+            bad++;
+          }
+        }
       }
     }
     __syncthreads();
