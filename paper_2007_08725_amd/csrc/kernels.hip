@@ -403,6 +403,10 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
 // into a per-wave topic -> count table in LDS, so each token's C1 and C2 are
 // two LDS reads; the table is cleared again from the row afterwards.
 constexpr uint32_t kDocBatch = 32;
+// Documents per batch of the D rebuild: a smaller window of documents in
+// flight keeps more of its topic gathers in the caches (at 16 and below the
+// counters' atomics start to bound the kernel).
+constexpr uint32_t kRebuildBatch = 24;
 
 // Next batch [d0, d1) of documents for a wave of the D rebuild.  The
 // documents are split into kXcds ranges of equal token counts; workgroups are
@@ -417,12 +421,12 @@ __device__ __forceinline__ bool next_docs(uint32_t *__restrict__ cnt, const Para
   while (part < kXcds) {
     const int r = (x + part) % kXcds;
     uint32_t o = 0;
-    if (lane == 0) o = atomicAdd(&cnt[r], kDocBatch);
+    if (lane == 0) o = atomicAdd(&cnt[r], kRebuildBatch);
     o = __shfl(o, 0);
     const uint32_t b = p.xcd_doc[r] + o, e = p.xcd_doc[r + 1];
     if (o < e - p.xcd_doc[r]) {
       d0 = b;
-      d1 = min(b + kDocBatch, e);
+      d1 = min(b + kRebuildBatch, e);
       return true;
     }
     ++part;
@@ -2251,7 +2255,11 @@ hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s) {
   const size_t dlds = sizeof(uint32_t) * d_rebuild_lds_words(p.K) * size_t(p.doc_waves);
   err = allow_lds(k_rebuild_d, dlds);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(k_rebuild_d, dim3(uint32_t(p.grid_docs)), dim3(kWave * p.doc_waves), dlds, s, d, p);
+  // half the document grid (4 workgroups per CU): fewer waves in flight keep
+  // a narrower window of documents, whose topic gathers then hit the caches
+  // more often
+  const uint32_t dgrid = uint32_t(std::max(1, p.grid_docs / 2));
+  hipLaunchKernelGGL(k_rebuild_d, dim3(dgrid), dim3(kWave * p.doc_waves), dlds, s, d, p);
   return hipGetLastError();
 }
 
