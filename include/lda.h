@@ -87,7 +87,14 @@ typedef struct {
    * limits how many workgroups a CU holds).  LDA_E_RANGE if the size asked
    * for does not fit.  Performance switch; the draws are unchanged. */
   int32_t sampler_block;
-  int32_t reserved[2];
+  /* How the step-3 skip decisions reach the sampler (Sec. 3.3): 0 = chosen
+   * per iteration from the previous iteration's skip rate (default); 1 =
+   * always a bitmap in word order (one scattered bit per skipped token); 2 =
+   * a bitmap in document order (coalesced bits, read by the sampler at each
+   * token's key) whenever the input is sorted by document and K fits the
+   * regular sampler, else as 1.  Performance switch; the draws are unchanged. */
+  int32_t skip_marks;
+  int32_t reserved[1];
 } lda_options;
 
 /* Per-iteration statistics (filled by lda_iterate when requested). */

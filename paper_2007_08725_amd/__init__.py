@@ -33,7 +33,8 @@ class Options(ctypes.Structure):
     _fields_ = [("stream", ctypes.c_void_p), ("dev_alloc", ALLOC_FN), ("dev_free", FREE_FN),
                 ("alloc_ctx", ctypes.c_void_p), ("g", ctypes.c_int32), ("region_tokens", ctypes.c_int32),
                 ("no_skip", ctypes.c_int32), ("dense_cutoff", ctypes.c_int32), ("two_branch", ctypes.c_int32),
-                ("sampler_block", ctypes.c_int32), ("reserved", ctypes.c_int32 * 2)]
+                ("sampler_block", ctypes.c_int32), ("skip_marks", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 1)]
 
 
 class IterStats(ctypes.Structure):
@@ -146,12 +147,14 @@ class LDA:
     the options of ``lda_options``; none of them changes the draws.
     ``two_branch`` samples over [S | Q] (Sec. 2.2): same distribution, other
     canonical order.  ``sampler_block`` (256, 512, 1024; 0 = by occupancy)
-    sets the sampler's workgroup size.
+    sets the sampler's workgroup size; ``skip_marks`` (0 auto, 1 word order,
+    2 document order) how skip decisions reach the sampler.
     """
 
     def __init__(self, word, doc, V: int, K: int, alpha: float, beta: float = 0.01, seed: int = 42, *, g: int = 2,
                  region_tokens: int = 0, no_skip: bool = False, dense_cutoff: int = 0, two_branch: bool = False,
-                 sampler_block: int = 0, torch_stream: bool = True, torch_allocator: bool = True):
+                 sampler_block: int = 0, skip_marks: int = 0, torch_stream: bool = True,
+                 torch_allocator: bool = True):
         self._lib = load_library()
         self._h = ctypes.c_void_p()
         word = np.ascontiguousarray(word, np.int32)
@@ -165,6 +168,7 @@ class LDA:
         opts.dense_cutoff = dense_cutoff
         opts.two_branch = 1 if two_branch else 0
         opts.sampler_block = sampler_block
+        opts.skip_marks = skip_marks
         self._keep = []
         if torch_stream or torch_allocator:
             import torch

@@ -197,10 +197,28 @@ __global__ void k_init_topics(const uint32_t *__restrict__ wt_key, uint16_t *__r
     z_w[j] = initial_topic(seed, wt_key[j], K);
 }
 
-// The skip bitmap starts every iteration clear.
-__global__ void k_clear_skips(uint32_t *__restrict__ bits, int64_t n) {
-  for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < n; q += int64_t(gridDim.x) * blockDim.x)
-    bits[q] = 0u;
+// The skip bitmaps start every iteration clear, and so does this
+// iteration's skip count (the other parity's count, the previous
+// iteration's, stays for the choice of bitmap).
+__global__ void k_clear_skips(uint32_t *__restrict__ bits, uint32_t *__restrict__ doc_bits, int64_t n, int64_t n_doc,
+                              unsigned long long *__restrict__ hist, uint32_t t) {
+  const int64_t i0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x, step = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t q = i0; q < n; q += step) bits[q] = 0u;
+  if (doc_bits)
+    for (int64_t q = i0; q < n_doc; q += step) doc_bits[q] = 0u;
+  if (i0 == 0) hist[t & 1u] = 0ull;
+}
+
+// Whether iteration t carries its skip decisions in the document-ordered
+// bitmap: coalesced writes in the doc pass and one dependent read per token
+// in the sampler, against one scattered write per skipped token for the
+// word-ordered bitmap.  By default it does once the previous iteration
+// skipped more than a fifth of the tokens, where the scattered writes cost
+// more than the reads.
+__device__ __forceinline__ bool doc_marks(const DevState &d, const Params &p, uint32_t t) {
+  if (!p.doc_marks_ok || p.skip_marks == 1) return false;
+  if (p.skip_marks == 2) return true;
+  return t > 0u && 5ull * d.skip_hist[(t + 1u) & 1u] > uint64_t(p.n);
 }
 
 __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, double *__restrict__ bden, int32_t K,
@@ -486,7 +504,22 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
     }
     return !p.no_skip && (u * ((Mm + Sest) + h.qp) < Mm * (1.0f - 0x1p-15f));
   };
+  // A skipped token's decision goes to the sampler either as a bit at its
+  // word-order slot (one scattered write per skipped token) or, in the
+  // document-ordered bitmap, as a bit at its document position: the chunk's
+  // 64 bits from a ballot, in at most three words, whose neighbours other
+  // waves may set too.
+  const bool by_doc = doc_marks(d, p, t);
   auto mark = [&](uint32_t slot) { atomicOr(&d.skip_bits[slot >> 5], 1u << (slot & 31u)); };
+  auto mark_chunk = [&](unsigned long long m, uint32_t p0) {  // m: lanes (positions p0 + lane) skipped
+    if (m == 0ull) return;
+    const uint32_t sh = p0 & 31u;
+    const uint32_t v0 = uint32_t(m << sh);
+    const uint32_t v1 = sh ? uint32_t(m >> (32u - sh)) : uint32_t(m >> 32);
+    const uint32_t v2 = sh ? uint32_t(m >> (64u - sh)) : 0u;
+    const uint32_t v = lane == 0 ? v0 : lane == 1 ? v1 : v2;
+    if (lane < 3 && v != 0u) atomicOr(&d.skip_doc[(p0 >> 5) + uint32_t(lane)], v);
+  };
   for (;;) {
     uint32_t d0 = 0;
     if (lane == 0) d0 = atomicAdd(&d.counters[CNT_DOCPASS], kDocBatch);
@@ -559,10 +592,10 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
 #pragma unroll
       for (int c = 0; c < kDocAhead; ++c) {
         const uint32_t pp = b + uint32_t(c * kWave + lane);
-        if (pp < e && test(pp, len, hv[c], wv[c])) {
-          nskip++;
-          mark(d.dt_wpos[pp]);
-        }
+        const bool skip = pp < e && test(pp, len, hv[c], wv[c]);
+        nskip += skip ? 1ull : 0ull;
+        if (by_doc) mark_chunk(__ballot(skip), b + uint32_t(c * kWave));
+        else if (skip) mark(d.dt_wpos[pp]);
       }
       // the rest of a long document, two chunks per step
       for (uint32_t p0 = b + uint32_t(kDocAhead * kWave); p0 < e; p0 += 2u * kWave) {
@@ -575,10 +608,10 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           const uint32_t pp = p0 + uint32_t(c * kWave + lane);
-          if (pp < e && test(pp, len, h[c], v[c])) {
-            nskip++;
-            mark(d.dt_wpos[pp]);
-          }
+          const bool skip = pp < e && test(pp, len, h[c], v[c]);
+          nskip += skip ? 1ull : 0ull;
+          if (by_doc) mark_chunk(__ballot(skip), p0 + uint32_t(c * kWave));
+          else if (skip) mark(d.dt_wpos[pp]);
         }
       }
       __builtin_amdgcn_wave_barrier();
@@ -592,7 +625,10 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
     }
   }
   nskip = group_sum_u64<kWave>(nskip);
-  if (lane == 0 && nskip) atomicAdd(&stats[ST_SKIP3], nskip);
+  if (lane == 0 && nskip) {
+    atomicAdd(&stats[ST_SKIP3], nskip);
+    atomicAdd(&d.skip_hist[t & 1u], nskip);
+  }
 }
 
 // Steps 4-6 for the tokens of one region that step 3 left to draw; the W^ row of the word
@@ -1149,6 +1185,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
   const int K = p.K;
   const int nb = (K + kGroup - 1) / kGroup;
   const int nbp = q_blocks_padded(nb);
+  const bool by_doc = doc_marks(d, p, t);  // which bitmap carries this iteration's skip decisions
   // dynamic LDS only (sampler_lds_bytes)
   double *wh = lds;                  // [wh_entries(K)]: W^' of the region's word, zeros past K
   double *qb = lds + wh_entries(K);  // [nbp + 1]: qb[b] = sum of alpha*W^' over topics < b*kGroup; +inf past nb
@@ -1249,11 +1286,13 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       // row header only for the tokens left to draw
       uint32_t sk = 0, key = 0, off = 0;
       if (j < e) {
-        sk = d.skip_bits[j >> 5];
         key = d.wt_key[j];
         off = d.wt_rowoff[j];  // the row's first slot (its header)
+        // the skip bit at the word-order slot, or at the key (the token's
+        // document position) in the document-ordered bitmap
+        sk = by_doc ? d.skip_doc[key >> 5] >> (key & 31u) : d.skip_bits[j >> 5] >> (j & 31u);
       }
-      const bool und = j < e && !((sk >> (j & 31u)) & 1u);
+      const bool und = j < e && !(sk & 1u);
       uint32_t nnz = 0;
       if (und) {
         nnz = d.d_ent[off] & 0xFFFFu;
@@ -2123,10 +2162,11 @@ hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s)
   return hipGetLastError();
 }
 
-hipError_t launch_clear_skips(const DevState &d, const Params &p, hipStream_t s) {
+hipError_t launch_clear_skips(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
   const int64_t n = skip_words(p.n);
   const int64_t blocks = std::min<int64_t>((n + kBlock - 1) / kBlock, int64_t(p.grid_docs) * 4);
-  hipLaunchKernelGGL(k_clear_skips, dim3(uint32_t(std::max<int64_t>(blocks, 1))), dim3(kBlock), 0, s, d.skip_bits, n);
+  hipLaunchKernelGGL(k_clear_skips, dim3(uint32_t(std::max<int64_t>(blocks, 1))), dim3(kBlock), 0, s, d.skip_bits,
+                     d.skip_doc, n, n + 64, d.skip_hist, t);
   return hipGetLastError();
 }
 

@@ -260,6 +260,15 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(dalloc(h, &d.split, L.split.size()));
   LDA_TRY(dalloc(h, &d.z_w, n));
   LDA_TRY(dalloc(h, &d.skip_bits, skip_words(int64_t(n))));
+  // the document-ordered skip bitmap (bit = the token's key, which is its
+  // document position when the input is sorted by document; 64 spare words
+  // for the 3-word writes of a document's last chunk) and the per-parity skip
+  // counts that choose between the two bitmaps
+  p.doc_marks_ok = (identity && !p.big_k) ? 1 : 0;
+  d.skip_doc = nullptr;
+  if (p.doc_marks_ok) LDA_TRY(dalloc(h, &d.skip_doc, size_t(skip_words(int64_t(n))) + 64));
+  LDA_TRY(dalloc(h, &d.skip_hist, 2));
+  HIP_TRY(h, hipMemsetAsync(d.skip_hist, 0, 2 * sizeof(unsigned long long), h->stream));
   LDA_TRY(dalloc(h, &d.d_ent, size_t(L.d_cap.back()) + kRowPad));
   LDA_TRY(dalloc(h, &d.w_dense, size_t(L.n_dense) * size_t(L.K)));
   LDA_TRY(dalloc(h, &d.ws_cap, L.ws_cap.size()));
@@ -345,7 +354,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   if (K < 2 || K > LDA_MAX_TOPICS) return fail(nullptr, LDA_E_ARG, "K must be in [2, 32768]");
   if (!std::isfinite(alpha) || !(alpha > 0.0)) return fail(nullptr, LDA_E_ARG, "alpha must be finite and positive");
   if (!std::isfinite(beta) || !(beta > 0.0)) return fail(nullptr, LDA_E_ARG, "beta must be finite and positive");
-  int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0, two_branch = 0;
+  int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0, two_branch = 0, skip_marks = 0;
   if (opts) {
     if (opts->g < 0 || opts->g > 3) return fail(nullptr, LDA_E_ARG, "g must be 1, 2 or 3");
     if (opts->g) g = opts->g;
@@ -360,6 +369,8 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
     const int32_t sb = opts->sampler_block;
     if (sb != 0 && sb != 256 && sb != 512 && sb != 1024)
       return fail(nullptr, LDA_E_ARG, "sampler_block must be 0, 256, 512 or 1024");
+    if (opts->skip_marks < 0 || opts->skip_marks > 2) return fail(nullptr, LDA_E_ARG, "skip_marks must be 0, 1 or 2");
+    skip_marks = opts->skip_marks;
   }
   lda_handle *h = new (std::nothrow) lda_handle();
   if (!h) return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
@@ -395,6 +406,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   p.no_skip = no_skip;
   p.two_branch = two_branch;
   p.key_identity = sorted ? 1 : 0;
+  p.skip_marks = skip_marks;
   try {
     st = create_device(h, opts, word, doc, R, dense_cutoff);
   } catch (const std::bad_alloc &) {
@@ -426,7 +438,7 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       if (ev) HIP_TRY(h, hipEventRecord(ev[0], h->stream));
       HIP_TRY(h, launch_begin_iteration(d, h->p, h->stream));
       HIP_TRY(h, launch_word_pre(d, h->p, h->stream));
-      HIP_TRY(h, launch_clear_skips(d, h->p, h->stream));
+      HIP_TRY(h, launch_clear_skips(d, h->p, t, h->stream));
       if (ev) HIP_TRY(h, hipEventRecord(ev[1], h->stream));
       if (!h->p.no_skip) HIP_TRY(h, launch_doc_pass(d, h->p, t, h->stream));  // steps 2-3 only decide skips
       if (ev) HIP_TRY(h, hipEventRecord(ev[2], h->stream));

@@ -117,6 +117,8 @@ struct DevState {
   // assignment, word order
   uint16_t *z_w;
   uint32_t *skip_bits;  // one bit per word-ordered token: the step-3 test drew K1
+  uint32_t *skip_doc;   // the same decisions in document order (null when not usable)
+  unsigned long long *skip_hist;  // tokens skipped at step 3 by iteration parity: [t & 1]
   // counts
   uint32_t *d_cap, *d_ent;  // D row of doc d at d_cap[d]: header (len << 16 | nnz), then entries
   int32_t *w_dense;
@@ -165,6 +167,8 @@ struct Params {
   int32_t doc_waves;     // waves per workgroup of the doc pass and the D rebuild (LDS tables of K entries per wave)
   int32_t sparse_pre;    // per-word precompute of sparse words from their row and a topic list (large K)
   int32_t top_list;      // length of that topic list
+  int32_t skip_marks;    // 0 auto, 1 word-ordered bitmap, 2 document-ordered bitmap (lda_options)
+  int32_t doc_marks_ok;  // the document-ordered bitmap is usable: keys are document positions, regular sampler
   uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
 
@@ -180,7 +184,7 @@ hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s)
 hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_beta_sum(const DevState &d, const Params &p, hipStream_t s);
-hipError_t launch_clear_skips(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_clear_skips(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 int sampler_block(int K, int want);

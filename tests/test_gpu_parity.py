@@ -84,10 +84,11 @@ def test_c1_free_running_trajectory_and_llpt(c1, c1_traj):
 @pytest.mark.parametrize("opts", [dict(region_tokens=7), dict(region_tokens=100), dict(g=1), dict(g=3), dict(no_skip=True),
                                   dict(dense_cutoff=-1), dict(dense_cutoff=1 << 30), dict(dense_cutoff=3),
                                   dict(sampler_block=256), dict(sampler_block=512), dict(sampler_block=1024),
+                                  dict(skip_marks=1), dict(skip_marks=2),
                                   dict(torch_allocator=False, torch_stream=False)])
 def test_schedule_invariance(c1, opts):
     """Region size, S_est depth, the skip test, the hybrid-W cutoff (all dense, all sparse),
-    the sampler's workgroup size, allocator and stream never change the draws."""
+    the sampler's workgroup size, the skip bitmap, allocator and stream never change the draws."""
     say("invariance %s" % opts)
     with make_lda(c1) as a:
         a.iterate(3)
@@ -96,6 +97,33 @@ def test_schedule_invariance(c1, opts):
         b.iterate(3)
         zb = b.counts(D=False, W=False)["z"]
     assert np.array_equal(za, zb)
+
+
+def test_skip_bitmaps_leave_the_draws_unchanged():
+    """Skip decisions carried by the word-ordered bitmap, the document-ordered
+    bitmap, or the per-iteration choice between them (which switches once a
+    fifth of the tokens skip) give the same draws, over iterations whose skip
+    rate climbs past that threshold; shuffled input has no document-ordered
+    bitmap and falls back to the word-ordered one."""
+    c = lda_synth.make_corpus("c3", n_docs=12000)
+    say("skip bitmaps c3 reduced N=%d" % c.N)
+    zs, rates = [], None
+    for marks in (1, 2, 0):
+        with make_lda(c, skip_marks=marks) as m:
+            st = m.iterate(60, stats=True)
+            zs.append(m.counts(D=False, W=False)["z"])
+        r = [s["skip_step3"] / c.N for s in st]
+        rates = r if rates is None else rates
+        assert r == rates  # the skip decisions themselves are the same
+    say("  skip rate at iterations 0, 30, 59: %.3f %.3f %.3f" % (rates[0], rates[30], rates[59]))
+    assert np.array_equal(zs[0], zs[1]) and np.array_equal(zs[0], zs[2])
+    cs = lda_synth.generate(lda_synth.SPECS["c1"], n_docs=300, shuffle=True)
+    out = []
+    for marks in (1, 2):
+        with make_lda(cs, skip_marks=marks) as m:
+            m.iterate(3)
+            out.append(m.counts(D=False, W=False)["z"])
+    assert np.array_equal(out[0], out[1])
 
 
 @pytest.mark.parametrize("g", [1, 3])
