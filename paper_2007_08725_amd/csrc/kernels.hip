@@ -213,12 +213,12 @@ __global__ void k_clear_skips(uint32_t *__restrict__ bits, uint32_t *__restrict_
 // bitmap: coalesced writes in the doc pass and one dependent read per token
 // in the sampler, against one scattered write per skipped token for the
 // word-ordered bitmap.  By default it does once the previous iteration
-// skipped more than 15% of the tokens, about where the scattered writes
-// start to cost more than the reads.
+// skipped more than a fifth of the tokens, where the scattered writes cost
+// more than the reads.
 __device__ __forceinline__ bool doc_marks(const DevState &d, const Params &p, uint32_t t) {
   if (!p.doc_marks_ok || p.skip_marks == 1) return false;
   if (p.skip_marks == 2) return true;
-  return t > 0u && 100ull * d.skip_hist[(t + 1u) & 1u] > 15ull * uint64_t(p.n);
+  return t > 0u && 5ull * d.skip_hist[(t + 1u) & 1u] > uint64_t(p.n);
 }
 
 __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, double *__restrict__ bden, int32_t K,

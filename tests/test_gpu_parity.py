@@ -101,8 +101,8 @@ def test_schedule_invariance(c1, opts):
 
 def test_skip_bitmaps_leave_the_draws_unchanged():
     """Skip decisions carried by the word-ordered bitmap, the document-ordered
-    bitmap, or the per-iteration choice between them (which switches once
-    15% of the tokens skip) give the same draws, over iterations whose skip
+    bitmap, or the per-iteration choice between them (which switches once a
+    fifth of the tokens skip) give the same draws, over iterations whose skip
     rate climbs past that threshold; shuffled input has no document-ordered
     bitmap and falls back to the word-ordered one."""
     c = lda_synth.make_corpus("c3", n_docs=12000)
