@@ -12,6 +12,8 @@ with everything else at its default:
   all_dense      every W row dense
   all_sparse     every W row sparse (except words above 65,535 tokens)
   no_split       large words are not split: one region per word (Sec. 5.1)
+  word_marks     skip decisions always in the word-ordered bitmap
+  doc_marks      skip decisions always in the document-ordered bitmap
 
 Only two_branch changes the draws (another canonical order of the same
 distribution); the rest draw exactly the same topics.
@@ -33,6 +35,8 @@ CONFIGS = {
     "all_dense": dict(dense_cutoff=-1),
     "all_sparse": dict(dense_cutoff=(1 << 31) - 1),
     "no_split": dict(region_tokens=(1 << 31) - 1),
+    "word_marks": dict(skip_marks=1),
+    "doc_marks": dict(skip_marks=2),
 }
 
 
