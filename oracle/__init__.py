@@ -13,12 +13,20 @@ Every function follows the paper's definitions (arXiv 2007.08725):
   * ``build_counts`` -- D (CSR), W (dense), T = column sums of W, Sec. 2.2.
   * ``philox``, ``uniform``, ``init_topics`` -- Philox4x32-10 draws
                     (Salmon et al., SC'11); the paper only says u ~ U[0,1].
+  * ``Snapshot``   -- one counts snapshot drawn from in several calls: whole
+                    token ranges from several host threads (``iterate_threaded``,
+                    ``llpt_threaded``), or the words and documents of a token
+                    sample only (``iterate(..., idx=..., restricted=True)``).
+                    The C code stays single-threaded; threads only split the
+                    tokens, and each draw depends on (seed, t, i) and the
+                    snapshot alone.
 """
 from __future__ import annotations
 
 import ctypes
 import os
 import subprocess
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -62,7 +70,16 @@ def _load():
         lib.ora_draw_given_u.argtypes = [ctypes.c_int, I64, P, P, P, I32, I32, I32, D, D, I64, D, P, P]
         lib.ora_draw_given_u.restype = I32
         lib.ora_what_row.argtypes = [I64, P, P, P, I32, I32, I32, D, I32, P]
+        lib.ora_snapshot_new.argtypes = [I64, P, P, P, I32, I32, I32, D, D, ctypes.c_int, I64, P,
+                                         ctypes.POINTER(P)]
+        lib.ora_snapshot_draw.argtypes = [P, ctypes.c_int, ctypes.c_int, U64, U32, I64, I64, P, P, P, P, P]
+        lib.ora_snapshot_llpt.argtypes = [P, I64, I64, ctypes.POINTER(D), ctypes.POINTER(D)]
+        lib.ora_snapshot_free.argtypes = [P]
+        lib.ora_snapshot_free.restype = None
+        lib.ora_init_range.argtypes = [I64, I64, I32, U64, P]
+        lib.ora_init_range.restype = None
         lib.ora_word_stats.argtypes = [I64, P, P, P, I32, I32, I32, D, D, P, P, P, P, P, P]
+        lib.ora_word_top4.argtypes = [I64, P, P, P, I32, I32, I32, D, D, P, P]
         _lib = lib
     return _lib
 
@@ -89,9 +106,26 @@ def uniform(seed: int, t: int, i: int) -> float:
     return float(_load().ora_uniform(seed, t, i))
 
 
-def init_topics(n: int, K: int, seed: int) -> np.ndarray:
+def _ranges(n: int, parts: int):
+    parts = max(1, min(parts, n))
+    cuts = [n * q // parts for q in range(parts + 1)]
+    return [(cuts[q], cuts[q + 1] - cuts[q]) for q in range(parts) if cuts[q + 1] > cuts[q]]
+
+
+def default_threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def init_topics(n: int, K: int, seed: int, threads: int = 1) -> np.ndarray:
+    """Initial topic of every token; ``threads`` host threads split the range."""
     z = np.empty(n, dtype=np.int32)
-    _load().ora_init(n, K, seed, _p(z))
+    lib = _load()
+    if threads <= 1 or n < 1 << 20:
+        lib.ora_init(n, K, seed, _p(z))
+        return z
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(lambda r: lib.ora_init_range(r[0], r[1], K, seed, ctypes.c_void_p(z.ctypes.data + 4 * r[0])),
+                    _ranges(n, 4 * threads)))
     return z
 
 
@@ -118,13 +152,22 @@ def _mode(mode: str, branches: int) -> int:
 
 
 def iterate(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float, seed: int, t: int,
-            mode: str = "sparse", g: int = 2, idx=None, want_Z: bool = False, branches: int = 3):
+            mode: str = "sparse", g: int = 2, idx=None, want_Z: bool = False, branches: int = 3,
+            restricted: bool = False):
     """One synchronous iteration from the snapshot built from ``z``.
 
     Returns ``(z_new, flags, stats[, Z])``; with ``idx`` only those tokens are
     drawn and the outputs are aligned with ``idx``.  flags bit0 = draw within
-    1e-9*Z of a CDF edge, bit1 = step-3 skip test fired.
+    1e-9*Z of a CDF edge, bit1 = step-3 skip test fired.  ``restricted`` (with
+    ``idx``) builds only the W and D rows those tokens read: one pass over the
+    corpus instead of every row and every word's top topics.
     """
+    if restricted:
+        if idx is None:
+            raise ValueError("restricted needs idx")
+        with Snapshot(word, doc, z, M=M, V=V, K=K, alpha=alpha, beta=beta, idx=idx,
+                      with_words=(mode == "sparse")) as s:
+            return s.draw(seed, t, idx=idx, mode=mode, g=g, want_Z=want_Z, branches=branches)
     lib = _load()
     word, doc, z = _i32(word), _i32(doc), _i32(z)
     n = word.shape[0]
@@ -162,6 +205,12 @@ def word_stats(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: floa
                             _p(out["K2"]), _p(out["a1"]), _p(out["a2"]), _p(out["a3"]), _p(out["Qp"]))
     if rc:
         raise ValueError("ora_word_stats failed (%d)" % rc)
+    out["K3"] = np.empty(V, np.int32)
+    out["a4"] = np.empty(V)
+    rc = lib.ora_word_top4(word.shape[0], _p(word), _p(doc), _p(z), M, V, K, alpha, beta, _p(out["K3"]),
+                           _p(out["a4"]))
+    if rc:
+        raise ValueError("ora_word_top4 failed (%d)" % rc)
     return out
 
 
@@ -196,3 +245,120 @@ def what_row(word, doc, z, v: int, *, M: int, V: int, K: int, beta: float) -> np
     if _load().ora_what_row(word.shape[0], _p(word), _p(doc), _p(z), M, V, K, beta, v, _p(out)):
         raise ValueError("ora_what_row failed")
     return out
+
+
+class Snapshot:
+    """Counts built once from ``z`` (all rows, or with ``idx`` only the rows of
+    those tokens' words and documents), drawn from by several calls."""
+
+    def __init__(self, word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float, idx=None,
+                 with_words: bool = True):
+        self._lib = _load()
+        self.word, self.doc = _i32(word), _i32(doc)  # borrowed by the C snapshot: kept alive here
+        self.n = int(self.word.shape[0])
+        z = _i32(z)
+        self._idx = None if idx is None else np.ascontiguousarray(idx, dtype=np.int64)
+        self._h = ctypes.c_void_p()
+        rc = self._lib.ora_snapshot_new(self.n, _p(self.word), _p(self.doc), _p(z), M, V, K, alpha, beta,
+                                        1 if with_words else 0, 0 if self._idx is None else self._idx.shape[0],
+                                        _p(self._idx), ctypes.byref(self._h))
+        if rc:
+            raise ValueError("ora_snapshot_new failed (%d)" % rc)
+
+    def close(self):
+        if self._h.value:
+            self._lib.ora_snapshot_free(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _draw_into(self, seed, t, first, cnt, idx_ptr, mode, g, branches, z_out, flags, Z, st, off):
+        rc = self._lib.ora_snapshot_draw(self._h, _mode(mode, branches), g, seed, t, first, cnt, idx_ptr,
+                                         ctypes.c_void_p(z_out.ctypes.data + 4 * off),
+                                         ctypes.c_void_p(flags.ctypes.data + off),
+                                         None if Z is None else ctypes.c_void_p(Z.ctypes.data + 8 * off), _p(st))
+        if rc:
+            raise ValueError("ora_snapshot_draw failed (%d)" % rc)
+
+    def draw(self, seed: int, t: int, *, idx=None, mode: str = "sparse", g: int = 2, want_Z: bool = False,
+             branches: int = 3, threads: int = 1):
+        """Draw the tokens ``idx`` (default: every token), as ``iterate`` returns them."""
+        if idx is not None:
+            idx = np.ascontiguousarray(idx, dtype=np.int64)
+        m = self.n if idx is None else int(idx.shape[0])
+        z_out = np.empty(m, np.int32)
+        flags = np.empty(m, np.uint8)
+        Z = np.empty(m, np.float64) if want_Z else None
+        parts = _ranges(m, 8 * threads) if m else []
+        stats = np.zeros((max(len(parts), 1), 8), np.int64)
+
+        def run(q):
+            off, cnt = parts[q]
+            if idx is None:
+                self._draw_into(seed, t, off, cnt, None, mode, g, branches, z_out, flags, Z, stats[q], off)
+            else:
+                self._draw_into(seed, t, 0, cnt, ctypes.c_void_p(idx.ctypes.data + 8 * off), mode, g, branches,
+                                z_out, flags, Z, stats[q], off)
+
+        if threads <= 1:
+            for q in range(len(parts)):
+                run(q)
+        else:
+            with ThreadPoolExecutor(threads) as ex:
+                list(ex.map(run, range(len(parts))))
+        tot = stats.sum(axis=0)
+        st = {name: int(tot[j]) for j, name in enumerate(STAT_NAMES)}
+        if want_Z:
+            return z_out, flags, st, Z
+        return z_out, flags, st
+
+    def llpt(self, threads: int = 1) -> float:
+        """LLPT (sparse form) of the snapshot; partial compensated sums per token range, added in range order."""
+        parts = _ranges(self.n, 8 * threads)
+        out = [None] * len(parts)
+
+        def run(q):
+            s, c = ctypes.c_double(), ctypes.c_double()
+            if self._lib.ora_snapshot_llpt(self._h, parts[q][0], parts[q][1], ctypes.byref(s), ctypes.byref(c)):
+                raise ValueError("ora_snapshot_llpt failed")
+            out[q] = (s.value, c.value)
+
+        if threads <= 1:
+            for q in range(len(parts)):
+                run(q)
+        else:
+            with ThreadPoolExecutor(threads) as ex:
+                list(ex.map(run, range(len(parts))))
+        total, comp = 0.0, 0.0
+        for s, c in out:
+            comp += c
+            t = total + s
+            comp += ((total - t) + s) if abs(total) >= abs(s) else ((s - t) + total)
+            total = t
+        return (total + comp) / self.n
+
+
+def iterate_threaded(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float, seed: int, t: int,
+                     threads: int | None = None, mode: str = "sparse", g: int = 2):
+    """``iterate`` over every token, the tokens split over host threads (same result)."""
+    threads = threads or default_threads()
+    with Snapshot(word, doc, z, M=M, V=V, K=K, alpha=alpha, beta=beta, with_words=(mode == "sparse")) as s:
+        return s.draw(seed, t, mode=mode, g=g, threads=threads)
+
+
+def llpt_threaded(word, doc, z, *, M: int, V: int, K: int, alpha: float, beta: float,
+                  threads: int | None = None) -> float:
+    """``llpt`` (sparse form) with the tokens split over host threads (equal up to summation rounding)."""
+    threads = threads or default_threads()
+    with Snapshot(word, doc, z, M=M, V=V, K=K, alpha=alpha, beta=beta) as s:
+        return s.llpt(threads=threads)

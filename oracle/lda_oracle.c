@@ -132,22 +132,34 @@ int ora_build_counts(int64_t n, const int32_t *word, const int32_t *doc, const i
 
 /* ------------------------------------------------------- snapshot ctx ---- */
 
-typedef struct {
+typedef struct ora_snapshot {
   int64_t n;
   const int32_t *word, *doc;
   int32_t M, V, K;
   double alpha, beta;
-  /* counts snapshot */
+  /* Rows held: a full snapshot holds every word (row v) and document (row d);
+   * a restricted one only those of a token sample, at rows wslot[v] and
+   * dslot[d] (-1 = not held).  The counts of the rows it holds are the same. */
+  int32_t *wslot, *dslot;
+  int32_t nW, nD;
+  /* counts snapshot, by row */
   int64_t *len, *doff;
   int32_t *dtop, *dcnt, *W;
   int64_t *T;
   double *den; /* den[k] = T[k] + V*beta */
-  /* per-word quantities (sparse form) */
+  /* per-word quantities (sparse form), by row */
   int32_t *K1, *K2, *K3;
   double *a1, *a2, *a3, *a4, *Qp, *Qall, *sumWh;
 } snap;
 
+/* Row of word v and of document d in the snapshot (v and d themselves in a
+ * full snapshot). */
+static inline int64_t wrow(const snap *s, int32_t v) { return s->wslot ? (int64_t)s->wslot[v] : (int64_t)v; }
+static inline int64_t drow(const snap *s, int32_t d) { return s->dslot ? (int64_t)s->dslot[d] : (int64_t)d; }
+
 static void snap_free(snap *s) {
+  free(s->wslot);
+  free(s->dslot);
   free(s->len);
   free(s->doff);
   free(s->dtop);
@@ -168,13 +180,14 @@ static void snap_free(snap *s) {
   memset(s, 0, sizeof(*s));
 }
 
-/* W^[v][k], Eq. 1-2: an IEEE fp64 divide (the argmax below depends on it). */
-static inline double what(const snap *s, int32_t v, int32_t k) {
-  return ((double)s->W[(size_t)v * (size_t)s->K + (size_t)k] + s->beta) / s->den[k];
+/* W^[v][k], Eq. 1-2, for the word held at row wr: an IEEE fp64 divide (the
+ * argmax below depends on it). */
+static inline double what(const snap *s, int64_t wr, int32_t k) {
+  return ((double)s->W[(size_t)wr * (size_t)s->K + (size_t)k] + s->beta) / s->den[k];
 }
 
-static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M,
-                      int32_t V, int32_t K, double alpha, double beta, int with_words) {
+static void snap_init(snap *s, int64_t n, const int32_t *word, const int32_t *doc, int32_t M, int32_t V,
+                      int32_t K, double alpha, double beta) {
   memset(s, 0, sizeof(*s));
   s->n = n;
   s->word = word;
@@ -184,41 +197,119 @@ static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *do
   s->K = K;
   s->alpha = alpha;
   s->beta = beta;
+}
+
+/* Counts of every word and document. */
+static int snap_counts_full(snap *s, const int32_t *z) {
+  const int64_t n = s->n;
+  const int32_t M = s->M, V = s->V, K = s->K;
   size_t nn = (size_t)(n > 0 ? n : 1);
+  s->nW = V;
+  s->nD = M;
   s->len = malloc(sizeof(int64_t) * (size_t)(M > 0 ? M : 1));
   s->doff = malloc(sizeof(int64_t) * ((size_t)M + 1));
   s->dtop = malloc(sizeof(int32_t) * nn);
   s->dcnt = malloc(sizeof(int32_t) * nn);
   s->W = malloc(sizeof(int32_t) * (size_t)V * (size_t)K);
   s->T = malloc(sizeof(int64_t) * (size_t)K);
-  s->den = malloc(sizeof(double) * (size_t)K);
-  if (!s->len || !s->doff || !s->dtop || !s->dcnt || !s->W || !s->T || !s->den) {
-    snap_free(s);
+  if (!s->len || !s->doff || !s->dtop || !s->dcnt || !s->W || !s->T) return 2;
+  return ora_build_counts(n, s->word, s->doc, z, M, V, K, s->len, s->doff, s->dtop, s->dcnt, s->W, s->T);
+}
+
+/* Counts of the words and documents of tokens idx[0..n_idx) only: T over
+ * every token, W rows of those words, D rows of those documents (the same
+ * definitions as ora_build_counts, restricted to the rows a sample of draws
+ * reads). */
+static int snap_counts_sub(snap *s, const int32_t *z, int64_t n_idx, const int64_t *idx) {
+  const int64_t n = s->n;
+  const int32_t M = s->M, V = s->V, K = s->K;
+  const int32_t *word = s->word, *doc = s->doc;
+  s->wslot = malloc(sizeof(int32_t) * (size_t)V);
+  s->dslot = malloc(sizeof(int32_t) * (size_t)(M > 0 ? M : 1));
+  if (!s->wslot || !s->dslot) return 2;
+  for (int32_t v = 0; v < V; v++) s->wslot[v] = -1;
+  for (int32_t d = 0; d < M; d++) s->dslot[d] = -1;
+  for (int64_t j = 0; j < n_idx; j++) {
+    const int64_t i = idx[j];
+    if (i < 0 || i >= n || word[i] < 0 || word[i] >= V || doc[i] < 0 || doc[i] >= M) return 1;
+    if (s->wslot[word[i]] < 0) s->wslot[word[i]] = s->nW++;
+    if (s->dslot[doc[i]] < 0) s->dslot[doc[i]] = s->nD++;
+  }
+  s->W = calloc((size_t)(s->nW > 0 ? s->nW : 1) * (size_t)K, sizeof(int32_t));
+  s->T = calloc((size_t)K, sizeof(int64_t));
+  s->len = calloc((size_t)(s->nD > 0 ? s->nD : 1), sizeof(int64_t));
+  s->doff = malloc(sizeof(int64_t) * ((size_t)s->nD + 1));
+  if (!s->W || !s->T || !s->len || !s->doff) return 2;
+  /* pass 1: T, the held W rows and the held documents' lengths */
+  for (int64_t i = 0; i < n; i++) {
+    if (word[i] < 0 || word[i] >= V || doc[i] < 0 || doc[i] >= M || z[i] < 0 || z[i] >= K) return 1;
+    s->T[z[i]]++;
+    const int32_t wr = s->wslot[word[i]], dr = s->dslot[doc[i]];
+    if (wr >= 0) s->W[(size_t)wr * (size_t)K + (size_t)z[i]]++;
+    if (dr >= 0) s->len[dr]++;
+  }
+  /* pass 2: the held documents' topics, then each row sorted and run-length encoded */
+  int64_t *pos = malloc(sizeof(int64_t) * ((size_t)s->nD + 1));
+  if (!pos) return 2;
+  pos[0] = 0;
+  for (int32_t r = 0; r < s->nD; r++) pos[r + 1] = pos[r] + s->len[r];
+  const int64_t tot = pos[s->nD];
+  int32_t *zt = malloc(sizeof(int32_t) * (size_t)(tot > 0 ? tot : 1));
+  s->dtop = malloc(sizeof(int32_t) * (size_t)(tot > 0 ? tot : 1));
+  s->dcnt = malloc(sizeof(int32_t) * (size_t)(tot > 0 ? tot : 1));
+  if (!zt || !s->dtop || !s->dcnt) {
+    free(pos);
+    free(zt);
     return 2;
   }
-  int rc = ora_build_counts(n, word, doc, z, M, V, K, s->len, s->doff, s->dtop, s->dcnt, s->W, s->T);
-  if (rc) {
-    snap_free(s);
-    return rc;
+  for (int64_t i = 0; i < n; i++) {
+    const int32_t dr = s->dslot[doc[i]];
+    if (dr >= 0) zt[pos[dr]++] = z[i];
   }
-  const double Vbeta = (double)V * beta;
+  int64_t nnz = 0, b = 0;
+  for (int32_t r = 0; r < s->nD; r++) {
+    const int64_t e = b + s->len[r];
+    qsort(zt + b, (size_t)(e - b), sizeof(int32_t), cmp_i32);
+    s->doff[r] = nnz;
+    for (int64_t j = b; j < e; j++) {
+      if (j == b || zt[j] != zt[j - 1]) {
+        s->dtop[nnz] = zt[j];
+        s->dcnt[nnz] = 0;
+        nnz++;
+      }
+      s->dcnt[nnz - 1]++;
+    }
+    b = e;
+  }
+  s->doff[s->nD] = nnz;
+  free(pos);
+  free(zt);
+  return 0;
+}
+
+/* den[k] and, with with_words, the per-word quantities of every held word. */
+static int snap_finish(snap *s, int with_words) {
+  const int32_t K = s->K;
+  const double alpha = s->alpha;
+  s->den = malloc(sizeof(double) * (size_t)K);
+  if (!s->den) return 2;
+  const double Vbeta = (double)s->V * s->beta;
   for (int32_t k = 0; k < K; k++) s->den[k] = (double)s->T[k] + Vbeta;
   if (!with_words) return 0;
-  s->K1 = malloc(sizeof(int32_t) * (size_t)V);
-  s->K2 = malloc(sizeof(int32_t) * (size_t)V);
-  s->K3 = malloc(sizeof(int32_t) * (size_t)V);
-  s->a1 = malloc(sizeof(double) * (size_t)V);
-  s->a2 = malloc(sizeof(double) * (size_t)V);
-  s->a3 = malloc(sizeof(double) * (size_t)V);
-  s->a4 = malloc(sizeof(double) * (size_t)V);
-  s->Qp = malloc(sizeof(double) * (size_t)V);
-  s->Qall = malloc(sizeof(double) * (size_t)V);
-  s->sumWh = malloc(sizeof(double) * (size_t)V);
-  if (!s->K1 || !s->K2 || !s->K3 || !s->a1 || !s->a2 || !s->a3 || !s->a4 || !s->Qp || !s->Qall || !s->sumWh) {
-    snap_free(s);
+  const size_t nw = (size_t)(s->nW > 0 ? s->nW : 1);
+  s->K1 = malloc(sizeof(int32_t) * nw);
+  s->K2 = malloc(sizeof(int32_t) * nw);
+  s->K3 = malloc(sizeof(int32_t) * nw);
+  s->a1 = malloc(sizeof(double) * nw);
+  s->a2 = malloc(sizeof(double) * nw);
+  s->a3 = malloc(sizeof(double) * nw);
+  s->a4 = malloc(sizeof(double) * nw);
+  s->Qp = malloc(sizeof(double) * nw);
+  s->Qall = malloc(sizeof(double) * nw);
+  s->sumWh = malloc(sizeof(double) * nw);
+  if (!s->K1 || !s->K2 || !s->K3 || !s->a1 || !s->a2 || !s->a3 || !s->a4 || !s->Qp || !s->Qall || !s->sumWh)
     return 2;
-  }
-  for (int32_t v = 0; v < V; v++) {
+  for (int32_t v = 0; v < s->nW; v++) {
     /* step 1 of the three-branch procedure: top topics of W^[v] (Sec. 3.2).
      * K1 = lowest topic id among the maxima; K2 = lowest id among the maxima
      * over k != K1; K3 = lowest id among the maxima over k not in {K1, K2}
@@ -287,9 +378,18 @@ static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *do
   return 0;
 }
 
-/* Count of topic k in document d (0 if absent). */
-static int32_t dcount(const snap *s, int32_t d, int32_t k) {
-  for (int64_t e = s->doff[d]; e < s->doff[d + 1]; e++)
+static int snap_build(snap *s, int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M,
+                      int32_t V, int32_t K, double alpha, double beta, int with_words) {
+  snap_init(s, n, word, doc, M, V, K, alpha, beta);
+  int rc = snap_counts_full(s, z);
+  if (!rc) rc = snap_finish(s, with_words);
+  if (rc) snap_free(s);
+  return rc;
+}
+
+/* Count of topic k in the document held at row dr (0 if absent). */
+static int32_t dcount(const snap *s, int64_t dr, int32_t k) {
+  for (int64_t e = s->doff[dr]; e < s->doff[dr + 1]; e++)
     if (s->dtop[e] == k) return s->dcnt[e];
   return 0;
 }
@@ -308,7 +408,8 @@ static double s_est(int g, double a2, double a3, double a4, int32_t C1, int32_t 
 /* ------------------------------------------------------- sparse draw ---- */
 
 static int32_t draw_sparse(const snap *s, int g, double u, int64_t i, double *Zo, uint8_t *flag, int64_t *st) {
-  const int32_t v = s->word[i], d = s->doc[i], K = s->K;
+  const int64_t v = wrow(s, s->word[i]), d = drow(s, s->doc[i]);
+  const int32_t K = s->K;
   const double alpha = s->alpha;
   const int32_t K1 = s->K1[v];
   const double a1 = s->a1[v];
@@ -400,7 +501,8 @@ static int32_t draw_sparse(const snap *s, int g, double u, int64_t i, double *Zo
 
 static int32_t draw_dense(const snap *s, int g, double u, int64_t i, double *wh, int32_t *Dd, double *Zo,
                           uint8_t *flag, int64_t *st) {
-  const int32_t v = s->word[i], d = s->doc[i], K = s->K;
+  const int64_t v = wrow(s, s->word[i]), d = drow(s, s->doc[i]);
+  const int32_t K = s->K;
   const double alpha = s->alpha;
   for (int32_t k = 0; k < K; k++) {
     Dd[k] = 0;
@@ -515,7 +617,8 @@ static uint8_t boundary_flag(double x, double lo, double hi, double Z) {
 }
 
 static int32_t draw2_sparse(const snap *s, double u, int64_t i, double *Zo, uint8_t *flag, int64_t *st) {
-  const int32_t v = s->word[i], d = s->doc[i], K = s->K;
+  const int64_t v = wrow(s, s->word[i]), d = drow(s, s->doc[i]);
+  const int32_t K = s->K;
   const double alpha = s->alpha;
   const int64_t b = s->doff[d], e = s->doff[d + 1];
   double S = 0.0;
@@ -562,7 +665,8 @@ static int32_t draw2_sparse(const snap *s, double u, int64_t i, double *Zo, uint
 
 static int32_t draw2_dense(const snap *s, double u, int64_t i, double *wh, int32_t *Dd, double *Zo, uint8_t *flag,
                            int64_t *st) {
-  const int32_t v = s->word[i], d = s->doc[i], K = s->K;
+  const int64_t v = wrow(s, s->word[i]), d = drow(s, s->doc[i]);
+  const int32_t K = s->K;
   const double alpha = s->alpha;
   for (int32_t k = 0; k < K; k++) {
     Dd[k] = 0;
@@ -613,16 +717,14 @@ static int32_t draw2_dense(const snap *s, double u, int64_t i, double *wh, int32
 
 /* ---------------------------------------------------------- iterate ---- */
 
-int ora_iterate(int mode, int g, int64_t n, const int32_t *word, const int32_t *doc, int32_t M, int32_t V, int32_t K,
-                double alpha, double beta, uint64_t seed, uint32_t t, const int32_t *z_in, int64_t n_sub,
-                const int64_t *idx, int32_t *z_out, uint8_t *flags, double *Zout, int64_t *stats) {
-  if (mode < 0 || mode > 3 || g < 1 || g > 3 || K < 2 || !(alpha > 0) || !(beta > 0)) return 1;
+/* Draws tokens idx[0..cnt) (or first..first+cnt-1 when idx is NULL) from
+ * the snapshot; outputs at [0, cnt).  Statistics are added to st. */
+static int draw_tokens(const snap *s, int mode, int g, uint64_t seed, uint32_t t, int64_t first, int64_t cnt,
+                       const int64_t *idx, int32_t *z_out, uint8_t *flags, double *Zout, int64_t *st) {
+  if (mode < 0 || mode > 3 || g < 1 || g > 3) return 1;
   const int dense = mode & 1, two = mode & 2;
-  snap s;
-  int rc = snap_build(&s, n, word, doc, z_in, M, V, K, alpha, beta, !dense);
-  if (rc) return rc;
-  int64_t st[ORA_N_STATS];
-  memset(st, 0, sizeof(st));
+  if (!dense && !s->K1) return 1; /* the sparse form needs the per-word quantities */
+  const int32_t K = s->K;
   double *wh = NULL;
   int32_t *Dd = NULL;
   if (dense) {
@@ -631,14 +733,13 @@ int ora_iterate(int mode, int g, int64_t n, const int32_t *word, const int32_t *
     if (!wh || !Dd) {
       free(wh);
       free(Dd);
-      snap_free(&s);
       return 2;
     }
   }
-  const int64_t cnt = idx ? n_sub : n;
+  int rc = 0;
   for (int64_t j = 0; j < cnt; j++) {
-    int64_t i = idx ? idx[j] : j;
-    if (i < 0 || i >= n) {
+    const int64_t i = idx ? idx[j] : first + j;
+    if (i < 0 || i >= s->n || wrow(s, s->word[i]) < 0 || drow(s, s->doc[i]) < 0) {
       rc = 1;
       break;
     }
@@ -646,15 +747,28 @@ int ora_iterate(int mode, int g, int64_t n, const int32_t *word, const int32_t *
     uint8_t f;
     const double u = ora_uniform(seed, t, (uint64_t)i);
     int32_t k;
-    if (two) k = dense ? draw2_dense(&s, u, i, wh, Dd, &Z, &f, st) : draw2_sparse(&s, u, i, &Z, &f, st);
-    else k = dense ? draw_dense(&s, g, u, i, wh, Dd, &Z, &f, st) : draw_sparse(&s, g, u, i, &Z, &f, st);
+    if (two) k = dense ? draw2_dense(s, u, i, wh, Dd, &Z, &f, st) : draw2_sparse(s, u, i, &Z, &f, st);
+    else k = dense ? draw_dense(s, g, u, i, wh, Dd, &Z, &f, st) : draw_sparse(s, g, u, i, &Z, &f, st);
     z_out[j] = k;
     if (flags) flags[j] = f;
     if (Zout) Zout[j] = Z;
   }
-  if (stats) memcpy(stats, st, sizeof(st));
   free(wh);
   free(Dd);
+  return rc;
+}
+
+int ora_iterate(int mode, int g, int64_t n, const int32_t *word, const int32_t *doc, int32_t M, int32_t V, int32_t K,
+                double alpha, double beta, uint64_t seed, uint32_t t, const int32_t *z_in, int64_t n_sub,
+                const int64_t *idx, int32_t *z_out, uint8_t *flags, double *Zout, int64_t *stats) {
+  if (mode < 0 || mode > 3 || g < 1 || g > 3 || K < 2 || !(alpha > 0) || !(beta > 0)) return 1;
+  snap s;
+  int rc = snap_build(&s, n, word, doc, z_in, M, V, K, alpha, beta, !(mode & 1));
+  if (rc) return rc;
+  int64_t st[ORA_N_STATS];
+  memset(st, 0, sizeof(st));
+  rc = draw_tokens(&s, mode, g, seed, t, 0, idx ? n_sub : n, idx, z_out, flags, Zout, st);
+  if (stats) memcpy(stats, st, sizeof(st));
   snap_free(&s);
   return rc;
 }
@@ -710,6 +824,17 @@ int ora_word_stats(int64_t n, const int32_t *word, const int32_t *doc, const int
   return 0;
 }
 
+int ora_word_top4(int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M, int32_t V,
+                  int32_t K, double alpha, double beta, int32_t *K3, double *a4) {
+  snap s;
+  int rc = snap_build(&s, n, word, doc, z, M, V, K, alpha, beta, 1);
+  if (rc) return rc;
+  memcpy(K3, s.K3, sizeof(int32_t) * (size_t)V);
+  memcpy(a4, s.a4, sizeof(double) * (size_t)V);
+  snap_free(&s);
+  return 0;
+}
+
 int32_t ora_draw_given_u(int mode, int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M,
                          int32_t V, int32_t K, double alpha, double beta, int64_t i, double u, double *Z,
                          uint8_t *flag) {
@@ -743,4 +868,65 @@ int ora_what_row(int64_t n, const int32_t *word, const int32_t *doc, const int32
   for (int32_t k = 0; k < K; k++) out[k] = what(&s, v, k);
   snap_free(&s);
   return 0;
+}
+
+/* ------------------------------------------------------ snapshot API ---- */
+
+int ora_snapshot_new(int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M, int32_t V,
+                     int32_t K, double alpha, double beta, int with_words, int64_t n_idx, const int64_t *idx,
+                     ora_snapshot **out) {
+  *out = NULL;
+  if (n < 0 || M < 0 || V <= 0 || K < 2 || !(alpha > 0) || !(beta > 0) || (idx == NULL && n_idx != 0)) return 1;
+  snap *s = malloc(sizeof(snap));
+  if (!s) return 2;
+  snap_init(s, n, word, doc, M, V, K, alpha, beta);
+  int rc = idx ? snap_counts_sub(s, z, n_idx, idx) : snap_counts_full(s, z);
+  if (!rc) rc = snap_finish(s, with_words);
+  if (rc) {
+    snap_free(s);
+    free(s);
+    return rc;
+  }
+  *out = s;
+  return 0;
+}
+
+int ora_snapshot_draw(const ora_snapshot *s, int mode, int g, uint64_t seed, uint32_t t, int64_t first, int64_t cnt,
+                      const int64_t *idx, int32_t *z_out, uint8_t *flags, double *Zout, int64_t *stats) {
+  if (!s || cnt < 0) return 1;
+  int64_t st[ORA_N_STATS];
+  memset(st, 0, sizeof(st));
+  const int rc = draw_tokens(s, mode, g, seed, t, first, cnt, idx, z_out, flags, Zout, st);
+  if (stats) memcpy(stats, st, sizeof(st));
+  return rc;
+}
+
+int ora_snapshot_llpt(const ora_snapshot *s, int64_t first, int64_t cnt, double *sum_out, double *comp_out) {
+  if (!s || !s->sumWh || s->wslot || first < 0 || cnt < 0 || first + cnt > s->n) return 1;
+  const double Kalpha = (double)s->K * s->alpha;
+  double sum = 0.0, comp = 0.0;
+  for (int64_t i = first; i < first + cnt; i++) {
+    const int32_t v = s->word[i], d = s->doc[i];
+    double num = 0.0;
+    for (int64_t j = s->doff[d]; j < s->doff[d + 1]; j++) num += (double)s->dcnt[j] * what(s, v, s->dtop[j]);
+    num += s->alpha * s->sumWh[v];
+    const double term = log2(num / ((double)s->len[d] + Kalpha));
+    const double tsum = sum + term;
+    if (fabs(sum) >= fabs(term)) comp += (sum - tsum) + term;
+    else comp += (term - tsum) + sum;
+    sum = tsum;
+  }
+  *sum_out = sum;
+  *comp_out = comp;
+  return 0;
+}
+
+void ora_snapshot_free(ora_snapshot *s) {
+  if (!s) return;
+  snap_free(s);
+  free(s);
+}
+
+void ora_init_range(int64_t first, int64_t cnt, int32_t K, uint64_t seed, int32_t *z) {
+  for (int64_t j = 0; j < cnt; j++) z[j] = ora_init_topic(seed, (uint64_t)(first + j), K);
 }

@@ -80,6 +80,12 @@ int ora_word_stats(int64_t n, const int32_t *word, const int32_t *doc, const int
                    int32_t K, double alpha, double beta, int32_t *K1, int32_t *K2, double *a1, double *a2, double *a3,
                    double *Qp);
 
+/* The third top topic K3 (lowest id among the maxima over k not in {K1, K2};
+ * -1 if K < 3) and the fourth top value a4 of W^[v] (0 if K < 4): what the
+ * S_est of Eq. 9 uses at depth g = 3. */
+int ora_word_top4(int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M, int32_t V,
+                  int32_t K, double alpha, double beta, int32_t *K3, double *a4);
+
 /* Draw token i of the snapshot built from z with a given u in [0,1) (test
  * hook for worked examples and exact enumeration).  Returns the topic, or -1
  * on a bad argument; Z and flag as in ora_iterate. */
@@ -90,6 +96,36 @@ int32_t ora_draw_given_u(int mode, int64_t n, const int32_t *word, const int32_t
 /* The normalised word row W^[v][k] = (W[v][k]+beta)/(T[k]+V*beta), Eq. 2. */
 int ora_what_row(int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M, int32_t V, int32_t K,
                  double beta, int32_t v, double *out);
+
+/* A counts snapshot kept across calls, so that a caller can draw disjoint
+ * token ranges of one iteration from several threads (the draws depend only
+ * on (seed, t, i) and the snapshot, so the result does not depend on how the
+ * tokens are split).  The code itself is single-threaded and the snapshot is
+ * read-only after ora_snapshot_new.
+ *   idx == NULL: counts of every word and document (as ora_iterate builds).
+ *   idx != NULL: T over every token, but W and D rows only for the words and
+ *                documents of tokens idx[0..n_idx): enough to draw exactly
+ *                those tokens, in one pass over the corpus.
+ *   with_words:  also the per-word quantities (needed by the sparse form and
+ *                the LLPT).
+ * The word/doc arrays are borrowed and must outlive the snapshot; z is read
+ * only during ora_snapshot_new.  Returns 0, 1 (bad argument) or 2 (no memory). */
+typedef struct ora_snapshot ora_snapshot;
+int ora_snapshot_new(int64_t n, const int32_t *word, const int32_t *doc, const int32_t *z, int32_t M, int32_t V,
+                     int32_t K, double alpha, double beta, int with_words, int64_t n_idx, const int64_t *idx,
+                     ora_snapshot **out);
+/* Draw tokens idx[0..cnt) (idx NULL: tokens first..first+cnt-1) as
+ * ora_iterate does; outputs and stats as there, outputs at [0, cnt).
+ * Returns 1 for a token the snapshot does not hold. */
+int ora_snapshot_draw(const ora_snapshot *s, int mode, int g, uint64_t seed, uint32_t t, int64_t first, int64_t cnt,
+                      const int64_t *idx, int32_t *z_out, uint8_t *flags, double *Zout, int64_t *stats);
+/* Neumaier-compensated sum (and its compensation) of the LLPT terms of
+ * tokens first..first+cnt-1 (sparse form, full snapshot with words). */
+int ora_snapshot_llpt(const ora_snapshot *s, int64_t first, int64_t cnt, double *sum, double *comp);
+void ora_snapshot_free(ora_snapshot *s);
+
+/* Initial topics of tokens first..first+cnt-1 into z[0..cnt). */
+void ora_init_range(int64_t first, int64_t cnt, int32_t K, uint64_t seed, int32_t *z);
 
 #ifdef __cplusplus
 }

@@ -312,6 +312,69 @@ def test_skip_bound_and_exactness_on_c1(c1):
     assert skips[-1] > skips[0]
 
 
+def test_top_values_for_depth_three_by_hand():
+    """K3 and a4 of Eq. 9 (g = 3) on a case worked by hand.  V = 2, K = 5, beta = 1/2 (so
+    V*beta = 1); word 0 holds topics {0,0,0,2,3,3}, word 1 topics {0,1,1,2}; T = (4,2,2,2,0),
+    den = T + 1 = (5,3,3,3,1).
+      W^[0] = (3.5/5, 0.5/3, 1.5/3, 2.5/3, 0.5/1) = (0.7, 1/6, 0.5, 5/6, 0.5):
+              K1 = 3, K2 = 0, K3 = 2 (0.5 at topics 2 and 4: the lower id), a3 = 0.5, a4 = 0.5;
+      W^[1] = (1.5/5, 2.5/3, 1.5/3, 0.5/3, 0.5/1) = (0.3, 5/6, 0.5, 1/6, 0.5):
+              K1 = 1, K2 = 2 (the tie again), K3 = 4, a3 = 0.5, a4 = 0.3."""
+    word = np.array([0] * 6 + [1] * 4, np.int32)
+    z = np.array([0, 0, 0, 2, 3, 3, 0, 1, 1, 2], np.int32)
+    doc = np.zeros(10, np.int32)
+    st = ora.word_stats(word, doc, z, M=1, V=2, K=5, alpha=0.3, beta=0.5)
+    assert st["K1"].tolist() == [3, 1] and st["K2"].tolist() == [0, 2] and st["K3"].tolist() == [2, 4]
+    assert st["a1"] == pytest.approx([2.5 / 3, 2.5 / 3], rel=1e-15)
+    assert st["a2"] == pytest.approx([0.7, 0.5], rel=1e-15)
+    assert st["a3"] == pytest.approx([0.5, 0.5], rel=1e-15)
+    assert st["a4"] == pytest.approx([0.5, 0.3], rel=1e-15)
+    # Q' = alpha * (sum of W^ over the topics other than K1)
+    assert st["Qp"] == pytest.approx([0.3 * (0.7 + 0.5 / 3 + 0.5 + 0.5), 0.3 * (0.3 + 0.5 + 0.5 / 3 + 0.5)],
+                                     rel=1e-14)
+
+
+# ------------------------------------------------- snapshots for large corpora
+
+def test_restricted_snapshot_draws_equal_the_full_snapshot():
+    """Counts built only for the words and documents of a token sample give the sample's draws,
+    normalisers, flags and statistics bit for bit as the full snapshot does, in every form."""
+    rng = np.random.default_rng(21)
+    for trial in range(12):
+        word, doc, M, V, K = _random_corpus(rng, max_m=40, max_v=50, kmax=12, max_n=600)
+        z = rng.integers(0, K, len(word)).astype(np.int32)
+        idx = np.sort(rng.choice(len(word), max(1, len(word) // 5), replace=False))
+        kw = dict(M=M, V=V, K=K, alpha=0.3, beta=0.02, seed=7, t=trial, idx=idx, want_Z=True)
+        for mode in ("sparse", "dense"):
+            for branches, g in ((3, 1), (3, 2), (3, 3), (2, 2)):
+                full = ora.iterate(word, doc, z, mode=mode, branches=branches, g=g, **kw)
+                sub = ora.iterate(word, doc, z, mode=mode, branches=branches, g=g, restricted=True, **kw)
+                for a, b in zip(full, sub):
+                    if isinstance(a, dict):
+                        assert a == b
+                    else:
+                        assert np.array_equal(a, b)
+
+
+def test_threaded_draws_equal_single_thread(c1):
+    """Token ranges drawn from one snapshot by several host threads reproduce the single-threaded
+    iteration exactly (each draw depends on (seed, t, i) and the snapshot only); the threaded
+    LLPT differs from the sequential one by summation rounding only; threaded initial topics are
+    the same topics."""
+    kw = dict(M=c1.n_docs, V=c1.V, K=c1.K, alpha=c1.alpha, beta=c1.beta)
+    z = ora.init_topics(c1.N, c1.K, 42)
+    assert np.array_equal(z, ora.init_topics(c1.N, c1.K, 42, threads=4))
+    big = ora.init_topics(3 << 20, 1000, 42)
+    assert np.array_equal(big, ora.init_topics(3 << 20, 1000, 42, threads=5))
+    for t in range(2):
+        a = ora.iterate(c1.word, c1.doc, z, seed=42, t=t, **kw)
+        b = ora.iterate_threaded(c1.word, c1.doc, z, seed=42, t=t, threads=3, **kw)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2]
+        z = a[0]
+    assert ora.llpt_threaded(c1.word, c1.doc, z, threads=3, **kw) == pytest.approx(
+        ora.llpt(c1.word, c1.doc, z, **kw), rel=1e-14)
+
+
 # ---------------------------------------------------------------------- LLPT
 
 def test_llpt_closed_form_limits():
