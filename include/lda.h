@@ -174,6 +174,26 @@ lda_status lda_loglik(lda_handle *h, double *llpt);
  */
 lda_status lda_set_assignments(lda_handle *h, const int32_t *z, int64_t iteration);
 
+/*
+ * lda_loglik for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * computation and the same result, bit for bit, as lda_loglik; its scratch
+ * (the per-region partial sums, the scheduler counter and the result) lives in
+ * a fixed device array of the library instead of handle memory, so the call
+ * itself allocates nothing (no hipMalloc, hipFree or allocating library
+ * routine).  The array holds 512 B plus 8 B per region, up to
+ * LDA_NOALLOC_MAX_REGIONS regions (16 MiB); each device the library runs on
+ * keeps its own copy until the process ends.
+ *   llpt: host pointer to one double (output).
+ * Errors: LDA_E_ARG (llpt NULL), LDA_E_RANGE (the handle's layout has more
+ * than LDA_NOALLOC_MAX_REGIONS regions), LDA_E_DEVICE, LDA_E_STATE.
+ * Every call on one device shares that device's array, whichever handle makes
+ * it: calls that overlap in time on one GPU (other host threads, other
+ * streams) race and must be serialised by the caller.
+ */
+#define LDA_NOALLOC_MAX_REGIONS (1 << 21)
+lda_status lda_loglik_noalloc(lda_handle *h, double *llpt);
+
 /* Release every resource of the handle.  NULL is allowed. */
 void lda_destroy(lda_handle *h);
 

@@ -55,7 +55,8 @@ class Counts(ctypes.Structure):
 
 # Every symbol include/lda.h declares.
 EXPORTS = ("lda_create", "lda_iterate", "lda_get_counts", "lda_loglik", "lda_set_assignments", "lda_destroy",
-           "lda_last_error", "lda_describe_layout")
+           "lda_last_error", "lda_describe_layout", "lda_loglik_noalloc")
+NOALLOC_MAX_REGIONS = 1 << 21
 
 
 class LDAError(RuntimeError):
@@ -85,6 +86,8 @@ def load_library():
     lib.lda_get_counts.restype = ctypes.c_int
     lib.lda_loglik.argtypes = [P, ctypes.POINTER(D)]
     lib.lda_loglik.restype = ctypes.c_int
+    lib.lda_loglik_noalloc.argtypes = [P, ctypes.POINTER(D)]
+    lib.lda_loglik_noalloc.restype = ctypes.c_int
     lib.lda_set_assignments.argtypes = [P, P, I64]
     lib.lda_set_assignments.restype = ctypes.c_int
     lib.lda_destroy.argtypes = [P]
@@ -229,6 +232,12 @@ class LDA:
     def loglik(self) -> float:
         out = ctypes.c_double()
         _check(self._lib, self._h, self._lib.lda_loglik(self._h, ctypes.byref(out)))
+        return out.value
+
+    def loglik_noalloc(self) -> float:
+        """``loglik`` through the entry point that allocates nothing (fixed device scratch)."""
+        out = ctypes.c_double()
+        _check(self._lib, self._h, self._lib.lda_loglik_noalloc(self._h, ctypes.byref(out)))
         return out.value
 
     def set_assignments(self, z, iteration: int):

@@ -20,6 +20,8 @@
 // contraction so that the values match a plain sequential evaluation.
 #include "lda_internal.h"
 
+#include <mutex>
+
 namespace lda {
 namespace {
 
@@ -140,20 +142,20 @@ __device__ __forceinline__ void top_insert(TopN &t, double v, uint32_t k) {
 }
 
 // Block-wide sum of a double over 256 threads (fixed order).
-__device__ double block_sum(double v, double *scratch) {
+__device__ double block_sum(double v, double *red) {
   v = group_sum<kWave>(v);
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   __syncthreads();
-  if (lane == 0) scratch[wave] = v;
+  if (lane == 0) red[wave] = v;
   __syncthreads();
   double s = 0.0;
-  for (int q = 0; q < kBlock / kWave; ++q) s += scratch[q];
+  for (int q = 0; q < kBlock / kWave; ++q) s += red[q];
   __syncthreads();
   return s;
 }
 
 // Block-wide exclusive prefix of a uint32 over 256 threads; *total gets the sum.
-__device__ uint32_t block_exclusive_u32(uint32_t v, uint32_t *scratch, uint32_t *total) {
+__device__ uint32_t block_exclusive_u32(uint32_t v, uint32_t *red, uint32_t *total) {
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   uint32_t incl = v;
 #pragma unroll
@@ -162,12 +164,12 @@ __device__ uint32_t block_exclusive_u32(uint32_t v, uint32_t *scratch, uint32_t 
     if (lane >= o) incl += y;
   }
   __syncthreads();
-  if (lane == kWave - 1) scratch[wave] = incl;
+  if (lane == kWave - 1) red[wave] = incl;
   __syncthreads();
   uint32_t off = 0, all = 0;
   for (int q = 0; q < kBlock / kWave; ++q) {
-    if (q < wave) off += scratch[q];
-    all += scratch[q];
+    if (q < wave) off += red[q];
+    all += red[q];
   }
   *total = all;
   return off + incl - v;
@@ -301,13 +303,13 @@ __device__ void write_word_records(const DevState &d, const Params &p, int r, co
 // Large K: the sum over all topics of beta/den[k] (one workgroup, a fixed
 // order), for the sparse words' sums in k_word_pre.
 __global__ __launch_bounds__(kBlock) void k_beta_sum(DevState d, Params p) {
-  __shared__ double scratch[kBlock / kWave];
+  __shared__ double red[kBlock / kWave];
   const int K = p.K;
   const int cs = (K + kBlock - 1) / kBlock;
   const int c0 = min(K, int(threadIdx.x) * cs), c1 = min(K, c0 + cs);
   double s = 0.0;
   for (int k = c0; k < c1; ++k) s += d.bden[k];
-  s = block_sum(s, scratch);
+  s = block_sum(s, red);
   if (threadIdx.x == 0) d.beta_sum[0] = s;
 }
 
@@ -316,7 +318,7 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
   const int K = p.K;
   __shared__ double sv[kBlock * kTop];
   __shared__ uint32_t sk[kBlock * kTop];
-  __shared__ double scratch[kBlock / kWave];
+  __shared__ double red[kBlock / kWave];
   const bool dense = r < p.n_dense;
   const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
   const uint32_t *ents = nullptr;
@@ -362,8 +364,8 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
       }
       s_full = found < want;  // the list ran out: scan every topic instead
     }
-    snz = block_sum(snz, scratch);
-    sb = block_sum(sb, scratch);
+    snz = block_sum(snz, red);
+    sb = block_sum(sb, red);
     __syncthreads();
     if (!s_full) {
       WordTop top;
@@ -410,8 +412,8 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
       if (p.two_branch || uint32_t(k) != K1) q += p.alpha * w;
     }
   }
-  q = block_sum(q, scratch);
-  sw = block_sum(sw, scratch);
+  q = block_sum(q, red);
+  sw = block_sum(sw, red);
   if (tid == 0) write_word_records(d, p, r, top, q, sw);
 }
 
@@ -2127,10 +2129,10 @@ __global__ __launch_bounds__(kBlock) void k_loglik(DevState d, Params p) {
 
 __global__ __launch_bounds__(kBlock) void k_loglik_reduce(const double *__restrict__ part, int64_t n,
                                                           double *__restrict__ out) {
-  __shared__ double scratch[kBlock / kWave];
+  __shared__ double red[kBlock / kWave];
   double s = 0.0;
   for (int64_t q = threadIdx.x; q < n; q += kBlock) s += part[q];
-  s = block_sum(s, scratch);
+  s = block_sum(s, red);
   if (threadIdx.x == 0) out[0] = s;
 }
 
@@ -2308,6 +2310,50 @@ hipError_t launch_sum_nnz(const DevState &d, const Params &p, unsigned long long
   hipLaunchKernelGGL(k_sum_nnz, dim3(uint32_t(std::max<int64_t>(blocks, 1))), dim3(kBlock), 0, s, d.d_ent, d.d_cap,
                      p.M, out);
   return hipGetLastError();
+}
+
+// ------------------------------------------------- allocation-free LLPT ----
+// The scratch of lda_loglik_noalloc: the scheduler counters, the result and
+// the per-region partial sums of the LLPT kernels, in one fixed device array
+// that every handle on a device shares.  In host code the array's name is not
+// a device address: only the address hipGetSymbolAddress returns (one per
+// device) may reach a kernel or a copy.
+static __device__ __align__(256) unsigned char scratch[kNoAllocHead + sizeof(double) * size_t(LDA_NOALLOC_MAX_REGIONS)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_addr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch_address(void **out) {
+  *out = nullptr;
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void *ptr = nullptr;
+    err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (err != hipSuccess) return err;
+    g_scratch_addr[dev] = ptr;
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_loglik_noalloc(DevState d, const Params &p, void *scratch_dev, hipStream_t s) {
+  if (p.n_regions > int64_t(LDA_NOALLOC_MAX_REGIONS)) return hipErrorInvalidValue;
+  unsigned char *base = static_cast<unsigned char *>(scratch_dev);
+  d.counters = reinterpret_cast<uint32_t *>(base);                  // cleared by k_begin
+  d.ll_out = reinterpret_cast<double *>(base + kNoAllocResult);      // written by k_loglik_reduce
+  d.ll_part = reinterpret_cast<double *>(base + kNoAllocHead);       // one slot per region, each written
+  d.stats = nullptr;
+  hipError_t err = launch_begin_iteration(d, p, s);
+  if (err == hipSuccess) err = launch_word_pre(d, p, s);
+  if (err == hipSuccess) err = launch_loglik(d, p, s);
+  return err;
 }
 
 hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s) {

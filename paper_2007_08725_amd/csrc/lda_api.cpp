@@ -33,6 +33,7 @@ struct lda_handle {
   std::vector<void *> allocations;
   unsigned long long *stats_base = nullptr;  // [kStatSlots * kStatsPerIter]
   std::vector<hipEvent_t> events;            // [kStatSlots * kEventsPerIter]
+  void *noalloc_scratch = nullptr;           // this device's fixed LLPT scratch (lda_loglik_noalloc)
   int64_t iteration = 0;
   bool poisoned = false;
   std::string err = "no error";
@@ -149,6 +150,8 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
     HIP_TRY(h, hipStreamCreateWithFlags(&h->stream, hipStreamNonBlocking));
     h->own_stream = true;
   }
+  // the fixed scratch of the allocation-free LLPT, looked up once per device
+  HIP_TRY(h, noalloc_scratch_address(&h->noalloc_scratch));
   Params &p = h->p;
   p.grid_regions = std::max(1, cus * 8);
   const int want = o ? o->sampler_block : 0;
@@ -588,6 +591,23 @@ lda_status lda_loglik(lda_handle *h, double *llpt) {
   HIP_TRY(h, launch_loglik(d, h->p, h->stream));
   double sum = 0.0;
   HIP_TRY(h, hipMemcpyAsync(&sum, h->d.ll_out, sizeof(double), hipMemcpyDeviceToHost, h->stream));
+  HIP_TRY(h, hipStreamSynchronize(h->stream));
+  *llpt = sum / double(h->L.n);
+  return LDA_OK;
+}
+
+lda_status lda_loglik_noalloc(lda_handle *h, double *llpt) {
+  LDA_TRY(check_handle(h));
+  if (!llpt) return fail(h, LDA_E_ARG, "llpt is NULL");
+  if (h->p.n_regions > int64_t(LDA_NOALLOC_MAX_REGIONS))
+    return fail(h, LDA_E_RANGE, "lda_loglik_noalloc holds partial sums for at most " +
+                                    std::to_string(LDA_NOALLOC_MAX_REGIONS) + " regions; this layout has " +
+                                    std::to_string(h->p.n_regions) + " (use lda_loglik)");
+  HIP_TRY(h, launch_loglik_noalloc(h->d, h->p, h->noalloc_scratch, h->stream));
+  double sum = 0.0;
+  const double *result = reinterpret_cast<const double *>(static_cast<unsigned char *>(h->noalloc_scratch) +
+                                                          kNoAllocResult);
+  HIP_TRY(h, hipMemcpyAsync(&sum, result, sizeof(double), hipMemcpyDeviceToHost, h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   *llpt = sum / double(h->L.n);
   return LDA_OK;

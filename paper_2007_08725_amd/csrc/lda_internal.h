@@ -198,6 +198,15 @@ inline int tiled_grid(const Params &p) { return p.grid_regions / 8 > 0 ? p.grid_
 inline int loglik_grid_big_k(const Params &p) { return tiled_grid(p); }
 hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s);
+// Allocation-free LLPT: the layout of the fixed scratch array (counters at 0,
+// the result at kNoAllocResult, per-region partials from kNoAllocHead), its
+// device address on the current device (looked up once per device), and the
+// LLPT launches on it.  hipErrorInvalidValue past LDA_NOALLOC_MAX_REGIONS.
+constexpr size_t kNoAllocResult = 256;
+constexpr size_t kNoAllocHead = 512;
+static_assert(sizeof(uint32_t) * kCounters <= kNoAllocResult, "counters overlap the result");
+hipError_t noalloc_scratch_address(void **out);
+hipError_t launch_loglik_noalloc(DevState d, const Params &p, void *scratch_dev, hipStream_t s);
 hipError_t launch_sum_nnz(const DevState &d, const Params &p, unsigned long long *out, hipStream_t s);
 
 }  // namespace lda
