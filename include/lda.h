@@ -94,7 +94,14 @@ typedef struct {
    * token's key) whenever the input is sorted by document and K fits the
    * regular sampler, else as 1.  Performance switch; the draws are unchanged. */
   int32_t skip_marks;
-  int32_t reserved[1];
+  /* Steps 2-3 (the per-document C1/C2 pass and the skip test, Sec. 3.3)
+   * only save work, and they cost about as much as the sampler work of a
+   * tenth of the tokens.  0 (default): they run in every eighth iteration,
+   * which measures the skip rate, and in every iteration after one that
+   * skipped at least an eighth of the tokens; 1: every iteration.
+   * Performance switch; the draws are unchanged (a token not skipped is
+   * drawn in full). */
+  int32_t always_skip_test;
 } lda_options;
 
 /* Per-iteration statistics (filled by lda_iterate when requested). */
@@ -113,6 +120,8 @@ typedef struct {
   int64_t dense_regions; /* of which regions of dense (full-row) words */
   int64_t row_bytes;     /* bytes of W rows the sampler needs: 4*K per dense word, 4*nnz per sparse word */
   int64_t sampler_block; /* threads per sampler workgroup */
+  int64_t skip_marks;    /* how step-3 decisions reached the sampler: 1 word-ordered bitmap, 2 document-ordered */
+  int64_t skip_test_ran; /* 1 if steps 2-3 ran in this iteration (see always_skip_test), else 0 */
 } lda_iter_stats;
 
 /* Count tables in the caller's ids.  Caller-allocated; a call with every array

@@ -176,3 +176,44 @@ def make_corpus(name: str, *, n_docs: int | None = None, V: int | None = None, K
     if K is not None:
         spec = dataclasses.replace(spec, K=int(K))
     return generate(spec, n_docs=n_docs, V=V, shuffle=shuffle, nthreads=nthreads)
+
+
+def fingerprint(c: Corpus) -> str:
+    """Hash of a corpus's shape and of a strided sample of its tokens (cheap at
+    any size): stored next to values computed from a corpus, so that a changed
+    generator shows up as such."""
+    import hashlib
+    h = hashlib.sha256()
+    step = max(1, c.N // 4_000_000)
+    for a in (np.array([c.N, c.V, c.n_docs, c.K], np.int64), c.word[::step], c.doc[::step],
+              np.array([int(c.word.sum(dtype=np.int64)), int(c.doc.sum(dtype=np.int64))], np.int64)):
+        h.update(np.ascontiguousarray(a).tobytes())
+    return h.hexdigest()
+
+
+def concentrated(n_docs: int = 4000, K: int = 64, words_per_topic: int = 40, single_frac: float = 0.6,
+                 mean_len: float = 60.0, alpha: float = 0.1, beta: float = 0.01, seed: int = 1009) -> Corpus:
+    """A corpus whose planted assignment is already concentrated, for tests that
+    need a high step-3 skip rate from the first iteration on.
+
+    Topic j owns words [j*words_per_topic, (j+1)*words_per_topic).  A fraction
+    ``single_frac`` of the documents draws every token from one topic (the
+    planted topic of each of those tokens); the other documents mix three
+    topics, and their tokens' planted topics are uniform over K.  Documents are
+    sorted (doc ids ascend).  ``topic`` holds the planted assignment.
+    """
+    rng = np.random.default_rng([seed, 3])
+    V = K * words_per_topic
+    lens = np.maximum(rng.poisson(mean_len, n_docs), 1)
+    doc = np.repeat(np.arange(n_docs, dtype=np.int32), lens)
+    N = int(doc.shape[0])
+    single = rng.random(n_docs) < single_frac
+    main = rng.integers(0, K, n_docs)
+    mix = rng.integers(0, K, (n_docs, 3))
+    pick = rng.integers(0, 3, N)
+    src = np.where(single[doc], main[doc], mix[doc, pick])          # topic each token's word comes from
+    word = (src * words_per_topic + rng.integers(0, words_per_topic, N)).astype(np.int32)
+    topic = np.where(single[doc], main[doc], rng.integers(0, K, N)).astype(np.int32)
+    spec = CorpusSpec("concentrated", n_docs, ("poisson", mean_len), V, 0.0, K, K, alpha, beta=beta, iters=3,
+                      seed=seed)
+    return Corpus(spec, word, doc, V, n_docs, topic)

@@ -34,7 +34,7 @@ class Options(ctypes.Structure):
                 ("alloc_ctx", ctypes.c_void_p), ("g", ctypes.c_int32), ("region_tokens", ctypes.c_int32),
                 ("no_skip", ctypes.c_int32), ("dense_cutoff", ctypes.c_int32), ("two_branch", ctypes.c_int32),
                 ("sampler_block", ctypes.c_int32), ("skip_marks", ctypes.c_int32),
-                ("reserved", ctypes.c_int32 * 1)]
+                ("always_skip_test", ctypes.c_int32)]
 
 
 class IterStats(ctypes.Structure):
@@ -42,7 +42,8 @@ class IterStats(ctypes.Structure):
                 ("ms_docpass", ctypes.c_double), ("ms_rebuild", ctypes.c_double), ("ms_precompute", ctypes.c_double),
                 ("skip_step3", ctypes.c_int64), ("skip_after_s", ctypes.c_int64), ("sampled", ctypes.c_int64),
                 ("nnz_scanned", ctypes.c_int64), ("regions", ctypes.c_int64), ("dense_regions", ctypes.c_int64),
-                ("row_bytes", ctypes.c_int64), ("sampler_block", ctypes.c_int64)]
+                ("row_bytes", ctypes.c_int64), ("sampler_block", ctypes.c_int64), ("skip_marks", ctypes.c_int64),
+                ("skip_test_ran", ctypes.c_int64)]
 
 
 class Counts(ctypes.Structure):
@@ -151,13 +152,14 @@ class LDA:
     ``two_branch`` samples over [S | Q] (Sec. 2.2): same distribution, other
     canonical order.  ``sampler_block`` (256, 512, 1024; 0 = by occupancy)
     sets the sampler's workgroup size; ``skip_marks`` (0 auto, 1 word order,
-    2 document order) how skip decisions reach the sampler.
+    2 document order) how skip decisions reach the sampler; ``always_skip_test``
+    runs steps 2-3 in every iteration instead of when they pay.
     """
 
     def __init__(self, word, doc, V: int, K: int, alpha: float, beta: float = 0.01, seed: int = 42, *, g: int = 2,
                  region_tokens: int = 0, no_skip: bool = False, dense_cutoff: int = 0, two_branch: bool = False,
-                 sampler_block: int = 0, skip_marks: int = 0, torch_stream: bool = True,
-                 torch_allocator: bool = True):
+                 sampler_block: int = 0, skip_marks: int = 0, always_skip_test: bool = False,
+                 torch_stream: bool = True, torch_allocator: bool = True):
         self._lib = load_library()
         self._h = ctypes.c_void_p()
         word = np.ascontiguousarray(word, np.int32)
@@ -172,6 +174,7 @@ class LDA:
         opts.two_branch = 1 if two_branch else 0
         opts.sampler_block = sampler_block
         opts.skip_marks = skip_marks
+        opts.always_skip_test = 1 if always_skip_test else 0
         self._keep = []
         if torch_stream or torch_allocator:
             import torch

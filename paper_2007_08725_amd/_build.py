@@ -8,7 +8,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB_PATH = os.path.join(HERE, "liblda.so")
-SOURCES = ["kernels.hip", "layout_gpu.hip", "lda_api.cpp", "layout.cpp"]
+SOURCES = ["kernels.hip", "layout_gpu.hip", "lda_api.cpp", "layout.cpp", "chunks.cpp"]
 ARCH = "gfx950"
 
 

@@ -14,6 +14,9 @@ with everything else at its default:
   no_split       large words are not split: one region per word (Sec. 5.1)
   word_marks     skip decisions always in the word-ordered bitmap
   doc_marks      skip decisions always in the document-ordered bitmap
+  always_test    steps 2-3 in every iteration (by default they run when the
+                 previous iteration skipped at least an eighth of the tokens,
+                 and in every eighth iteration)
 
 Only two_branch changes the draws (another canonical order of the same
 distribution); the rest draw exactly the same topics.
@@ -37,6 +40,7 @@ CONFIGS = {
     "no_split": dict(region_tokens=(1 << 31) - 1),
     "word_marks": dict(skip_marks=1),
     "doc_marks": dict(skip_marks=2),
+    "always_test": dict(always_skip_test=True),
 }
 
 

@@ -223,6 +223,20 @@ __device__ __forceinline__ bool doc_marks(const DevState &d, const Params &p, ui
   return t > 0u && 5ull * d.skip_hist[(t + 1u) & 1u] > uint64_t(p.n);
 }
 
+// Whether steps 2-3 run in iteration t.  They only save work: a token they
+// skip costs the sampler a bit test instead of its D row, so they pay once
+// enough tokens skip (the doc pass costs about as much as the sampler work of
+// a tenth of the tokens).  By default they run in every kProbeEvery-th
+// iteration, which measures the skip rate, and in every iteration after one
+// that skipped at least an eighth of the tokens; a token left unmarked is
+// drawn in full, so the draws are the same either way.
+constexpr uint32_t kProbeEvery = 8;
+__device__ __forceinline__ bool skip_test_runs(const DevState &d, const Params &p, uint32_t t) {
+  if (p.no_skip) return false;
+  if (p.always_skip_test || t % kProbeEvery == 0u) return true;
+  return 8ull * d.skip_hist[(t + 1u) & 1u] >= uint64_t(p.n);
+}
+
 __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, double *__restrict__ bden, int32_t K,
                         double beta, double vbeta, uint32_t *__restrict__ counters,
                         unsigned long long *__restrict__ stats) {
@@ -476,6 +490,8 @@ template <bool KeyId>
 __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint32_t t,
                                                      unsigned long long *__restrict__ stats) {
   extern __shared__ uint16_t cmap_all[];
+  if (!skip_test_runs(d, p, t)) return;  // uniform over the grid
+  if (blockIdx.x == 0 && threadIdx.x == 0) stats[ST_TEST_RAN] = 1ull;
   const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
   const int K = p.K;
   uint16_t *cmap = cmap_all + size_t(wave) * size_t(K);
@@ -1201,6 +1217,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  if (blockIdx.x == 0 && tid == 0) stats[ST_MARKS] = by_doc ? 2ull : 1ull;
   const BatchLds bt{s_off + wave * kWave, s_nnz + wave * kWave, s_u + wave * kWave, s_top + wave * kWave,
                     s_hand + wave * (kWave / kGroup) * kMaxRun, s_list + wave * kWave};
   const int qhalf = nbp / 2;
@@ -1483,6 +1500,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
   uint32_t *s_reg = s_hand + kTiledBlock / kGroup * kMaxRun;     // [4]
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = tid / kWave, grp = lane / kGroup, li = lane % kGroup;
+  if (blockIdx.x == 0 && tid == 0) stats[ST_MARKS] = 1ull;  // the word-ordered bitmap only
   uint32_t *hand = s_hand + (tid / kGroup) * kMaxRun;
   const uint32_t pad = uint32_t(K) << 16;
   // per-workgroup scratch slices, indexed by the token's place in its region

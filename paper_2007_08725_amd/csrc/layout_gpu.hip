@@ -81,7 +81,98 @@ __global__ void k_gather_z(const int32_t *__restrict__ z_in, const uint32_t *__r
   if (nbad) atomicAdd(bad, nbad);
 }
 
+// ----------------------------------------------------- out-of-core chunks --
+// A chunk keeps only dt_wpos (word-order slot of each doc-ordered token) and
+// its topics in host memory; the other per-token arrays are derived on the
+// device when the chunk is loaded.
+
+// dt_wpos[wpos[q]] = q: the word-order slot of each doc-order position, from
+// the doc-order positions listed in word order.
+__global__ void k_invert(const uint32_t *__restrict__ wpos, int64_t n, uint32_t *__restrict__ dt_wpos) {
+  for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < n; q += int64_t(gridDim.x) * blockDim.x)
+    dt_wpos[wpos[q]] = uint32_t(q);
+}
+
+// slot_word[s] = the word of word-order slot s, one workgroup per region
+// (the regions cover every slot exactly once).
+__global__ void k_slot_words(const uint32_t *__restrict__ region, int64_t n_regions, uint32_t *__restrict__ slot_word) {
+  for (int64_t r = blockIdx.x; r < n_regions; r += gridDim.x) {
+    const uint32_t v = region[3 * r], b = region[3 * r + 1], e = region[3 * r + 2];
+    for (uint32_t s = b + threadIdx.x; s < e; s += blockDim.x) slot_word[s] = v;
+  }
+}
+
+// Per document, one wave: for each of its tokens p (slot s = dt_wpos[p]) the
+// word id in doc order, and the key (key_base + p, the input index: chunks
+// need input sorted by document) and D-row offset in word order.  slot_word
+// and wt_rowoff share storage: slot s is read and then overwritten by the one
+// token that owns it.
+__global__ void k_inflate(const uint32_t *__restrict__ doc_off, const uint32_t *__restrict__ d_cap, int32_t M,
+                          const uint32_t *__restrict__ dt_wpos, uint32_t key_base, uint32_t *__restrict__ dt_word,
+                          uint32_t *__restrict__ wt_key, uint32_t *__restrict__ slot_word_rowoff) {
+  const int lane = threadIdx.x & 63, waves = int(blockDim.x) / 64;
+  for (int64_t d = int64_t(blockIdx.x) * waves + threadIdx.x / 64; d < M; d += int64_t(gridDim.x) * waves) {
+    const uint32_t b = doc_off[d], e = doc_off[d + 1], cap = d_cap[d];
+    for (uint32_t p = b + uint32_t(lane); p < e; p += 64u) {
+      const uint32_t s = dt_wpos[p];
+      dt_word[p] = slot_word_rowoff[s];
+      wt_key[s] = key_base + p;
+      slot_word_rowoff[s] = cap;
+    }
+  }
+}
+
+// Topics in doc order (int32) from topics in word order, and back with a
+// range check (bad counts topics outside [0, K), which are stored as 0).
+__global__ void k_doc_gather_z(const uint32_t *__restrict__ dt_wpos, const uint16_t *__restrict__ z_w, int64_t n,
+                               int32_t *__restrict__ z_doc) {
+  for (int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; p < n; p += int64_t(gridDim.x) * blockDim.x)
+    z_doc[p] = int32_t(z_w[dt_wpos[p]]);
+}
+
+__global__ void k_doc_scatter_z(const int32_t *__restrict__ z_doc, const uint32_t *__restrict__ dt_wpos, int64_t n,
+                                int32_t K, uint16_t *__restrict__ z_w, unsigned long long *__restrict__ bad) {
+  unsigned long long nbad = 0;
+  for (int64_t p = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; p < n; p += int64_t(gridDim.x) * blockDim.x) {
+    const int32_t z = z_doc[p];
+    const bool ok = z >= 0 && z < K;
+    z_w[dt_wpos[p]] = ok ? uint16_t(z) : uint16_t(0);
+    nbad += ok ? 0ull : 1ull;
+  }
+  if (nbad) atomicAdd(bad, nbad);
+}
+
 }  // namespace
+
+hipError_t launch_invert(const uint32_t *wpos, int64_t n, uint32_t *dt_wpos, hipStream_t s) {
+  hipLaunchKernelGGL(k_invert, dim3(grid_for(n)), dim3(kThreads), 0, s, wpos, n, dt_wpos);
+  return hipGetLastError();
+}
+
+hipError_t launch_inflate(const uint32_t *region, int64_t n_regions, const uint32_t *doc_off, const uint32_t *d_cap,
+                          int32_t M, const uint32_t *dt_wpos, uint32_t key_base, uint32_t *dt_word, uint32_t *wt_key,
+                          uint32_t *wt_rowoff, hipStream_t s) {
+  const uint32_t rg = uint32_t(std::min<int64_t>(std::max<int64_t>(n_regions, 1), 1 << 16));
+  hipLaunchKernelGGL(k_slot_words, dim3(rg), dim3(kThreads), 0, s, region, n_regions, wt_rowoff);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const int64_t waves = kThreads / 64;
+  const uint32_t dg = uint32_t(std::min<int64_t>(std::max<int64_t>((int64_t(M) + waves - 1) / waves, 1), 1 << 16));
+  hipLaunchKernelGGL(k_inflate, dim3(dg), dim3(kThreads), 0, s, doc_off, d_cap, M, dt_wpos, key_base, dt_word, wt_key,
+                     wt_rowoff);
+  return hipGetLastError();
+}
+
+hipError_t launch_doc_gather_z(const uint32_t *dt_wpos, const uint16_t *z_w, int64_t n, int32_t *z_doc, hipStream_t s) {
+  hipLaunchKernelGGL(k_doc_gather_z, dim3(grid_for(n)), dim3(kThreads), 0, s, dt_wpos, z_w, n, z_doc);
+  return hipGetLastError();
+}
+
+hipError_t launch_doc_scatter_z(const int32_t *z_doc, const uint32_t *dt_wpos, int64_t n, int32_t K, uint16_t *z_w,
+                                unsigned long long *bad, hipStream_t s) {
+  hipLaunchKernelGGL(k_doc_scatter_z, dim3(grid_for(n)), dim3(kThreads), 0, s, z_doc, dt_wpos, n, K, z_w, bad);
+  return hipGetLastError();
+}
 
 unsigned bits_for(uint64_t max_value) {
   unsigned b = 1;

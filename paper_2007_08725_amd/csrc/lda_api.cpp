@@ -8,100 +8,15 @@
 #include <string>
 #include <vector>
 
-#include "lda_internal.h"
+#include "handle.h"
 
 using namespace lda;
 
-namespace {
-
+namespace lda {
 thread_local std::string g_create_error = "no error";
-constexpr int kStatSlots = 256;   // iterations between two statistics read-backs
-constexpr int kEventsPerIter = 5;
-
-}  // namespace
-
-struct lda_handle {
-  Layout L;  // host copy of the layout (only the parts needed later are kept)
-  DevState d{};
-  Params p{};
-  hipStream_t stream = nullptr;
-  bool own_stream = false;
-  int device = 0;
-  void *(*dev_alloc)(size_t, void *) = nullptr;
-  void (*dev_free)(void *, void *) = nullptr;
-  void *alloc_ctx = nullptr;
-  std::vector<void *> allocations;
-  unsigned long long *stats_base = nullptr;  // [kStatSlots * kStatsPerIter]
-  std::vector<hipEvent_t> events;            // [kStatSlots * kEventsPerIter]
-  void *noalloc_scratch = nullptr;           // this device's fixed LLPT scratch (lda_loglik_noalloc)
-  int64_t iteration = 0;
-  bool poisoned = false;
-  std::string err = "no error";
-};
+}  // namespace lda
 
 namespace {
-
-lda_status fail(lda_handle *h, lda_status st, const std::string &msg) {
-  if (h) {
-    h->err = msg;
-    if (st == LDA_E_DEVICE) h->poisoned = true;
-  } else {
-    g_create_error = msg;
-  }
-  return st;
-}
-
-lda_status hip_fail(lda_handle *h, hipError_t e, const char *what) {
-  return fail(h, e == hipErrorOutOfMemory ? LDA_E_NOMEM : LDA_E_DEVICE,
-              std::string(what) + ": " + hipGetErrorString(e));
-}
-
-#define HIP_TRY(h, expr)                                  \
-  do {                                                    \
-    hipError_t e_ = (expr);                               \
-    if (e_ != hipSuccess) return hip_fail((h), e_, #expr); \
-  } while (0)
-
-template <typename T>
-lda_status dalloc(lda_handle *h, T **out, size_t count) {
-  size_t bytes = std::max<size_t>(count, 1) * sizeof(T);
-  bytes = (bytes + 255) & ~size_t(255);
-  void *ptr = nullptr;
-  if (h->dev_alloc) {
-    ptr = h->dev_alloc(bytes, h->alloc_ctx);
-    if (!ptr) return fail(h, LDA_E_NOMEM, "device allocation of " + std::to_string(bytes) + " bytes failed");
-  } else {
-    hipError_t e = hipMalloc(&ptr, bytes);
-    if (e != hipSuccess) return fail(h, LDA_E_NOMEM, "hipMalloc(" + std::to_string(bytes) + "): " + hipGetErrorString(e));
-  }
-  h->allocations.push_back(ptr);
-  *out = static_cast<T *>(ptr);
-  return LDA_OK;
-}
-
-template <typename T>
-lda_status upload(lda_handle *h, T *dst, const std::vector<T> &src) {
-  if (src.empty()) return LDA_OK;
-  HIP_TRY(h, hipMemcpyAsync(dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice, h->stream));
-  return LDA_OK;
-}
-
-#define LDA_TRY(expr)                 \
-  do {                                \
-    lda_status s_ = (expr);           \
-    if (s_ != LDA_OK) return s_;      \
-  } while (0)
-
-lda_status check_handle(lda_handle *h) {
-  if (!h) return LDA_E_ARG;
-  if (h->poisoned) return LDA_E_STATE;
-  return LDA_OK;
-}
-
-lda_status check_errors(lda_handle *h, const unsigned long long *st) {
-  if (st[ST_ERRORS]) return fail(h, LDA_E_DEVICE, "kernel found " + std::to_string(st[ST_ERRORS]) + " topic slots outside [0, K)");
-  return LDA_OK;
-}
 
 // Count tables of the current assignment z_w (Sec. 4.3 update step).
 lda_status rebuild_counts(lda_handle *h) {
@@ -109,29 +24,6 @@ lda_status rebuild_counts(lda_handle *h) {
   d.stats = h->stats_base;
   HIP_TRY(h, launch_begin_iteration(d, h->p, h->stream));
   HIP_TRY(h, launch_rebuild(d, h->p, h->stream));
-  return LDA_OK;
-}
-
-template <typename T>
-void dfree(lda_handle *h, T *&ptr) {
-  if (!ptr) return;
-  void *v = static_cast<void *>(ptr);
-  auto it = std::find(h->allocations.begin(), h->allocations.end(), v);
-  if (it != h->allocations.end()) h->allocations.erase(it);
-  if (h->dev_alloc) h->dev_free(v, h->alloc_ctx);
-  else (void)hipFree(v);
-  ptr = nullptr;
-}
-
-lda_status sort_pairs(lda_handle *h, const uint32_t *keys_in, uint32_t *keys_out, const uint32_t *vals_in,
-                      uint32_t *vals_out, unsigned end_bit) {
-  size_t bytes = 0;
-  HIP_TRY(h, sort_pairs_u32(nullptr, bytes, keys_in, keys_out, vals_in, vals_out, h->L.n, end_bit, h->stream));
-  uint8_t *tmp = nullptr;
-  LDA_TRY(dalloc(h, &tmp, bytes));
-  HIP_TRY(h, sort_pairs_u32(tmp, bytes, keys_in, keys_out, vals_in, vals_out, h->L.n, end_bit, h->stream));
-  HIP_TRY(h, hipStreamSynchronize(h->stream));
-  dfree(h, tmp);
   return LDA_OK;
 }
 
@@ -358,6 +250,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   if (!std::isfinite(alpha) || !(alpha > 0.0)) return fail(nullptr, LDA_E_ARG, "alpha must be finite and positive");
   if (!std::isfinite(beta) || !(beta > 0.0)) return fail(nullptr, LDA_E_ARG, "beta must be finite and positive");
   int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0, two_branch = 0, skip_marks = 0;
+  int32_t always_skip_test = 0;
   if (opts) {
     if (opts->g < 0 || opts->g > 3) return fail(nullptr, LDA_E_ARG, "g must be 1, 2 or 3");
     if (opts->g) g = opts->g;
@@ -374,6 +267,9 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
       return fail(nullptr, LDA_E_ARG, "sampler_block must be 0, 256, 512 or 1024");
     if (opts->skip_marks < 0 || opts->skip_marks > 2) return fail(nullptr, LDA_E_ARG, "skip_marks must be 0, 1 or 2");
     skip_marks = opts->skip_marks;
+    if (opts->always_skip_test < 0 || opts->always_skip_test > 1)
+      return fail(nullptr, LDA_E_ARG, "always_skip_test must be 0 or 1");
+    always_skip_test = opts->always_skip_test;
   }
   lda_handle *h = new (std::nothrow) lda_handle();
   if (!h) return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
@@ -410,6 +306,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   p.two_branch = two_branch;
   p.key_identity = sorted ? 1 : 0;
   p.skip_marks = skip_marks;
+  p.always_skip_test = always_skip_test;
   try {
     st = create_device(h, opts, word, doc, R, dense_cutoff);
   } catch (const std::bad_alloc &) {
@@ -480,6 +377,8 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       o.dense_regions = int64_t(s[ST_DENSE_REGIONS]);
       o.row_bytes = int64_t(s[ST_ROW_BYTES]);
       o.sampler_block = h->p.sampler_block;
+      o.skip_marks = int64_t(s[ST_MARKS]);
+      o.skip_test_ran = int64_t(s[ST_TEST_RAN]);
     }
     done += chunk;
   }
@@ -632,6 +531,8 @@ lda_status lda_set_assignments(lda_handle *h, const int32_t *z, int64_t iteratio
   HIP_TRY(h, hipMemcpy(st, h->stats_base, sizeof(st), hipMemcpyDeviceToHost));
   LDA_TRY(check_errors(h, st));
   LDA_TRY(rebuild_counts(h));
+  // the skip counts of earlier iterations describe another assignment
+  HIP_TRY(h, hipMemsetAsync(h->d.skip_hist, 0, 2 * sizeof(unsigned long long), h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   HIP_TRY(h, hipMemcpy(st, h->stats_base, sizeof(st), hipMemcpyDeviceToHost));
   LDA_TRY(check_errors(h, st));

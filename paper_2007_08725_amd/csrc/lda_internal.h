@@ -90,6 +90,17 @@ hipError_t launch_word_order(const uint32_t *wkey, const uint32_t *wpos, int64_t
 hipError_t launch_scatter_z(const uint16_t *z_w, const uint32_t *wt_key, int64_t n, int32_t *z_in, hipStream_t s);
 hipError_t launch_gather_z(const int32_t *z_in, const uint32_t *wt_key, int64_t n, int32_t K, uint16_t *z_w,
                            unsigned long long *bad, hipStream_t s);
+// Out-of-core chunks: the word-order slot of each doc-order position from the
+// positions listed in word order; the per-token arrays derived from dt_wpos
+// and the chunk's regions and document tables; topics between doc order
+// (int32) and word order.
+hipError_t launch_invert(const uint32_t *wpos, int64_t n, uint32_t *dt_wpos, hipStream_t s);
+hipError_t launch_inflate(const uint32_t *region, int64_t n_regions, const uint32_t *doc_off, const uint32_t *d_cap,
+                          int32_t M, const uint32_t *dt_wpos, uint32_t key_base, uint32_t *dt_word, uint32_t *wt_key,
+                          uint32_t *wt_rowoff, hipStream_t s);
+hipError_t launch_doc_gather_z(const uint32_t *dt_wpos, const uint16_t *z_w, int64_t n, int32_t *z_doc, hipStream_t s);
+hipError_t launch_doc_scatter_z(const int32_t *z_doc, const uint32_t *dt_wpos, int64_t n, int32_t K, uint16_t *z_w,
+                                unsigned long long *bad, hipStream_t s);
 
 // ---------------------------------------------------------- device state --
 struct WordRec {  // per relabelled word, refreshed every iteration (Sec. 3.2, steps 1 and 4)
@@ -168,6 +179,7 @@ struct Params {
   int32_t sparse_pre;    // per-word precompute of sparse words from their row and a topic list (large K)
   int32_t top_list;      // length of that topic list
   int32_t skip_marks;    // 0 auto, 1 word-ordered bitmap, 2 document-ordered bitmap (lda_options)
+  int32_t always_skip_test;  // steps 2-3 every iteration instead of when they pay (lda_options)
   int32_t doc_marks_ok;  // the document-ordered bitmap is usable: keys are document positions, regular sampler
   uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
@@ -176,8 +188,9 @@ struct Params {
 // kXcds (one per document range) for the D rebuild.
 enum { CNT_SAMPLER = 0, CNT_REBUILD_W = 1, CNT_DOCPASS = 2, CNT_LOGLIK = 4, CNT_REBUILD_D = 16 };
 constexpr int kCounters = 32;
-enum { ST_SKIP3 = 0, ST_SKIP_AFTER_S = 1, ST_SAMPLED = 2, ST_NNZ = 3, ST_REGIONS = 4, ST_DENSE_REGIONS = 5, ST_ERRORS = 6, ST_ROW_BYTES = 7 };
-constexpr int kStatsPerIter = 8;
+enum { ST_SKIP3 = 0, ST_SKIP_AFTER_S = 1, ST_SAMPLED = 2, ST_NNZ = 3, ST_REGIONS = 4, ST_DENSE_REGIONS = 5, ST_ERRORS = 6,
+       ST_ROW_BYTES = 7, ST_MARKS = 8, ST_TEST_RAN = 9 };
+constexpr int kStatsPerIter = 16;
 
 // Kernel launchers (all asynchronous on `s`); return hipGetLastError().
 hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s);

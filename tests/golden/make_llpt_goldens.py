@@ -13,7 +13,6 @@ time of the run.
     python tests/golden/make_llpt_goldens.py [case ...] [--threads N]
 """
 import argparse
-import hashlib
 import json
 import os
 import platform
@@ -42,16 +41,6 @@ CASES = {
     "c2": ("c2", {}),
     "c3": ("c3", {}),
 }
-
-
-def fingerprint(c) -> str:
-    """Hash of the corpus shape and a strided sample of its tokens (cheap at any size)."""
-    h = hashlib.sha256()
-    step = max(1, c.N // 4_000_000)
-    for a in (np.array([c.N, c.V, c.n_docs, c.K], np.int64), c.word[::step], c.doc[::step],
-              np.array([int(c.word.sum(dtype=np.int64)), int(c.doc.sum(dtype=np.int64))], np.int64)):
-        h.update(np.ascontiguousarray(a).tobytes())
-    return h.hexdigest()
 
 
 def cpu_model() -> str:
@@ -84,7 +73,7 @@ def run_case(name, threads):
     out = dict(case=name, workload=workload, overrides=over, N=c.N, V=c.V, K=c.K, M=c.n_docs, alpha=c.alpha,
                beta=c.beta, seed=SEED, iterations=ITERS, llpt=traj[ITERS],
                llpt_trajectory={str(k): v for k, v in sorted(traj.items())},
-               corpus_fingerprint=fingerprint(c), threads=threads, cpu_model=cpu_model(),
+               corpus_fingerprint=lda_synth.fingerprint(c), threads=threads, cpu_model=cpu_model(),
                wall_s=round(wall, 1),
                source="oracle/lda_oracle.c sparse form, tokens split over host threads by range")
     path = os.path.join(HERE, "llpt50_%s.json" % name)

@@ -72,7 +72,8 @@ def test_create_argument_errors(lib):
     assert st == lda.LDA_E_ARG and not h.value
     # bad options
     for field, value in (("g", 4), ("g", -1), ("region_tokens", -2), ("sampler_block", 300),
-                         ("sampler_block", 128), ("sampler_block", 2048), ("skip_marks", 3), ("skip_marks", -1)):
+                         ("sampler_block", 128), ("sampler_block", 2048), ("skip_marks", 3), ("skip_marks", -1),
+                         ("always_skip_test", 2), ("always_skip_test", -1)):
         o = lda.Options()
         setattr(o, field, value)
         st, h = _create(lib, pw, pd, 3, 3, 4, 0.5, 0.01, ctypes.byref(o))

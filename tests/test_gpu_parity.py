@@ -5,6 +5,9 @@ draw and there are fewer than 1e-6*N of them; D, W and T are bit-exact given
 the GPU's assignment; LLPT agrees with the oracle to 1e-12 relative on the same
 assignment (1e-3 after trajectories diverge).
 """
+import json
+import os
+
 import numpy as np
 import pytest
 
@@ -14,6 +17,7 @@ from gpu_common import (SEED, check_counts_are_histograms, compare_draws, corpus
                         say)
 
 pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
 @pytest.fixture(scope="module")
@@ -44,7 +48,7 @@ def test_init_topics_match_oracle(c1, c1_traj):
 
 def test_c1_every_iteration_from_oracle_snapshot(c1, c1_traj):
     """At each t the GPU starts from the oracle's z_t and must reproduce z_{t+1}."""
-    with make_lda(c1) as m:
+    with make_lda(c1, always_skip_test=True) as m:
         for t in range(c1.spec.iters):
             say("c1 snapshot t=%d" % t)
             m.set_assignments(c1_traj[t][0], t)
@@ -99,31 +103,105 @@ def test_schedule_invariance(c1, opts):
     assert np.array_equal(za, zb)
 
 
-def test_skip_bitmaps_leave_the_draws_unchanged():
-    """Skip decisions carried by the word-ordered bitmap, the document-ordered
-    bitmap, or the per-iteration choice between them (which switches once a
-    fifth of the tokens skip) give the same draws, over iterations whose skip
-    rate climbs past that threshold; shuffled input has no document-ordered
-    bitmap and falls back to the word-ordered one."""
-    c = lda_synth.make_corpus("c3", n_docs=12000)
-    say("skip bitmaps c3 reduced N=%d" % c.N)
-    zs, rates = [], None
-    for marks in (1, 2, 0):
+def test_skip_bitmap_switch_follows_the_oracle():
+    """The per-iteration choice between the two skip bitmaps, taken where it fires.  The corpus
+    starts from a concentrated planted assignment, so iteration 0 skips well over a fifth of its
+    tokens and carries its decisions in the word-ordered bitmap; iteration 1 then switches to the
+    document-ordered bitmap.  Both iterations draw what the oracle draws from the same snapshot,
+    and forcing either bitmap gives the same draws; shuffled input has no document-ordered bitmap
+    and falls back to the word-ordered one."""
+    c = lda_synth.concentrated()
+    say("skip bitmap switch N=%d K=%d" % (c.N, c.K))
+    runs = {}
+    for marks in (0, 1, 2):
         with make_lda(c, skip_marks=marks) as m:
-            st = m.iterate(60, stats=True)
-            zs.append(m.counts(D=False, W=False)["z"])
-        r = [s["skip_step3"] / c.N for s in st]
-        rates = r if rates is None else rates
-        assert r == rates  # the skip decisions themselves are the same
-    say("  skip rate at iterations 0, 30, 59: %.3f %.3f %.3f" % (rates[0], rates[30], rates[59]))
-    assert np.array_equal(zs[0], zs[1]) and np.array_equal(zs[0], zs[2])
+            m.set_assignments(c.topic, 0)
+            z = c.topic
+            rec = []
+            for t in range(3):
+                zo, flags, ost = oracle_step(c, z, t)
+                st = m.iterate(1, stats=True)[0]
+                zg = m.counts(D=False, W=False)["z"]
+                compare_draws(zg, zo, flags, c.N)
+                assert 0 <= ost["skip3"] - st["skip_step3"] <= max(2, 1e-3 * c.N)
+                rec.append((st["skip_step3"] / c.N, st["skip_marks"], zg))
+                z = zg  # the GPU's own state is the next snapshot
+            runs[marks] = rec
+    rates = [r[0] for r in runs[0]]
+    say("  skip rates %s, bitmaps (auto) %s" % (["%.3f" % x for x in rates], [r[1] for r in runs[0]]))
+    assert rates[0] > 0.2  # the threshold is crossed at once
+    assert [r[1] for r in runs[0]] == [1, 2, 2]  # word order first (no previous count), then document order
+    assert [r[1] for r in runs[1]] == [1, 1, 1] and [r[1] for r in runs[2]] == [2, 2, 2]
+    for t in range(3):
+        assert np.array_equal(runs[0][t][2], runs[1][t][2]) and np.array_equal(runs[0][t][2], runs[2][t][2])
+        assert runs[0][t][0] == runs[1][t][0] == runs[2][t][0]
     cs = lda_synth.generate(lda_synth.SPECS["c1"], n_docs=300, shuffle=True)
     out = []
     for marks in (1, 2):
         with make_lda(cs, skip_marks=marks) as m:
-            m.iterate(3)
+            st = m.iterate(3, stats=True)
+            assert all(s["skip_marks"] == 1 for s in st)
             out.append(m.counts(D=False, W=False)["z"])
     assert np.array_equal(out[0], out[1])
+
+
+@pytest.fixture(scope="module")
+def switch_snapshots(c1, c1_traj):
+    """Snapshots every option is checked on, with the oracle's draws from each: c1 at t = 8, a
+    reduced c3 at t = 0 and the concentrated corpus (most tokens skip) at t = 0 (iterations in
+    which steps 2-3 run by default)."""
+    c3 = lda_synth.make_corpus("c3", n_docs=12000)
+    cc = lda_synth.concentrated()
+    out = []
+    for c, z, t in ((c1, c1_traj[8][0], 8), (c3, oracle.init_topics(c3.N, c3.K, SEED), 0), (cc, cc.topic, 0)):
+        zo, flags, ost = oracle.iterate_threaded(c.word, c.doc, z, seed=SEED, t=t, **corpus_kw(c))
+        out.append((c, z, t, zo, flags, ost))
+    return out
+
+
+@pytest.mark.parametrize("opts", [dict(no_skip=True), dict(dense_cutoff=-1), dict(dense_cutoff=1 << 30),
+                                  dict(sampler_block=256), dict(sampler_block=512), dict(sampler_block=1024),
+                                  dict(skip_marks=1), dict(skip_marks=2), dict(region_tokens=97), dict(g=1),
+                                  dict(g=3), dict(always_skip_test=True)],
+                         ids=lambda o: "-".join("%s=%s" % kv for kv in o.items()))
+def test_every_option_follows_the_oracle(switch_snapshots, opts):
+    """Each performance or ablation switch that must leave the draws unchanged, against the
+    oracle (not only against the GPU's default): same snapshot, same draws up to flagged
+    near-boundary cases, counts the histograms of z."""
+    for c, z, t, zo, flags, ost in switch_snapshots:
+        say("option %s on N=%d K=%d t=%d" % (opts, c.N, c.K, t))
+        with make_lda(c, **opts) as m:
+            m.set_assignments(z, t)
+            st = m.iterate(1, stats=True)[0]
+            cnt = m.counts()
+        compare_draws(cnt["z"], zo, flags, c.N)
+        check_counts_are_histograms(c, cnt, c.K)
+        if opts.get("no_skip"):
+            assert st["skip_step3"] == 0 and st["sampled"] == c.N and st["skip_test_ran"] == 0
+        else:
+            assert st["skip_step3"] + st["sampled"] == c.N and st["skip_test_ran"] == 1
+            if "g" in opts:  # the skip statistics at the same S_est depth (the draws do not depend on it)
+                ost = oracle.iterate_threaded(c.word, c.doc, z, seed=SEED, t=t, g=opts["g"], **corpus_kw(c))[2]
+            assert 0 <= ost["skip3"] - st["skip_step3"] <= max(2, 1e-3 * c.N)
+
+
+def test_skip_test_runs_when_it_pays():
+    """By default steps 2-3 run in every eighth iteration and after an iteration that skipped at
+    least an eighth of the tokens; the draws are those of running them in every iteration."""
+    for c, z0, want in ((lda_synth.make_corpus("c2", n_docs=2500), None, [1, 0, 0, 0, 0, 0, 0, 0, 1, 0]),
+                        (lda_synth.concentrated(), "planted", [1] * 10)):
+        zs, ran = [], []
+        for always in (False, True):
+            with make_lda(c, always_skip_test=always) as m:
+                if z0 == "planted":
+                    m.set_assignments(c.topic, 0)
+                st = m.iterate(10, stats=True)
+                zs.append(m.counts(D=False, W=False)["z"])
+                ran.append([s["skip_test_ran"] for s in st])
+                rates = [s["skip_step3"] / c.N for s in st]
+        say("  N=%d skip rates %s ran %s" % (c.N, ["%.3f" % r for r in rates], ran[0]))
+        assert ran[0] == want and ran[1] == [1] * 10
+        assert np.array_equal(zs[0], zs[1])
 
 
 @pytest.mark.parametrize("g", [1, 3])
@@ -131,7 +209,7 @@ def test_skip_counts_follow_the_oracle_for_every_depth(c1, c1_traj, g):
     """Step-3 skips at S_est depth g (Eq. 9) against the oracle's fp64 test on the same
     snapshots: the GPU's single-precision test with its margin skips a few tokens fewer,
     never more."""
-    with make_lda(c1, g=g) as m:
+    with make_lda(c1, g=g, always_skip_test=True) as m:
         for t in range(3):
             z = c1_traj[t][0]
             zo, flags, ost = oracle_step(c1, z, t, g=g)
@@ -212,7 +290,7 @@ def test_reduced_config_late_snapshot(name, over):
     """Iteration 49 from the GPU's own state after 49 iterations (higher skip rates than at the start)."""
     c = lda_synth.make_corpus(name, **over)
     say("late snapshot %s N=%d" % (name, c.N))
-    with make_lda(c) as m:
+    with make_lda(c, always_skip_test=True) as m:
         m.iterate(49)
         z = m.counts(D=False, W=False)["z"]
         zo, flags, ost = oracle_step(c, z, 49)
@@ -226,26 +304,32 @@ def test_reduced_config_late_snapshot(name, over):
     say("  skip3 gpu %d oracle %d of %d" % (st["skip_step3"], ost["skip3"], c.N))
 
 
-@pytest.mark.timeout(600)
-def test_llpt_after_fifty_iterations_reduced_c2():
+def load_golden(case):
+    with open(os.path.join(GOLDEN, "llpt50_%s.json" % case)) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("case", ["c2_reduced", "c3_reduced", "c4_reduced", "c5_reduced"])
+def test_llpt_after_fifty_iterations_reduced(case):
     """Free-running GPU and oracle trajectories from the same initial topics diverge token by
-    token, but after 50 iterations their per-token log-likelihoods agree within 1e-3 relative;
-    the GPU's LLPT of its own state equals the oracle's LLPT of that state to 1e-12."""
-    c = lda_synth.make_corpus("c2", n_docs=2500)
+    token, but after 50 iterations their per-token log-likelihoods agree within 1e-3 relative
+    (the oracle's value: tests/golden, written on the CPU by make_llpt_goldens.py); the GPU's
+    LLPT of its own state equals the oracle's LLPT of that state to 1e-12."""
+    g = load_golden(case)
+    c = lda_synth.make_corpus(g["workload"], **g["overrides"])
+    assert lda_synth.fingerprint(c) == g["corpus_fingerprint"]
     kw = corpus_kw(c)
-    say("LLPT-50 c2 reduced N=%d" % c.N)
-    z = oracle.init_topics(c.N, c.K, SEED)
-    for t in range(50):
-        z, _, _ = oracle_step(c, z, t)
-    lo = oracle.llpt(c.word, c.doc, z, **kw)
+    say("LLPT-50 %s N=%d" % (case, c.N))
     with make_lda(c) as m:
+        ll0 = m.loglik()
         m.iterate(50)
         lg = m.loglik()
         zg = m.counts(D=False, W=False)["z"]
-    say("  LLPT gpu %.6f oracle %.6f" % (lg, lo))
-    assert lg == pytest.approx(lo, rel=1e-3)
+    say("  LLPT gpu %.6f oracle %.6f" % (lg, g["llpt"]))
+    assert ll0 == pytest.approx(g["llpt_trajectory"]["0"], rel=1e-12)  # the same initial state
+    assert lg == pytest.approx(g["llpt"], rel=1e-3)
     assert lg == pytest.approx(oracle.llpt(c.word, c.doc, zg, **kw), rel=1e-12)
-    assert lg > oracle.llpt(c.word, c.doc, oracle.init_topics(c.N, c.K, SEED), **kw)
+    assert lg > ll0
 
 
 def test_shuffled_input_order():
