@@ -24,6 +24,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+PCIE_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "k_sampler_c3_counters.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2007_08725_amd", "csrc", "kernels.hip")
 
@@ -84,6 +85,8 @@ def main():
     ap.add_argument("--cpu-docs", type=int, default=200000, help="documents in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dump-stats", default=None, help="write the per-iteration statistics (JSON lines) here")
+    ap.add_argument("--chunks", type=int, default=0,
+                    help="out-of-core mode: per-token arrays in pinned host memory, streamed in this many chunks")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -104,7 +107,7 @@ def main():
     log("generated %s: N=%d docs=%d V=%d K=%d in %.1f s" % (args.workload, c.N, c.n_docs, c.V, c.K,
                                                             time.perf_counter() - t0))
     t0 = time.perf_counter()
-    m = lda.LDA(c.word, c.doc, c.V, c.K, c.alpha, c.beta, lda_synth.SAMPLER_SEED)
+    m = lda.LDA(c.word, c.doc, c.V, c.K, c.alpha, c.beta, lda_synth.SAMPLER_SEED, chunks=args.chunks)
     torch.cuda.synchronize()
     t_create = time.perf_counter() - t0
     log("lda_create %.1f s" % t_create)
@@ -135,9 +138,21 @@ def main():
     value = N * args.steps / elapsed
     ms_sampler = np.array([s["ms_sampler"] for s in st])
     alg = np.array([sampler_alg_bytes(s, N) for s in st], dtype=np.float64)
-    achieved = alg.sum() / (ms_sampler.sum() * 1e-3) / 1e9
     alg_per_launch = float(alg.mean())
-    traffic = traffic_from_profile(alg_per_launch)
+    if args.chunks > 1:
+        # out of core: the stream of per-token arrays over PCIe bounds the
+        # iteration (6 B a token up: word-order slot and topic; 2 B down)
+        h2d = 6.0 * N
+        achieved = h2d * args.steps / elapsed / 1e9
+        roofline = {"bound": "pcie", "achieved": achieved, "peak": PCIE_PEAK_GBS, "unit": "GB/s",
+                    "frac": achieved / PCIE_PEAK_GBS, "traffic": None, "kernel": "host-to-device copies",
+                    "h2d_bytes_per_iteration": h2d, "d2h_bytes_per_iteration": 2.0 * N, "chunks": args.chunks}
+    else:
+        achieved = alg.sum() / (ms_sampler.sum() * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_from_profile(alg_per_launch),
+                    "kernel": "k_sampler", "alg_bytes_per_launch": alg_per_launch,
+                    "avg_launch_ms": float(ms_sampler.mean())}
     stage_ms = {k: float(np.mean([s[k] for s in st])) for k in
                 ("ms_precompute", "ms_docpass", "ms_sampler", "ms_rebuild", "ms_iter")}
     line = {
@@ -155,11 +170,8 @@ def main():
         "data": "synthetic planted-LDA corpus (seeded), random initial topics",
         "config": {"workload": "%s: %d docs, %d tokens, V=%d, K=%d, alpha=%g, beta=%g, iterations %d-%d" % (
             args.workload, c.n_docs, N, c.V, c.K, c.alpha, c.beta, args.warmup, args.warmup + args.steps - 1),
-            "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "kernel": "k_sampler",
-                     "alg_bytes_per_launch": alg_per_launch, "avg_launch_ms": float(ms_sampler.mean())},
+            "parallelism": "single GPU" + (", out of core in %d chunks" % args.chunks if args.chunks > 1 else "")},
+        "roofline": roofline,
         "breakdown_ms": stage_ms,
         "skip_step3_frac": float(np.mean([s["skip_step3"] for s in st]) / N),
         "llpt_after": llpt,

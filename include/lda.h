@@ -56,6 +56,8 @@ typedef enum {
 #define LDA_MAX_TOPICS 32768
 /* Longest document: its per-topic counts must fit 16 bits (Sec. 4.2). */
 #define LDA_MAX_DOC_LEN 65535
+/* Most chunks of an out-of-core corpus (lda_options.chunks). */
+#define LDA_MAX_CHUNKS 256
 
 typedef struct {
   /* hipStream_t to run on; NULL = the handle creates its own stream. */
@@ -102,6 +104,16 @@ typedef struct {
    * Performance switch; the draws are unchanged (a token not skipped is
    * drawn in full). */
   int32_t always_skip_test;
+  /* Out-of-core corpus (Sec. 4.1 and 4.3): 0 or 1 = every per-token array
+   * resident on the device (default); C in [2, LDA_MAX_CHUNKS] = the
+   * documents are cut into C chunks of near-equal token counts whose
+   * per-token arrays (6 bytes a token) live in pinned host memory and stream
+   * through two device buffers every iteration, transfers overlapping the
+   * previous chunk's work.  W is then dense for every word and kept twice
+   * (the snapshot and the next counts), so the draws equal the resident
+   * path's.  Needs input sorted by document (LDA_E_ARG otherwise); the
+   * per-stage times of lda_iter_stats are 0 (ms_iter is kept). */
+  int32_t chunks;
 } lda_options;
 
 /* Per-iteration statistics (filled by lda_iterate when requested). */
@@ -190,9 +202,10 @@ lda_status lda_set_assignments(lda_handle *h, const int32_t *z, int64_t iteratio
  * (the per-region partial sums, the scheduler counter and the result) lives in
  * a fixed device array of the library instead of handle memory, so the call
  * itself allocates nothing (no hipMalloc, hipFree or allocating library
- * routine).  The array holds 512 B plus 8 B per region, up to
- * LDA_NOALLOC_MAX_REGIONS regions (16 MiB); each device the library runs on
- * keeps its own copy until the process ends.
+ * routine).  The array holds 4 KiB plus 8 B per region (of the largest
+ * chunk, with lda_options.chunks), up to LDA_NOALLOC_MAX_REGIONS regions
+ * (16 MiB); each device the library runs on keeps its own copy until the
+ * process ends.
  *   llpt: host pointer to one double (output).
  * Errors: LDA_E_ARG (llpt NULL), LDA_E_RANGE (the handle's layout has more
  * than LDA_NOALLOC_MAX_REGIONS regions), LDA_E_DEVICE, LDA_E_STATE.

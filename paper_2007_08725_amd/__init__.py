@@ -24,6 +24,7 @@ STATUS_NAMES = {0: "LDA_OK", 1: "LDA_E_ARG", 2: "LDA_E_RANGE", 3: "LDA_E_NOMEM",
                 5: "LDA_E_STATE"}
 MAX_TOPICS = 32768
 MAX_DOC_LEN = 65535
+MAX_CHUNKS = 256
 
 ALLOC_FN = ctypes.CFUNCTYPE(ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p)
 FREE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_void_p)
@@ -34,7 +35,7 @@ class Options(ctypes.Structure):
                 ("alloc_ctx", ctypes.c_void_p), ("g", ctypes.c_int32), ("region_tokens", ctypes.c_int32),
                 ("no_skip", ctypes.c_int32), ("dense_cutoff", ctypes.c_int32), ("two_branch", ctypes.c_int32),
                 ("sampler_block", ctypes.c_int32), ("skip_marks", ctypes.c_int32),
-                ("always_skip_test", ctypes.c_int32)]
+                ("always_skip_test", ctypes.c_int32), ("chunks", ctypes.c_int32)]
 
 
 class IterStats(ctypes.Structure):
@@ -153,12 +154,14 @@ class LDA:
     canonical order.  ``sampler_block`` (256, 512, 1024; 0 = by occupancy)
     sets the sampler's workgroup size; ``skip_marks`` (0 auto, 1 word order,
     2 document order) how skip decisions reach the sampler; ``always_skip_test``
-    runs steps 2-3 in every iteration instead of when they pay.
+    runs steps 2-3 in every iteration instead of when they pay; ``chunks`` > 1
+    keeps the per-token arrays in pinned host memory and streams them through
+    the device in that many chunks of documents (input sorted by document).
     """
 
     def __init__(self, word, doc, V: int, K: int, alpha: float, beta: float = 0.01, seed: int = 42, *, g: int = 2,
                  region_tokens: int = 0, no_skip: bool = False, dense_cutoff: int = 0, two_branch: bool = False,
-                 sampler_block: int = 0, skip_marks: int = 0, always_skip_test: bool = False,
+                 sampler_block: int = 0, skip_marks: int = 0, always_skip_test: bool = False, chunks: int = 0,
                  torch_stream: bool = True, torch_allocator: bool = True):
         self._lib = load_library()
         self._h = ctypes.c_void_p()
@@ -175,6 +178,7 @@ class LDA:
         opts.sampler_block = sampler_block
         opts.skip_marks = skip_marks
         opts.always_skip_test = 1 if always_skip_test else 0
+        opts.chunks = chunks
         self._keep = []
         if torch_stream or torch_allocator:
             import torch

@@ -42,6 +42,7 @@ struct lda_handle {
   // out-of-core mode (lda_options.chunks > 1): the chunks, their host arrays
   // and the device slots they stream through; null when everything is resident
   std::unique_ptr<lda::ChunkMode, lda::ChunkModeDeleter> chunks;
+  int32_t chunks_wanted = 0;  // lda_options.chunks
   int64_t iteration = 0;
   bool poisoned = false;
   std::string err = "no error";
@@ -122,17 +123,32 @@ inline void dfree(lda_handle *h, T *&ptr) {
   ptr = nullptr;
 }
 
+// Stable radix sort of n (default: every token) key/value pairs on the
+// handle's stream, with temporary storage allocated for the call.
 inline lda_status sort_pairs(lda_handle *h, const uint32_t *keys_in, uint32_t *keys_out, const uint32_t *vals_in,
-                      uint32_t *vals_out, unsigned end_bit) {
+                      uint32_t *vals_out, unsigned end_bit, int64_t n = -1) {
+  if (n < 0) n = h->L.n;
   size_t bytes = 0;
-  HIP_TRY(h, sort_pairs_u32(nullptr, bytes, keys_in, keys_out, vals_in, vals_out, h->L.n, end_bit, h->stream));
+  HIP_TRY(h, sort_pairs_u32(nullptr, bytes, keys_in, keys_out, vals_in, vals_out, n, end_bit, h->stream));
   uint8_t *tmp = nullptr;
   LDA_TRY(dalloc(h, &tmp, bytes));
-  HIP_TRY(h, sort_pairs_u32(tmp, bytes, keys_in, keys_out, vals_in, vals_out, h->L.n, end_bit, h->stream));
+  HIP_TRY(h, sort_pairs_u32(tmp, bytes, keys_in, keys_out, vals_in, vals_out, n, end_bit, h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   dfree(h, tmp);
   return LDA_OK;
 }
 
+
+// Stream, workgroup sizes and grids for this device and K (lda_api.cpp).
+lda_status setup_device(lda_handle *h, const lda_options *o);
+
+// The out-of-core chunked mode (chunks.cpp); each mirrors the resident call.
+// chunked_loglik with scratch = the fixed array of lda_loglik_noalloc keeps its
+// partial sums there instead of in handle memory.
+lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc, int32_t R, int32_t n_chunks);
+lda_status chunked_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats);
+lda_status chunked_counts(lda_handle *h, lda_counts *out);
+lda_status chunked_loglik(lda_handle *h, double *llpt, void *scratch);
+lda_status chunked_set_assignments(lda_handle *h, const int32_t *z, int64_t iteration);
 
 }  // namespace lda

@@ -203,12 +203,16 @@ __global__ void k_init_topics(const uint32_t *__restrict__ wt_key, uint16_t *__r
 // iteration's skip count (the other parity's count, the previous
 // iteration's, stays for the choice of bitmap).
 __global__ void k_clear_skips(uint32_t *__restrict__ bits, uint32_t *__restrict__ doc_bits, int64_t n, int64_t n_doc,
-                              unsigned long long *__restrict__ hist, uint32_t t) {
+                              unsigned long long *__restrict__ hist, uint32_t t, int reset_count) {
   const int64_t i0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x, step = int64_t(gridDim.x) * blockDim.x;
   for (int64_t q = i0; q < n; q += step) bits[q] = 0u;
   if (doc_bits)
     for (int64_t q = i0; q < n_doc; q += step) doc_bits[q] = 0u;
-  if (i0 == 0) hist[t & 1u] = 0ull;
+  if (i0 == 0 && reset_count) hist[t & 1u] = 0ull;
+}
+
+__global__ void k_reset_counters(uint32_t *__restrict__ counters) {
+  if (threadIdx.x < kCounters) counters[threadIdx.x] = 0u;
 }
 
 // Whether iteration t carries its skip decisions in the document-ordered
@@ -220,7 +224,7 @@ __global__ void k_clear_skips(uint32_t *__restrict__ bits, uint32_t *__restrict_
 __device__ __forceinline__ bool doc_marks(const DevState &d, const Params &p, uint32_t t) {
   if (!p.doc_marks_ok || p.skip_marks == 1) return false;
   if (p.skip_marks == 2) return true;
-  return t > 0u && 5ull * d.skip_hist[(t + 1u) & 1u] > uint64_t(p.n);
+  return t > 0u && 5ull * d.skip_hist[(t + 1u) & 1u] > uint64_t(p.n_all);
 }
 
 // Whether steps 2-3 run in iteration t.  They only save work: a token they
@@ -234,7 +238,7 @@ constexpr uint32_t kProbeEvery = 8;
 __device__ __forceinline__ bool skip_test_runs(const DevState &d, const Params &p, uint32_t t) {
   if (p.no_skip) return false;
   if (p.always_skip_test || t % kProbeEvery == 0u) return true;
-  return 8ull * d.skip_hist[(t + 1u) & 1u] >= uint64_t(p.n);
+  return 8ull * d.skip_hist[(t + 1u) & 1u] >= uint64_t(p.n_all);
 }
 
 __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den, double *__restrict__ bden, int32_t K,
@@ -507,7 +511,7 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
   auto test = [&](uint32_t pp, uint32_t len, const SkipHead &h, uint32_t v) -> bool {
     const uint32_t K1 = h.k12 & 0xFFFFu, K2 = h.k12 >> 16;
     const uint32_t C1 = cmap[K1], C2 = cmap[K2];
-    const uint32_t key = KeyId ? pp : d.dt_key[pp];
+    const uint32_t key = KeyId ? p.key_base + pp : d.dt_key[pp];
     const float u = float(uniform_draw(p.seed, t, key));
     const float Mm = h.a1 * (float(C1) + p.alpha_f);
     float Sest;
@@ -2182,11 +2186,16 @@ hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s)
   return hipGetLastError();
 }
 
-hipError_t launch_clear_skips(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
+hipError_t launch_clear_skips(const DevState &d, const Params &p, uint32_t t, hipStream_t s, bool reset_count) {
   const int64_t n = skip_words(p.n);
   const int64_t blocks = std::min<int64_t>((n + kBlock - 1) / kBlock, int64_t(p.grid_docs) * 4);
   hipLaunchKernelGGL(k_clear_skips, dim3(uint32_t(std::max<int64_t>(blocks, 1))), dim3(kBlock), 0, s, d.skip_bits,
-                     d.skip_doc, n, n + 64, d.skip_hist, t);
+                     d.skip_doc, n, n + 64, d.skip_hist, t, reset_count ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_reset_counters(uint32_t *counters, hipStream_t s) {
+  hipLaunchKernelGGL(k_reset_counters, dim3(1), dim3(kWave), 0, s, counters);
   return hipGetLastError();
 }
 
@@ -2293,10 +2302,20 @@ hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStr
 }
 
 hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s) {
+  hipError_t err = launch_zero_split(d, p, s);
+  if (err == hipSuccess) err = launch_rebuild_w(d, p, s);
+  if (err == hipSuccess) err = launch_rebuild_d(d, p, s);
+  return err;
+}
+
+hipError_t launch_zero_split(const DevState &d, const Params &p, hipStream_t s) {
   const int64_t zb = std::min<int64_t>((int64_t(p.n_dense) * p.K + kBlock - 1) / kBlock + 1, 65536);
   hipLaunchKernelGGL(k_zero_split, dim3(uint32_t(zb)), dim3(kBlock), 0, s, d, p);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  return hipGetLastError();
+}
+
+hipError_t launch_rebuild_w(const DevState &d, const Params &p, hipStream_t s) {
+  hipError_t err;
   // large K: the bitmap variants, whose work follows the tokens instead of K
   const size_t nwords = size_t((p.K + 31) / 32);
   if (p.big_k) {
@@ -2310,8 +2329,11 @@ hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s) {
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(k_rebuild_w, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
   }
-  err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  return hipGetLastError();
+}
+
+hipError_t launch_rebuild_d(const DevState &d, const Params &p, hipStream_t s) {
+  hipError_t err;
   const size_t dlds = sizeof(uint32_t) * d_rebuild_lds_words(p.K) * size_t(p.doc_waves);
   err = allow_lds(k_rebuild_d, dlds);
   if (err != hipSuccess) return err;
@@ -2372,6 +2394,11 @@ hipError_t launch_loglik_noalloc(DevState d, const Params &p, void *scratch_dev,
   if (err == hipSuccess) err = launch_word_pre(d, p, s);
   if (err == hipSuccess) err = launch_loglik(d, p, s);
   return err;
+}
+
+hipError_t launch_sum_f64(const double *part, int64_t n, double *out, hipStream_t s) {
+  hipLaunchKernelGGL(k_loglik_reduce, dim3(1), dim3(kBlock), 0, s, part, n, out);
+  return hipGetLastError();
 }
 
 hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s) {

@@ -56,8 +56,60 @@ lda_status scan_tokens(const int32_t *word, const int32_t *doc, int64_t n, int32
   return LDA_OK;
 }
 
+void make_regions(const std::vector<uint32_t> &word_off, int32_t nd, int32_t R, std::vector<uint8_t> &split,
+                  std::vector<uint32_t> &region, int64_t &n_dense_regions) {
+  const int32_t np = int32_t(word_off.size()) - 1;
+  auto count = [&](uint32_t r) { return word_off[r + 1] - word_off[r]; };
+  // regions (Sec. 5.1): a dense word with c tokens becomes ceil(c/R) regions
+  // of near-equal size; a sparse word is always one region; a word without
+  // tokens has none
+  split.assign(size_t(std::max(nd, 0)), 0);
+  region.clear();
+  n_dense_regions = 0;
+  for (int32_t r = 0; r < np; r++) {
+    const uint32_t b = word_off[size_t(r)], c = count(uint32_t(r));
+    if (c == 0) continue;
+    uint64_t nreg = 1;
+    if (r < nd) nreg = (uint64_t(c) + uint64_t(R) - 1) / uint64_t(R);
+    if (r < nd && nreg > 1) split[size_t(r)] = 1;
+    for (uint64_t q = 0; q < nreg; q++) {
+      region.push_back(uint32_t(r));
+      region.push_back(b + uint32_t(uint64_t(c) * q / nreg));
+      region.push_back(b + uint32_t(uint64_t(c) * (q + 1) / nreg));
+      if (r < nd) n_dense_regions++;
+    }
+  }
+  // Hand-out order (a choice of this implementation, not the paper's): the
+  // regions of split words by the middle of their span of the word's
+  // document-sorted tokens, which tracks the document ids they touch, so the
+  // regions that run at the same time read the D rows of nearby documents and
+  // the device's last-level cache serves the repeated reads; then the
+  // unsplit words in word order (the small regions last, filling the tail).
+  const size_t nr = region.size() / 3;
+  std::vector<size_t> split_idx, rest_idx;
+  for (size_t i = 0; i < nr; ++i) {
+    const uint32_t r = region[3 * i];
+    (int32_t(r) < nd && split[r] ? split_idx : rest_idx).push_back(i);
+  }
+  // middle of region i as a fraction of its word: (b + e - 2 wb) / (2 c), compared exactly
+  auto mid_num = [&](size_t i) {
+    const uint32_t r = region[3 * i];
+    return uint64_t(region[3 * i + 1] - word_off[r]) + uint64_t(region[3 * i + 2] - word_off[r]);
+  };
+  std::stable_sort(split_idx.begin(), split_idx.end(), [&](size_t x, size_t y) {
+    const unsigned __int128 lhs = (unsigned __int128)mid_num(x) * count(region[3 * y]);
+    const unsigned __int128 rhs = (unsigned __int128)mid_num(y) * count(region[3 * x]);
+    return lhs < rhs;
+  });
+  std::vector<uint32_t> ordered;
+  ordered.reserve(region.size());
+  for (const std::vector<size_t> *part : {&split_idx, &rest_idx})
+    for (size_t i : *part) ordered.insert(ordered.end(), region.begin() + 3 * i, region.begin() + 3 * i + 3);
+  region.swap(ordered);
+}
+
 lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t R, int32_t dense_cutoff, Layout &L,
-                            std::string &msg) {
+                            std::string &msg, bool rows) {
   const int32_t V = int32_t(cnt.size());
   const int32_t M = int32_t(L.doc_off.size()) - 1;
   for (int32_t d = 0; d < M; d++) {
@@ -90,6 +142,7 @@ lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t
   L.word_off.assign(size_t(np) + 1, 0);
   for (int32_t r = 0; r < np; r++) L.word_off[size_t(r) + 1] = L.word_off[size_t(r)] + L.count[size_t(r)];
 
+  if (!rows) return LDA_OK;
   // capacities: a D row is one header slot (len << 16 | nnz) followed by at
   // most min(len, K) packed entries (Sec. 4.2), padded to the sampler's
   // chunk (multiples of 32 slots); sparse W rows = token count
@@ -108,52 +161,7 @@ lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t
   L.ws_cap.assign(size_t(ns) + 1, 0);
   for (int32_t s = 0; s < ns; s++) L.ws_cap[size_t(s) + 1] = L.ws_cap[size_t(s)] + L.count[size_t(nd + s)];
 
-  // regions (Sec. 5.1): a dense word with c tokens becomes ceil(c/R) regions
-  // of near-equal size; a sparse word is always one region
-  L.split.assign(size_t(nd), 0);
-  L.region.clear();
-  L.n_dense_regions = 0;
-  for (int32_t r = 0; r < np; r++) {
-    const uint32_t b = L.word_off[size_t(r)], c = L.count[size_t(r)];
-    uint64_t nreg = 1;
-    if (r < nd) nreg = (uint64_t(c) + uint64_t(R) - 1) / uint64_t(R);
-    if (r < nd && nreg > 1) L.split[size_t(r)] = 1;
-    for (uint64_t q = 0; q < nreg; q++) {
-      L.region.push_back(uint32_t(r));
-      L.region.push_back(b + uint32_t(uint64_t(c) * q / nreg));
-      L.region.push_back(b + uint32_t(uint64_t(c) * (q + 1) / nreg));
-      if (r < nd) L.n_dense_regions++;
-    }
-  }
-  // Hand-out order (a choice of this implementation, not the paper's): the
-  // regions of split words by the middle of their span of the word's
-  // document-sorted tokens, which tracks the document ids they touch, so the
-  // regions that run at the same time read the D rows of nearby documents and
-  // the device's last-level cache serves the repeated reads; then the
-  // unsplit words in word order (the small regions last, filling the tail).
-  {
-    const size_t nr = L.region.size() / 3;
-    std::vector<size_t> split_idx, rest_idx;
-    for (size_t i = 0; i < nr; ++i) {
-      const uint32_t r = L.region[3 * i];
-      (int32_t(r) < nd && L.split[r] ? split_idx : rest_idx).push_back(i);
-    }
-    // middle of region i as a fraction of its word: (b + e - 2 wb) / (2 c), compared exactly
-    auto mid_num = [&](size_t i) {
-      const uint32_t r = L.region[3 * i];
-      return uint64_t(L.region[3 * i + 1] - L.word_off[r]) + uint64_t(L.region[3 * i + 2] - L.word_off[r]);
-    };
-    std::stable_sort(split_idx.begin(), split_idx.end(), [&](size_t x, size_t y) {
-      const unsigned __int128 lhs = (unsigned __int128)mid_num(x) * L.count[L.region[3 * y]];
-      const unsigned __int128 rhs = (unsigned __int128)mid_num(y) * L.count[L.region[3 * x]];
-      return lhs < rhs;
-    });
-    std::vector<uint32_t> ordered;
-    ordered.reserve(L.region.size());
-    for (const std::vector<size_t> *part : {&split_idx, &rest_idx})
-      for (size_t i : *part) ordered.insert(ordered.end(), L.region.begin() + 3 * i, L.region.begin() + 3 * i + 3);
-    L.region.swap(ordered);
-  }
+  make_regions(L.word_off, nd, R, L.split, L.region, L.n_dense_regions);
   L.n_regions = int64_t(L.region.size() / 3);
   return LDA_OK;
 }

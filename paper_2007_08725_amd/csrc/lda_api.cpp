@@ -27,10 +27,12 @@ lda_status rebuild_counts(lda_handle *h) {
   return LDA_OK;
 }
 
-// Device layout (Sec. 4.2-4.3, 5.1): both token orders are built with radix
-// sorts on the GPU; only per-word and per-document counts visit the host.
-lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *word, const int32_t *doc, int32_t R,
-                         int32_t dense_cutoff) {
+}  // namespace
+
+namespace lda {
+
+// Stream, workgroup sizes and grids for this device and K (both modes).
+lda_status setup_device(lda_handle *h, const lda_options *o) {
   Layout &L = h->L;
   HIP_TRY(h, hipGetDevice(&h->device));
   int cus = 0, lds_max = 0;
@@ -66,6 +68,21 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   // the same table plus a bitmap of the touched topics and a list of them
   p.doc_waves = std::max(1, std::min(kBlock / 64, int(size_t(lds_max) / (sizeof(uint32_t) * d_rebuild_lds_words(p.K)))));
   p.grid_docs = std::max(1, cus * 8);
+  return LDA_OK;
+}
+
+}  // namespace lda
+
+namespace {
+
+// Device layout (Sec. 4.2-4.3, 5.1): both token orders are built with radix
+// sorts on the GPU; only per-word and per-document counts visit the host.
+lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *word, const int32_t *doc, int32_t R,
+                         int32_t dense_cutoff) {
+  Layout &L = h->L;
+  LDA_TRY(setup_device(h, o));
+  if (h->chunks_wanted > 1) return chunked_create(h, word, doc, R, h->chunks_wanted);
+  Params &p = h->p;
   const size_t n = size_t(L.n);
   const bool identity = L.key_identity;
   DevState &d = h->d;
@@ -225,6 +242,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
 void release(lda_handle *h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
+  h->chunks.reset();  // drains the copy streams before the device memory goes
   for (hipEvent_t ev : h->events)
     if (ev) (void)hipEventDestroy(ev);
   for (void *ptr : h->allocations) {
@@ -250,7 +268,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   if (!std::isfinite(alpha) || !(alpha > 0.0)) return fail(nullptr, LDA_E_ARG, "alpha must be finite and positive");
   if (!std::isfinite(beta) || !(beta > 0.0)) return fail(nullptr, LDA_E_ARG, "beta must be finite and positive");
   int32_t g = 2, R = kDefaultRegionTokens, no_skip = 0, dense_cutoff = 0, two_branch = 0, skip_marks = 0;
-  int32_t always_skip_test = 0;
+  int32_t always_skip_test = 0, chunks = 0;
   if (opts) {
     if (opts->g < 0 || opts->g > 3) return fail(nullptr, LDA_E_ARG, "g must be 1, 2 or 3");
     if (opts->g) g = opts->g;
@@ -270,6 +288,9 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
     if (opts->always_skip_test < 0 || opts->always_skip_test > 1)
       return fail(nullptr, LDA_E_ARG, "always_skip_test must be 0 or 1");
     always_skip_test = opts->always_skip_test;
+    if (opts->chunks < 0 || opts->chunks > LDA_MAX_CHUNKS)
+      return fail(nullptr, LDA_E_ARG, "chunks must be in [0, " + std::to_string(LDA_MAX_CHUNKS) + "]");
+    chunks = opts->chunks;
   }
   lda_handle *h = new (std::nothrow) lda_handle();
   if (!h) return fail(nullptr, LDA_E_NOMEM, "host allocation failed");
@@ -286,6 +307,11 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   h->L.K = K;
   h->L.M = M;
   h->L.key_identity = sorted;
+  if (chunks > 1 && !sorted) {
+    delete h;
+    return fail(nullptr, LDA_E_ARG, "chunks need the input sorted by document");
+  }
+  h->chunks_wanted = chunks;
   if (opts) {
     h->dev_alloc = opts->dev_alloc;
     h->dev_free = opts->dev_free;
@@ -293,6 +319,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
   }
   Params &p = h->p;
   p.n = n_tokens;
+  p.n_all = n_tokens;
   p.M = M;
   p.V = V;
   p.K = K;
@@ -324,6 +351,7 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
 lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
   LDA_TRY(check_handle(h));
   if (n_iters < 0) return fail(h, LDA_E_ARG, "n_iters must be >= 0");
+  if (h->chunks) return chunked_iterate(h, n_iters, stats);
   if (stats && h->events.empty()) {
     h->events.assign(size_t(kStatSlots) * kEventsPerIter, nullptr);
     for (auto &ev : h->events) HIP_TRY(h, hipEventCreate(&ev));
@@ -388,6 +416,7 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
 lda_status lda_get_counts(lda_handle *h, lda_counts *out) {
   LDA_TRY(check_handle(h));
   if (!out) return fail(h, LDA_E_ARG, "out is NULL");
+  if (h->chunks) return chunked_counts(h, out);
   const Layout &L = h->L;
   const size_t n = size_t(L.n);
   const int32_t K = L.K;
@@ -483,6 +512,7 @@ lda_status lda_get_counts(lda_handle *h, lda_counts *out) {
 lda_status lda_loglik(lda_handle *h, double *llpt) {
   LDA_TRY(check_handle(h));
   if (!llpt) return fail(h, LDA_E_ARG, "llpt is NULL");
+  if (h->chunks) return chunked_loglik(h, llpt, nullptr);
   DevState d = h->d;
   d.stats = h->stats_base;
   HIP_TRY(h, launch_begin_iteration(d, h->p, h->stream));
@@ -498,6 +528,7 @@ lda_status lda_loglik(lda_handle *h, double *llpt) {
 lda_status lda_loglik_noalloc(lda_handle *h, double *llpt) {
   LDA_TRY(check_handle(h));
   if (!llpt) return fail(h, LDA_E_ARG, "llpt is NULL");
+  if (h->chunks) return chunked_loglik(h, llpt, h->noalloc_scratch);
   if (h->p.n_regions > int64_t(LDA_NOALLOC_MAX_REGIONS))
     return fail(h, LDA_E_RANGE, "lda_loglik_noalloc holds partial sums for at most " +
                                     std::to_string(LDA_NOALLOC_MAX_REGIONS) + " regions; this layout has " +
@@ -516,6 +547,7 @@ lda_status lda_set_assignments(lda_handle *h, const int32_t *z, int64_t iteratio
   LDA_TRY(check_handle(h));
   if (!z) return fail(h, LDA_E_ARG, "z is NULL");
   if (iteration < 0 || iteration >= (int64_t(1) << 32)) return fail(h, LDA_E_ARG, "iteration out of range");
+  if (h->chunks) return chunked_set_assignments(h, z, iteration);
   const Layout &L = h->L;
   const size_t n = size_t(L.n);
   for (size_t i = 0; i < n; ++i)

@@ -71,8 +71,16 @@ lda_status scan_tokens(const int32_t *word, const int32_t *doc, int64_t n, int32
 // prefix, relabelled word offsets, capacities and regions.  LDA_E_RANGE for a
 // document longer than LDA_MAX_DOC_LEN.
 // dense_cutoff as in lda_options (0 = K, negative = all words dense)
+// rows = false: relabel, dense prefix and word offsets only (no D and sparse-W
+// capacities, no regions: the out-of-core chunks plan their own).
 lda_status plan_from_counts(const std::vector<uint32_t> &cnt, int32_t K, int32_t R, int32_t dense_cutoff, Layout &L,
-                            std::string &msg);
+                            std::string &msg, bool rows = true);
+// Regions of the words with offsets word_off (Sec. 5.1): words below nd are
+// cut into ceil(count / R) regions (split[word] = 1 when more than one), the
+// others form one region each, words without tokens none; split words' regions
+// first, by the middle of their span, then the rest in word order.
+void make_regions(const std::vector<uint32_t> &word_off, int32_t nd, int32_t R, std::vector<uint8_t> &split,
+                  std::vector<uint32_t> &region, int64_t &n_dense_regions);
 // All-host reference of the layout (lda_describe_layout); fills L.wt_key.
 lda_status build_layout(const int32_t *word, const int32_t *doc, int64_t n, int32_t V, int32_t K, int32_t R,
                         int32_t dense_cutoff, Layout &L, std::string &msg);
@@ -160,6 +168,7 @@ struct DevState {
 
 struct Params {
   int64_t n;
+  int64_t n_all;  // tokens of the whole corpus (n is a chunk's share in the out-of-core mode)
   int32_t M, V, K, n_present, n_dense;
   int64_t n_regions;
   double alpha, beta, vbeta;
@@ -180,6 +189,7 @@ struct Params {
   int32_t top_list;      // length of that topic list
   int32_t skip_marks;    // 0 auto, 1 word-ordered bitmap, 2 document-ordered bitmap (lda_options)
   int32_t always_skip_test;  // steps 2-3 every iteration instead of when they pay (lda_options)
+  uint32_t key_base;     // out-of-core chunks: input index of the chunk's first doc-ordered token (else 0)
   int32_t doc_marks_ok;  // the document-ordered bitmap is usable: keys are document positions, regular sampler
   uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
@@ -197,7 +207,10 @@ hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s)
 hipError_t launch_begin_iteration(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_beta_sum(const DevState &d, const Params &p, hipStream_t s);
-hipError_t launch_clear_skips(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
+// reset_count: also clear this iteration's skip count (false for the second
+// and later chunks of an out-of-core iteration, which add to it)
+hipError_t launch_clear_skips(const DevState &d, const Params &p, uint32_t t, hipStream_t s, bool reset_count = true);
+hipError_t launch_reset_counters(uint32_t *counters, hipStream_t s);
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 int sampler_block(int K, int want);
@@ -209,14 +222,24 @@ constexpr int kTiledThreads = 1024;
 // large-K LLPT kernel; the scratch slices are sized for these grids.
 inline int tiled_grid(const Params &p) { return p.grid_regions / 8 > 0 ? p.grid_regions / 8 : 1; }
 inline int loglik_grid_big_k(const Params &p) { return tiled_grid(p); }
+// The count rebuild (Sec. 4.3): launch_rebuild = launch_zero_split, then
+// launch_rebuild_w and launch_rebuild_d.
 hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_zero_split(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_rebuild_w(const DevState &d, const Params &p, hipStream_t s);
+hipError_t launch_rebuild_d(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_loglik(const DevState &d, const Params &p, hipStream_t s);
+// out[0] = sum of part[0..n) in a fixed order (one workgroup).
+hipError_t launch_sum_f64(const double *part, int64_t n, double *out, hipStream_t s);
 // Allocation-free LLPT: the layout of the fixed scratch array (counters at 0,
-// the result at kNoAllocResult, per-region partials from kNoAllocHead), its
+// the result at kNoAllocResult, out-of-core per-chunk sums at
+// kNoAllocChunkSums, per-region partials from kNoAllocHead), its
 // device address on the current device (looked up once per device), and the
 // LLPT launches on it.  hipErrorInvalidValue past LDA_NOALLOC_MAX_REGIONS.
 constexpr size_t kNoAllocResult = 256;
-constexpr size_t kNoAllocHead = 512;
+constexpr size_t kNoAllocChunkSums = 512;
+constexpr size_t kNoAllocHead = 4096;
+static_assert(kNoAllocChunkSums + sizeof(double) * LDA_MAX_CHUNKS <= kNoAllocHead, "chunk sums overlap the partials");
 static_assert(sizeof(uint32_t) * kCounters <= kNoAllocResult, "counters overlap the result");
 hipError_t noalloc_scratch_address(void **out);
 hipError_t launch_loglik_noalloc(DevState d, const Params &p, void *scratch_dev, hipStream_t s);

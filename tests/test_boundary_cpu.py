@@ -78,6 +78,17 @@ def test_create_argument_errors(lib):
         setattr(o, field, value)
         st, h = _create(lib, pw, pd, 3, 3, 4, 0.5, 0.01, ctypes.byref(o))
         assert st == lda.LDA_E_ARG, field
+    # chunks: out of range, and the out-of-core mode needs input sorted by document
+    for value in (-1, lda.MAX_CHUNKS + 1):
+        o = lda.Options()
+        o.chunks = value
+        st, h = _create(lib, pw, pd, 3, 3, 4, 0.5, 0.01, ctypes.byref(o))
+        assert st == lda.LDA_E_ARG and not h.value
+    o = lda.Options()
+    o.chunks = 2
+    d_uns = np.array([1, 0, 1], np.int32)
+    st, h = _create(lib, pw, ctypes.c_void_p(d_uns.ctypes.data), 3, 3, 4, 0.5, 0.01, ctypes.byref(o))
+    assert st == lda.LDA_E_ARG and b"sorted by document" in lib.lda_last_error(None)
     o = lda.Options()
     o.dev_alloc = lda.ALLOC_FN(lambda n, c: None)
     st, h = _create(lib, pw, pd, 3, 3, 4, 0.5, 0.01, ctypes.byref(o))
