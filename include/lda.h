@@ -178,7 +178,9 @@ lda_status lda_create(const int32_t *word, const int32_t *doc, int64_t n_tokens,
  */
 lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats);
 
-/* Copy the current assignment and count tables to caller memory (see lda_counts). */
+/* Copy the current assignment and the count tables of Sec. 2.2 to caller
+ * memory (see lda_counts): D[d][k] = tokens of document d with topic k, W[v][k]
+ * = tokens of word v with topic k, T[k] = sum_v W[v][k]. */
 lda_status lda_get_counts(lda_handle *h, lda_counts *out);
 
 /*

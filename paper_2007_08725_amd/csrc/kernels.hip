@@ -1928,7 +1928,7 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
   return v;
 }
 
-// D rebuild (Sec. 5.2): per document gather the new topics through the
+// D rebuild (Sec. 4.3): per document gather the new topics through the
 // inverted index (doc order -> word-order slot) into a per-wave LDS table of
 // 16-bit counts, marking each touched topic in a bitmap.  The row is then
 // emitted in ascending topic order: each lane expands one bitmap word into a
