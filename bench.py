@@ -85,6 +85,7 @@ def main():
     ap.add_argument("--cpu-docs", type=int, default=200000, help="documents in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dump-stats", default=None, help="write the per-iteration statistics (JSON lines) here")
+    ap.add_argument("--always-skip-test", action="store_true", help="run steps 2-3 in every iteration")
     ap.add_argument("--chunks", type=int, default=0,
                     help="out-of-core mode: per-token arrays in pinned host memory, streamed in this many chunks")
     ap.add_argument("--calib-copy", action="store_true",
@@ -107,7 +108,8 @@ def main():
     log("generated %s: N=%d docs=%d V=%d K=%d in %.1f s" % (args.workload, c.N, c.n_docs, c.V, c.K,
                                                             time.perf_counter() - t0))
     t0 = time.perf_counter()
-    m = lda.LDA(c.word, c.doc, c.V, c.K, c.alpha, c.beta, lda_synth.SAMPLER_SEED, chunks=args.chunks)
+    m = lda.LDA(c.word, c.doc, c.V, c.K, c.alpha, c.beta, lda_synth.SAMPLER_SEED, chunks=args.chunks,
+                always_skip_test=args.always_skip_test)
     torch.cuda.synchronize()
     t_create = time.perf_counter() - t0
     log("lda_create %.1f s" % t_create)

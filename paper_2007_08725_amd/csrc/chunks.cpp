@@ -32,6 +32,7 @@ struct ChunkInfo {
   uint32_t *h_wpos = nullptr;   // pinned host [ntok]
   uint16_t *h_z = nullptr;      // pinned host [ntok]
   uint32_t *doc_off = nullptr, *d_cap = nullptr, *word_off = nullptr, *region = nullptr;  // device, chunk-local
+  uint32_t *heavy_docs = nullptr;  // device: the chunk's documents longer than kHeavyDocTokens (chunk-local ids)
   uint32_t d_slots = 0;         // D-row slots of the chunk's documents
   Params p{};                   // launch parameters of the chunk
 };
@@ -98,6 +99,7 @@ DevState chunk_state(const lda_handle *h, const ChunkInfo &ci, const ChunkSlot &
   d.d_cap = ci.d_cap;
   d.word_off = ci.word_off;
   d.region = ci.region;
+  d.heavy_docs = ci.heavy_docs;
   d.dt_word = sl.dt_word;
   d.dt_wpos = sl.dt_wpos;
   d.wt_key = sl.wt_key;
@@ -259,10 +261,15 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
     LDA_TRY(dalloc(h, &ci.d_cap, dcap.size()));
     LDA_TRY(upload(h, ci.doc_off, doff));
     LDA_TRY(upload(h, ci.d_cap, dcap));
+    const std::vector<uint32_t> heavy = heavy_documents(doff.data(), ci.ndoc);
+    LDA_TRY(dalloc(h, &ci.heavy_docs, heavy.size()));
+    LDA_TRY(upload(h, ci.heavy_docs, heavy));
     ci.p = p;
+    ci.p.n_heavy = int32_t(heavy.size());
     ci.p.n = ci.ntok;
     ci.p.M = int32_t(ci.ndoc);
     ci.p.n_regions = int64_t(region.size() / 3);
+    ci.p.light_begin = light_region_start(region, K, p.big_k != 0);
     ci.p.key_base = ci.tok0;
     ci.p.xcd_doc[0] = 0;
     for (int x = 1; x < kXcds; ++x) {
@@ -338,7 +345,7 @@ lda_status chunked_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats
         LDA_TRY(prepare_chunk(h, ci, dc, h->stream));
         HIP_TRY(h, launch_clear_skips(dc, ci.p, t, h->stream, c == 0));
         if (!p.no_skip) HIP_TRY(h, launch_doc_pass(dc, ci.p, t, h->stream));
-        HIP_TRY(h, launch_sampler(dc, ci.p, t, h->stream));
+        LDA_TRY(run_sampler(h, dc, ci.p, t));
         DevState dw = dc;
         dw.w_dense = cm.w_next;
         dw.T = cm.t_next;

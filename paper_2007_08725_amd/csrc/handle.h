@@ -39,6 +39,9 @@ struct lda_handle {
   unsigned long long *stats_base = nullptr;  // [kStatSlots * kStatsPerIter]
   std::vector<hipEvent_t> events;            // [kStatSlots * kEventsPerIter]
   void *noalloc_scratch = nullptr;           // this device's fixed LLPT scratch (lda_loglik_noalloc)
+  // the light-word sampler runs beside the main sampler on a second stream
+  hipStream_t side = nullptr;
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   // out-of-core mode (lda_options.chunks > 1): the chunks, their host arrays
   // and the device slots they stream through; null when everything is resident
   std::unique_ptr<lda::ChunkMode, lda::ChunkModeDeleter> chunks;
@@ -138,6 +141,30 @@ inline lda_status sort_pairs(lda_handle *h, const uint32_t *keys_in, uint32_t *k
   return LDA_OK;
 }
 
+
+// The documents of doc_off (M + 1 offsets) longer than kHeavyDocTokens.
+inline std::vector<uint32_t> heavy_documents(const uint32_t *doc_off, uint32_t M) {
+  std::vector<uint32_t> out;
+  for (uint32_t q = 0; q < M; ++q)
+    if (doc_off[q + 1] - doc_off[q] > kHeavyDocTokens) out.push_back(q);
+  return out;
+}
+
+// Steps 4-6 of one iteration on h->stream: the light regions (one wave each)
+// on the side stream, forked after the work queued so far and joined before
+// whatever is queued next, beside the main sampler.
+inline lda_status run_sampler(lda_handle *h, const DevState &d, const Params &p, uint32_t t) {
+  const bool light = p.light_begin < p.n_regions;
+  if (light) {
+    HIP_TRY(h, hipEventRecord(h->fork_ev, h->stream));
+    HIP_TRY(h, hipStreamWaitEvent(h->side, h->fork_ev, 0));
+    HIP_TRY(h, launch_sampler_light(d, p, t, h->side));
+    HIP_TRY(h, hipEventRecord(h->join_ev, h->side));
+  }
+  HIP_TRY(h, launch_sampler(d, p, t, h->stream));
+  if (light) HIP_TRY(h, hipStreamWaitEvent(h->stream, h->join_ev, 0));
+  return LDA_OK;
+}
 
 // Stream, workgroup sizes and grids for this device and K (lda_api.cpp).
 lda_status setup_device(lda_handle *h, const lda_options *o);

@@ -484,6 +484,59 @@ __device__ __forceinline__ SkipHead skip_head(const SkipRec *__restrict__ r) {
 
 constexpr int kDocAhead = 2;  // chunks of 64 tokens per document loaded one document ahead
 
+// Documents longer than this are walked by a whole workgroup in the doc pass
+// and the D rebuild (the skew-aware mapping of Sec. 5.1: heavy units to
+// workgroups, light ones to waves); the per-wave kernels skip them.
+constexpr uint32_t kHeavyDoc = kHeavyDocTokens;
+
+// Step 3 for token pp of a document of length len, in single precision with a
+// relative margin of 2^-15, far above the fp32 rounding of these few
+// operations (a few 2^-24): a token is skipped only if u*(M + S_est + Q') < M
+// holds exactly, so its draw is K1 (S' <= S_est, Eq. 8-9).  cmap is the
+// document's topic -> count table.
+template <bool KeyId>
+__device__ __forceinline__ bool skip_test(const DevState &d, const Params &p, uint32_t t, const uint16_t *cmap,
+                                          uint32_t pp, uint32_t len, const SkipHead &h, uint32_t v) {
+  const uint32_t K1 = h.k12 & 0xFFFFu, K2 = h.k12 >> 16;
+  const uint32_t C1 = cmap[K1], C2 = cmap[K2];
+  const uint32_t key = KeyId ? p.key_base + pp : d.dt_key[pp];
+  const float u = float(uniform_draw(p.seed, t, key));
+  const float Mm = h.a1 * (float(C1) + p.alpha_f);
+  float Sest;
+  if (p.g == 1) {
+    Sest = h.a2 * float(len - C1);
+  } else if (p.g == 2) {
+    Sest = h.a2 * float(C2) + h.a3 * float(len - C1 - C2);
+  } else {
+    const SkipRec &r = d.wskip[v];
+    const uint32_t C3 = r.k3 < uint32_t(p.K) ? uint32_t(cmap[r.k3]) : 0u;
+    Sest = h.a2 * float(C2) + h.a3 * float(C3) + r.a4 * float(len - C1 - C2 - C3);
+  }
+  return !p.no_skip && (u * ((Mm + Sest) + h.qp) < Mm * (1.0f - 0x1p-15f));
+}
+
+// A skipped token's decision goes to the sampler either as a bit at its
+// word-order slot (one scattered write per skipped token) or, in the
+// document-ordered bitmap, as a bit at its document position: a chunk's 64
+// bits (lanes = positions p0 + lane) from a ballot, in at most three words,
+// whose neighbours other waves may set too.
+__device__ __forceinline__ void mark_slot(const DevState &d, uint32_t slot) {
+  atomicOr(&d.skip_bits[slot >> 5], 1u << (slot & 31u));
+}
+__device__ __forceinline__ void mark_chunk(const DevState &d, unsigned long long m, uint32_t p0, int lane) {
+  if (m == 0ull) return;
+  const uint32_t sh = p0 & 31u;
+  const uint32_t v0 = uint32_t(m << sh);
+  const uint32_t v1 = sh ? uint32_t(m >> (32u - sh)) : uint32_t(m >> 32);
+  const uint32_t v2 = sh ? uint32_t(m >> (64u - sh)) : 0u;
+  const uint32_t v = lane == 0 ? v0 : lane == 1 ? v1 : v2;
+  if (lane < 3 && v != 0u) atomicOr(&d.skip_doc[(p0 >> 5) + uint32_t(lane)], v);
+}
+
+template <bool KeyId>
+__device__ void heavy_doc_pass(const DevState &d, const Params &p, uint32_t t, uint16_t *__restrict__ cmap,
+                               bool by_doc, unsigned long long &nskip);
+
 // Steps 2-3 per document (Sec. 3.3): the D row spread into a per-wave
 // topic -> count table in LDS, then for every token C1 and C2 by lookup, u,
 // M, S_est and the skip test.  A skipped token's bit is set in the
@@ -501,46 +554,13 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
   uint16_t *cmap = cmap_all + size_t(wave) * size_t(K);
   for (int k = lane; k < K; k += kWave) cmap[k] = 0;
   unsigned long long nskip = 0;
+  const bool by_doc = doc_marks(d, p, t);
+  // the heavy documents first, each by the whole workgroup (wave 0's table shared)
+  if (p.n_heavy) heavy_doc_pass<KeyId>(d, p, t, cmap_all, by_doc, nskip);
   const uint32_t M = uint32_t(p.M);
   const uint32_t last = uint32_t(p.n - 1);
-  // Step 3 for token pp of a document of length len, in single precision
-  // with a relative margin of 2^-15, far above the fp32 rounding of these
-  // few operations (a few 2^-24): a token is skipped only if
-  // u*(M + S_est + Q') < M holds exactly, so its draw is K1 (S' <= S_est,
-  // Eq. 8-9).
   auto test = [&](uint32_t pp, uint32_t len, const SkipHead &h, uint32_t v) -> bool {
-    const uint32_t K1 = h.k12 & 0xFFFFu, K2 = h.k12 >> 16;
-    const uint32_t C1 = cmap[K1], C2 = cmap[K2];
-    const uint32_t key = KeyId ? p.key_base + pp : d.dt_key[pp];
-    const float u = float(uniform_draw(p.seed, t, key));
-    const float Mm = h.a1 * (float(C1) + p.alpha_f);
-    float Sest;
-    if (p.g == 1) {
-      Sest = h.a2 * float(len - C1);
-    } else if (p.g == 2) {
-      Sest = h.a2 * float(C2) + h.a3 * float(len - C1 - C2);
-    } else {
-      const SkipRec &r = d.wskip[v];
-      const uint32_t C3 = r.k3 < uint32_t(K) ? uint32_t(cmap[r.k3]) : 0u;
-      Sest = h.a2 * float(C2) + h.a3 * float(C3) + r.a4 * float(len - C1 - C2 - C3);
-    }
-    return !p.no_skip && (u * ((Mm + Sest) + h.qp) < Mm * (1.0f - 0x1p-15f));
-  };
-  // A skipped token's decision goes to the sampler either as a bit at its
-  // word-order slot (one scattered write per skipped token) or, in the
-  // document-ordered bitmap, as a bit at its document position: the chunk's
-  // 64 bits from a ballot, in at most three words, whose neighbours other
-  // waves may set too.
-  const bool by_doc = doc_marks(d, p, t);
-  auto mark = [&](uint32_t slot) { atomicOr(&d.skip_bits[slot >> 5], 1u << (slot & 31u)); };
-  auto mark_chunk = [&](unsigned long long m, uint32_t p0) {  // m: lanes (positions p0 + lane) skipped
-    if (m == 0ull) return;
-    const uint32_t sh = p0 & 31u;
-    const uint32_t v0 = uint32_t(m << sh);
-    const uint32_t v1 = sh ? uint32_t(m >> (32u - sh)) : uint32_t(m >> 32);
-    const uint32_t v2 = sh ? uint32_t(m >> (64u - sh)) : 0u;
-    const uint32_t v = lane == 0 ? v0 : lane == 1 ? v1 : v2;
-    if (lane < 3 && v != 0u) atomicOr(&d.skip_doc[(p0 >> 5) + uint32_t(lane)], v);
+    return skip_test<KeyId>(d, p, t, cmap, pp, len, h, v);
   };
   for (;;) {
     uint32_t d0 = 0;
@@ -598,6 +618,7 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
       rows_of(i + 1, rowA);
       words_of(i + 2, wB);
       heads_of(i + 1, wA, hA);
+      if (len > kHeavyDoc) continue;  // a workgroup's document (heavy_doc_pass)
       const uint32_t *row = d.d_ent + cap + 1;  // entries; slot 0 is the header
       const uint32_t nnz = uint32_t(__builtin_amdgcn_readfirstlane(int(rowv[0]))) & 0xFFFFu;
       // spread the row into the topic -> count table
@@ -616,8 +637,8 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
         const uint32_t pp = b + uint32_t(c * kWave + lane);
         const bool skip = pp < e && test(pp, len, hv[c], wv[c]);
         nskip += skip ? 1ull : 0ull;
-        if (by_doc) mark_chunk(__ballot(skip), b + uint32_t(c * kWave));
-        else if (skip) mark(d.dt_wpos[pp]);
+        if (by_doc) mark_chunk(d, __ballot(skip), b + uint32_t(c * kWave), lane);
+        else if (skip) mark_slot(d, d.dt_wpos[pp]);
       }
       // the rest of a long document, two chunks per step
       for (uint32_t p0 = b + uint32_t(kDocAhead * kWave); p0 < e; p0 += 2u * kWave) {
@@ -632,8 +653,8 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
           const uint32_t pp = p0 + uint32_t(c * kWave + lane);
           const bool skip = pp < e && test(pp, len, h[c], v[c]);
           nskip += skip ? 1ull : 0ull;
-          if (by_doc) mark_chunk(__ballot(skip), p0 + uint32_t(c * kWave));
-          else if (skip) mark(d.dt_wpos[pp]);
+          if (by_doc) mark_chunk(d, __ballot(skip), p0 + uint32_t(c * kWave), lane);
+          else if (skip) mark_slot(d, d.dt_wpos[pp]);
         }
       }
       __builtin_amdgcn_wave_barrier();
@@ -651,6 +672,48 @@ __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint3
     atomicAdd(&stats[ST_SKIP3], nskip);
     atomicAdd(&d.skip_hist[t & 1u], nskip);
   }
+}
+
+// Steps 2-3 for the heavy documents (longer than kHeavyDoc), one workgroup
+// per document, taken from a list (d.heavy_docs) through one atomic counter
+// before the workgroup's waves turn to the light documents: the D row spread
+// into a topic -> count table shared by the workgroup (cmap, left clear),
+// then each wave tests chunks of 64 consecutive tokens.
+template <bool KeyId>
+__device__ void heavy_doc_pass(const DevState &d, const Params &p, uint32_t t, uint16_t *__restrict__ cmap,
+                               bool by_doc, unsigned long long &nskip) {
+  __shared__ uint32_t s_next;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave, nthr = int(blockDim.x);
+  for (;;) {
+    __syncthreads();  // the table is clear, s_next is free
+    if (tid == 0) s_next = atomicAdd(&d.counters[CNT_HEAVY_PASS], 1u);
+    __syncthreads();
+    const uint32_t h = s_next;
+    if (h >= uint32_t(p.n_heavy)) break;
+    const uint32_t dd = d.heavy_docs[h];
+    const uint32_t b = d.doc_off[dd], e = d.doc_off[dd + 1], len = e - b;
+    const uint32_t *row = d.d_ent + d.d_cap[dd];  // header, then the entries
+    const uint32_t nnz = row[0] & 0xFFFFu;
+    for (uint32_t q = uint32_t(tid); q < nnz; q += uint32_t(nthr)) {
+      const uint32_t ent = row[1u + q];
+      cmap[ent >> 16] = uint16_t(ent & 0xFFFFu);
+    }
+    __syncthreads();
+    for (uint32_t p0 = b + uint32_t(wave * kWave); p0 < e; p0 += uint32_t(nthr)) {
+      const uint32_t pp = p0 + uint32_t(lane);
+      bool skip = false;
+      if (pp < e) {
+        const uint32_t v = d.dt_word[pp];
+        skip = skip_test<KeyId>(d, p, t, cmap, pp, len, skip_head(d.wskip + v), v);
+      }
+      nskip += skip ? 1ull : 0ull;
+      if (by_doc) mark_chunk(d, __ballot(skip), p0, lane);
+      else if (skip) mark_slot(d, d.dt_wpos[pp]);
+    }
+    __syncthreads();
+    for (uint32_t q = uint32_t(tid); q < nnz; q += uint32_t(nthr)) cmap[row[1u + q] >> 16] = 0;
+  }
+  __syncthreads();  // wave 0's table is clear again
 }
 
 // Steps 4-6 for the tokens of one region that step 3 left to draw; the W^ row of the word
@@ -1201,7 +1264,11 @@ __device__ void draw_batch_small(bool und, uint32_t nnz, const BatchLds &bt, con
 // The sampler for workgroups of NB threads (NB / 64 waves); every wave works
 // on its own batches, so NB only changes how many waves share a region's W^
 // row in LDS (larger workgroups for large K, where LDS bounds the residency).
-template <int NB>
+// Light: the workgroup is one wave and takes the light regions (the suffix
+// [p.light_begin, n_regions) of the region table: words with at most
+// kLightTokens tokens, one batch each) from their own counter; otherwise the
+// regions before p.light_begin.
+template <int NB, bool Light>
 __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, unsigned long long *__restrict__ stats) {
   extern __shared__ double lds[];
   const int K = p.K;
@@ -1235,8 +1302,9 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
 
   for (;;) {
     if (tid == 0) {
-      const uint32_t r = atomicAdd(&d.counters[CNT_SAMPLER], 1u);
-      s_reg[3] = int64_t(r) < p.n_regions ? 1u : 0u;
+      const int64_t r = Light ? p.light_begin + int64_t(atomicAdd(&d.counters[CNT_LIGHT], 1u))
+                              : int64_t(atomicAdd(&d.counters[CNT_SAMPLER], 1u));
+      s_reg[3] = r < (Light ? p.n_regions : p.light_begin) ? 1u : 0u;
       if (s_reg[3]) {
         s_reg[0] = d.region[3 * size_t(r)];
         s_reg[1] = d.region[3 * size_t(r) + 1];
@@ -1353,15 +1421,22 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
 
 __global__ __launch_bounds__(256, 7) void k_sampler(DevState d, Params p, uint32_t t,
                                                  unsigned long long *__restrict__ stats) {
-  sampler_body<256>(d, p, t, stats);
+  sampler_body<256, false>(d, p, t, stats);
 }
 __global__ __launch_bounds__(512, 4) void k_sampler_512(DevState d, Params p, uint32_t t,
                                                      unsigned long long *__restrict__ stats) {
-  sampler_body<512>(d, p, t, stats);
+  sampler_body<512, false>(d, p, t, stats);
 }
 __global__ __launch_bounds__(1024, 4) void k_sampler_1024(DevState d, Params p, uint32_t t,
                                                        unsigned long long *__restrict__ stats) {
-  sampler_body<1024>(d, p, t, stats);
+  sampler_body<1024, false>(d, p, t, stats);
+}
+// The light regions, one wave each (Sec. 5.1: light units to wavefronts): a
+// word of at most kLightTokens tokens stages its W^' row and Q' prefix with
+// one wave and wave-local barriers instead of tying up a whole workgroup.
+__global__ __launch_bounds__(64) void k_sampler_light(DevState d, Params p, uint32_t t,
+                                                      unsigned long long *__restrict__ stats) {
+  sampler_body<64, true>(d, p, t, stats);
 }
 
 // ---------------------------------------------------------- large K ----
@@ -1928,6 +2003,116 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
   return v;
 }
 
+// The D row of one document from its topic histogram (16-bit counts, two
+// per word of hist) and the bitmap of its topics, by one wave: 64 bitmap
+// words (2048 topics) per step, one per lane, each lane listing its word's
+// topics at its prefix-sum offset, then one lane per listed topic writing the
+// packed entry (topic << 16 | count) in ascending topic order.  The two
+// topics of a count word share a bitmap word, so both are listed in the same
+// step.  The table and the bitmap are left clear; out points at the row's
+// first entry, the header (len << 16 | nnz) goes before it and the padding
+// entries (topic K, count 0) after the entries.
+__device__ __forceinline__ void emit_row(uint32_t *__restrict__ hist, uint32_t *__restrict__ bits, uint16_t *__restrict__ list, int nw,
+                         int K, uint32_t *__restrict__ out, uint32_t len, int lane) {
+  uint32_t base = 0;
+  for (int q0 = 0; q0 < nw; q0 += kWave) {
+    const int q = q0 + lane;
+    uint32_t m = 0;
+    if (q < nw) {
+      m = bits[q];
+      bits[q] = 0u;
+    }
+    const uint32_t cnt = uint32_t(__popc(m));
+    const uint32_t incl = wave_incl_scan_u32(cnt, lane);
+    const uint32_t n = __builtin_amdgcn_readlane(incl, kWave - 1);
+    if (n == 0u) continue;
+    uint32_t o = incl - cnt;
+    while (m) {
+      const uint32_t bit = uint32_t(__ffs(m) - 1);
+      m &= m - 1u;
+      list[o++] = uint16_t(uint32_t(q) * 32u + bit);
+    }
+    __threadfence_block();
+    for (uint32_t j = uint32_t(lane); j < n; j += kWave) {
+      const uint32_t z = list[j];
+      const uint32_t zn = j + 1u < n ? uint32_t(list[j + 1u]) : 0xFFFFFFFFu;
+      const uint32_t w = hist[z >> 1];
+      out[base + j] = (z << 16) | ((z & 1u) ? (w >> 16) : (w & 0xFFFFu));
+      // clear a count word after its last listed topic has been read
+      if ((z & 1u) || zn != z + 1u) hist[z >> 1] = 0u;
+    }
+    __threadfence_block();
+    base += n;
+  }
+  for (uint32_t q = base + uint32_t(lane); q + 1u < d_row_slots(base); q += kWave) out[q] = uint32_t(K) << 16;
+  if (lane == 0) out[-1] = (len << 16) | base;
+  __threadfence_block();
+}
+
+// The D rows of the heavy documents (longer than kHeavyDoc), one workgroup
+// per document, before the workgroup's waves turn to the light documents.
+// Each wave gathers topics of its share of the tokens through the inverted
+// index into its own histogram and bitmap (so that LDS atomics contend only
+// inside a wave), the tables are added into wave 0's (two 16-bit counts per
+// word: a document's counts stay below 2^16, so the halves never carry), and
+// wave 0 emits the row.  Every table is left clear.
+__device__ void heavy_rebuild_d(const DevState &d, const Params &p, uint32_t *__restrict__ lds, uint32_t &bad) {
+  __shared__ uint32_t s_next;
+  const int K = p.K, half = (K + 1) / 2, nw = (K + 31) / 32;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), nthr = int(blockDim.x), waves = nthr / kWave;
+  const size_t words = d_rebuild_lds_words(K);
+  uint32_t *hist = lds + size_t(tid / kWave) * words;
+  uint32_t *bits = hist + half;
+  for (;;) {
+    __syncthreads();  // the tables are clear, s_next is free
+    if (tid == 0) s_next = atomicAdd(&d.counters[CNT_HEAVY_REBUILD], 1u);
+    __syncthreads();
+    const uint32_t h = s_next;
+    if (h >= uint32_t(p.n_heavy)) break;
+    const uint32_t dd = d.heavy_docs[h];
+    const uint32_t b = d.doc_off[dd], e = d.doc_off[dd + 1];
+    for (uint32_t p0 = b + uint32_t(tid); p0 < e; p0 += uint32_t(4 * nthr)) {
+      uint32_t zz[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t pp = p0 + uint32_t(c * nthr);
+        zz[c] = pp < e ? d.dt_wpos[pp] : 0u;
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (p0 + uint32_t(c * nthr) < e) zz[c] = d.z_w[zz[c]];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        if (p0 + uint32_t(c * nthr) < e) {
+          const uint32_t z = zz[c];
+          if (z < uint32_t(K)) {
+            atomicAdd(&hist[z >> 1], (z & 1u) ? 0x10000u : 1u);
+            atomicOr(&bits[z >> 5], 1u << (z & 31u));
+          } else {
+            bad++;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    // the other waves' tables added into wave 0's, and cleared
+    for (int q = tid; q < half + nw; q += nthr) {
+      uint32_t acc = lds[q];
+      for (int w = 1; w < waves; ++w) {
+        uint32_t *src = lds + size_t(w) * words + q;
+        acc = q < half ? acc + *src : acc | *src;
+        *src = 0u;
+      }
+      lds[q] = acc;
+    }
+    __syncthreads();
+    if (tid < kWave)
+      emit_row(lds, lds + half, reinterpret_cast<uint16_t *>(lds + half + nw), nw, K, d.d_ent + d.d_cap[dd] + 1u,
+               e - b, lane);
+  }
+  __syncthreads();  // every table is clear again
+}
+
 // D rebuild (Sec. 4.3): per document gather the new topics through the
 // inverted index (doc order -> word-order slot) into a per-wave LDS table of
 // 16-bit counts, marking each touched topic in a bitmap.  The row is then
@@ -1946,15 +2131,30 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
   for (int q = lane; q < half; q += kWave) hist[q] = 0u;
   for (int q = lane; q < nw; q += kWave) bits[q] = 0u;
   uint32_t bad = 0;
+  // the heavy documents first, each by the whole workgroup (wave 0's tables shared)
+  if (p.n_heavy)
+    heavy_rebuild_d(d, p, ldsu, bad);
   int part = 0;
   for (;;) {
     uint32_t d0 = 0, d1 = 0;
     if (!next_docs(d.counters + CNT_REBUILD_D, p, part, lane, d0, d1)) break;
-    const int nd = int(d1 - d0);
+    const int nb = int(d1 - d0);
     // the batch's document offsets and D-row offsets, one per lane (loaded
     // here so that no later wait for them also waits for the prefetches)
-    const uint32_t offv = lane <= nd ? d.doc_off[d0 + uint32_t(lane)] : 0u;
-    const uint32_t capv = lane < nd ? d.d_cap[d0 + uint32_t(lane)] : 0u;
+    const uint32_t b_all = lane <= nb ? d.doc_off[d0 + uint32_t(lane)] : 0u;
+    const uint32_t cap_all = lane < nb ? d.d_cap[d0 + uint32_t(lane)] : 0u;
+    const uint32_t e_all = uint32_t(__shfl_down(int(b_all), 1, kWave));
+    // the batch's light documents moved to the first lanes (a heavy one is a
+    // workgroup's, heavy_rebuild_d), so that the loop below has no branch
+    // around them: lane j holds begin, end and D-row offset of light document j
+    const bool light = lane < nb && e_all - b_all <= kHeavyDoc;
+    const unsigned long long lm = __ballot(light);
+    const int nd = __popcll(lm);
+    const uint32_t below = __builtin_amdgcn_mbcnt_hi(uint32_t(lm >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(lm), 0u));
+    const uint32_t target = light ? below : uint32_t(nd) + (uint32_t(lane) - below);  // distinct lanes
+    const uint32_t bv = uint32_t(__builtin_amdgcn_ds_permute(int(target * 4u), int(b_all)));
+    const uint32_t ev = uint32_t(__builtin_amdgcn_ds_permute(int(target * 4u), int(e_all)));
+    const uint32_t capv = uint32_t(__builtin_amdgcn_ds_permute(int(target * 4u), int(cap_all)));
     // pipeline over the first kPre*64 tokens of each document: the
     // word-order slots of document i+3 and the topics of document i+2 are
     // loaded while document i is processed.  Every load is issued (slot
@@ -1963,12 +2163,12 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
     // drain the pipeline.
     const uint32_t last = uint32_t(p.n - 1);
     auto slots_of = [&](int doc, uint32_t (&w)[kPre]) {
-      const uint32_t bn = __builtin_amdgcn_readlane(offv, doc);
+      const uint32_t bn = __builtin_amdgcn_readlane(bv, doc);
 #pragma unroll
       for (int c = 0; c < kPre; ++c) w[c] = d.dt_wpos[min(bn + uint32_t(c * kWave + lane), last)];
     };
     auto topics_of = [&](int doc, const uint32_t (&w)[kPre], uint32_t (&z)[kPre]) {
-      const uint32_t bn = __builtin_amdgcn_readlane(offv, doc), en = __builtin_amdgcn_readlane(offv, doc + 1);
+      const uint32_t bn = __builtin_amdgcn_readlane(bv, doc), en = __builtin_amdgcn_readlane(ev, doc);
 #pragma unroll
       for (int c = 0; c < kPre; ++c) z[c] = d.z_w[bn + uint32_t(c * kWave + lane) < en ? w[c] : 0u];
     };
@@ -1979,7 +2179,7 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
     topics_of(1, wD, zB);
     slots_of(2, wC);
     for (int i = 0; i < nd; ++i) {
-      const uint32_t b = __builtin_amdgcn_readlane(offv, i), e = __builtin_amdgcn_readlane(offv, i + 1);
+      const uint32_t b = __builtin_amdgcn_readlane(bv, i), e = __builtin_amdgcn_readlane(ev, i);
       uint32_t zv[kPre];
 #pragma unroll
       for (int c = 0; c < kPre; ++c) {
@@ -2032,43 +2232,7 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
       __threadfence_block();
       // (readlane returns a signed int: the offset is taken back to unsigned,
       // since D has more than 2^31 slots on the largest corpora)
-      uint32_t *out = d.d_ent + uint32_t(__builtin_amdgcn_readlane(capv, i)) + 1u;
-      uint32_t base = 0;
-      // 64 bitmap words (2048 topics) per step, one per lane; the two
-      // topics of a count word share a bitmap word, so both are listed in
-      // the same step
-      for (int q0 = 0; q0 < nw; q0 += kWave) {
-        const int q = q0 + lane;
-        uint32_t m = 0;
-        if (q < nw) {
-          m = bits[q];
-          bits[q] = 0u;
-        }
-        const uint32_t cnt = uint32_t(__popc(m));
-        const uint32_t incl = wave_incl_scan_u32(cnt, lane);
-        const uint32_t n = __builtin_amdgcn_readlane(incl, kWave - 1);
-        if (n == 0u) continue;
-        uint32_t o = incl - cnt;
-        while (m) {
-          const uint32_t bit = uint32_t(__ffs(m) - 1);
-          m &= m - 1u;
-          list[o++] = uint16_t(uint32_t(q) * 32u + bit);
-        }
-        __threadfence_block();
-        for (uint32_t j = uint32_t(lane); j < n; j += kWave) {
-          const uint32_t z = list[j];
-          const uint32_t zn = j + 1u < n ? uint32_t(list[j + 1u]) : 0xFFFFFFFFu;
-          const uint32_t w = hist[z >> 1];
-          out[base + j] = (z << 16) | ((z & 1u) ? (w >> 16) : (w & 0xFFFFu));
-          // clear a count word after its last listed topic has been read
-          if ((z & 1u) || zn != z + 1u) hist[z >> 1] = 0u;
-        }
-        __threadfence_block();
-        base += n;
-      }
-      for (uint32_t q = base + lane; q + 1u < d_row_slots(base); q += kWave) out[q] = uint32_t(K) << 16;
-      if (lane == 0) out[-1] = ((e - b) << 16) | base;
-      __threadfence_block();
+      emit_row(hist, bits, list, nw, K, d.d_ent + uint32_t(__builtin_amdgcn_readlane(capv, i)) + 1u, e - b, lane);
     }
   }
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
@@ -2285,6 +2449,7 @@ hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStr
   const size_t lds = sampler_lds_bytes(p.K, nb);
   const uint32_t grid = uint32_t(std::max<int64_t>(1, int64_t(p.grid_regions) * kBlock / nb));
   hipError_t err;
+  if (p.light_begin == 0) return hipSuccess;  // every region is light
   if (nb == 1024) {
     err = allow_lds(k_sampler_1024, lds);
     if (err != hipSuccess) return err;
@@ -2298,6 +2463,17 @@ hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStr
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(k_sampler, dim3(grid), dim3(256), lds, s, d, p, t, d.stats);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_sampler_light(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
+  if (p.light_begin >= p.n_regions) return hipSuccess;
+  const size_t lds = sampler_lds_bytes(p.K, kWave);
+  hipError_t err = allow_lds(k_sampler_light, lds);
+  if (err != hipSuccess) return err;
+  const int64_t n_light = p.n_regions - p.light_begin;
+  const uint32_t grid = uint32_t(std::min<int64_t>(n_light, int64_t(p.grid_regions) * 2));
+  hipLaunchKernelGGL(k_sampler_light, dim3(grid), dim3(kWave), lds, s, d, p, t, d.stats);
   return hipGetLastError();
 }
 

@@ -44,6 +44,9 @@ lda_status setup_device(lda_handle *h, const lda_options *o) {
     HIP_TRY(h, hipStreamCreateWithFlags(&h->stream, hipStreamNonBlocking));
     h->own_stream = true;
   }
+  HIP_TRY(h, hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking));
+  HIP_TRY(h, hipEventCreateWithFlags(&h->fork_ev, hipEventDisableTiming));
+  HIP_TRY(h, hipEventCreateWithFlags(&h->join_ev, hipEventDisableTiming));
   // the fixed scratch of the allocation-free LLPT, looked up once per device
   HIP_TRY(h, noalloc_scratch_address(&h->noalloc_scratch));
   Params &p = h->p;
@@ -143,6 +146,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   p.n_present = L.n_present;
   p.n_dense = L.n_dense;
   p.n_regions = L.n_regions;
+  p.light_begin = light_region_start(L.region, L.K, p.big_k != 0);
 
   // 5. word order in relabelled ids and the links between the two orders
   int32_t *relabel_d = nullptr;
@@ -169,6 +173,13 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
 
   // 6. count tables and scheduler state
   LDA_TRY(dalloc(h, &d.region, L.region.size()));
+  {
+    // heavy documents: one workgroup each in the doc pass and the D rebuild (Sec. 5.1)
+    const std::vector<uint32_t> heavy = heavy_documents(L.doc_off.data(), uint32_t(L.M));
+    p.n_heavy = int32_t(heavy.size());
+    LDA_TRY(dalloc(h, &d.heavy_docs, heavy.size()));
+    LDA_TRY(upload(h, d.heavy_docs, heavy));
+  }
   LDA_TRY(dalloc(h, &d.split, L.split.size()));
   LDA_TRY(dalloc(h, &d.z_w, n));
   LDA_TRY(dalloc(h, &d.skip_bits, skip_words(int64_t(n))));
@@ -243,6 +254,10 @@ void release(lda_handle *h) {
   if (!h) return;
   if (h->stream) (void)hipStreamSynchronize(h->stream);
   h->chunks.reset();  // drains the copy streams before the device memory goes
+  if (h->side) (void)hipStreamSynchronize(h->side);
+  for (hipEvent_t ev : {h->fork_ev, h->join_ev})
+    if (ev) (void)hipEventDestroy(ev);
+  if (h->side) (void)hipStreamDestroy(h->side);
   for (hipEvent_t ev : h->events)
     if (ev) (void)hipEventDestroy(ev);
   for (void *ptr : h->allocations) {
@@ -370,7 +385,7 @@ lda_status lda_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats) {
       if (ev) HIP_TRY(h, hipEventRecord(ev[1], h->stream));
       if (!h->p.no_skip) HIP_TRY(h, launch_doc_pass(d, h->p, t, h->stream));  // steps 2-3 only decide skips
       if (ev) HIP_TRY(h, hipEventRecord(ev[2], h->stream));
-      HIP_TRY(h, launch_sampler(d, h->p, t, h->stream));
+      LDA_TRY(run_sampler(h, d, h->p, t));
       if (ev) HIP_TRY(h, hipEventRecord(ev[3], h->stream));
       HIP_TRY(h, launch_rebuild(d, h->p, h->stream));
       if (ev) HIP_TRY(h, hipEventRecord(ev[4], h->stream));

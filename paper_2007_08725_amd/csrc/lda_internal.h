@@ -37,6 +37,9 @@ __host__ __device__ inline size_t d_rebuild_lds_words(int K) {
 constexpr int kDefaultRegionTokens = 10000;  // Sec. 5.1
 constexpr int kBlock = 256;                  // threads per workgroup (4 wave64)
 constexpr int kXcds = 8;                     // accelerator dies (XCDs), each with its own L2
+// Documents longer than this many tokens are heavy: the doc pass and the D
+// rebuild give each a whole workgroup instead of a wave (Sec. 5.1).
+constexpr uint32_t kHeavyDocTokens = 4096;
 
 // ----------------------------------------------------------------- layout --
 // Host-side token layout (Sec. 4.2-4.3 and 5.1).
@@ -132,6 +135,7 @@ struct DevState {
   // layout
   uint32_t *doc_off, *dt_word, *dt_key, *dt_wpos, *word_off, *wt_rowoff, *wt_key;
   uint32_t *region;   // 3 per region
+  uint32_t *heavy_docs;  // documents longer than kHeavyDoc tokens (one workgroup each in the doc kernels)
   uint8_t *split;     // per dense word
   // assignment, word order
   uint16_t *z_w;
@@ -190,13 +194,16 @@ struct Params {
   int32_t skip_marks;    // 0 auto, 1 word-ordered bitmap, 2 document-ordered bitmap (lda_options)
   int32_t always_skip_test;  // steps 2-3 every iteration instead of when they pay (lda_options)
   uint32_t key_base;     // out-of-core chunks: input index of the chunk's first doc-ordered token (else 0)
+  int32_t n_heavy;       // entries of heavy_docs
+  int64_t light_begin;   // regions [light_begin, n_regions): light words, one wave each in the sampler
   int32_t doc_marks_ok;  // the document-ordered bitmap is usable: keys are document positions, regular sampler
   uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
 
 // Scheduler counters: one each for the region kernels and the doc pass,
 // kXcds (one per document range) for the D rebuild.
-enum { CNT_SAMPLER = 0, CNT_REBUILD_W = 1, CNT_DOCPASS = 2, CNT_LOGLIK = 4, CNT_REBUILD_D = 16 };
+enum { CNT_SAMPLER = 0, CNT_REBUILD_W = 1, CNT_DOCPASS = 2, CNT_LOGLIK = 4, CNT_HEAVY_PASS = 5,
+       CNT_HEAVY_REBUILD = 6, CNT_LIGHT = 7, CNT_REBUILD_D = 16 };
 constexpr int kCounters = 32;
 enum { ST_SKIP3 = 0, ST_SKIP_AFTER_S = 1, ST_SAMPLED = 2, ST_NNZ = 3, ST_REGIONS = 4, ST_DENSE_REGIONS = 5, ST_ERRORS = 6,
        ST_ROW_BYTES = 7, ST_MARKS = 8, ST_TEST_RAN = 9 };
@@ -212,8 +219,26 @@ hipError_t launch_beta_sum(const DevState &d, const Params &p, hipStream_t s);
 hipError_t launch_clear_skips(const DevState &d, const Params &p, uint32_t t, hipStream_t s, bool reset_count = true);
 hipError_t launch_reset_counters(uint32_t *counters, hipStream_t s);
 hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
+// The sampler of the regions before p.light_begin (or every region with the
+// tiled sampler), and that of the light regions, one wave each (nothing when
+// there are none); the two touch disjoint topic slots and may run at once.
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
+hipError_t launch_sampler_light(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 int sampler_block(int K, int want);
+// The sampler's dynamic LDS for K topics and workgroups of nb threads.
+size_t sampler_lds_bytes(int K, int nb);
+// Regions of at most this many tokens (one batch of the sampler) are light:
+// a wave takes each of them, when the per-wave W^' row is small (K up to
+// about 2,000).  They form a suffix of the region table, which lists the
+// unsplit words by descending token count after the split ones.
+constexpr uint32_t kLightTokens = 64;
+constexpr size_t kLightLdsMax = 20 * 1024;
+inline int64_t light_region_start(const std::vector<uint32_t> &region, int K, bool big_k) {
+  int64_t r = int64_t(region.size() / 3);
+  if (big_k || sampler_lds_bytes(K, 64) > kLightLdsMax) return r;
+  while (r > 0 && region[3 * size_t(r - 1) + 2] - region[3 * size_t(r - 1) + 1] <= kLightTokens) --r;
+  return r;
+}
 // Large K: topics per tile and the tiled sampler's dynamic LDS.
 int tiled_topics(int K);
 size_t tiled_lds_bytes(int K, int kt);

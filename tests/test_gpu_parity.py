@@ -396,6 +396,38 @@ def test_edge_cases(name, c):
 
 
 
+@pytest.mark.parametrize("K,marks,shuffle", [(64, 1, False), (64, 2, False), (1000, 0, False), (1000, 1, True),
+                                              (20000, 0, False)])
+def test_heavy_documents_follow_the_oracle(K, marks, shuffle):
+    """Documents longer than 4,096 tokens get a whole workgroup in the doc pass and the D rebuild
+    (the others one wave): with heavy documents of 4,097 to 30,000 tokens among light ones, both
+    skip bitmaps, shuffled input and the tiled sampler, the draws are the oracle's and the counts
+    the histograms of z.  The first snapshot gives every word one topic, so many tokens skip."""
+    rng = np.random.default_rng(99)
+    lens = np.concatenate([rng.integers(1, 300, 200), [4097, 8000, 30000, 4096, 12345]])
+    rng.shuffle(lens)
+    doc = np.repeat(np.arange(lens.shape[0], dtype=np.int32), lens)
+    word = (rng.zipf(1.2, doc.shape[0]) % 500).astype(np.int32)
+    if shuffle:
+        perm = rng.permutation(doc.shape[0])
+        word, doc = word[perm], doc[perm]
+    c = _Tiny(word, doc, 500, K, 0.1)
+    kw = dict(M=c.n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta)
+    z = ((c.word.astype(np.int64) * 7) % K).astype(np.int32)
+    say("heavy documents K=%d marks=%d shuffle=%s N=%d" % (K, marks, shuffle, c.N))
+    with lda_make(c, skip_marks=marks, always_skip_test=True) as m:
+        for t in range(3):
+            zo, flags, ost = oracle.iterate(c.word, c.doc, z, seed=SEED, t=t, **kw)
+            m.set_assignments(z, t)
+            st = m.iterate(1, stats=True)[0]
+            cnt = m.counts()
+            compare_draws(cnt["z"], zo, flags, c.N)
+            check_counts_are_histograms(c, cnt, c.K)
+            assert 0 <= ost["skip3"] - st["skip_step3"] <= max(2, 1e-3 * c.N)
+            say("  t=%d skipped %d (oracle %d)" % (t, st["skip_step3"], ost["skip3"]))
+            z = zo
+
+
 @pytest.mark.parametrize("K", [16384, 5000])
 @pytest.mark.parametrize("block", [0, 256, 512, 1024])
 def test_sampler_block_sizes_at_large_K(K, block):
