@@ -10,7 +10,9 @@ per-document C1/C2 + skip pass, the word-major sampler and the count rebuild.
 
 Prints one JSON line: tokens/s over the timed steps, the sampler kernel's
 algorithmic HBM bytes per launch divided by its HIP-event duration against the
-8 TB/s peak, and the oracle timed on a bounded sample of the same workload.
+8 TB/s peak (and against a plain device copy's measured rate), and the oracle
+timed on two bounded samples of the same workload, one early and one from the
+GPU's state after the timed iterations.
 """
 import argparse
 import hashlib
@@ -25,7 +27,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 PCIE_PEAK_GBS = 64.0  # PCIe 5.0 x16, one direction
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "k_sampler_c3_counters.md")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "kernels_c3_counters.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2007_08725_amd", "csrc", "kernels.hip")
 
 
@@ -43,14 +45,16 @@ def sampler_alg_bytes(st, N):
     return (N / 8 + 2 * N + 12 * st["sampled"] + 4 * st["nnz_scanned"] + st["row_bytes"] + 60 * st["regions"])
 
 
-def traffic_from_profile(alg_per_launch):
-    """HBM bytes per sampler launch from the committed counter summary, if it
-    was taken on the current kernel source; else None."""
-    if not os.path.exists(PMC_SUMMARY):
+def traffic_from_profile(workload):
+    """Bytes per sampler launch that the L2 requested from the memory fabric
+    (reads by request size plus writes), from the committed counter summary,
+    if it covers this workload and was taken on the current kernel source;
+    else None."""
+    if workload != "c3" or not os.path.exists(PMC_SUMMARY):
         return None
     txt = open(PMC_SUMMARY).read()
     m = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", txt)
-    b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", txt)
+    b = re.search(r"k_sampler_fabric_bytes_per_launch:\s*([0-9.eE+]+)", txt)
     if not m or not b:
         return None
     sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
@@ -59,21 +63,91 @@ def traffic_from_profile(alg_per_launch):
     return float(b.group(1))
 
 
-def cpu_baseline(c, n_docs):
-    """The oracle as it stands: one synchronous iteration on the first n_docs documents."""
+def copy_ceiling_gbs(torch, reps=10):
+    """Bytes moved per second (read + write) by a plain 1 GiB device-to-device
+    copy, timed with HIP events on torch's stream: the streaming rate this
+    GPU sustains, stated beside the 8 TB/s peak."""
+    a = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(2):
+        b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    e1.synchronize()
+    gbs = 2.0 * a.numel() * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    return gbs
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+class _OneCore:
+    """Runs the enclosed code on one core of this process's set (the calling
+    thread's affinity), restoring the previous set afterwards."""
+
+    def __enter__(self):
+        self.old = os.sched_getaffinity(0)
+        self.core = min(self.old)
+        os.sched_setaffinity(0, {self.core})
+        return self
+
+    def __exit__(self, *exc):
+        os.sched_setaffinity(0, self.old)
+
+
+def cpu_baseline(c, n_docs, z_late, t_late, n_docs_late):
+    """The oracle as it stands, single thread pinned to one core.  Early sample:
+    one synchronous iteration on the first n_docs documents from the Philox
+    initial topics (counts, per-word precompute and every draw timed).  Late
+    sample: the draws of the first n_docs_late documents' tokens at iteration
+    t_late from the GPU's own state after its timed iterations (counts and
+    per-word precompute built beforehand, untimed)."""
     import numpy as np
     import oracle
 
     m = int(np.searchsorted(c.doc, n_docs))
     w, d = c.word[:m], c.doc[:m]
-    z = oracle.init_topics(m, c.K, 42)
-    t0 = time.perf_counter()
-    oracle.iterate(w, d, z, M=n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta, seed=42, t=0)
-    dt = time.perf_counter() - t0
-    return {"value": m / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": "one synchronous iteration (counts rebuilt from the Philox initial topics, per-word "
-                      "precompute over all %d words, every token drawn) on the first %d documents = %d tokens "
-                      "of the same corpus, single thread, %.1f s" % (c.V, n_docs, m, dt)}
+    z = oracle.init_topics(m, c.K, lda_seed())
+    with _OneCore() as pin:
+        t0 = time.perf_counter()
+        oracle.iterate(w, d, z, M=n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta, seed=lda_seed(), t=0)
+        dt = time.perf_counter() - t0
+    out = {"value": m / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle", "cpu_model": cpu_model(),
+           "pinned_core": pin.core,
+           "sample": "one synchronous iteration (counts rebuilt from the Philox initial topics, per-word "
+                     "precompute over all %d words, every token drawn) on the first %d documents = %d tokens "
+                     "of the same corpus, one thread pinned to one core, %.1f s" % (c.V, n_docs, m, dt)}
+    if z_late is not None:
+        ml = int(np.searchsorted(c.doc, n_docs_late))
+        idx = np.arange(ml, dtype=np.int64)
+        with oracle.Snapshot(c.word, c.doc, z_late, M=c.n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta,
+                             idx=idx) as s:
+            with _OneCore():
+                t0 = time.perf_counter()
+                _, _, st = s.draw(lda_seed(), t_late, idx=idx)
+                dl = time.perf_counter() - t0
+        out["late"] = {"value": ml / dl, "unit": "tokens/s", "cores": 1,
+                       "sample": "the draws of iteration %d for the first %d documents = %d tokens, from the GPU's "
+                                 "assignments after its timed iterations (counts and per-word precompute over the "
+                                 "whole corpus built untimed), one thread pinned to one core, %.1f s; %d of them "
+                                 "skipped at step 3" % (t_late, n_docs_late, ml, dl, st.get("skip3", 0))}
+    return out
+
+
+def lda_seed():
+    import lda_synth
+    return lda_synth.SAMPLER_SEED
 
 
 def main():
@@ -88,8 +162,8 @@ def main():
     ap.add_argument("--always-skip-test", action="store_true", help="run steps 2-3 in every iteration")
     ap.add_argument("--chunks", type=int, default=0,
                     help="out-of-core mode: per-token arrays in pinned host memory, streamed in this many chunks")
-    ap.add_argument("--calib-copy", action="store_true",
-                    help="also run a plain 1 GiB device copy (counter calibration under rocprofv3)")
+    ap.add_argument("--cpu-docs-late", type=int, default=100000,
+                    help="documents in the oracle's late-state sample")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: the library runs on exactly one GPU; --gpus %d is not supported "
@@ -114,13 +188,8 @@ def main():
     t_create = time.perf_counter() - t0
     log("lda_create %.1f s" % t_create)
 
-    if args.calib_copy:
-        a = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
-        b = torch.empty_like(a)
-        for _ in range(5):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        del a, b
+    copy_gbs = copy_ceiling_gbs(torch)
+    log("plain 1 GiB device copy: %.0f GB/s (read + write)" % copy_gbs)
 
     if args.warmup:
         m.iterate(args.warmup)
@@ -135,6 +204,7 @@ def main():
             for s in st:
                 f.write(json.dumps(s) + "\n")
     llpt = m.loglik()
+    z_late = None if args.no_cpu_baseline else m.counts(z=True, D=False, W=False)["z"]
 
     N = c.N
     value = N * args.steps / elapsed
@@ -148,13 +218,21 @@ def main():
         achieved = h2d * args.steps / elapsed / 1e9
         roofline = {"bound": "pcie", "achieved": achieved, "peak": PCIE_PEAK_GBS, "unit": "GB/s",
                     "frac": achieved / PCIE_PEAK_GBS, "traffic": None, "kernel": "host-to-device copies",
-                    "h2d_bytes_per_iteration": h2d, "d2h_bytes_per_iteration": 2.0 * N, "chunks": args.chunks}
+                    "h2d_bytes_per_iteration": h2d, "d2h_bytes_per_iteration": 2.0 * N, "chunks": args.chunks,
+                    "hbm_copy_ceiling_gbs": copy_gbs}
     else:
         achieved = alg.sum() / (ms_sampler.sum() * 1e-3) / 1e9
+        traffic = traffic_from_profile(args.workload)
         roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_from_profile(alg_per_launch),
+                    "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                    "traffic_kind": "fabric: bytes the L2 requested from memory per launch (reads by request "
+                                    "size + writes, rocprofv3 TCC_EA0 counters over the same iterations); "
+                                    "last-level-cache hits are inside it, so it bounds DRAM bytes from above",
                     "kernel": "k_sampler", "alg_bytes_per_launch": alg_per_launch,
-                    "avg_launch_ms": float(ms_sampler.mean())}
+                    "avg_launch_ms": float(ms_sampler.mean()),
+                    "copy_ceiling_gbs": copy_gbs, "frac_of_copy": achieved / copy_gbs}
+        if traffic is not None:
+            roofline["traffic_gbs"] = traffic / (ms_sampler.mean() * 1e-3) / 1e9
     stage_ms = {k: float(np.mean([s[k] for s in st])) for k in
                 ("ms_precompute", "ms_docpass", "ms_sampler", "ms_rebuild", "ms_iter")}
     line = {
@@ -182,7 +260,8 @@ def main():
     m.close()
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample ...")
-        line["cpu_baseline"] = cpu_baseline(c, args.cpu_docs)
+        line["cpu_baseline"] = cpu_baseline(c, args.cpu_docs, z_late, args.warmup + args.steps,
+                                            args.cpu_docs_late)
     else:
         line["cpu_baseline"] = None
     print(json.dumps(line), flush=True)
