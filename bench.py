@@ -63,6 +63,22 @@ def traffic_from_profile(workload):
     return float(b.group(1))
 
 
+def valu_from_profile(workload):
+    """k_sampler's VALU wave instructions per launch from the committed
+    counter summary (same conditions as traffic_from_profile); else None."""
+    if workload != "c3" or not os.path.exists(PMC_SUMMARY):
+        return None
+    txt = open(PMC_SUMMARY).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", txt)
+    b = re.search(r"k_sampler_valu_per_launch:\s*([0-9.eE+]+)", txt)
+    if not m or not b or hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest() != m.group(1):
+        return None
+    return float(b.group(1))
+
+
+VALU_ISSUE_PER_S = 1024 * 2.4e9 / 4  # wave instructions per second: 1,024 SIMDs, 4 cycles each at 2.4 GHz
+
+
 def copy_ceiling_gbs(torch, reps=10):
     """Bytes moved per second (read + write) by a plain 1 GiB device-to-device
     copy, timed with HIP events on torch's stream: the streaming rate this
@@ -233,6 +249,10 @@ def main():
                     "copy_ceiling_gbs": copy_gbs, "frac_of_copy": achieved / copy_gbs}
         if traffic is not None:
             roofline["traffic_gbs"] = traffic / (ms_sampler.mean() * 1e-3) / 1e9
+        valu = valu_from_profile(args.workload)
+        if valu is not None:
+            # the limit the kernel actually meets: VALU instruction issue
+            roofline["valu_issue_frac"] = valu / VALU_ISSUE_PER_S / (ms_sampler.mean() * 1e-3)
     stage_ms = {k: float(np.mean([s[k] for s in st])) for k in
                 ("ms_precompute", "ms_docpass", "ms_sampler", "ms_rebuild", "ms_iter")}
     line = {
