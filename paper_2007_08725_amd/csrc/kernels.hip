@@ -753,7 +753,10 @@ struct WordState {
   int qhalf;  // half the padded block count of qb (0 for a single block): the binary search's first step
   uint32_t K1;
   double a1, qp, alpha;
+  const double *qw;   // kQwStride per block: the partial sums before each of its kGroup topics, then its total (or null)
+  const uint8_t *ql;  // per block: the offset of its last topic with a positive term (or its first)
 };
+constexpr int kQwStride = kGroup + 1;
 
 
 // W^' of a packed D entry's topic (entry = topic << 16 | count) from the
@@ -1089,6 +1092,16 @@ __device__ __forceinline__ uint32_t q_draw(double xq, const WordState &w) {
   int lo = 0;  // the largest block with qb[lo] <= xq (qb is +inf from nb + 1 up to 2 * qhalf)
   for (int step = w.qhalf; step > 0; step >>= 1) lo = w.qb[lo + step] <= xq ? lo + step : lo;
   const double xs = xq - w.qb[lo];
+  if (w.qw) {
+    // the walk below, by a binary search over the same partial sums (kept
+    // per region): the last topic whose partial sum before it is <= xs
+    const double *pw = w.qw + lo * kQwStride;
+    if (!(xs < pw[kGroup])) return uint32_t(lo * kGroup + w.ql[lo]);
+    int i = 0;
+#pragma unroll
+    for (int step = kGroup / 2; step > 0; step >>= 1) i = pw[i + step] <= xs ? i + step : i;
+    return uint32_t(lo * kGroup + i);
+  }
   const int k0 = lo * kGroup;
   double p = 0.0;
   int kk = k0, last = k0;
@@ -1285,6 +1298,11 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
   uint32_t *s_reg = s_hand + NB / kGroup * kMaxRun;          // [4]: the region (word, begin, end) and a valid flag
   uint16_t *s_top = reinterpret_cast<uint16_t *>(s_reg + 4); // [NB]
   uint8_t *s_list = reinterpret_cast<uint8_t *>(s_top + NB); // [NB]
+  // with p.q_table: [nb * kQwStride] partial sums of the Q' blocks, then [nb] last-positive offsets
+  // (the 21 * NB + 16 bytes after s_u keep them 8-byte aligned)
+  static_assert((21 * NB + 16) % 8 == 0, "the Q' partial sums must be 8-byte aligned");
+  double *s_qw = p.q_table ? reinterpret_cast<double *>(s_list + NB) : nullptr;
+  uint8_t *s_ql = p.q_table ? reinterpret_cast<uint8_t *>(s_qw + nb * kQwStride) : nullptr;
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -1349,8 +1367,22 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       __syncthreads();
       for (int blk = tid; blk < nb; blk += NB) {
         double s = 0.0;
-        const int k1 = min(K, (blk + 1) * kGroup);
-        for (int k = blk * kGroup; k < k1; ++k) s += p.alpha * wh[k];
+        if (s_qw) {
+          // every topic of the block (zeros past K), as q_draw's walk adds them
+          double *pw = s_qw + blk * kQwStride;
+          int last = 0;
+          for (int i = 0; i < kGroup; ++i) {
+            pw[i] = s;
+            const double t = p.alpha * wh[blk * kGroup + i];
+            s += t;
+            last = t > 0.0 ? i : last;
+          }
+          pw[kGroup] = s;
+          s_ql[blk] = uint8_t(last);
+        } else {
+          const int k1 = min(K, (blk + 1) * kGroup);
+          for (int k = blk * kGroup; k < k1; ++k) s += p.alpha * wh[k];
+        }
         qb[blk + 1] = s;
       }
       __syncthreads();
@@ -1369,7 +1401,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       __syncthreads();
     }
 
-    const WordState w{wh, qb, nb, K, qhalf, K1, a1, qp, p.alpha};
+    const WordState w{wh, qb, nb, K, qhalf, K1, a1, qp, p.alpha, s_qw, s_ql};
     for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += NB) {
       const int ln = lane_here();  // the lane, recomputed per batch
       const uint32_t j = base + uint32_t(ln);
@@ -2398,37 +2430,47 @@ hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipSt
 // The sampler's dynamic LDS for K topics and workgroups of nb threads: the
 // W^' row, the Q' block prefix, the per-wave batch slices (u, row offset,
 // length, drawn topic, list place; the long-row hand-off) and the region.
-size_t sampler_lds_bytes(int K, int nb) {
-  const size_t words = size_t(wh_entries(K)) + size_t(q_blocks_padded((K + kGroup - 1) / kGroup)) + 1;
-  return sizeof(double) * words + size_t(nb) * (sizeof(double) + 2 * sizeof(uint32_t) + sizeof(uint16_t) + 1) +
-         sizeof(uint32_t) * (size_t(nb) / kGroup * kMaxRun + 4);
+size_t sampler_lds_bytes(int K, int nb, bool q_table) {
+  const size_t blocks = size_t((K + kGroup - 1) / kGroup);
+  const size_t words = size_t(wh_entries(K)) + size_t(q_blocks_padded(int(blocks))) + 1;
+  size_t bytes = sizeof(double) * words + size_t(nb) * (sizeof(double) + 2 * sizeof(uint32_t) + sizeof(uint16_t) + 1) +
+                 sizeof(uint32_t) * (size_t(nb) / kGroup * kMaxRun + 4);
+  if (q_table) bytes += blocks * (kQwStride * sizeof(double) + 1);
+  return bytes;
 }
 
 // Threads per sampler workgroup for this K: `want` when nonzero, else the
 // size with the most resident waves per CU (ties to the smaller).  LDS holds
 // the W^ row, so a large K leaves room for few workgroups and larger ones
 // keep more waves busy.  0 when the size asked for (or none) fits.
-int sampler_block(int K, int want) {
+// *q_table: whether the per-topic partial sums of the Q' blocks are kept in
+// LDS (q_draw's search instead of its walk; the same draws), which they are
+// when they leave the chosen size as many resident waves.
+static int sampler_waves(int K, int nb, bool q_table) {
+  const size_t lds = sampler_lds_bytes(K, nb, q_table);
+  hipError_t err = nb == 256 ? allow_lds(k_sampler, lds) : nb == 512 ? allow_lds(k_sampler_512, lds)
+                                                                      : allow_lds(k_sampler_1024, lds);
+  int blocks = 0;
+  if (err == hipSuccess)
+    err = nb == 256 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler, nb, lds)
+        : nb == 512 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler_512, nb, lds)
+                    : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler_1024, nb, lds);
+  (void)hipGetLastError();
+  return err == hipSuccess ? blocks * nb / kWave : 0;
+}
+int sampler_block(int K, int want, bool *q_table) {
   int best = 0, best_waves = 0;
   const int sizes[3] = {256, 512, 1024};
   for (int q = 0; q < 3; ++q) {
     const int nb = sizes[q];
-    const size_t lds = sampler_lds_bytes(K, nb);
     if (want && nb != want) continue;
-    hipError_t err = nb == 256 ? allow_lds(k_sampler, lds) : nb == 512 ? allow_lds(k_sampler_512, lds)
-                                                                        : allow_lds(k_sampler_1024, lds);
-    int blocks = 0;
-    if (err == hipSuccess)
-      err = nb == 256 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler, nb, lds)
-          : nb == 512 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler_512, nb, lds)
-                      : hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k_sampler_1024, nb, lds);
-    const int waves = err == hipSuccess ? blocks * nb / kWave : 0;
+    const int waves = sampler_waves(K, nb, false);
     if (waves > best_waves) {
       best = nb;
       best_waves = waves;
     }
   }
-  (void)hipGetLastError();
+  *q_table = best && sampler_waves(K, best, true) >= best_waves;
   return best;
 }
 
@@ -2446,7 +2488,7 @@ hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStr
     return hipGetLastError();
   }
   const int nb = p.sampler_block;
-  const size_t lds = sampler_lds_bytes(p.K, nb);
+  const size_t lds = sampler_lds_bytes(p.K, nb, p.q_table != 0);
   const uint32_t grid = uint32_t(std::max<int64_t>(1, int64_t(p.grid_regions) * kBlock / nb));
   hipError_t err;
   if (p.light_begin == 0) return hipSuccess;  // every region is light
@@ -2468,7 +2510,7 @@ hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStr
 
 hipError_t launch_sampler_light(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
   if (p.light_begin >= p.n_regions) return hipSuccess;
-  const size_t lds = sampler_lds_bytes(p.K, kWave);
+  const size_t lds = sampler_lds_bytes(p.K, kWave, p.q_table != 0);
   hipError_t err = allow_lds(k_sampler_light, lds);
   if (err != hipSuccess) return err;
   const int64_t n_light = p.n_regions - p.light_begin;

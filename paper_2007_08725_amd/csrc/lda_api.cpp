@@ -52,7 +52,9 @@ lda_status setup_device(lda_handle *h, const lda_options *o) {
   Params &p = h->p;
   p.grid_regions = std::max(1, cus * 8);
   const int want = o ? o->sampler_block : 0;
-  p.sampler_block = sampler_block(p.K, want);
+  bool q_table = false;
+  p.sampler_block = sampler_block(p.K, want, &q_table);
+  p.q_table = q_table ? 1 : 0;
   if (!p.sampler_block && want)
     return fail(h, LDA_E_RANGE, "no sampler workgroup of " + std::to_string(want) + " threads fits the LDS of K = " +
                                     std::to_string(L.K));

@@ -197,6 +197,7 @@ struct Params {
   int32_t n_heavy;       // entries of heavy_docs
   int64_t light_begin;   // regions [light_begin, n_regions): light words, one wave each in the sampler
   int32_t doc_marks_ok;  // the document-ordered bitmap is usable: keys are document positions, regular sampler
+  int32_t q_table;       // the sampler keeps the Q' blocks' partial sums in LDS (search instead of walk)
   uint32_t xcd_doc[kXcds + 1];  // document ranges with equal token counts, one per XCD (D rebuild)
 };
 
@@ -224,9 +225,9 @@ hipError_t launch_doc_pass(const DevState &d, const Params &p, uint32_t t, hipSt
 // there are none); the two touch disjoint topic slots and may run at once.
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
 hipError_t launch_sampler_light(const DevState &d, const Params &p, uint32_t t, hipStream_t s);
-int sampler_block(int K, int want);
+int sampler_block(int K, int want, bool *q_table);
 // The sampler's dynamic LDS for K topics and workgroups of nb threads.
-size_t sampler_lds_bytes(int K, int nb);
+size_t sampler_lds_bytes(int K, int nb, bool q_table);
 // Regions of at most this many tokens (one batch of the sampler) are light:
 // a wave takes each of them, when the per-wave W^' row is small (K up to
 // about 2,000).  They form a suffix of the region table, which lists the
@@ -235,7 +236,7 @@ constexpr uint32_t kLightTokens = 64;
 constexpr size_t kLightLdsMax = 20 * 1024;
 inline int64_t light_region_start(const std::vector<uint32_t> &region, int K, bool big_k) {
   int64_t r = int64_t(region.size() / 3);
-  if (big_k || sampler_lds_bytes(K, 64) > kLightLdsMax) return r;
+  if (big_k || sampler_lds_bytes(K, 64, true) > kLightLdsMax) return r;
   while (r > 0 && region[3 * size_t(r - 1) + 2] - region[3 * size_t(r - 1) + 1] <= kLightTokens) --r;
   return r;
 }
