@@ -1849,27 +1849,20 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
   const int K = p.K;
   uint32_t *hist = ldsu;                           // [K]
   uint32_t *tloc = p.big_k ? nullptr : ldsu + K;  // [K]; large K: T is added per region instead
-  __shared__ uint32_t s_reg[3];
-  __shared__ int s_valid;
   __shared__ uint32_t s_scan[kBlock / kWave];
   const int tid = threadIdx.x;
   uint32_t bad = 0;
   if (tloc)
     for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
-  for (;;) {
-    if (tid == 0) {
-      const uint32_t r = atomicAdd(&d.counters[CNT_REBUILD_W], 1u);
-      s_valid = int64_t(r) < p.n_regions;
-      if (s_valid) {
-        s_reg[0] = d.region[3 * size_t(r)];
-        s_reg[1] = d.region[3 * size_t(r) + 1];
-        s_reg[2] = d.region[3 * size_t(r) + 2];
-      }
-    }
+  // regions dealt round-robin: every thread reads its region's record itself,
+  // so no counter atomic and no broadcast through LDS sits in front of each
+  // region's loads (the work of a region follows its tokens, and the table
+  // interleaves large and small regions well enough that the tail stays short)
+  for (int64_t r = blockIdx.x;; r += gridDim.x) {
     for (int k = tid; k < K; k += kBlock) hist[k] = 0u;
     __syncthreads();
-    if (!s_valid) break;
-    const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2];
+    if (r >= p.n_regions) break;
+    const uint32_t v = d.region[3 * size_t(r)], b = d.region[3 * size_t(r) + 1], e = d.region[3 * size_t(r) + 2];
     // kHistAhead topic loads per thread in flight at once
     for (uint32_t j0 = b + tid; j0 < e; j0 += uint32_t(kHistAhead * kBlock)) {
       uint32_t zz[kHistAhead];
@@ -1928,8 +1921,6 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
   uint32_t *hist = ldsu;                              // [K]: the region's topic counts
   uint32_t *bits = ldsu + K;                          // [nw]: topics with a nonzero count
   uint32_t *tloc = p.big_k ? nullptr : bits + nw;     // [K]; large K: T is added per region instead
-  __shared__ uint32_t s_reg[3];
-  __shared__ int s_valid;
   __shared__ uint32_t s_scan[kBlock / kWave];
   const int tid = threadIdx.x;
   uint32_t bad = 0;
@@ -1938,19 +1929,9 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
   if (tloc)
     for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
   __syncthreads();
-  for (;;) {
-    if (tid == 0) {
-      const uint32_t r = atomicAdd(&d.counters[CNT_REBUILD_W], 1u);
-      s_valid = int64_t(r) < p.n_regions;
-      if (s_valid) {
-        s_reg[0] = d.region[3 * size_t(r)];
-        s_reg[1] = d.region[3 * size_t(r) + 1];
-        s_reg[2] = d.region[3 * size_t(r) + 2];
-      }
-    }
-    __syncthreads();
-    if (!s_valid) break;
-    const uint32_t v = s_reg[0], b = s_reg[1], e = s_reg[2];
+  // regions dealt round-robin, as in k_rebuild_w
+  for (int64_t r = blockIdx.x; r < p.n_regions; r += gridDim.x) {
+    const uint32_t v = d.region[3 * size_t(r)], b = d.region[3 * size_t(r) + 1], e = d.region[3 * size_t(r) + 2];
     // kHistAhead topic loads per thread in flight at once
     for (uint32_t j0 = b + tid; j0 < e; j0 += uint32_t(kHistAhead * kBlock)) {
       uint32_t zz[kHistAhead];

@@ -203,7 +203,7 @@ struct Params {
 
 // Scheduler counters: one each for the region kernels and the doc pass,
 // kXcds (one per document range) for the D rebuild.
-enum { CNT_SAMPLER = 0, CNT_REBUILD_W = 1, CNT_DOCPASS = 2, CNT_LOGLIK = 4, CNT_HEAVY_PASS = 5,
+enum { CNT_SAMPLER = 0, CNT_DOCPASS = 2, CNT_LOGLIK = 4, CNT_HEAVY_PASS = 5,
        CNT_HEAVY_REBUILD = 6, CNT_LIGHT = 7, CNT_REBUILD_D = 16 };
 constexpr int kCounters = 32;
 enum { ST_SKIP3 = 0, ST_SKIP_AFTER_S = 1, ST_SAMPLED = 2, ST_NNZ = 3, ST_REGIONS = 4, ST_DENSE_REGIONS = 5, ST_ERRORS = 6,
