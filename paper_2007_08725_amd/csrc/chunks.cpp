@@ -38,7 +38,8 @@ struct ChunkInfo {
 };
 
 struct ChunkSlot {
-  uint32_t *dt_word = nullptr, *dt_wpos = nullptr, *wt_key = nullptr, *wt_rowoff = nullptr;
+  uint32_t *dt_word = nullptr, *dt_wpos = nullptr;
+  uint2 *wt_kr = nullptr;
   uint32_t *skip_bits = nullptr, *d_ent = nullptr;
   uint16_t *z_w = nullptr;
   hipEvent_t loaded = nullptr, computed = nullptr, unloaded = nullptr;
@@ -79,8 +80,7 @@ namespace {
 lda_status alloc_slot(lda_handle *h, ChunkSlot &s, uint32_t max_tok, uint32_t max_slots) {
   LDA_TRY(dalloc(h, &s.dt_word, max_tok));
   LDA_TRY(dalloc(h, &s.dt_wpos, max_tok));
-  LDA_TRY(dalloc(h, &s.wt_key, max_tok));
-  LDA_TRY(dalloc(h, &s.wt_rowoff, max_tok));
+  LDA_TRY(dalloc(h, &s.wt_kr, max_tok));
   LDA_TRY(dalloc(h, &s.z_w, max_tok));
   LDA_TRY(dalloc(h, &s.skip_bits, size_t(skip_words(max_tok))));
   LDA_TRY(dalloc(h, &s.d_ent, size_t(max_slots) + kRowPad));
@@ -102,8 +102,7 @@ DevState chunk_state(const lda_handle *h, const ChunkInfo &ci, const ChunkSlot &
   d.heavy_docs = ci.heavy_docs;
   d.dt_word = sl.dt_word;
   d.dt_wpos = sl.dt_wpos;
-  d.wt_key = sl.wt_key;
-  d.wt_rowoff = sl.wt_rowoff;
+  d.wt_kr = sl.wt_kr;
   d.z_w = sl.z_w;
   d.skip_bits = sl.skip_bits;
   d.d_ent = sl.d_ent;
@@ -116,7 +115,7 @@ DevState chunk_state(const lda_handle *h, const ChunkInfo &ci, const ChunkSlot &
 // on stream st.
 lda_status prepare_chunk(lda_handle *h, const ChunkInfo &ci, const DevState &d, hipStream_t st) {
   HIP_TRY(h, launch_inflate(ci.region, ci.p.n_regions, ci.doc_off, ci.d_cap, int32_t(ci.ndoc), d.dt_wpos, ci.tok0,
-                            d.dt_word, d.wt_key, d.wt_rowoff, st));
+                            d.dt_word, d.wt_kr, st));
   HIP_TRY(h, launch_reset_counters(d.counters, st));
   HIP_TRY(h, launch_rebuild_d(d, ci.p, st));
   return LDA_OK;
@@ -231,7 +230,8 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
   LDA_TRY(upload(h, relabel_d, L.relabel));
   ChunkSlot &s0 = cm.slot[0], &s1 = cm.slot[1];
   int32_t *word_tmp = reinterpret_cast<int32_t *>(s1.dt_word);  // scratch of the build
-  uint32_t *wnew = s1.dt_wpos, *wkey = s1.wt_key, *wpos = s1.wt_rowoff;
+  // (the second slot's 8-byte records hold two max_tok arrays of 4 bytes)
+  uint32_t *wnew = s1.dt_wpos, *wkey = reinterpret_cast<uint32_t *>(s1.wt_kr), *wpos = wkey + cm.max_tok;
   HIP_TRY(h, launch_zero_split(d, p, h->stream));
   int64_t total_regions = 0;
   uint32_t max_region = 1;
@@ -282,7 +282,7 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
     cm.max_regions = std::max(cm.max_regions, ci.p.n_regions);
     DevState dc = chunk_state(h, ci, s0);
     HIP_TRY(h, launch_inflate(ci.region, ci.p.n_regions, ci.doc_off, ci.d_cap, int32_t(ci.ndoc), s0.dt_wpos, ci.tok0,
-                              s0.dt_word, s0.wt_key, s0.wt_rowoff, h->stream));
+                              s0.dt_word, s0.wt_kr, h->stream));
     HIP_TRY(h, launch_init_topics(dc, ci.p, h->stream));
     HIP_TRY(h, launch_reset_counters(d.counters, h->stream));
     HIP_TRY(h, launch_rebuild_w(dc, ci.p, h->stream));

@@ -193,10 +193,10 @@ __device__ __forceinline__ uint16_t initial_topic(uint64_t seed, uint32_t i, int
   return uint16_t((uint64_t(x.x) * uint64_t(uint32_t(K))) >> 32);
 }
 
-__global__ void k_init_topics(const uint32_t *__restrict__ wt_key, uint16_t *__restrict__ z_w, int64_t n, int32_t K,
+__global__ void k_init_topics(const uint2 *__restrict__ wt_kr, uint16_t *__restrict__ z_w, int64_t n, int32_t K,
                               uint64_t seed) {
   for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < n; j += int64_t(gridDim.x) * blockDim.x)
-    z_w[j] = initial_topic(seed, wt_key[j], K);
+    z_w[j] = initial_topic(seed, wt_kr[j].x, K);
 }
 
 // The skip bitmaps start every iteration clear, and so does this
@@ -1409,8 +1409,9 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       // row header only for the tokens left to draw
       uint32_t sk = 0, key = 0, off = 0;
       if (j < e) {
-        key = d.wt_key[j];
-        off = d.wt_rowoff[j];  // the row's first slot (its header)
+        const uint2 kr = d.wt_kr[j];
+        key = kr.x;
+        off = kr.y;  // the row's first slot (its header)
         // the skip bit at the word-order slot, or at the key (the token's
         // document position) in the document-ordered bitmap
         sk = by_doc ? d.skip_doc[key >> 5] >> (key & 31u) : d.skip_bits[j >> 5] >> (j & 31u);
@@ -1680,7 +1681,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
         const uint32_t j = j0 + uint32_t(grp);
         const uint32_t q = j - b;  // place in the region
         const uint32_t jj = min(j, e - 1u);
-        const uint32_t sk = d.skip_bits[jj >> 5], off = d.wt_rowoff[jj];
+        const uint32_t sk = d.skip_bits[jj >> 5], off = d.wt_kr[jj].y;
         const uint32_t code0 = pass == 2 ? sc_code[jj - b] : 0u;
         const bool skipped = j < e && ((sk >> (j & 31u)) & 1u);
         if (pass == 0 && skipped && li == 0) d.z_w[j] = uint16_t(K1);  // decided by the step-3 test
@@ -1744,7 +1745,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
           const uint32_t c1 = sc_c1[q];
           const double Mm = rec.a1 * (double(c1) + p.alpha);  // Eq. 7
           const double S = S0 + S1;
-          const double u = uniform_draw(p.seed, t, d.wt_key[j]);
+          const double u = uniform_draw(p.seed, t, d.wt_kr[j].x);
           const double x = u * ((Mm + S) + rec.qp);
           uint32_t topic = K1, code = 0u;
           double keep = 0.0;
@@ -2303,7 +2304,7 @@ __global__ __launch_bounds__(kBlock) void k_loglik(DevState d, Params p) {
     }
     double part = 0.0;
     for (uint32_t j = b + uint32_t(gid); j < e; j += kBlock / kGroup) {
-      const uint32_t *row = d.d_ent + d.wt_rowoff[j] + 1;
+      const uint32_t *row = d.d_ent + d.wt_kr[j].y + 1;
       const uint32_t hdr = row[-1];
       const uint32_t nnz = hdr & 0xFFFFu;
       double acc = 0.0;
@@ -2359,7 +2360,7 @@ hipError_t allow_lds(F *kernel, size_t bytes) {
 
 hipError_t launch_init_topics(const DevState &d, const Params &p, hipStream_t s) {
   const int64_t blocks = std::min<int64_t>((p.n + kBlock - 1) / kBlock, int64_t(p.grid_docs) * 8);
-  hipLaunchKernelGGL(k_init_topics, dim3(uint32_t(blocks)), dim3(kBlock), 0, s, d.wt_key, d.z_w, p.n, p.K, p.seed);
+  hipLaunchKernelGGL(k_init_topics, dim3(uint32_t(blocks)), dim3(kBlock), 0, s, d.wt_kr, d.z_w, p.n, p.K, p.seed);
   return hipGetLastError();
 }
 

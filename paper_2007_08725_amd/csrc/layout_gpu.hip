@@ -47,8 +47,7 @@ __global__ void k_word_order(const uint32_t *__restrict__ wkey, const uint32_t *
                              const uint32_t *__restrict__ woff_new, const uint32_t *__restrict__ doc_sorted,
                              const int32_t *__restrict__ doc_in, const uint32_t *__restrict__ dt_key,
                              uint32_t *__restrict__ dt_word, uint32_t *__restrict__ dt_wpos,
-                             const uint32_t *__restrict__ d_cap, uint32_t *__restrict__ wt_rowoff,
-                             uint32_t *__restrict__ wt_key) {
+                             const uint32_t *__restrict__ d_cap, uint2 *__restrict__ wt_kr) {
   for (int64_t q = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; q < n; q += int64_t(gridDim.x) * blockDim.x) {
     const uint32_t v = wkey[q];
     const uint32_t r = uint32_t(relabel[v]);
@@ -56,22 +55,21 @@ __global__ void k_word_order(const uint32_t *__restrict__ wkey, const uint32_t *
     const uint32_t p = wpos[q];
     dt_word[p] = r;
     dt_wpos[p] = j;
-    wt_rowoff[j] = d_cap[doc_sorted ? doc_sorted[p] : uint32_t(doc_in[p])];
-    wt_key[j] = dt_key ? dt_key[p] : p;
+    wt_kr[j] = make_uint2(dt_key ? dt_key[p] : p, d_cap[doc_sorted ? doc_sorted[p] : uint32_t(doc_in[p])]);
   }
 }
 
-__global__ void k_scatter_z(const uint16_t *__restrict__ z_w, const uint32_t *__restrict__ wt_key, int64_t n,
+__global__ void k_scatter_z(const uint16_t *__restrict__ z_w, const uint2 *__restrict__ wt_kr, int64_t n,
                             int32_t *__restrict__ z_in) {
   for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < n; j += int64_t(gridDim.x) * blockDim.x)
-    z_in[wt_key[j]] = int32_t(z_w[j]);
+    z_in[wt_kr[j].x] = int32_t(z_w[j]);
 }
 
-__global__ void k_gather_z(const int32_t *__restrict__ z_in, const uint32_t *__restrict__ wt_key, int64_t n,
+__global__ void k_gather_z(const int32_t *__restrict__ z_in, const uint2 *__restrict__ wt_kr, int64_t n,
                            int32_t K, uint16_t *__restrict__ z_w, unsigned long long *__restrict__ bad) {
   unsigned long long nbad = 0;
   for (int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; j < n; j += int64_t(gridDim.x) * blockDim.x) {
-    const int32_t z = z_in[wt_key[j]];
+    const int32_t z = z_in[wt_kr[j].x];
     if (z >= 0 && z < K) z_w[j] = uint16_t(z);
     else {
       z_w[j] = 0;
@@ -95,29 +93,29 @@ __global__ void k_invert(const uint32_t *__restrict__ wpos, int64_t n, uint32_t 
 
 // slot_word[s] = the word of word-order slot s, one workgroup per region
 // (the regions cover every slot exactly once).
-__global__ void k_slot_words(const uint32_t *__restrict__ region, int64_t n_regions, uint32_t *__restrict__ slot_word) {
+__global__ void k_slot_words(const uint32_t *__restrict__ region, int64_t n_regions, uint2 *__restrict__ wt_kr) {
   for (int64_t r = blockIdx.x; r < n_regions; r += gridDim.x) {
     const uint32_t v = region[3 * r], b = region[3 * r + 1], e = region[3 * r + 2];
-    for (uint32_t s = b + threadIdx.x; s < e; s += blockDim.x) slot_word[s] = v;
+    for (uint32_t s = b + threadIdx.x; s < e; s += blockDim.x) wt_kr[s] = make_uint2(0u, v);
   }
 }
 
 // Per document, one wave: for each of its tokens p (slot s = dt_wpos[p]) the
 // word id in doc order, and the key (key_base + p, the input index: chunks
-// need input sorted by document) and D-row offset in word order.  slot_word
-// and wt_rowoff share storage: slot s is read and then overwritten by the one
-// token that owns it.
+// need input sorted by document) and D-row offset in word order.  The word of
+// slot s (k_slot_words) waits in the second half of its (key, row offset)
+// record, which the one token that owns the slot reads and then overwrites:
+// one scattered 8-byte record per token, read and written in the same line.
 __global__ void k_inflate(const uint32_t *__restrict__ doc_off, const uint32_t *__restrict__ d_cap, int32_t M,
                           const uint32_t *__restrict__ dt_wpos, uint32_t key_base, uint32_t *__restrict__ dt_word,
-                          uint32_t *__restrict__ wt_key, uint32_t *__restrict__ slot_word_rowoff) {
+                          uint2 *__restrict__ wt_kr) {
   const int lane = threadIdx.x & 63, waves = int(blockDim.x) / 64;
   for (int64_t d = int64_t(blockIdx.x) * waves + threadIdx.x / 64; d < M; d += int64_t(gridDim.x) * waves) {
     const uint32_t b = doc_off[d], e = doc_off[d + 1], cap = d_cap[d];
     for (uint32_t p = b + uint32_t(lane); p < e; p += 64u) {
       const uint32_t s = dt_wpos[p];
-      dt_word[p] = slot_word_rowoff[s];
-      wt_key[s] = key_base + p;
-      slot_word_rowoff[s] = cap;
+      dt_word[p] = wt_kr[s].y;
+      wt_kr[s] = make_uint2(key_base + p, cap);
     }
   }
 }
@@ -150,16 +148,15 @@ hipError_t launch_invert(const uint32_t *wpos, int64_t n, uint32_t *dt_wpos, hip
 }
 
 hipError_t launch_inflate(const uint32_t *region, int64_t n_regions, const uint32_t *doc_off, const uint32_t *d_cap,
-                          int32_t M, const uint32_t *dt_wpos, uint32_t key_base, uint32_t *dt_word, uint32_t *wt_key,
-                          uint32_t *wt_rowoff, hipStream_t s) {
+                          int32_t M, const uint32_t *dt_wpos, uint32_t key_base, uint32_t *dt_word, uint2 *wt_kr,
+                          hipStream_t s) {
   const uint32_t rg = uint32_t(std::min<int64_t>(std::max<int64_t>(n_regions, 1), 1 << 16));
-  hipLaunchKernelGGL(k_slot_words, dim3(rg), dim3(kThreads), 0, s, region, n_regions, wt_rowoff);
+  hipLaunchKernelGGL(k_slot_words, dim3(rg), dim3(kThreads), 0, s, region, n_regions, wt_kr);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int64_t waves = kThreads / 64;
   const uint32_t dg = uint32_t(std::min<int64_t>(std::max<int64_t>((int64_t(M) + waves - 1) / waves, 1), 1 << 16));
-  hipLaunchKernelGGL(k_inflate, dim3(dg), dim3(kThreads), 0, s, doc_off, d_cap, M, dt_wpos, key_base, dt_word, wt_key,
-                     wt_rowoff);
+  hipLaunchKernelGGL(k_inflate, dim3(dg), dim3(kThreads), 0, s, doc_off, d_cap, M, dt_wpos, key_base, dt_word, wt_kr);
   return hipGetLastError();
 }
 
@@ -202,20 +199,20 @@ hipError_t launch_boundaries(const uint32_t *keys, int64_t n, uint32_t nbins, ui
 hipError_t launch_word_order(const uint32_t *wkey, const uint32_t *wpos, int64_t n, const int32_t *relabel,
                              const uint32_t *woff_orig, const uint32_t *woff_new, const uint32_t *doc_sorted,
                              const int32_t *doc_in, const uint32_t *dt_key, uint32_t *dt_word, uint32_t *dt_wpos,
-                             const uint32_t *d_cap, uint32_t *wt_rowoff, uint32_t *wt_key, hipStream_t s) {
+                             const uint32_t *d_cap, uint2 *wt_kr, hipStream_t s) {
   hipLaunchKernelGGL(k_word_order, dim3(grid_for(n)), dim3(kThreads), 0, s, wkey, wpos, n, relabel, woff_orig,
-                     woff_new, doc_sorted, doc_in, dt_key, dt_word, dt_wpos, d_cap, wt_rowoff, wt_key);
+                     woff_new, doc_sorted, doc_in, dt_key, dt_word, dt_wpos, d_cap, wt_kr);
   return hipGetLastError();
 }
 
-hipError_t launch_scatter_z(const uint16_t *z_w, const uint32_t *wt_key, int64_t n, int32_t *z_in, hipStream_t s) {
-  hipLaunchKernelGGL(k_scatter_z, dim3(grid_for(n)), dim3(kThreads), 0, s, z_w, wt_key, n, z_in);
+hipError_t launch_scatter_z(const uint16_t *z_w, const uint2 *wt_kr, int64_t n, int32_t *z_in, hipStream_t s) {
+  hipLaunchKernelGGL(k_scatter_z, dim3(grid_for(n)), dim3(kThreads), 0, s, z_w, wt_kr, n, z_in);
   return hipGetLastError();
 }
 
-hipError_t launch_gather_z(const int32_t *z_in, const uint32_t *wt_key, int64_t n, int32_t K, uint16_t *z_w,
+hipError_t launch_gather_z(const int32_t *z_in, const uint2 *wt_kr, int64_t n, int32_t K, uint16_t *z_w,
                            unsigned long long *bad, hipStream_t s) {
-  hipLaunchKernelGGL(k_gather_z, dim3(grid_for(n)), dim3(kThreads), 0, s, z_in, wt_key, n, K, z_w, bad);
+  hipLaunchKernelGGL(k_gather_z, dim3(grid_for(n)), dim3(kThreads), 0, s, z_in, wt_kr, n, K, z_w, bad);
   return hipGetLastError();
 }
 

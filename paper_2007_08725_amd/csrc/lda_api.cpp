@@ -158,12 +158,11 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
   LDA_TRY(upload(h, d.word_off, L.word_off));
   LDA_TRY(dalloc(h, &d.dt_word, n));
   LDA_TRY(dalloc(h, &d.dt_wpos, n));
-  LDA_TRY(dalloc(h, &d.wt_rowoff, n));
-  LDA_TRY(dalloc(h, &d.wt_key, n));
+  LDA_TRY(dalloc(h, &d.wt_kr, n));
   LDA_TRY(dalloc(h, &d.d_cap, L.d_cap.size()));
   LDA_TRY(upload(h, d.d_cap, L.d_cap));
   HIP_TRY(h, launch_word_order(wkey, wpos, L.n, relabel_d, woff_orig, d.word_off, doc_sorted, doc_d, d.dt_key,
-                               d.dt_word, d.dt_wpos, d.d_cap, d.wt_rowoff, d.wt_key, h->stream));
+                               d.dt_word, d.dt_wpos, d.d_cap, d.wt_kr, h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   dfree(h, relabel_d);
   dfree(h, woff_orig);
@@ -467,7 +466,7 @@ lda_status lda_get_counts(lda_handle *h, lda_counts *out) {
   if (out->z) {
     int32_t *zin = nullptr;
     LDA_TRY(dalloc(h, &zin, n));
-    HIP_TRY(h, launch_scatter_z(h->d.z_w, h->d.wt_key, L.n, zin, h->stream));
+    HIP_TRY(h, launch_scatter_z(h->d.z_w, h->d.wt_kr, L.n, zin, h->stream));
     HIP_TRY(h, hipMemcpyAsync(out->z, zin, n * 4, hipMemcpyDeviceToHost, h->stream));
     HIP_TRY(h, hipStreamSynchronize(h->stream));
     dfree(h, zin);
@@ -573,7 +572,7 @@ lda_status lda_set_assignments(lda_handle *h, const int32_t *z, int64_t iteratio
   LDA_TRY(dalloc(h, &zin, n));
   HIP_TRY(h, hipMemcpyAsync(zin, z, n * 4, hipMemcpyHostToDevice, h->stream));
   HIP_TRY(h, hipMemsetAsync(h->stats_base, 0, sizeof(unsigned long long) * kStatsPerIter, h->stream));
-  HIP_TRY(h, launch_gather_z(zin, h->d.wt_key, L.n, L.K, h->d.z_w, h->stats_base + ST_ERRORS, h->stream));
+  HIP_TRY(h, launch_gather_z(zin, h->d.wt_kr, L.n, L.K, h->d.z_w, h->stats_base + ST_ERRORS, h->stream));
   HIP_TRY(h, hipStreamSynchronize(h->stream));
   dfree(h, zin);
   unsigned long long st[kStatsPerIter];

@@ -97,9 +97,9 @@ hipError_t launch_boundaries(const uint32_t *keys, int64_t n, uint32_t nbins, ui
 hipError_t launch_word_order(const uint32_t *wkey, const uint32_t *wpos, int64_t n, const int32_t *relabel,
                              const uint32_t *woff_orig, const uint32_t *woff_new, const uint32_t *doc_sorted,
                              const int32_t *doc_in, const uint32_t *dt_key, uint32_t *dt_word, uint32_t *dt_wpos,
-                             const uint32_t *d_cap, uint32_t *wt_rowoff, uint32_t *wt_key, hipStream_t s);
-hipError_t launch_scatter_z(const uint16_t *z_w, const uint32_t *wt_key, int64_t n, int32_t *z_in, hipStream_t s);
-hipError_t launch_gather_z(const int32_t *z_in, const uint32_t *wt_key, int64_t n, int32_t K, uint16_t *z_w,
+                             const uint32_t *d_cap, uint2 *wt_kr, hipStream_t s);
+hipError_t launch_scatter_z(const uint16_t *z_w, const uint2 *wt_kr, int64_t n, int32_t *z_in, hipStream_t s);
+hipError_t launch_gather_z(const int32_t *z_in, const uint2 *wt_kr, int64_t n, int32_t K, uint16_t *z_w,
                            unsigned long long *bad, hipStream_t s);
 // Out-of-core chunks: the word-order slot of each doc-order position from the
 // positions listed in word order; the per-token arrays derived from dt_wpos
@@ -107,8 +107,8 @@ hipError_t launch_gather_z(const int32_t *z_in, const uint32_t *wt_key, int64_t 
 // (int32) and word order.
 hipError_t launch_invert(const uint32_t *wpos, int64_t n, uint32_t *dt_wpos, hipStream_t s);
 hipError_t launch_inflate(const uint32_t *region, int64_t n_regions, const uint32_t *doc_off, const uint32_t *d_cap,
-                          int32_t M, const uint32_t *dt_wpos, uint32_t key_base, uint32_t *dt_word, uint32_t *wt_key,
-                          uint32_t *wt_rowoff, hipStream_t s);
+                          int32_t M, const uint32_t *dt_wpos, uint32_t key_base, uint32_t *dt_word, uint2 *wt_kr,
+                          hipStream_t s);
 hipError_t launch_doc_gather_z(const uint32_t *dt_wpos, const uint16_t *z_w, int64_t n, int32_t *z_doc, hipStream_t s);
 hipError_t launch_doc_scatter_z(const int32_t *z_doc, const uint32_t *dt_wpos, int64_t n, int32_t K, uint16_t *z_w,
                                 unsigned long long *bad, hipStream_t s);
@@ -133,7 +133,8 @@ struct SkipRec {
 
 struct DevState {
   // layout
-  uint32_t *doc_off, *dt_word, *dt_key, *dt_wpos, *word_off, *wt_rowoff, *wt_key;
+  uint32_t *doc_off, *dt_word, *dt_key, *dt_wpos, *word_off;
+  uint2 *wt_kr;       // per word-ordered token: (input index = RNG key, D-row offset of its document)
   uint32_t *region;   // 3 per region
   uint32_t *heavy_docs;  // documents longer than kHeavyDoc tokens (one workgroup each in the doc kernels)
   uint8_t *split;     // per dense word
