@@ -1402,13 +1402,19 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
     }
 
     const WordState w{wh, qb, nb, K, qhalf, K1, a1, qp, p.alpha, s_qw, s_ql};
-    for (uint32_t base = b + uint32_t(wave) * kWave; base < e; base += NB) {
+    // tokens per batch: 64, or fewer when the region has too few tokens to
+    // give every wave a whole batch, so that a small region's batches (each
+    // a chain of dependent loads and rounds) run side by side on several
+    // waves instead of one after another on one
+    const uint32_t bsz = min(uint32_t(kWave), max(16u, ((e - b + uint32_t(NB / kWave) - 1u) / uint32_t(NB / kWave) + 15u) & ~15u));
+    for (uint32_t base = b + uint32_t(wave) * bsz; base < e; base += uint32_t(NB / kWave) * bsz) {
       const int ln = lane_here();  // the lane, recomputed per batch
       const uint32_t j = base + uint32_t(ln);
+      const uint32_t be = min(e, base + bsz);  // the batch's end
       // the slot, key and row offset are loaded together (one latency); the
       // row header only for the tokens left to draw
       uint32_t sk = 0, key = 0, off = 0;
-      if (j < e) {
+      if (j < be) {
         const uint2 kr = d.wt_kr[j];
         key = kr.x;
         off = kr.y;  // the row's first slot (its header)
@@ -1416,7 +1422,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
         // document position) in the document-ordered bitmap
         sk = by_doc ? d.skip_doc[key >> 5] >> (key & 31u) : d.skip_bits[j >> 5] >> (j & 31u);
       }
-      const bool und = j < e && !(sk & 1u);
+      const bool und = j < be && !(sk & 1u);
       uint32_t nnz = 0;
       if (und) {
         nnz = d.d_ent[off] & 0xFFFFu;
@@ -1435,7 +1441,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       // (K1 for the tokens the step-3 test decided) leave in one coalesced store
       uint32_t topic = K1;
       if (und) topic = finish_draw(ln, bt, w, d.d_ent);
-      if (j < e) d.z_w[j] = uint16_t(topic);
+      if (j < be) d.z_w[j] = uint16_t(topic);
     }
     __syncthreads();
   }
