@@ -48,6 +48,11 @@ struct ChunkSlot {
 struct ChunkMode {
   std::vector<ChunkInfo> c;
   ChunkSlot slot[2];
+  // topics on their way home: a chunk's new topics are copied here on the
+  // device, so that its slot takes the next upload without waiting for the
+  // download (two buffers, alternating like the slots)
+  uint16_t *z_out[2] = {nullptr, nullptr};
+  hipEvent_t z_out_free[2] = {nullptr, nullptr};
   hipStream_t h2d = nullptr, d2h = nullptr;
   std::vector<hipEvent_t> z_home;  // per chunk: its topics are back in host memory
   int32_t *w_next = nullptr;
@@ -69,6 +74,8 @@ void release_chunks(ChunkMode *cm) {
     for (hipEvent_t ev : {s.loaded, s.computed, s.unloaded})
       if (ev) (void)hipEventDestroy(ev);
   for (hipEvent_t ev : cm->z_home)
+    if (ev) (void)hipEventDestroy(ev);
+  for (hipEvent_t ev : cm->z_out_free)
     if (ev) (void)hipEventDestroy(ev);
   if (cm->h2d) (void)hipStreamDestroy(cm->h2d);
   if (cm->d2h) (void)hipStreamDestroy(cm->d2h);
@@ -216,6 +223,10 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
   HIP_TRY(h, hipStreamCreateWithFlags(&cm.d2h, hipStreamNonBlocking));
   cm.z_home.assign(cm.c.size(), nullptr);
   for (hipEvent_t &ev : cm.z_home) HIP_TRY(h, hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+  for (int q = 0; q < 2; ++q) {
+    LDA_TRY(dalloc(h, &cm.z_out[q], cm.max_tok));
+    HIP_TRY(h, hipEventCreateWithFlags(&cm.z_out_free[q], hipEventDisableTiming));
+  }
   for (ChunkInfo &ci : cm.c) {
     HIP_TRY(h, hipHostMalloc(reinterpret_cast<void **>(&ci.h_wpos), size_t(ci.ntok) * 4, hipHostMallocDefault));
     HIP_TRY(h, hipHostMalloc(reinterpret_cast<void **>(&ci.h_z), size_t(ci.ntok) * 2, hipHostMallocDefault));
@@ -350,12 +361,18 @@ lda_status chunked_iterate(lda_handle *h, int32_t n_iters, lda_iter_stats *stats
         dw.w_dense = cm.w_next;
         dw.T = cm.t_next;
         HIP_TRY(h, launch_rebuild_w(dw, ci.p, h->stream));
+        // the new topics leave the slot for a download buffer (once that
+        // buffer's previous download is done), which frees the slot
+        uint16_t *zo = cm.z_out[c & 1];
+        HIP_TRY(h, hipStreamWaitEvent(h->stream, cm.z_out_free[c & 1], 0));
+        HIP_TRY(h, hipMemcpyAsync(zo, sl.z_w, size_t(ci.ntok) * 2, hipMemcpyDeviceToDevice, h->stream));
         HIP_TRY(h, hipEventRecord(sl.computed, h->stream));
+        HIP_TRY(h, hipEventRecord(sl.unloaded, h->stream));
         // download the new topics
         HIP_TRY(h, hipStreamWaitEvent(cm.d2h, sl.computed, 0));
-        HIP_TRY(h, hipMemcpyAsync(ci.h_z, sl.z_w, size_t(ci.ntok) * 2, hipMemcpyDeviceToHost, cm.d2h));
+        HIP_TRY(h, hipMemcpyAsync(ci.h_z, zo, size_t(ci.ntok) * 2, hipMemcpyDeviceToHost, cm.d2h));
         HIP_TRY(h, hipEventRecord(cm.z_home[c], cm.d2h));
-        HIP_TRY(h, hipEventRecord(sl.unloaded, cm.d2h));
+        HIP_TRY(h, hipEventRecord(cm.z_out_free[c & 1], cm.d2h));
       }
       if (ev) HIP_TRY(h, hipEventRecord(ev[4], h->stream));
       std::swap(h->d.w_dense, cm.w_next);
