@@ -885,6 +885,7 @@ __device__ void draw_long(unsigned long long mask, const BatchLds &bt, const Wor
     const uint32_t nch = (t_nnz + 1u + kChunk - 1) / kChunk;
     uint32_t r[R];
     double s = 0.0, incl = 0.0, S = 0.0;
+    double tot = 0.0;  // lane c of the group (c < kGroup): the total of chunk c
     uint32_t c1 = 0xFFFFFFFFu;
     for (uint32_t ch = 0; ch < nch; ++ch) {
       load_run<R>(row + ch * kChunk, li, r);
@@ -892,7 +893,9 @@ __device__ void draw_long(unsigned long long mask, const BatchLds &bt, const Wor
       c1 = run_count_of<R>(r, w.K1, c1);
       s = run_sum<R>(r, w.wh);
       incl = row_incl_scan(s);
-      S += __shfl(incl, kGroup - 1, kGroup);
+      const double tch = __shfl(incl, kGroup - 1, kGroup);
+      S += tch;
+      tot = uint32_t(li) == ch ? tch : tot;
     }
     // max-topic branch, Eq. 7: M = W^[v][K1] * (D[d][K1] + alpha)
     const double Mm = w.a1 * (double(row_sum_u32(c1 <= 0xFFFFu ? c1 : 0u)) + w.alpha);
@@ -903,16 +906,37 @@ __device__ void draw_long(unsigned long long mask, const BatchLds &bt, const Wor
       // locate the chunk, then 16 candidate segments
       double cbase = Mm;
       bool in_s = false;
-      for (uint32_t ch = 0; ch < nch && !in_s; ++ch) {
-        if (nch > 1) {
-          load_run<R>(row + ch * kChunk, li, r);
-          if (ch == 0u && li == 0) r[0] = pad;
+      if (nch > 1 && nch <= uint32_t(kGroup)) {
+        // the chunk from the totals kept in the lanes: lane c's base is
+        // M + t_0 + ... + t_(c-1), added left to right as the walk below
+        // adds them, so only the chunk that holds x is read again
+        double mine = Mm;
+        for (uint32_t c = 0; c < nch; ++c) {
+          mine = uint32_t(li) == c ? cbase : mine;
+          cbase += __shfl(tot, int(c), kGroup);
+        }
+        const uint32_t hm = uint32_t(__ballot(uint32_t(li) < nch && x < mine + tot) >> (grp * kGroup)) & kGroupMask;
+        if (hm) {
+          const int cs = __ffs(hm) - 1;
+          in_s = true;
+          cbase = __shfl(mine, cs, kGroup);
+          load_run<R>(row + uint32_t(cs) * kChunk, li, r);
+          if (cs == 0 && li == 0) r[0] = pad;
           s = run_sum<R>(r, w.wh);
           incl = row_incl_scan(s);
         }
-        const double total = __shfl(incl, kGroup - 1, kGroup);
-        if (x < cbase + total) in_s = true;
-        else cbase += total;
+      } else {
+        for (uint32_t ch = 0; ch < nch && !in_s; ++ch) {
+          if (nch > 1) {
+            load_run<R>(row + ch * kChunk, li, r);
+            if (ch == 0u && li == 0) r[0] = pad;
+            s = run_sum<R>(r, w.wh);
+            incl = row_incl_scan(s);
+          }
+          const double total = __shfl(incl, kGroup - 1, kGroup);
+          if (x < cbase + total) in_s = true;
+          else cbase += total;
+        }
       }
       uint32_t k;
       double term, start;
