@@ -863,10 +863,17 @@ __device__ __forceinline__ uint32_t pick_segment(uint32_t k, double term, double
 
 // Draw the tokens of `mask` (rows longer than the small-group rounds take),
 // four at a time, one per 16-lane group, walking each row in chunks of
-// kChunk entries.
-__device__ void draw_long(unsigned long long mask, const BatchLds &bt, const WordState &w,
-                          const uint32_t *__restrict__ d_ent, int grp, int li, unsigned long long &after_s) {
+// kChunk entries.  `foll` marks the later tokens of runs of one word in one
+// document (same row; `starts` marks where runs begin): they share the row,
+// M, S' and Q' with the run's first token (Sec. 3.3), so the group that draws
+// the first one also draws them from the sums it holds, reading at most the
+// one chunk that holds each x.  Every draw is the one the token would get on
+// its own, bit for bit.
+__device__ void draw_long(unsigned long long mask, unsigned long long foll, unsigned long long starts,
+                          const BatchLds &bt, const WordState &w, const uint32_t *__restrict__ d_ent, int grp, int li,
+                          unsigned long long &after_s) {
   constexpr int R = kMaxRun;
+  mask &= ~foll;  // the runs' first tokens
   while (mask) {
     // the four lowest tokens of the mask, one per group (wave-uniform bit
     // arithmetic; a group with none gets src = -1)
@@ -875,11 +882,10 @@ __device__ void draw_long(unsigned long long mask, const BatchLds &bt, const Wor
     const int f2 = __ffsll((long long)m2) - 1, f3 = __ffsll((long long)m3) - 1;
     mask = m3 & (m3 - 1ull);
     const int src = grp == 0 ? f0 : grp == 1 ? f1 : grp == 2 ? f2 : f3;
-    bool in_m = false;
+    uint32_t n_m = 0;  // draws of this group in the max-topic branch
     if (src >= 0) {
     const uint32_t t_off = bt.off[src];
     const uint32_t t_nnz = bt.nnz[src];
-    const double t_u = bt.u[src];
     const uint32_t *row = d_ent + t_off;  // slot 0 is the row header
     const uint32_t pad = uint32_t(w.K) << 16;
     const uint32_t nch = (t_nnz + 1u + kChunk - 1) / kChunk;
@@ -899,23 +905,30 @@ __device__ void draw_long(unsigned long long mask, const BatchLds &bt, const Wor
     }
     // max-topic branch, Eq. 7: M = W^[v][K1] * (D[d][K1] + alpha)
     const double Mm = w.a1 * (double(row_sum_u32(c1 <= 0xFFFFu ? c1 : 0u)) + w.alpha);
-    const double x = t_u * ((Mm + S) + w.qp);
-    uint32_t topic = w.K1;
-    in_m = x < Mm;
-    if (!in_m) {
+    // with the totals kept in the lanes: lane c's chunk base
+    // M + t_0 + ... + t_(c-1), added left to right as the walk over the
+    // chunks adds them, and the base after the last chunk
+    const bool kept = nch > 1 && nch <= uint32_t(kGroup);
+    double mine = Mm, cb_end = Mm;
+    if (kept) {
+      for (uint32_t c = 0; c < nch; ++c) {
+        mine = uint32_t(li) == c ? cb_end : mine;
+        cb_end += __shfl(tot, int(c), kGroup);
+      }
+    }
+    // the draw of one token of the row from x = u * Z
+    auto draw_x = [&](double x) -> uint32_t {
+      if (x < Mm) {
+        n_m++;
+        return w.K1;
+      }
       // locate the chunk, then 16 candidate segments
       double cbase = Mm;
       bool in_s = false;
-      if (nch > 1 && nch <= uint32_t(kGroup)) {
-        // the chunk from the totals kept in the lanes: lane c's base is
-        // M + t_0 + ... + t_(c-1), added left to right as the walk below
-        // adds them, so only the chunk that holds x is read again
-        double mine = Mm;
-        for (uint32_t c = 0; c < nch; ++c) {
-          mine = uint32_t(li) == c ? cbase : mine;
-          cbase += __shfl(tot, int(c), kGroup);
-        }
+      if (kept) {
+        // only the chunk that holds x is read again
         const uint32_t hm = uint32_t(__ballot(uint32_t(li) < nch && x < mine + tot) >> (grp * kGroup)) & kGroupMask;
+        cbase = cb_end;
         if (hm) {
           const int cs = __ffs(hm) - 1;
           in_s = true;
@@ -950,9 +963,9 @@ __device__ void draw_long(unsigned long long mask, const BatchLds &bt, const Wor
 #pragma unroll
           for (int i = 0; i < R; ++i) hand[i] = r[i];
         }
-        const uint32_t mine = li < R ? hand[li] : 0u;
-        k = mine >> 16;
-        term = double(mine & 0xFFFFu) * w.wh[k];
+        const uint32_t own = li < R ? hand[li] : 0u;
+        k = own >> 16;
+        term = double(own & 0xFFFFu) * w.wh[k];
       } else {
         // Q' branch: boundaries (M + S') + Qcdf
         const double qstart = cbase;
@@ -970,12 +983,23 @@ __device__ void draw_long(unsigned long long mask, const BatchLds &bt, const Wor
       }
       const bool fallback = !in_s && term == 0.0 && start == 0.0;
       const uint32_t picked = pick_segment(k, term, start, x, grp);
-      topic = fallback ? k : picked;
-    }
+      return fallback ? k : picked;
+    };
+    const uint32_t topic = draw_x(bt.u[src] * ((Mm + S) + w.qp));
     if (li == 0) bt.top[src] = uint16_t(topic);
+    // the run's later tokens: lanes after src up to the next run start
+    const unsigned long long after = ~((2ull << src) - 1ull);  // the lanes above src
+    const unsigned long long nxt = starts & after;
+    unsigned long long fl = foll & after & (nxt ? (nxt & (0ull - nxt)) - 1ull : ~0ull);
+    while (fl) {
+      const int f = __ffsll((long long)fl) - 1;
+      fl &= fl - 1ull;
+      const uint32_t tf = draw_x(bt.u[f] * ((Mm + S) + w.qp));
+      if (li == 0) bt.top[f] = uint16_t(tf);
+    }
     }
     // outside the divergent part, so the count stays wave-uniform
-    after_s += uint32_t(__popcll(__ballot(in_m && li == 0)));
+    after_s += wave_sum_u32(li == 0 ? n_m : 0u);
   }
 }
 
@@ -1454,13 +1478,25 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
         bt.nnz[ln] = nnz;
         bt.u[ln] = uniform_draw(p.seed, t, key);
       }
+      // long rows: runs of tokens of one document (same row offset), whose
+      // later tokens draw from the sums of the run's first one
+      const unsigned long long lmask = __ballot(und && nnz + 1u > 512u);
+      unsigned long long starts = 0ull;
+      bool fol = false;
+      if (lmask) {
+        const uint32_t prev_off = uint32_t(__shfl(int(off), ln - 1));
+        starts = __ballot(ln == 0 || off != prev_off);
+        const unsigned long long below = ln ? ~0ull >> (64 - ln) : 0ull;
+        const int rs = 63 - __clzll((long long)(starts & (below | (1ull << ln))));  // this lane's run start
+        fol = ((lmask >> ln) & 1ull) && (lmask & below & (~0ull << rs)) != 0ull;
+      }
       n_sampled += uint32_t(__popcll(__ballot(und)));
-      nnz_sum += wave_sum_u32(nnz);
+      nnz_sum += wave_sum_u32(fol ? min(nnz, uint32_t(kChunk)) : nnz);  // a follower reads one chunk of its row
       // rows of up to 128 slots (header and entries): 4 lanes per token; up
       // to 256: 8 lanes; up to 512: 16 lanes; longer rows: 16 lanes, one
       // chunk of kChunk slots at a time
       draw_batch_small(und, nnz, bt, w, d.d_ent, ln, n_after_s);
-      draw_long(__ballot(und && nnz + 1u > 512u), bt, w, d.d_ent, ln / kGroup, ln % kGroup, n_after_s);
+      if (lmask) draw_long(lmask, __ballot(fol), starts, bt, w, d.d_ent, ln / kGroup, ln % kGroup, n_after_s);
       // the S' walks and Q' searches, one lane per token; the batch's topics
       // (K1 for the tokens the step-3 test decided) leave in one coalesced store
       uint32_t topic = K1;
