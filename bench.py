@@ -38,10 +38,11 @@ def log(msg):
 def sampler_alg_bytes(st, N):
     """Bytes the sampler must move per launch: per token its skip bit (read)
     and its topic slot (written: the drawn topic, or K1 for a skipped token);
-    per sampled token its key (4 B), D-row offset (4 B), row header (4 B) and
-    the nnz entries of its D row (4 B each); the W rows (4*K B per dense word,
-    4*nnz B per sparse word); the region and word records (12 + 48 B per
-    region)."""
+    per sampled token its key and D-row offset (8 B), row header (4 B) and
+    the entries of its D row it reads (4 B each: the whole row, or one chunk
+    for a later token of a long-row run of one word in one document); the W
+    rows (4*K B per dense word, 4*nnz B per sparse word); the region and word
+    records (12 + 48 B per region)."""
     return (N / 8 + 2 * N + 12 * st["sampled"] + 4 * st["nnz_scanned"] + st["row_bytes"] + 60 * st["regions"])
 
 

@@ -127,7 +127,9 @@ typedef struct {
   int64_t skip_step3;    /* tokens set to K1 by the step-3 test */
   int64_t skip_after_s;  /* tokens drawn as K1 by the second max-topic test */
   int64_t sampled;       /* tokens whose S' was built (not skipped at step 3) */
-  int64_t nnz_scanned;   /* sum of nnz(D[d]) over the sampled tokens */
+  int64_t nnz_scanned;   /* D-row entries the sampler read: nnz(D[d]) per sampled token, except one chunk
+                          * (at most 128) for a later token of a run of one word in one document whose row
+                          * is longer than 511 entries (it draws from the run's first token's sums) */
   int64_t regions;       /* regions handed out by the scheduler */
   int64_t dense_regions; /* of which regions of dense (full-row) words */
   int64_t row_bytes;     /* bytes of W rows the sampler needs: 4*K per dense word, 4*nnz per sparse word */
