@@ -42,8 +42,11 @@ def sampler_alg_bytes(st, N):
     the entries of its D row it reads (4 B each: the whole row, or one chunk
     for a later token of a long-row run of one word in one document); the W
     rows (4*K B per dense word, 4*nnz B per sparse word); the region and word
-    records (12 + 48 B per region)."""
-    return (N / 8 + 2 * N + 12 * st["sampled"] + 4 * st["nnz_scanned"] + st["row_bytes"] + 60 * st["regions"])
+    records (12 + 48 B per region).  The skip bits are N/8 coalesced bytes in
+    word order; with the document-ordered bitmap each token reads the 4-byte
+    word that holds its bit at its document position instead."""
+    skip = 4 * N if st.get("skip_marks") == 2 else N / 8
+    return (skip + 2 * N + 12 * st["sampled"] + 4 * st["nnz_scanned"] + st["row_bytes"] + 60 * st["regions"])
 
 
 def traffic_from_profile(workload):

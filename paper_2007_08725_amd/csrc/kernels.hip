@@ -540,9 +540,11 @@ __device__ void heavy_doc_pass(const DevState &d, const Params &p, uint32_t t, u
 // Steps 2-3 per document (Sec. 3.3): the D row spread into a per-wave
 // topic -> count table in LDS, then for every token C1 and C2 by lookup, u,
 // M, S_est and the skip test.  A skipped token's bit is set in the
-// word-ordered skip bitmap; the sampler writes K1 into its slot with the rest
-// of its batch.  KeyId: the input is sorted by document, so a token's key
-// (its input index) is its document-order position.
+// word-ordered skip bitmap (one scattered bit at its word-order slot) or, in
+// the iterations doc_marks chooses, in the document-ordered one (coalesced
+// bits at its document position); the sampler writes K1 into its slot with
+// the rest of its batch.  KeyId: the input is sorted by document, so a
+// token's key (its input index) is its document-order position.
 template <bool KeyId>
 __global__ __launch_bounds__(kBlock) void k_doc_pass(DevState d, Params p, uint32_t t,
                                                      unsigned long long *__restrict__ stats) {
