@@ -331,9 +331,11 @@ __global__ __launch_bounds__(kBlock) void k_beta_sum(DevState d, Params p) {
   if (threadIdx.x == 0) d.beta_sum[0] = s;
 }
 
+constexpr int kWordTab = 4096;  // topics of the sparse-row count table of k_word_pre
 __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
   const int r = blockIdx.x, tid = threadIdx.x;
   const int K = p.K;
+  __shared__ uint16_t ctab[kWordTab];
   __shared__ double sv[kBlock * kTop];
   __shared__ uint32_t sk[kBlock * kTop];
   __shared__ double red[kBlock / kWave];
@@ -399,8 +401,22 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
       t.k[q] = 0xFFFFFFFFu;
     }
   }
+  // a sparse row spread into a table of counts in LDS (K up to kWordTab),
+  // so that each thread reads its topics' counts instead of searching the row
+  const bool tab = !dense && K <= kWordTab;
+  if (tab) {
+    for (int k = tid; k < K; k += kBlock) ctab[k] = 0;
+    __syncthreads();
+    for (uint32_t q = uint32_t(tid); q < nnz; q += kBlock) {
+      const uint32_t ent = ents[q];
+      ctab[ent >> 16] = uint16_t(ent & 0xFFFFu);
+    }
+    __syncthreads();
+  }
   if (dense) {
     for (int k = tid; k < K; k += kBlock) top_insert(t, what(uint32_t(wrow[k]), p.beta, d.den[k]), uint32_t(k));
+  } else if (tab) {
+    for (int k = c0; k < c1; ++k) top_insert(t, what(ctab[k], p.beta, d.den[k]), uint32_t(k));
   } else {
     uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
     for (int k = c0; k < c1; ++k) {
@@ -417,6 +433,12 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
   if (dense) {
     for (int k = tid; k < K; k += kBlock) {
       const double w = what(uint32_t(wrow[k]), p.beta, d.den[k]);
+      sw += w;
+      if (p.two_branch || uint32_t(k) != K1) q += p.alpha * w;
+    }
+  } else if (tab) {
+    for (int k = c0; k < c1; ++k) {
+      const double w = what(ctab[k], p.beta, d.den[k]);
       sw += w;
       if (p.two_branch || uint32_t(k) != K1) q += p.alpha * w;
     }
