@@ -312,6 +312,7 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
     LDA_TRY(dalloc(h, &d.ts_x, sl));
     LDA_TRY(dalloc(h, &d.ts_c1, sl));
     LDA_TRY(dalloc(h, &d.ts_code, sl));
+    LDA_TRY(dalloc(h, &d.ts_list, sl));
     LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(K)));
   }
   unsigned long long stt[kStatsPerIter];

@@ -1570,7 +1570,12 @@ __global__ __launch_bounds__(64) void k_sampler_light(DevState d, Params p, uint
 //   pass 1, tile 1: the S' terms of the other topics, then the draw (Eq. 5);
 //                   draws in M, in the tile-1 part of S' or in a tile-1 Q'
 //                   block finish here, the others are recorded;
-//   pass 2, tile 0: the recorded draws finish.
+//   pass 2, tile 0: the recorded draws finish, over the list of their
+//                   tokens that pass 1 keeps.
+// A row is in ascending topic order, so pass 0 reads its chunks only up to
+// the first one that reaches topic KT (the split chunk, kept per token),
+// pass 1 only from there on, and pass 2's S' walk ends there: every chunk
+// left out holds only terms of the other tile, which add exact zeros.
 // The canonical order [K1 | S' ascending | Q' ascending] is unchanged: the
 // tile-0 part of S' precedes the tile-1 part.  A 16-lane group draws one
 // token at a time and reads its D row in chunks of kChunk slots; entries of
@@ -1579,6 +1584,7 @@ __global__ __launch_bounds__(64) void k_sampler_light(DevState d, Params p, uint
 struct TileState {
   const double *wt;  // the tile: W^' of topics [base, base + KT), zeros past the tile's end
   uint32_t base, kt;
+  uint32_t lds;      // the tile's LDS address minus base * 8 (mod 2^32), for run_sum_in_tile
 };
 
 // W^' of a packed D entry's topic if it lies in the tile, else 0 (wt[kt] is 0).
@@ -1608,24 +1614,39 @@ __device__ __forceinline__ double run_sum_tile(const uint32_t (&r)[kMaxRun], con
   return s;
 }
 
+// The same sum for a run whose topics all lie in the tile [base, base + KT]:
+// the LDS address (topic - base) * 8 + tile is one v_mad_u32_u16 on the
+// entry's high half, with lds = the tile's LDS address - base * 8 (mod 2^32).
+__device__ __forceinline__ double run_sum_in_tile(const uint32_t (&r)[kMaxRun], uint32_t lds) {
+  double s = 0.0;
+#pragma unroll
+  for (int i = 0; i < kMaxRun; ++i) {
+    uint32_t a;
+    asm("v_mad_u32_u16 %0, %1, 8, %2 op_sel:[1,0,0,0]" : "=v"(a) : "v"(r[i]), "s"(lds));
+    s = __builtin_fma(double(r[i] & 0xFFFFu), *(lds_f64 *)(size_t)a, s);
+  }
+  return s;
+}
+
 // The S' draw inside one tile: the entry whose segment holds x, the tile's
-// terms starting at `base`; the chunks are walked again in order.  When
+// terms starting at `base`; chunks [ch0, nch) are walked again in order (the
+// others hold no term of the tile).  When
 // rounding leaves x past the tile's terms, the last positive term is taken.
 __device__ uint32_t tile_walk(const uint32_t *__restrict__ row, uint32_t slots, const TileState &ts, double base,
-                              double x, uint32_t pad, int grp, int li, uint32_t *__restrict__ hand) {
-  const uint32_t nch = (slots + kChunk - 1) / kChunk;
+                              double x, uint32_t pad, int grp, int li, uint32_t *__restrict__ hand, uint32_t ch0,
+                              uint32_t nch, uint32_t sc) {
   uint32_t r[kMaxRun];
   int last_pos = -1;
   double last_base = base;
   uint32_t pick = nch;
   double s = 0.0, incl = 0.0;
   uint32_t rn[kMaxRun];
-  load_run_masked(row, 0, slots, li, pad, rn);
-  for (uint32_t ch = 0; ch < nch; ++ch) {
+  load_run_masked(row, ch0, slots, li, pad, rn);
+  for (uint32_t ch = ch0; ch < nch; ++ch) {
 #pragma unroll
     for (int i = 0; i < kMaxRun; ++i) r[i] = rn[i];
     if (ch + 1 < nch) load_run_masked(row, ch + 1, slots, li, pad, rn);  // the next chunk's loads, in flight meanwhile
-    s = run_sum_tile(r, ts);
+    s = ch == sc ? run_sum_tile(r, ts) : run_sum_in_tile(r, ts.lds);
     incl = row_incl_scan(s);
     const double total = __shfl(incl, kGroup - 1, kGroup);
     if (total > 0.0) {
@@ -1644,7 +1665,7 @@ __device__ uint32_t tile_walk(const uint32_t *__restrict__ row, uint32_t slots, 
     pick = uint32_t(last_pos);
     base = last_base;
     load_run_masked(row, pick, slots, li, pad, r);
-    s = run_sum_tile(r, ts);
+    s = pick == sc ? run_sum_tile(r, ts) : run_sum_in_tile(r, ts.lds);
     incl = row_incl_scan(s);
   }
   const int sel = run_lane(s, incl, base, x, grp);
@@ -1660,32 +1681,81 @@ __device__ uint32_t tile_walk(const uint32_t *__restrict__ row, uint32_t slots, 
 }
 
 // Fills the tile [base, base + len) of the region's word (zeros elsewhere,
-// at K1 and at the padding topic K).
+// at K1 and at the padding topic K).  Each thread issues the loads of
+// kFillBatch topics (or row entries) before it uses the first, so that a
+// fill waits on a few memory latencies rather than one per topic.
+constexpr int kFillBatch = 8;
 __device__ void fill_tile(const DevState &d, const Params &p, uint32_t v, uint32_t K1, uint32_t base, uint32_t len,
                           uint32_t kt, double *__restrict__ wt, int tid, int nthreads) {
-  const int K = p.K;
+  const uint32_t K = uint32_t(p.K), n = kt + uint32_t(kGroup), nt = uint32_t(nthreads);
+  // loads at clamped (always valid) topics; the topics outside the tile get 0
   if (int32_t(v) < p.n_dense) {
     const int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
-    for (uint32_t q = uint32_t(tid); q < kt + uint32_t(kGroup); q += uint32_t(nthreads)) {
-      const uint32_t k = base + q;
-      wt[q] = q < len && k < uint32_t(K) && k != K1 ? what(uint32_t(wrow[k]), p.beta, d.den[k]) : 0.0;
+    uint32_t q0 = uint32_t(tid);
+    for (; q0 + (kFillBatch - 1) * nt < n; q0 += kFillBatch * nt) {
+      uint32_t cnt[kFillBatch];
+      double dn[kFillBatch];
+#pragma unroll
+      for (int u = 0; u < kFillBatch; ++u) {
+        const uint32_t k = min(base + q0 + uint32_t(u) * nt, K - 1u);
+        cnt[u] = uint32_t(wrow[k]);
+        dn[u] = d.den[k];
+      }
+#pragma unroll
+      for (int u = 0; u < kFillBatch; ++u) {
+        const uint32_t q = q0 + uint32_t(u) * nt, k = base + q;
+        wt[q] = q < len && k < K && k != K1 ? what(cnt[u], p.beta, dn[u]) : 0.0;
+      }
+    }
+    for (; q0 < n; q0 += nt) {
+      const uint32_t k = base + q0;
+      wt[q0] = q0 < len && k < K && k != K1 ? what(uint32_t(wrow[k]), p.beta, d.den[k]) : 0.0;
     }
   } else {
     const int s = int(v) - p.n_dense;
     const uint32_t *ents = d.ws_ent + d.ws_cap[s];
     const uint32_t nnz = d.ws_nnz[s];
-    for (uint32_t q = uint32_t(tid); q < kt + uint32_t(kGroup); q += uint32_t(nthreads)) {
-      const uint32_t k = base + q;
-      wt[q] = q < len && k < uint32_t(K) && k != K1 ? d.bden[k] : 0.0;
+    uint32_t q0 = uint32_t(tid);
+    for (; q0 + (kFillBatch - 1) * nt < n; q0 += kFillBatch * nt) {
+      double bd[kFillBatch];
+#pragma unroll
+      for (int u = 0; u < kFillBatch; ++u) bd[u] = d.bden[min(base + q0 + uint32_t(u) * nt, K - 1u)];
+#pragma unroll
+      for (int u = 0; u < kFillBatch; ++u) {
+        const uint32_t q = q0 + uint32_t(u) * nt, k = base + q;
+        wt[q] = q < len && k < K && k != K1 ? bd[u] : 0.0;
+      }
+    }
+    for (; q0 < n; q0 += nt) {
+      const uint32_t k = base + q0;
+      wt[q0] = q0 < len && k < K && k != K1 ? d.bden[k] : 0.0;
     }
     __syncthreads();
-    for (uint32_t q = uint32_t(tid); q < nnz; q += uint32_t(nthreads)) {
-      const uint32_t ent = ents[q], k = ent >> 16;
-      if (k >= base && k < base + len && k < uint32_t(K) && k != K1) wt[k - base] = what(ent & 0xFFFFu, p.beta, d.den[k]);
+    for (uint32_t q0 = uint32_t(tid); q0 < nnz; q0 += kFillBatch * nt) {
+      uint32_t ent[kFillBatch];
+#pragma unroll
+      for (int u = 0; u < kFillBatch; ++u) ent[u] = ents[min(q0 + uint32_t(u) * nt, nnz - 1u)];
+      double dn[kFillBatch];
+#pragma unroll
+      for (int u = 0; u < kFillBatch; ++u) dn[u] = d.den[min(ent[u] >> 16, K - 1u)];
+#pragma unroll
+      for (int u = 0; u < kFillBatch; ++u) {
+        const uint32_t k = ent[u] >> 16;
+        if (q0 + uint32_t(u) * nt < nnz && k >= base && k < base + len && k < K && k != K1)
+          wt[k - base] = what(ent[u] & 0xFFFFu, p.beta, dn[u]);
+      }
     }
   }
   __syncthreads();
 }
+
+constexpr int kScanBatch = 8;  // Q' block sums a lane of the prefix scan reads at a time
+
+// A token's records for one pass of the tiled sampler.
+struct TiledTok {
+  uint32_t sk, rec, cn;
+  uint2 kr;
+};
 
 constexpr int kTiledBlock = kTiledThreads;  // threads per workgroup of the tiled sampler (16 waves)
 constexpr int kTiledAhead = 2;              // chunks whose loads a group issues together
@@ -1699,7 +1769,8 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
   double *wt = lds;                                  // [kt + kGroup]
   double *qb = lds + kt + kGroup;                    // [nb + 1]: prefix of alpha*W^' over blocks of kGroup topics
   uint32_t *s_hand = reinterpret_cast<uint32_t *>(qb + nb + 1);  // [kTiledBlock / kGroup * kMaxRun]
-  uint32_t *s_reg = s_hand + kTiledBlock / kGroup * kMaxRun;     // [4]
+  uint32_t *s_reg = s_hand + kTiledBlock / kGroup * kMaxRun;     // [6]: region, flag, list length
+  double *s_u = reinterpret_cast<double *>(s_reg + 6);            // [kTiledBlock]: u of the next 16 steps per wave
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
   const int wave = tid / kWave, grp = lane / kGroup, li = lane % kGroup;
   if (blockIdx.x == 0 && tid == 0) stats[ST_MARKS] = 1ull;  // the word-ordered bitmap only
@@ -1710,12 +1781,14 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
   double *sc_x = d.ts_x + size_t(blockIdx.x) * size_t(p.max_region);
   uint32_t *sc_c1 = d.ts_c1 + size_t(blockIdx.x) * size_t(p.max_region);
   uint32_t *sc_code = d.ts_code + size_t(blockIdx.x) * size_t(p.max_region);
+  uint32_t *sc_list = d.ts_list + size_t(blockIdx.x) * size_t(p.max_region);
   unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0, n_reg = 0, n_dreg = 0, row_bytes = 0;
   const int waves = kTiledBlock / kWave;
   for (;;) {
     if (tid == 0) {
       const uint32_t r = atomicAdd(&d.counters[CNT_SAMPLER], 1u);
       s_reg[3] = int64_t(r) < p.n_regions ? 1u : 0u;
+      s_reg[4] = 0u;
       if (s_reg[3]) {
         s_reg[0] = d.region[3 * size_t(r)];
         s_reg[1] = d.region[3 * size_t(r) + 1];
@@ -1734,119 +1807,218 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
       row_bytes += int32_t(v) < p.n_dense ? 4ull * uint64_t(K) : 4ull * d.ws_nnz[int(v) - p.n_dense];
     const WordRec rec = d.wrec[v];
     const uint32_t K1 = rec.k1;
+    // the padding entry of tile 0: count 0, a topic inside the tile other
+    // than K1 (so that C1's search passes over it)
+    const uint32_t pad0 = (K1 == 0u ? 1u : 0u) << 16;
     for (int pass = 0; pass < 3; ++pass) {
       const uint32_t tbase = pass == 1 ? kt : 0u;
       const uint32_t tlen = pass == 1 ? uint32_t(K) + 1u - kt : kt;
       fill_tile(d, p, v, K1, tbase, tlen, kt, wt, tid, kTiledBlock);
-      const TileState ts{wt, tbase, kt};
+      const TileState ts{wt, tbase, kt, uint32_t(reinterpret_cast<uintptr_t>(wt)) - tbase * 8u};
       if (pass < 2) {
         // this tile's blocks of the Q' prefix, continuing the previous tile's
         const int b0 = int(tbase) / kGroup, b1 = min(nb, int(tbase + tlen + kGroup - 1) / kGroup);
+        // block sums, one thread per block adding its topics in order; lane l
+        // starts l % 16 steps late, so that the lanes of a row read 16
+        // different topics of their blocks (16 different LDS bank pairs)
+        // instead of all the same one
+        const int skew = lane & (kGroup - 1);
         for (int blk = b0 + tid; blk < b1; blk += kTiledBlock) {
+          const double *wb = wt + (blk - b0) * kGroup;
           double sum = 0.0;
-          for (int i = 0; i < kGroup; ++i) sum += p.alpha * wt[(blk - b0) * kGroup + i];
+#pragma unroll 8
+          for (int st = 0; st < 2 * kGroup - 1; ++st) {
+            const int i = st - skew;
+            const double w = wb[min(max(i, 0), kGroup - 1)];
+            sum = i >= 0 && i < kGroup ? __builtin_fma(p.alpha, w, sum) : sum;
+          }
           qb[blk + 1] = sum;
         }
         __syncthreads();
         if (wave == 0) {
+          // lane l scans a run of per consecutive blocks: their sum, a scan of
+          // the lane sums, then the running prefix over the run; the lane's
+          // block sums are read kScanBatch at a time (one LDS round trip each)
           const int n = b1 - b0;
           const int per = (n + kWave - 1) / kWave;
           const int q0 = min(n, lane * per), q1 = min(n, q0 + per);
           double sum = 0.0;
-          for (int q = q0; q < q1; ++q) sum += qb[b0 + q + 1];
+          for (int q = q0; q < q1; q += kScanBatch) {
+            double v[kScanBatch];
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i) v[i] = q + i < q1 ? qb[b0 + q + i + 1] : 0.0;
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i)
+              if (q + i < q1) sum += v[i];
+          }
           const double carry = pass == 0 ? 0.0 : qb[b0];
           double run = carry + (group_incl_scan<kWave>(sum, lane) - sum);
-          for (int q = q0; q < q1; ++q) {
-            run += qb[b0 + q + 1];
-            qb[b0 + q + 1] = run;
+          for (int q = q0; q < q1; q += kScanBatch) {
+            double v[kScanBatch];
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i) v[i] = q + i < q1 ? qb[b0 + q + i + 1] : 0.0;
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i)
+              if (q + i < q1) {
+                run += v[i];
+                qb[b0 + q + i + 1] = run;
+              }
           }
           if (pass == 0 && lane == 0) qb[0] = 0.0;
         }
         __syncthreads();
       }
+      const uint32_t stride = uint32_t(waves) * 4u;
+      if (pass == 2) {
+        // the draws pass 1 recorded, in the order it listed their tokens,
+        // four per wave at a time
+        const uint32_t nl = __builtin_amdgcn_readfirstlane(s_reg[4]);
+        for (uint32_t i0 = uint32_t(wave) * 4u; i0 < nl; i0 += stride) {
+          const uint32_t i = i0 + uint32_t(grp);
+          if (i >= nl) continue;
+          const uint32_t q = sc_list[i], j = b + q;
+          const uint32_t code = sc_code[q], cn = sc_c1[q];
+          const uint32_t *row = d.d_ent + d.wt_kr[j].y;
+          const double x = sc_x[q];
+          uint32_t topic;
+          if ((code & 3u) == 1u) {
+            const uint32_t slots = d_row_slots(cn >> 16);
+            const double Mm = rec.a1 * (double(cn & 0xFFFFu) + p.alpha);
+            topic = tile_walk(row, slots, ts, Mm, x, pad0, grp, li, hand, 0u, (code >> 2) + 1u, code >> 2);
+            if (topic == uint32_t(-1)) topic = K1;  // no positive S' term below KT: cannot happen for x in S'
+          } else {
+            const int lo = int(code >> 2);
+            const uint32_t k = uint32_t(lo * kGroup + li);
+            const double term = p.alpha * wt[k];
+            topic = pick_segment(k, term, sc_s[q] + qb[lo], x, grp);
+          }
+          if (li == 0) d.z_w[j] = uint16_t(topic);
+        }
+        __syncthreads();
+        continue;
+      }
       // four tokens per wave at a time, one per 16-lane group.  A token's
-      // skip word, row offset and pass-2 code are loaded together, then its
-      // row header and first chunk together (the header is slot 0)
-      for (uint32_t j0 = b + uint32_t(wave) * 4u; j0 < e; j0 += uint32_t(waves) * 4u) {
+      // skip word, key and row offset, and its records of pass 0 are loaded
+      // one step ahead, while the group works on the previous token (the
+      // fp64 record is loaded beside the row's first chunk); pass 0 then
+      // loads the row header and first chunk together (the header is slot 0)
+      auto tok_load = [&](uint32_t jt) {
+        const uint32_t jj = min(jt, e - 1u), qq = jj - b;
+        TiledTok o;
+        o.sk = d.skip_bits[jj >> 5];
+        o.kr = d.wt_kr[jj];
+        o.rec = pass == 0 ? 0u : sc_code[qq];  // pass 1: the split chunk
+        o.cn = pass == 0 ? 0u : sc_c1[qq];     // pass 1: pass 0's C1 and the row length
+        return o;
+      };
+      TiledTok nxt = tok_load(b + uint32_t(wave) * 4u + uint32_t(grp));
+      // pass 1: lane L draws u for the token of group L % 4 at step L / 4 of
+      // each block of 16 steps into the wave's slice of LDS
+      double *s_uw = s_u + wave * kWave;
+      uint32_t step = 0;
+      for (uint32_t j0 = b + uint32_t(wave) * 4u; j0 < e; j0 += stride, ++step) {
         const uint32_t j = j0 + uint32_t(grp);
         const uint32_t q = j - b;  // place in the region
-        const uint32_t jj = min(j, e - 1u);
-        const uint32_t sk = d.skip_bits[jj >> 5], off = d.wt_kr[jj].y;
-        const uint32_t code0 = pass == 2 ? sc_code[jj - b] : 0u;
+        const TiledTok tk = nxt;
+        if (j0 + stride < e) nxt = tok_load(j + stride);
+        if (pass == 1 && (step & 15u) == 0u) {
+          const uint32_t jl = j0 + uint32_t(lane >> 2) * stride + uint32_t(lane & 3);
+          s_uw[lane] = uniform_draw(p.seed, t, d.wt_kr[min(jl, e - 1u)].x);
+          __builtin_amdgcn_wave_barrier();
+        }
+        const uint32_t sk = tk.sk;
+        const uint2 kr = tk.kr;
+        const uint32_t rec0 = tk.rec, cn0 = tk.cn;
         const bool skipped = j < e && ((sk >> (j & 31u)) & 1u);
         if (pass == 0 && skipped && li == 0) d.z_w[j] = uint16_t(K1);  // decided by the step-3 test
-        bool live = j < e && !skipped;
-        if (pass == 2) live = live && code0 != 0u;
+        const bool live = j < e && !skipped;
         if (!live) continue;
-        const uint32_t *row = d.d_ent + off;
-        // the first chunk in full (a row start plus kChunk slots stays
-        // inside the kRowPad slots past the last row), masked below
-        uint32_t r0[kMaxRun];
-        if (pass < 2) {
+        const uint32_t *row = d.d_ent + kr.y;
+        if (pass == 0) {
+          // the first chunk in full (a row start plus kChunk slots stays
+          // inside the kRowPad slots past the last row), masked below
+          uint32_t r0[kMaxRun];
 #pragma unroll
           for (int i = 0; i < kMaxRun; ++i) r0[i] = row[uint32_t(li) * kMaxRun + uint32_t(i)];
-        }
-        const uint32_t nnz = uint32_t(__shfl(int(pass < 2 ? r0[0] : row[0]), 0, kGroup)) & 0xFFFFu;
-        const uint32_t slots = d_row_slots(nnz);
-        const uint32_t nch = (slots + kChunk - 1) / kChunk;
-        if (pass < 2) {
+          const uint32_t nnz = uint32_t(__shfl(int(r0[0]), 0, kGroup)) & 0xFFFFu;
+          const uint32_t slots = d_row_slots(nnz);
+          const uint32_t nch = (slots + kChunk - 1) / kChunk;
 #pragma unroll
           for (int i = 0; i < kMaxRun; ++i) {
             const uint32_t qs = uint32_t(li) * kMaxRun + uint32_t(i);
-            if (qs == 0u || qs >= slots) r0[i] = pad;
+            if (qs == 0u || qs >= slots) r0[i] = pad0;
           }
-        }
-        if (pass == 0) {
-          // S' over the tile-0 topics, and C1 over the whole row; the
-          // loads of up to kTiledAhead chunks are issued together
+          // S' over the tile-0 topics and C1, chunk by chunk up to the split
+          // chunk; the loads of up to kTiledAhead chunks are issued together.
+          // A chunk that ends below KT (not the split chunk) lies in the tile.
+          // Slots outside the row read pad0, a count-0 entry in the tile.
           double s0 = 0.0;
           uint32_t c1 = 0xFFFFFFFFu;
           c1 = run_count_of<kMaxRun>(r0, K1, c1);
-          s0 += run_sum_tile(r0, ts);
-          for (uint32_t c0 = 1; c0 < nch; c0 += kTiledAhead) {
+          uint32_t sc = 0;
+          bool open = nch > 1u && (uint32_t(__shfl(int(r0[kMaxRun - 1]), kGroup - 1, kGroup)) >> 16) < kt;
+          s0 += open ? run_sum_in_tile(r0, ts.lds) : run_sum_tile(r0, ts);
+          for (uint32_t c0 = 1; open; c0 += kTiledAhead) {
             uint32_t r[kTiledAhead][kMaxRun];
 #pragma unroll
-            for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
+            for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad0, r[c]);
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) {
-              c1 = run_count_of<kMaxRun>(r[c], K1, c1);
-              s0 += run_sum_tile(r[c], ts);
+              if (open) {
+                c1 = run_count_of<kMaxRun>(r[c], K1, c1);
+                sc = c0 + uint32_t(c);
+                open = sc + 1u < nch && (uint32_t(__shfl(int(r[c][kMaxRun - 1]), kGroup - 1, kGroup)) >> 16) < kt;
+                s0 += open ? run_sum_in_tile(r[c], ts.lds) : run_sum_tile(r[c], ts);
+              }
             }
           }
           const double S0 = gsum<kGroup>(s0);
           c1 = gsum_u32<kGroup>(c1 <= 0xFFFFu ? c1 : 0u);
           if (li == 0) {
             sc_s[q] = S0;
-            sc_c1[q] = c1;
-            sc_code[q] = 0u;
+            sc_c1[q] = c1 | (nnz << 16);
+            sc_code[q] = sc;
           }
-        } else if (pass == 1) {
+        } else {
+          const uint32_t sc = rec0;
+          const uint32_t nnz = cn0 >> 16;
+          const uint32_t slots = d_row_slots(nnz);
+          const uint32_t nch = (slots + kChunk - 1) / kChunk;
+          // S' over the tile-1 topics, and C1 where pass 0 did not read it,
+          // from the split chunk on (the chunks after it lie in the tile;
+          // slots past the row read the padding entry, topic K)
           double s1 = 0.0;
-          s1 += run_sum_tile(r0, ts);
-          for (uint32_t c0 = 1; c0 < nch; c0 += kTiledAhead) {
+          uint32_t c1 = 0xFFFFFFFFu;
+          for (uint32_t c0 = sc; c0 < nch; c0 += kTiledAhead) {
             uint32_t r[kTiledAhead][kMaxRun];
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
+            c1 = run_count_of<kMaxRun>(r[0], K1, c1);
+            s1 += c0 == sc ? run_sum_tile(r[0], ts) : run_sum_in_tile(r[0], ts.lds);
 #pragma unroll
-            for (int c = 0; c < kTiledAhead; ++c) s1 += run_sum_tile(r[c], ts);
+            for (int c = 1; c < kTiledAhead; ++c) {
+              c1 = run_count_of<kMaxRun>(r[c], K1, c1);
+              s1 += run_sum_in_tile(r[c], ts.lds);
+            }
           }
           const double S1 = gsum<kGroup>(s1);
           const double S0 = sc_s[q];
-          const uint32_t c1 = sc_c1[q];
-          const double Mm = rec.a1 * (double(c1) + p.alpha);  // Eq. 7
+          // topic K1's entry lies in one chunk: pass 0 or this pass saw it (both
+          // when it is the split chunk), the other read 0
+          const uint32_t C1 = max(cn0 & 0xFFFFu, gsum_u32<kGroup>(c1 <= 0xFFFFu ? c1 : 0u));
+          const double Mm = rec.a1 * (double(C1) + p.alpha);  // Eq. 7
           const double S = S0 + S1;
-          const double u = uniform_draw(p.seed, t, d.wt_kr[j].x);
-          const double x = u * ((Mm + S) + rec.qp);
+          const double x = s_uw[((step & 15u) << 2) | uint32_t(grp)] * ((Mm + S) + rec.qp);
           uint32_t topic = K1, code = 0u;
           double keep = 0.0;
           if (x < Mm) {
             if (li == 0) n_after_s++;
           } else if (x < Mm + S) {
             if (x < Mm + S0) {
-              code = 1u;  // S' draw in tile 0
+              code = 1u | (sc << 2);  // S' draw in tile 0, whose terms end at the split chunk
             } else {
-              const uint32_t k = tile_walk(row, slots, ts, Mm + S0, x, pad, grp, li, hand);
-              if (k == uint32_t(-1)) code = 1u;  // nothing positive in tile 1: rounding at the tile edge
+              const uint32_t k = tile_walk(row, slots, ts, Mm + S0, x, pad, grp, li, hand, sc, nch, sc);
+              if (k == uint32_t(-1)) code = 1u | (sc << 2);  // nothing positive in tile 1: rounding at the tile edge
               else topic = k;
             }
           } else {
@@ -1855,12 +2027,16 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
             if (!(xq < qb[nb])) {
               topic = (K1 == uint32_t(K - 1)) ? uint32_t(K - 2) : uint32_t(K - 1);  // last positive segment
             } else {
-              // the largest block lo < nb with qb[lo] <= xq
-              int lo = 0, hi = nb;
-              while (hi - lo > 1) {
-                const int mid = (lo + hi) >> 1;
-                if (qb[mid] <= xq) lo = mid;
-                else hi = mid;
+              // the largest block lo < nb with qb[lo] <= xq, 16 candidates at a time
+              int lo = 0, span = nb;
+              while (span > 1) {
+                const int step = (span + kGroup - 1) / kGroup;
+                const int off = li * step;
+                const bool ok = off < span && qb[lo + off] <= xq;
+                const uint32_t bm = uint32_t(__ballot(ok) >> (grp * kGroup)) & kGroupMask;
+                const int best = bm ? 31 - __clz(bm) : 0;
+                lo += best * step;
+                span = min(step, span - best * step);
               }
               const uint32_t k = uint32_t(lo * kGroup + li);
               if (uint32_t(lo * kGroup) >= kt) {
@@ -1875,29 +2051,16 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
           if (li == 0) {
             n_sampled++;
             nnz_sum += nnz;
+            sc_code[q] = code;
             if (code) {
-              sc_code[q] = code;
               sc_x[q] = x;
               sc_s[q] = keep;
+              sc_c1[q] = C1 | (nnz << 16);
+              sc_list[atomicAdd(&s_reg[4], 1u)] = q;
             } else {
               d.z_w[j] = uint16_t(topic);
             }
           }
-        } else {
-          const uint32_t code = code0;
-          const double x = sc_x[q];
-          uint32_t topic;
-          if (code == 1u) {
-            const double Mm = rec.a1 * (double(sc_c1[q]) + p.alpha);
-            topic = tile_walk(row, slots, ts, Mm, x, pad, grp, li, hand);
-            if (topic == uint32_t(-1)) topic = K1;  // no positive S' term below KT: cannot happen for x in S'
-          } else {
-            const int lo = int(code >> 2);
-            const uint32_t k = uint32_t(lo * kGroup + li);
-            const double term = p.alpha * wt[k];
-            topic = pick_segment(k, term, sc_s[q] + qb[lo], x, grp);
-          }
-          if (li == 0) d.z_w[j] = uint16_t(topic);
         }
       }
       __syncthreads();
@@ -2549,7 +2712,8 @@ int sampler_block(int K, int want, bool *q_table) {
 int tiled_topics(int K) { return ((K + 2) / 2 + kGroup - 1) / kGroup * kGroup; }
 size_t tiled_lds_bytes(int K, int kt) {
   const size_t nb = size_t((K + kGroup - 1) / kGroup);
-  return sizeof(double) * (size_t(kt) + kGroup + nb + 1) + sizeof(uint32_t) * (kTiledBlock / kGroup * kMaxRun + 4);
+  return sizeof(double) * (size_t(kt) + kGroup + nb + 1 + kTiledBlock) +
+         sizeof(uint32_t) * (kTiledBlock / kGroup * kMaxRun + 6);
 }
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
   if (p.big_k) {

@@ -233,6 +233,7 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
     LDA_TRY(dalloc(h, &d.ts_x, slots));
     LDA_TRY(dalloc(h, &d.ts_c1, slots));
     LDA_TRY(dalloc(h, &d.ts_code, slots));
+    LDA_TRY(dalloc(h, &d.ts_list, slots));
     LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(L.K)));
   }
   LDA_TRY(dalloc(h, &d.ll_out, 1));

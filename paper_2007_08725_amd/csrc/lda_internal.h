@@ -159,9 +159,10 @@ struct DevState {
   double *ll_out;               // [1]
   // large K only (the tiled sampler): per-workgroup slices of max_region
   // entries carrying a token's S' part, C1 and recorded draw between passes,
+  // the list of the region's tokens whose draw finishes in the last pass,
   // and the LLPT kernel's W^' rows
   double *ts_s, *ts_x;
-  uint32_t *ts_c1, *ts_code;
+  uint32_t *ts_c1, *ts_code, *ts_list;
   double *wscratch;
   // large K (p.sparse_pre): topics by ascending T (descending beta/den[k]),
   // their sort buffers, and the sum of beta/den[k] over all topics
