@@ -309,7 +309,6 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
   if (p.big_k) {
     const size_t sl = size_t(tiled_grid(p)) * size_t(max_region);
     LDA_TRY(dalloc(h, &d.ts_s, sl));
-    LDA_TRY(dalloc(h, &d.ts_x, sl));
     LDA_TRY(dalloc(h, &d.ts_c1, sl));
     LDA_TRY(dalloc(h, &d.ts_code, sl));
     LDA_TRY(dalloc(h, &d.ts_list, sl));

@@ -1584,12 +1584,19 @@ __global__ __launch_bounds__(64) void k_sampler_light(DevState d, Params p, uint
 struct TileState {
   const double *wt;  // the tile: W^' of topics [base, base + KT), zeros past the tile's end
   uint32_t base, kt;
-  uint32_t lds;      // the tile's LDS address minus base * 8 (mod 2^32), for run_sum_in_tile
+  uint32_t rel;      // -base * 8 (mod 2^32)
 };
 
-// W^' of a packed D entry's topic if it lies in the tile, else 0 (wt[kt] is 0).
+// W^' of a packed D entry's topic if it lies in the tile, else 0 (wt[kt] is
+// 0).  The tile starts at LDS address 0 (the kernel's LDS is all dynamic,
+// which launch_sampler checks), so the address (topic - base) * 8 is one
+// v_mad_u32_u16 on the entry's high half; topics below the tile wrap to
+// addresses near 2^32, and one unsigned min sends every topic outside the
+// tile to wt[kt].
 __device__ __forceinline__ double wt_of(const TileState &ts, uint32_t e) {
-  return ts.wt[min((e >> 16) - ts.base, ts.kt)];
+  uint32_t a;
+  asm("v_mad_u32_u16 %0, %1, 8, %2 op_sel:[1,0,0,0]" : "=v"(a) : "v"(e), "s"(ts.rel));
+  return *(lds_f64 *)(size_t)min(a, ts.kt * 8u);
 }
 
 // This lane's run of chunk ch of a row of `slots` padded slots; runs past
@@ -1614,18 +1621,48 @@ __device__ __forceinline__ double run_sum_tile(const uint32_t (&r)[kMaxRun], con
   return s;
 }
 
-// The same sum for a run whose topics all lie in the tile [base, base + KT]:
-// the LDS address (topic - base) * 8 + tile is one v_mad_u32_u16 on the
-// entry's high half, with lds = the tile's LDS address - base * 8 (mod 2^32).
-__device__ __forceinline__ double run_sum_in_tile(const uint32_t (&r)[kMaxRun], uint32_t lds) {
-  double s = 0.0;
+// The last step of an S' draw in a tile: in the chunk that holds x (this
+// lane's run r, lane sum s, inclusive scan incl, the chunk's terms starting
+// at base), the lane whose run holds x and then the entry in it.
+__device__ uint32_t walk_finish(const uint32_t (&r)[kMaxRun], double s, double incl, const TileState &ts,
+                                double base, double x, int grp, int li, uint32_t *__restrict__ hand) {
+  const int sel = run_lane(s, incl, base, x, grp);
+  const double start = base + __shfl(incl - s, sel, kGroup);
+  if (li == sel) {
 #pragma unroll
-  for (int i = 0; i < kMaxRun; ++i) {
-    uint32_t a;
-    asm("v_mad_u32_u16 %0, %1, 8, %2 op_sel:[1,0,0,0]" : "=v"(a) : "v"(r[i]), "s"(lds));
-    s = __builtin_fma(double(r[i] & 0xFFFFu), *(lds_f64 *)(size_t)a, s);
+    for (int i = 0; i < kMaxRun; ++i) hand[i] = r[i];
   }
-  return s;
+  __builtin_amdgcn_wave_barrier();
+  const uint32_t mine = li < kMaxRun ? hand[li] : 0u;
+  const double term = li < kMaxRun ? double(mine & 0xFFFFu) * wt_of(ts, mine) : 0.0;
+  return pick_segment(mine >> 16, term, start, x, grp);
+}
+
+// tile_walk over two chunks already in registers (runs r, lane sums t).
+__device__ uint32_t walk_pair(const uint32_t (&r)[2][kMaxRun], const double (&t)[2], const TileState &ts, double base,
+                              double x, int grp, int li, uint32_t *__restrict__ hand) {
+  double at = base;
+  int pick = -1, last = -1;
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const double total = __shfl(row_incl_scan(t[c]), kGroup - 1, kGroup);
+    if (pick < 0) {
+      if (total > 0.0) {
+        last = c;
+        at = base;
+      }
+      if (x < base + total) pick = c;
+      else base += total;
+    }
+  }
+  if (pick < 0) {
+    pick = last;  // rounding: x at or past the end of the tile's terms
+    base = at;
+  }
+  if (pick < 0) return uint32_t(-1);
+  const uint32_t(&rp)[kMaxRun] = pick == 0 ? r[0] : r[1];
+  const double sp = pick == 0 ? t[0] : t[1];
+  return walk_finish(rp, sp, row_incl_scan(sp), ts, base, x, grp, li, hand);
 }
 
 // The S' draw inside one tile: the entry whose segment holds x, the tile's
@@ -1634,7 +1671,7 @@ __device__ __forceinline__ double run_sum_in_tile(const uint32_t (&r)[kMaxRun], 
 // rounding leaves x past the tile's terms, the last positive term is taken.
 __device__ uint32_t tile_walk(const uint32_t *__restrict__ row, uint32_t slots, const TileState &ts, double base,
                               double x, uint32_t pad, int grp, int li, uint32_t *__restrict__ hand, uint32_t ch0,
-                              uint32_t nch, uint32_t sc) {
+                              uint32_t nch) {
   uint32_t r[kMaxRun];
   int last_pos = -1;
   double last_base = base;
@@ -1646,7 +1683,7 @@ __device__ uint32_t tile_walk(const uint32_t *__restrict__ row, uint32_t slots, 
 #pragma unroll
     for (int i = 0; i < kMaxRun; ++i) r[i] = rn[i];
     if (ch + 1 < nch) load_run_masked(row, ch + 1, slots, li, pad, rn);  // the next chunk's loads, in flight meanwhile
-    s = ch == sc ? run_sum_tile(r, ts) : run_sum_in_tile(r, ts.lds);
+    s = run_sum_tile(r, ts);
     incl = row_incl_scan(s);
     const double total = __shfl(incl, kGroup - 1, kGroup);
     if (total > 0.0) {
@@ -1665,20 +1702,12 @@ __device__ uint32_t tile_walk(const uint32_t *__restrict__ row, uint32_t slots, 
     pick = uint32_t(last_pos);
     base = last_base;
     load_run_masked(row, pick, slots, li, pad, r);
-    s = pick == sc ? run_sum_tile(r, ts) : run_sum_in_tile(r, ts.lds);
+    s = run_sum_tile(r, ts);
     incl = row_incl_scan(s);
   }
-  const int sel = run_lane(s, incl, base, x, grp);
-  const double start = base + __shfl(incl - s, sel, kGroup);
-  if (li == sel) {
-#pragma unroll
-    for (int i = 0; i < kMaxRun; ++i) hand[i] = r[i];
-  }
-  __builtin_amdgcn_wave_barrier();
-  const uint32_t mine = li < kMaxRun ? hand[li] : 0u;
-  const double term = li < kMaxRun ? double(mine & 0xFFFFu) * wt_of(ts, mine) : 0.0;
-  return pick_segment(mine >> 16, term, start, x, grp);
+  return walk_finish(r, s, incl, ts, base, x, grp, li, hand);
 }
+
 
 // Fills the tile [base, base + len) of the region's word (zeros elsewhere,
 // at K1 and at the padding topic K).  Each thread issues the loads of
@@ -1759,6 +1788,7 @@ struct TiledTok {
 
 constexpr int kTiledBlock = kTiledThreads;  // threads per workgroup of the tiled sampler (16 waves)
 constexpr int kTiledAhead = 2;              // chunks whose loads a group issues together
+static_assert(kTiledAhead == 2, "pass 1's walk in registers picks one of two chunks");
 
 __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Params p, uint32_t t,
                                                                unsigned long long *__restrict__ stats) {
@@ -1778,10 +1808,9 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
   const uint32_t pad = uint32_t(K) << 16;
   // per-workgroup scratch slices, indexed by the token's place in its region
   double *sc_s = d.ts_s + size_t(blockIdx.x) * size_t(p.max_region);
-  double *sc_x = d.ts_x + size_t(blockIdx.x) * size_t(p.max_region);
   uint32_t *sc_c1 = d.ts_c1 + size_t(blockIdx.x) * size_t(p.max_region);
   uint32_t *sc_code = d.ts_code + size_t(blockIdx.x) * size_t(p.max_region);
-  uint32_t *sc_list = d.ts_list + size_t(blockIdx.x) * size_t(p.max_region);
+  TiledRec *sc_list = d.ts_list + size_t(blockIdx.x) * size_t(p.max_region);
   unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0, n_reg = 0, n_dreg = 0, row_bytes = 0;
   const int waves = kTiledBlock / kWave;
   for (;;) {
@@ -1807,14 +1836,11 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
       row_bytes += int32_t(v) < p.n_dense ? 4ull * uint64_t(K) : 4ull * d.ws_nnz[int(v) - p.n_dense];
     const WordRec rec = d.wrec[v];
     const uint32_t K1 = rec.k1;
-    // the padding entry of tile 0: count 0, a topic inside the tile other
-    // than K1 (so that C1's search passes over it)
-    const uint32_t pad0 = (K1 == 0u ? 1u : 0u) << 16;
     for (int pass = 0; pass < 3; ++pass) {
       const uint32_t tbase = pass == 1 ? kt : 0u;
       const uint32_t tlen = pass == 1 ? uint32_t(K) + 1u - kt : kt;
       fill_tile(d, p, v, K1, tbase, tlen, kt, wt, tid, kTiledBlock);
-      const TileState ts{wt, tbase, kt, uint32_t(reinterpret_cast<uintptr_t>(wt)) - tbase * 8u};
+      const TileState ts{wt, tbase, kt, 0u - tbase * 8u};
       if (pass < 2) {
         // this tile's blocks of the Q' prefix, continuing the previous tile's
         const int b0 = int(tbase) / kGroup, b1 = min(nb, int(tbase + tlen + kGroup - 1) / kGroup);
@@ -1870,27 +1896,43 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
       }
       const uint32_t stride = uint32_t(waves) * 4u;
       if (pass == 2) {
-        // the draws pass 1 recorded, in the order it listed their tokens,
-        // four per wave at a time
+        // the draws pass 1 recorded, in the order it listed them, four per
+        // wave at a time; a group's next record is loaded one step ahead
         const uint32_t nl = __builtin_amdgcn_readfirstlane(s_reg[4]);
+        TiledRec nrec{};
+        if (nl) nrec = sc_list[min(uint32_t(wave) * 4u + uint32_t(grp), nl - 1u)];
         for (uint32_t i0 = uint32_t(wave) * 4u; i0 < nl; i0 += stride) {
           const uint32_t i = i0 + uint32_t(grp);
+          const TiledRec tr = nrec;
+          if (i0 + stride < nl) nrec = sc_list[min(i + stride, nl - 1u)];
           if (i >= nl) continue;
-          const uint32_t q = sc_list[i], j = b + q;
-          const uint32_t code = sc_code[q], cn = sc_c1[q];
-          const uint32_t *row = d.d_ent + d.wt_kr[j].y;
-          const double x = sc_x[q];
+          const uint32_t j = b + tr.q, code = tr.code, cn = tr.cn;
+          const uint32_t *row = d.d_ent + tr.off;
+          const double x = tr.x;
           uint32_t topic;
           if ((code & 3u) == 1u) {
             const uint32_t slots = d_row_slots(cn >> 16);
             const double Mm = rec.a1 * (double(cn & 0xFFFFu) + p.alpha);
-            topic = tile_walk(row, slots, ts, Mm, x, pad0, grp, li, hand, 0u, (code >> 2) + 1u, code >> 2);
+            const uint32_t sc = code >> 2;
+            if (sc < uint32_t(kTiledAhead)) {
+              // the tile-0 chunks, 0 to the split chunk, loaded together and
+              // walked in registers (a chunk past the split chunk adds nothing)
+              uint32_t rb[kTiledAhead][kMaxRun];
+              double tb[kTiledAhead];
+#pragma unroll
+              for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, uint32_t(c), slots, li, pad, rb[c]);
+#pragma unroll
+              for (int c = 0; c < kTiledAhead; ++c) tb[c] = run_sum_tile(rb[c], ts);
+              topic = walk_pair(rb, tb, ts, Mm, x, grp, li, hand);
+            } else {
+              topic = tile_walk(row, slots, ts, Mm, x, pad, grp, li, hand, 0u, sc + 1u);
+            }
             if (topic == uint32_t(-1)) topic = K1;  // no positive S' term below KT: cannot happen for x in S'
           } else {
             const int lo = int(code >> 2);
             const uint32_t k = uint32_t(lo * kGroup + li);
             const double term = p.alpha * wt[k];
-            topic = pick_segment(k, term, sc_s[q] + qb[lo], x, grp);
+            topic = pick_segment(k, term, tr.keep + qb[lo], x, grp);
           }
           if (li == 0) d.z_w[j] = uint16_t(topic);
         }
@@ -1935,40 +1977,50 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
         if (!live) continue;
         const uint32_t *row = d.d_ent + kr.y;
         if (pass == 0) {
-          // the first chunk in full (a row start plus kChunk slots stays
-          // inside the kRowPad slots past the last row), masked below
-          uint32_t r0[kMaxRun];
+          // the first two chunks in full (a row start plus 2 * kChunk slots
+          // stays inside the kRowPad slots past the last row), masked below
+          static_assert(kTiledAhead * kChunk <= kRowPad, "the speculative chunks stay inside the D array");
+          uint32_t r0[kTiledAhead][kMaxRun];
 #pragma unroll
-          for (int i = 0; i < kMaxRun; ++i) r0[i] = row[uint32_t(li) * kMaxRun + uint32_t(i)];
-          const uint32_t nnz = uint32_t(__shfl(int(r0[0]), 0, kGroup)) & 0xFFFFu;
+          for (int c = 0; c < kTiledAhead; ++c)
+#pragma unroll
+            for (int i = 0; i < kMaxRun; ++i) r0[c][i] = row[uint32_t(c) * kChunk + uint32_t(li) * kMaxRun + uint32_t(i)];
+          const uint32_t nnz = uint32_t(__shfl(int(r0[0][0]), 0, kGroup)) & 0xFFFFu;
           const uint32_t slots = d_row_slots(nnz);
           const uint32_t nch = (slots + kChunk - 1) / kChunk;
 #pragma unroll
-          for (int i = 0; i < kMaxRun; ++i) {
-            const uint32_t qs = uint32_t(li) * kMaxRun + uint32_t(i);
-            if (qs == 0u || qs >= slots) r0[i] = pad0;
-          }
+          for (int c = 0; c < kTiledAhead; ++c)
+#pragma unroll
+            for (int i = 0; i < kMaxRun; ++i) {
+              const uint32_t qs = uint32_t(c) * kChunk + uint32_t(li) * kMaxRun + uint32_t(i);
+              if (qs == 0u || qs >= slots) r0[c][i] = pad;
+            }
           // S' over the tile-0 topics and C1, chunk by chunk up to the split
-          // chunk; the loads of up to kTiledAhead chunks are issued together.
-          // A chunk that ends below KT (not the split chunk) lies in the tile.
-          // Slots outside the row read pad0, a count-0 entry in the tile.
+          // chunk; the loads of up to kTiledAhead chunks are issued together
           double s0 = 0.0;
           uint32_t c1 = 0xFFFFFFFFu;
-          c1 = run_count_of<kMaxRun>(r0, K1, c1);
           uint32_t sc = 0;
-          bool open = nch > 1u && (uint32_t(__shfl(int(r0[kMaxRun - 1]), kGroup - 1, kGroup)) >> 16) < kt;
-          s0 += open ? run_sum_in_tile(r0, ts.lds) : run_sum_tile(r0, ts);
-          for (uint32_t c0 = 1; open; c0 += kTiledAhead) {
+          bool open = true;
+#pragma unroll
+          for (int c = 0; c < kTiledAhead; ++c) {
+            if (open) {
+              c1 = run_count_of<kMaxRun>(r0[c], K1, c1);
+              sc = uint32_t(c);
+              open = sc + 1u < nch && (uint32_t(__shfl(int(r0[c][kMaxRun - 1]), kGroup - 1, kGroup)) >> 16) < kt;
+              s0 += run_sum_tile(r0[c], ts);
+            }
+          }
+          for (uint32_t c0 = kTiledAhead; open; c0 += kTiledAhead) {
             uint32_t r[kTiledAhead][kMaxRun];
 #pragma unroll
-            for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad0, r[c]);
+            for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) {
               if (open) {
                 c1 = run_count_of<kMaxRun>(r[c], K1, c1);
                 sc = c0 + uint32_t(c);
                 open = sc + 1u < nch && (uint32_t(__shfl(int(r[c][kMaxRun - 1]), kGroup - 1, kGroup)) >> 16) < kt;
-                s0 += open ? run_sum_in_tile(r[c], ts.lds) : run_sum_tile(r[c], ts);
+                s0 += run_sum_tile(r[c], ts);
               }
             }
           }
@@ -1985,20 +2037,28 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
           const uint32_t slots = d_row_slots(nnz);
           const uint32_t nch = (slots + kChunk - 1) / kChunk;
           // S' over the tile-1 topics, and C1 where pass 0 did not read it,
-          // from the split chunk on (the chunks after it lie in the tile;
-          // slots past the row read the padding entry, topic K)
+          // from the split chunk on; the first batch of chunks stays in
+          // registers for the draw
           double s1 = 0.0;
           uint32_t c1 = 0xFFFFFFFFu;
-          for (uint32_t c0 = sc; c0 < nch; c0 += kTiledAhead) {
+          uint32_t rb[kTiledAhead][kMaxRun];
+          double tb[kTiledAhead];
+#pragma unroll
+          for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, sc + uint32_t(c), slots, li, pad, rb[c]);
+#pragma unroll
+          for (int c = 0; c < kTiledAhead; ++c) {
+            c1 = run_count_of<kMaxRun>(rb[c], K1, c1);
+            tb[c] = run_sum_tile(rb[c], ts);
+            s1 += tb[c];
+          }
+          for (uint32_t c0 = sc + kTiledAhead; c0 < nch; c0 += kTiledAhead) {
             uint32_t r[kTiledAhead][kMaxRun];
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
-            c1 = run_count_of<kMaxRun>(r[0], K1, c1);
-            s1 += c0 == sc ? run_sum_tile(r[0], ts) : run_sum_in_tile(r[0], ts.lds);
 #pragma unroll
-            for (int c = 1; c < kTiledAhead; ++c) {
+            for (int c = 0; c < kTiledAhead; ++c) {
               c1 = run_count_of<kMaxRun>(r[c], K1, c1);
-              s1 += run_sum_in_tile(r[c], ts.lds);
+              s1 += run_sum_tile(r[c], ts);
             }
           }
           const double S1 = gsum<kGroup>(s1);
@@ -2016,8 +2076,13 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
           } else if (x < Mm + S) {
             if (x < Mm + S0) {
               code = 1u | (sc << 2);  // S' draw in tile 0, whose terms end at the split chunk
+            } else if (nch - sc <= uint32_t(kTiledAhead)) {
+              // every tile-1 chunk is in registers
+              const uint32_t k = walk_pair(rb, tb, ts, Mm + S0, x, grp, li, hand);
+              if (k == uint32_t(-1)) code = 1u | (sc << 2);  // nothing positive in tile 1: rounding at the tile edge
+              else topic = k;
             } else {
-              const uint32_t k = tile_walk(row, slots, ts, Mm + S0, x, pad, grp, li, hand, sc, nch, sc);
+              const uint32_t k = tile_walk(row, slots, ts, Mm + S0, x, pad, grp, li, hand, sc, nch);
               if (k == uint32_t(-1)) code = 1u | (sc << 2);  // nothing positive in tile 1: rounding at the tile edge
               else topic = k;
             }
@@ -2051,12 +2116,15 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
           if (li == 0) {
             n_sampled++;
             nnz_sum += nnz;
-            sc_code[q] = code;
             if (code) {
-              sc_x[q] = x;
-              sc_s[q] = keep;
-              sc_c1[q] = C1 | (nnz << 16);
-              sc_list[atomicAdd(&s_reg[4], 1u)] = q;
+              TiledRec tr;
+              tr.q = q;
+              tr.code = code;
+              tr.cn = C1 | (nnz << 16);
+              tr.off = kr.y;
+              tr.x = x;
+              tr.keep = keep;
+              sc_list[atomicAdd(&s_reg[4], 1u)] = tr;
             } else {
               d.z_w[j] = uint16_t(topic);
             }
@@ -2717,6 +2785,13 @@ size_t tiled_lds_bytes(int K, int kt) {
 }
 hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStream_t s) {
   if (p.big_k) {
+    // the tile must start at LDS address 0 (wt_of): no static LDS
+    static const hipError_t lds_at_0 = [] {
+      hipFuncAttributes a;
+      const hipError_t e = hipFuncGetAttributes(&a, reinterpret_cast<const void *>(k_sampler_tiled));
+      return e != hipSuccess ? e : a.sharedSizeBytes == 0 ? hipSuccess : hipErrorInvalidConfiguration;
+    }();
+    if (lds_at_0 != hipSuccess) return lds_at_0;
     const size_t lds = tiled_lds_bytes(p.K, p.tile_topics);
     hipError_t err = allow_lds(k_sampler_tiled, lds);
     if (err != hipSuccess) return err;

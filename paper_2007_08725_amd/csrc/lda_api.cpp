@@ -230,7 +230,6 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
     p.max_region = int32_t(max_region);
     const size_t slots = size_t(tiled_grid(p)) * size_t(max_region);
     LDA_TRY(dalloc(h, &d.ts_s, slots));
-    LDA_TRY(dalloc(h, &d.ts_x, slots));
     LDA_TRY(dalloc(h, &d.ts_c1, slots));
     LDA_TRY(dalloc(h, &d.ts_code, slots));
     LDA_TRY(dalloc(h, &d.ts_list, slots));

@@ -131,6 +131,14 @@ struct SkipRec {
   uint32_t pad;
 };
 
+// A token whose draw the tiled sampler's last pass finishes: its place in
+// the region, the recorded draw, C1 and row length, D-row offset, x and the
+// start of Q'.
+struct TiledRec {
+  uint32_t q, code, cn, off;
+  double x, keep;
+};
+
 struct DevState {
   // layout
   uint32_t *doc_off, *dt_word, *dt_key, *dt_wpos, *word_off;
@@ -158,11 +166,12 @@ struct DevState {
   double *ll_part;              // [n_regions]
   double *ll_out;               // [1]
   // large K only (the tiled sampler): per-workgroup slices of max_region
-  // entries carrying a token's S' part, C1 and recorded draw between passes,
-  // the list of the region's tokens whose draw finishes in the last pass,
+  // entries carrying a token's S' part, C1 and split chunk between passes,
+  // the records of the region's tokens whose draw finishes in the last pass,
   // and the LLPT kernel's W^' rows
-  double *ts_s, *ts_x;
-  uint32_t *ts_c1, *ts_code, *ts_list;
+  double *ts_s;
+  uint32_t *ts_c1, *ts_code;
+  TiledRec *ts_list;
   double *wscratch;
   // large K (p.sparse_pre): topics by ascending T (descending beta/den[k]),
   // their sort buffers, and the sum of beta/den[k] over all topics
