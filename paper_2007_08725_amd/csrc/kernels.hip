@@ -1988,13 +1988,16 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
           const uint32_t nnz = uint32_t(__shfl(int(r0[0][0]), 0, kGroup)) & 0xFFFFu;
           const uint32_t slots = d_row_slots(nnz);
           const uint32_t nch = (slots + kChunk - 1) / kChunk;
+          // a lane's run of kMaxRun slots lies wholly inside or past the row
+          // (slots is a multiple of 32)
 #pragma unroll
-          for (int c = 0; c < kTiledAhead; ++c)
+          for (int c = 0; c < kTiledAhead; ++c) {
+            if (uint32_t(c) * kChunk + uint32_t(li) * kMaxRun >= slots) {
 #pragma unroll
-            for (int i = 0; i < kMaxRun; ++i) {
-              const uint32_t qs = uint32_t(c) * kChunk + uint32_t(li) * kMaxRun + uint32_t(i);
-              if (qs == 0u || qs >= slots) r0[c][i] = pad;
+              for (int i = 0; i < kMaxRun; ++i) r0[c][i] = pad;
             }
+          }
+          if (li == 0) r0[0][0] = pad;  // the row header
           // S' over the tile-0 topics and C1, chunk by chunk up to the split
           // chunk; the loads of up to kTiledAhead chunks are issued together
           double s0 = 0.0;
