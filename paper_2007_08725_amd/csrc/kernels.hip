@@ -1294,7 +1294,7 @@ __device__ constexpr uint32_t kBucketEnd[8] = {32, 64, 96, 128, 192, 256, 384, 5
 // The small-group rounds over list places [from, to) (rows in ascending
 // bucket order), G lanes per token and 64/G tokens a round.  A round reads
 // as many chunks of G*kRun slots as its last (longest) row needs.
-template <int G>
+template <int G, int MaxNC>
 __device__ void draw_rounds(int from, int to, const int (&ends)[8], const BatchLds &bt, const WordState &w,
                             const uint32_t *__restrict__ d_ent, unsigned long long &after_s) {
   constexpr uint32_t kSpan = uint32_t(G) * kRun;
@@ -1312,8 +1312,13 @@ __device__ void draw_rounds(int from, int to, const int (&ends)[8], const BatchL
       draw_small<G, 2>(bt, slot, to, w, d_ent, li, after_s);
     } else if (nc == 3) {
       draw_small<G, 3>(bt, slot, to, w, d_ent, li, after_s);
-    } else {
+    } else if (MaxNC <= 4 || nc == 4) {
       draw_small<G, 4>(bt, slot, to, w, d_ent, li, after_s);
+    } else {
+      if constexpr (MaxNC > 4) {
+        if (nc <= 6) draw_small<G, 6>(bt, slot, to, w, d_ent, li, after_s);
+        else draw_small<G, MaxNC>(bt, slot, to, w, d_ent, li, after_s);
+      }
     }
   }
 }
@@ -1325,6 +1330,11 @@ __device__ void draw_rounds(int from, int to, const int (&ends)[8], const BatchL
 // 97-128 slots (two whole 64-slot chunks), those rows join the 8-lane
 // rounds instead: they fill free places there, or make a round that reads
 // half as many entries per lane as the partial 4-lane round would.
+// Wide (the 1024-thread workgroups, whose waves have registers to spare):
+// rows of up to 512 slots by 8 lanes as well, 8 tokens a round, so that a
+// round's per-token work (sums, scans, the split of x) serves twice the
+// tokens.
+template <bool Wide>
 __device__ void draw_batch_small(bool und, uint32_t nnz, const BatchLds &bt, const WordState &w,
                                  const uint32_t *__restrict__ d_ent, int lane, unsigned long long &after_s) {
   int n = 0, ends[8];
@@ -1341,9 +1351,13 @@ __device__ void draw_batch_small(bool und, uint32_t nnz, const BatchLds &bt, con
   }
   const int left = ends[3] % 16;
   const int a = left > 0 && left <= 8 && ends[3] - ends[2] >= left ? ends[3] - left : ends[3];
-  draw_rounds<4>(0, a, ends, bt, w, d_ent, after_s);
-  draw_rounds<8>(a, ends[5], ends, bt, w, d_ent, after_s);
-  draw_rounds<16>(ends[5], ends[7], ends, bt, w, d_ent, after_s);
+  draw_rounds<4, 4>(0, a, ends, bt, w, d_ent, after_s);
+  if (Wide) {
+    draw_rounds<8, 8>(a, ends[7], ends, bt, w, d_ent, after_s);
+  } else {
+    draw_rounds<8, 4>(a, ends[5], ends, bt, w, d_ent, after_s);
+    draw_rounds<16, 4>(ends[5], ends[7], ends, bt, w, d_ent, after_s);
+  }
 }
 
 // The sampler for workgroups of NB threads (NB / 64 waves); every wave works
@@ -1519,7 +1533,7 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       // rows of up to 128 slots (header and entries): 4 lanes per token; up
       // to 256: 8 lanes; up to 512: 16 lanes; longer rows: 16 lanes, one
       // chunk of kChunk slots at a time
-      draw_batch_small(und, nnz, bt, w, d.d_ent, ln, n_after_s);
+      draw_batch_small<(NB >= 1024)>(und, nnz, bt, w, d.d_ent, ln, n_after_s);
       if (lmask) draw_long(lmask, __ballot(fol), starts, bt, w, d.d_ent, ln / kGroup, ln % kGroup, n_after_s);
       // the S' walks and Q' searches, one lane per token; the batch's topics
       // (K1 for the tokens the step-3 test decided) leave in one coalesced store
