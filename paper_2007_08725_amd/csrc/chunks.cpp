@@ -244,6 +244,8 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
   // (the second slot's 8-byte records hold two max_tok arrays of 4 bytes)
   uint32_t *wnew = s1.dt_wpos, *wkey = reinterpret_cast<uint32_t *>(s1.wt_kr), *wpos = wkey + cm.max_tok;
   HIP_TRY(h, launch_zero_split(d, p, h->stream));
+  // large K: the scratch rows the W rebuild builds T in (it runs per chunk below)
+  if (p.big_k) LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(K)));
   int64_t total_regions = 0;
   uint32_t max_region = 1;
   for (ChunkInfo &ci : cm.c) {
@@ -312,7 +314,6 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
     LDA_TRY(dalloc(h, &d.ts_c1, sl));
     LDA_TRY(dalloc(h, &d.ts_code, sl));
     LDA_TRY(dalloc(h, &d.ts_list, sl));
-    LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(K)));
   }
   unsigned long long stt[kStatsPerIter];
   HIP_TRY(h, hipMemcpy(stt, h->stats_base, sizeof(stt), hipMemcpyDeviceToHost));

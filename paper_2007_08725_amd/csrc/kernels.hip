@@ -2253,17 +2253,25 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
 
 // W rebuild for large K: the touched topics of a region are marked in a
 // bitmap, so the work per region follows its tokens, not K.
+// Packed: two 16-bit counts per LDS word (every region shorter than 2^16
+// tokens), which halves the table and lets two workgroups share a CU at
+// K = 32,768.  Large K leaves T to k_topic_hist and k_topic_reduce: adding
+// each region's counts into T with device atomics cost more than the rest of
+// the rebuild.
+template <bool Packed>
 __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
   const int nw = (K + 31) / 32;
-  uint32_t *hist = ldsu;                              // [K]: the region's topic counts
-  uint32_t *bits = ldsu + K;                          // [nw]: topics with a nonzero count
-  uint32_t *tloc = p.big_k ? nullptr : bits + nw;     // [K]; large K: T is added per region instead
+  const int nh = Packed ? (K + 1) / 2 : K;
+  uint32_t *hist = ldsu;                              // [nh]: the region's topic counts
+  uint32_t *bits = ldsu + nh;                         // [nw]: topics with a nonzero count
+  uint32_t *tloc = p.big_k ? nullptr : bits + nw;     // [K]; large K: T comes from k_topic_hist
   __shared__ uint32_t s_scan[kBlock / kWave];
   const int tid = threadIdx.x;
   uint32_t bad = 0;
-  for (int k = tid; k < K; k += kBlock) hist[k] = 0u;
+  auto count = [&](int k) -> uint32_t { return Packed ? (hist[k >> 1] >> ((k & 1) << 4)) & 0xFFFFu : hist[k]; };
+  for (int k = tid; k < nh; k += kBlock) hist[k] = 0u;
   for (int q = tid; q < nw; q += kBlock) bits[q] = 0u;
   if (tloc)
     for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
@@ -2281,7 +2289,8 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
         if (uint32_t(u * kBlock) < e - j0) {
           const uint32_t z = zz[u];
           if (z < uint32_t(K)) {
-            atomicAdd(&hist[z], 1u);
+            if (Packed) atomicAdd(&hist[z >> 1], 1u << ((z & 1u) << 4));
+            else atomicAdd(&hist[z], 1u);
             atomicOr(&bits[z >> 5], 1u << (z & 31u));
           } else {
             bad++;
@@ -2299,10 +2308,10 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
         for (int q = q0; q < q1; ++q)
           for (uint32_t m = bits[q]; m; m &= m - 1u) {
             const int k = q * 32 + __ffs(m) - 1;
-            atomicAdd(&wrow[k], int32_t(hist[k]));
+            atomicAdd(&wrow[k], int32_t(count(k)));
           }
       } else {
-        for (int k = tid; k < K; k += kBlock) wrow[k] = int32_t(hist[k]);
+        for (int k = tid; k < K; k += kBlock) wrow[k] = int32_t(count(k));
       }
     } else {
       const int s = int(v) - p.n_dense;
@@ -2314,17 +2323,23 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
       for (int q = q0; q < q1; ++q)
         for (uint32_t m = bits[q]; m; m &= m - 1u) {
           const int k = q * 32 + __ffs(m) - 1;
-          out[off++] = (uint32_t(k) << 16) | hist[k];
+          out[off++] = (uint32_t(k) << 16) | count(k);
         }
       if (tid == 0) d.ws_nnz[s] = total;
     }
     __syncthreads();  // the non-split dense row reads every hist entry
     for (int q = q0; q < q1; ++q) {
-      for (uint32_t m = bits[q]; m; m &= m - 1u) {
+      const uint32_t mq = bits[q];
+      if (tloc)
+        for (uint32_t m = mq; m; m &= m - 1u) {
+          const int k = q * 32 + __ffs(m) - 1;
+          tloc[k] += count(k);
+        }
+      // cleared once both counts of a word are read (a word's two topics
+      // are in the same bitmap word)
+      for (uint32_t m = mq; m; m &= m - 1u) {
         const int k = q * 32 + __ffs(m) - 1;
-        if (tloc) tloc[k] += hist[k];
-        else atomicAdd(&d.T[k], hist[k]);
-        hist[k] = 0u;
+        hist[Packed ? k >> 1 : k] = 0u;
       }
       bits[q] = 0u;
     }
@@ -2334,6 +2349,47 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
     for (int k = tid; k < K; k += kBlock)
       if (tloc[k]) atomicAdd(&d.T[k], tloc[k]);
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
+}
+
+// T for large K: the histogram of the word-ordered topics.  Each workgroup
+// counts a slice of the tokens (8-token aligned, 8 topics a load) in LDS and
+// writes its counts to its row of scratch; k_topic_reduce adds the rows into
+// T (zeroed by k_zero_split, so out-of-core chunks add up).
+constexpr int kHistBlock = 1024;
+__global__ __launch_bounds__(kHistBlock) void k_topic_hist(DevState d, Params p, uint32_t *__restrict__ rows) {
+  extern __shared__ uint32_t ldsu[];
+  const int K = p.K;
+  for (int k = threadIdx.x; k < K; k += kHistBlock) ldsu[k] = 0u;
+  __syncthreads();
+  const int64_t n = p.n, g = blockIdx.x, G = gridDim.x;
+  const int64_t b = (n * g / G) & ~int64_t(7), e = g + 1 == G ? n : (n * (g + 1) / G) & ~int64_t(7);
+  int64_t j = b + int64_t(threadIdx.x) * 8;
+  for (; j + 8 <= e; j += int64_t(kHistBlock) * 8) {
+    const uint4 v = *reinterpret_cast<const uint4 *>(d.z_w + j);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t z0 = w[i] & 0xFFFFu, z1 = w[i] >> 16;
+      if (z0 < uint32_t(K)) atomicAdd(&ldsu[z0], 1u);
+      if (z1 < uint32_t(K)) atomicAdd(&ldsu[z1], 1u);
+    }
+  }
+  for (; j < e; ++j) {  // the slice's last tokens past a whole 8 (at most 7, one thread)
+    const uint32_t z = d.z_w[j];
+    if (z < uint32_t(K)) atomicAdd(&ldsu[z], 1u);
+  }
+  __syncthreads();
+  uint32_t *row = rows + size_t(g) * size_t(K);
+  for (int k = threadIdx.x; k < K; k += kHistBlock) row[k] = ldsu[k];
+}
+
+__global__ __launch_bounds__(kBlock) void k_topic_reduce(DevState d, Params p, const uint32_t *__restrict__ rows,
+                                                         int G) {
+  const int k = int(blockIdx.x) * kBlock + int(threadIdx.x);
+  if (k >= p.K) return;
+  uint32_t s = 0;
+  for (int g = 0; g < G; ++g) s += rows[size_t(g) * size_t(p.K) + size_t(k)];
+  if (s) atomicAdd(&d.T[k], s);
 }
 
 constexpr int kPre = 2;   // chunks of 64 tokens per document gathered one document ahead
@@ -2472,7 +2528,7 @@ __device__ void heavy_rebuild_d(const DevState &d, const Params &p, uint32_t *__
 // list of topics at its prefix-sum offset, and one lane per listed topic
 // writes the packed entry.  The work per document is K/2048 wave steps plus
 // about one per 32 touched topics, so it follows the tokens, not K.
-__global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
+__global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p, int light) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
   const int half = (K + 1) / 2, nw = (K + 31) / 32;
@@ -2486,7 +2542,7 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
   // the heavy documents first, each by the whole workgroup (wave 0's tables shared)
   if (p.n_heavy)
     heavy_rebuild_d(d, p, ldsu, bad);
-  int part = 0;
+  int part = light ? 0 : kXcds;  // heavy only: the light documents are k_rebuild_d_sort's
   for (;;) {
     uint32_t d0 = 0, d1 = 0;
     if (!next_docs(d.counters + CNT_REBUILD_D, p, part, lane, d0, d1)) break;
@@ -2585,6 +2641,104 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p) {
       // (readlane returns a signed int: the offset is taken back to unsigned,
       // since D has more than 2^31 slots on the largest corpora)
       emit_row(hist, bits, list, nw, K, d.d_ent + uint32_t(__builtin_amdgcn_readlane(capv, i)) + 1u, e - b, lane);
+    }
+  }
+  if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
+}
+
+// The D rows of the light documents for large K, one wave per document
+// without a table of K counts (which leaves room for two waves per CU at
+// K = 32,768): the wave gathers the document's topics into its LDS buffer,
+// sorts them (bitonic, ascending; topics >= K are errors and sort last as
+// 0xFFFF), and writes one entry per run of equal topics.  The rows are the
+// ones emit_row writes: entries in ascending topic order, padding entries
+// of topic K, the header (length << 16 | entries).
+constexpr int kSortGather = 8;  // slots per lane whose loads are in flight together
+__global__ __launch_bounds__(kBlock) void k_rebuild_d_sort(DevState d, Params p) {
+  extern __shared__ uint32_t ldsu[];
+  const int K = p.K;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  uint16_t *sz = reinterpret_cast<uint16_t *>(ldsu) + size_t(wave) * kHeavyDoc;
+  uint32_t bad = 0;
+  int part = 0;
+  for (;;) {
+    uint32_t d0 = 0, d1 = 0;
+    if (!next_docs(d.counters + CNT_REBUILD_D, p, part, lane, d0, d1)) break;
+    for (uint32_t dd = d0; dd < d1; ++dd) {
+      const uint32_t b = d.doc_off[dd], len = d.doc_off[dd + 1] - b;
+      if (len > uint32_t(kHeavyDoc)) continue;  // a heavy document: k_rebuild_d's
+      uint32_t P = kWave;
+      while (P < len) P <<= 1;
+      // the topics, kSortGather slots per lane at a time (slot loads, then gathers)
+      for (uint32_t q0 = 0; q0 < P; q0 += uint32_t(kSortGather * kWave)) {
+        uint32_t zz[kSortGather];
+#pragma unroll
+        for (int c = 0; c < kSortGather; ++c) {
+          const uint32_t q = q0 + uint32_t(c * kWave + lane);
+          zz[c] = q < len ? d.dt_wpos[b + q] : 0u;
+        }
+#pragma unroll
+        for (int c = 0; c < kSortGather; ++c) {
+          const uint32_t q = q0 + uint32_t(c * kWave + lane);
+          if (q < len) zz[c] = d.z_w[zz[c]];
+        }
+#pragma unroll
+        for (int c = 0; c < kSortGather; ++c) {
+          const uint32_t q = q0 + uint32_t(c * kWave + lane);
+          if (q < P) {
+            uint32_t z = 0xFFFFu;
+            if (q < len) {
+              if (zz[c] < uint32_t(K)) z = zz[c];
+              else bad++;
+            }
+            sz[q] = uint16_t(z);
+          }
+        }
+      }
+      __threadfence_block();
+      // bitonic sort of the P slots, ascending
+      for (uint32_t size = 2; size <= P; size <<= 1) {
+        for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+          for (uint32_t t = uint32_t(lane); t < P / 2; t += kWave) {
+            const uint32_t i = 2 * t - (t & (stride - 1)), j = i + stride;
+            const uint32_t a = sz[i], c = sz[j];
+            if ((a > c) == ((i & size) == 0)) {
+              sz[i] = uint16_t(c);
+              sz[j] = uint16_t(a);
+            }
+          }
+          __threadfence_block();
+        }
+      }
+      // entries: a run starts where the topic changes; first the number of
+      // entries, then the runs from the last 64 slots to the first, so that
+      // each run's end (the next run's start) is known
+      uint32_t nnz = 0;
+      for (uint32_t q0 = 0; q0 < len; q0 += kWave) {
+        const uint32_t i = q0 + uint32_t(lane);
+        const uint32_t zi = i < len ? sz[i] : 0xFFFFu, zp = i > 0 && i < len ? sz[i - 1] : 0xFFFFFFFFu;
+        nnz += uint32_t(__popcll(__ballot(i < len && zi != 0xFFFFu && zi != zp)));
+      }
+      uint32_t *out = d.d_ent + d.d_cap[dd] + 1u;
+      uint32_t after = nnz, next = len;  // entries and first run start past the current 64 slots
+      for (int q0 = int((len - 1u) & ~uint32_t(kWave - 1)); q0 >= 0; q0 -= kWave) {
+        const uint32_t i = uint32_t(q0 + lane);
+        const uint32_t zi = i < len ? sz[i] : 0xFFFFu, zp = i > 0 && i < len ? sz[i - 1] : 0xFFFFFFFFu;
+        const bool start = i < len && zi != zp;
+        const unsigned long long sm = __ballot(start), em = __ballot(start && zi != 0xFFFFu);
+        const unsigned long long above = lane == kWave - 1 ? 0ull : sm & (~0ull << (lane + 1));
+        const uint32_t end = above ? uint32_t(q0) + uint32_t(__ffsll(above) - 1) : next;
+        const uint32_t n_here = uint32_t(__popcll(em));
+        if (start && zi != 0xFFFFu) {
+          const uint32_t below = uint32_t(__popcll(em & ((1ull << lane) - 1ull)));
+          out[after - n_here + below] = (zi << 16) | (end - i);
+        }
+        after -= n_here;
+        next = sm ? uint32_t(q0) + uint32_t(__ffsll(sm) - 1) : next;
+      }
+      for (uint32_t q = nnz + uint32_t(lane); q + 1u < d_row_slots(nnz); q += kWave) out[q] = uint32_t(K) << 16;
+      if (lane == 0) out[-1] = (len << 16) | nnz;
+      __threadfence_block();
     }
   }
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
@@ -2865,10 +3019,30 @@ hipError_t launch_rebuild_w(const DevState &d, const Params &p, hipStream_t s) {
   // large K: the bitmap variants, whose work follows the tokens instead of K
   const size_t nwords = size_t((p.K + 31) / 32);
   if (p.big_k) {
-    const size_t wlds = sizeof(uint32_t) * (size_t(p.K) + nwords);
-    err = allow_lds(k_rebuild_w_bits, wlds);
+    // two 16-bit counts per word when every region is shorter than 2^16 tokens
+    const bool packed = p.max_region > 0 && p.max_region < 65536;
+    const size_t wlds = sizeof(uint32_t) * ((packed ? size_t(p.K + 1) / 2 : size_t(p.K)) + nwords);
+    if (packed) {
+      err = allow_lds(k_rebuild_w_bits<true>, wlds);
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL(k_rebuild_w_bits<true>, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
+    } else {
+      err = allow_lds(k_rebuild_w_bits<false>, wlds);
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL(k_rebuild_w_bits<false>, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
+    }
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    // T: per-workgroup histograms in the LLPT kernel's scratch (idle here:
+    // loglik_grid_big_k rows of K doubles hold as many rows of K counts)
+    if (!d.wscratch) return hipErrorInvalidValue;  // allocated before any rebuild
+    const int G = loglik_grid_big_k(p);
+    uint32_t *rows = reinterpret_cast<uint32_t *>(d.wscratch);
+    err = allow_lds(k_topic_hist, sizeof(uint32_t) * size_t(p.K));
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(k_rebuild_w_bits, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
+    hipLaunchKernelGGL(k_topic_hist, dim3(uint32_t(G)), dim3(kHistBlock), sizeof(uint32_t) * size_t(p.K), s, d, p,
+                       rows);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    hipLaunchKernelGGL(k_topic_reduce, dim3(uint32_t((p.K + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, d, p, rows, G);
   } else {
     const size_t wlds = sizeof(uint32_t) * 2 * size_t(p.K);
     err = allow_lds(k_rebuild_w, wlds);
@@ -2887,7 +3061,17 @@ hipError_t launch_rebuild_d(const DevState &d, const Params &p, hipStream_t s) {
   // a narrower window of documents, whose topic gathers then hit the caches
   // more often
   const uint32_t dgrid = uint32_t(std::max(1, p.grid_docs / 2));
-  hipLaunchKernelGGL(k_rebuild_d, dim3(dgrid), dim3(kWave * p.doc_waves), dlds, s, d, p);
+  if (!p.big_k) {
+    hipLaunchKernelGGL(k_rebuild_d, dim3(dgrid), dim3(kWave * p.doc_waves), dlds, s, d, p, 1);
+    return hipGetLastError();
+  }
+  // large K: the heavy documents with tables of K counts, the light ones by sorting
+  if (p.n_heavy) {
+    hipLaunchKernelGGL(k_rebuild_d, dim3(dgrid), dim3(kWave * p.doc_waves), dlds, s, d, p, 0);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+  }
+  const size_t slds = sizeof(uint16_t) * size_t(kHeavyDoc) * (kBlock / kWave);
+  hipLaunchKernelGGL(k_rebuild_d_sort, dim3(uint32_t(p.grid_docs)), dim3(kBlock), slds, s, d, p);
   return hipGetLastError();
 }
 
