@@ -1850,6 +1850,9 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
       row_bytes += int32_t(v) < p.n_dense ? 4ull * uint64_t(K) : 4ull * d.ws_nnz[int(v) - p.n_dense];
     const WordRec rec = d.wrec[v];
     const uint32_t K1 = rec.k1;
+    // C1 = D[d][K1] is sought only in the pass whose tile holds topic K1 (that
+    // pass reads every chunk with topics of its tile); the other reads 0
+    const bool k1_lo = K1 < kt;
     for (int pass = 0; pass < 3; ++pass) {
       const uint32_t tbase = pass == 1 ? kt : 0u;
       const uint32_t tlen = pass == 1 ? uint32_t(K) + 1u - kt : kt;
@@ -2021,7 +2024,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
 #pragma unroll
           for (int c = 0; c < kTiledAhead; ++c) {
             if (open) {
-              c1 = run_count_of<kMaxRun>(r0[c], K1, c1);
+              if (k1_lo) c1 = run_count_of<kMaxRun>(r0[c], K1, c1);
               sc = uint32_t(c);
               open = sc + 1u < nch && (uint32_t(__shfl(int(r0[c][kMaxRun - 1]), kGroup - 1, kGroup)) >> 16) < kt;
               s0 += run_sum_tile(r0[c], ts);
@@ -2034,7 +2037,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) {
               if (open) {
-                c1 = run_count_of<kMaxRun>(r[c], K1, c1);
+                if (k1_lo) c1 = run_count_of<kMaxRun>(r[c], K1, c1);
                 sc = c0 + uint32_t(c);
                 open = sc + 1u < nch && (uint32_t(__shfl(int(r[c][kMaxRun - 1]), kGroup - 1, kGroup)) >> 16) < kt;
                 s0 += run_sum_tile(r[c], ts);
@@ -2064,7 +2067,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
           for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, sc + uint32_t(c), slots, li, pad, rb[c]);
 #pragma unroll
           for (int c = 0; c < kTiledAhead; ++c) {
-            c1 = run_count_of<kMaxRun>(rb[c], K1, c1);
+            if (!k1_lo) c1 = run_count_of<kMaxRun>(rb[c], K1, c1);
             tb[c] = run_sum_tile(rb[c], ts);
             s1 += tb[c];
           }
@@ -2074,14 +2077,13 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
             for (int c = 0; c < kTiledAhead; ++c) load_run_masked(row, c0 + uint32_t(c), slots, li, pad, r[c]);
 #pragma unroll
             for (int c = 0; c < kTiledAhead; ++c) {
-              c1 = run_count_of<kMaxRun>(r[c], K1, c1);
+              if (!k1_lo) c1 = run_count_of<kMaxRun>(r[c], K1, c1);
               s1 += run_sum_tile(r[c], ts);
             }
           }
           const double S1 = gsum<kGroup>(s1);
           const double S0 = sc_s[q];
-          // topic K1's entry lies in one chunk: pass 0 or this pass saw it (both
-          // when it is the split chunk), the other read 0
+          // topic K1's entry was sought in one of the two passes, the other read 0
           const uint32_t C1 = max(cn0 & 0xFFFFu, gsum_u32<kGroup>(c1 <= 0xFFFFu ? c1 : 0u));
           const double Mm = rec.a1 * (double(C1) + p.alpha);  // Eq. 7
           const double S = S0 + S1;
