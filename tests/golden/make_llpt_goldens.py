@@ -40,6 +40,7 @@ CASES = {
     "c5_reduced": ("c5", dict(n_docs=3000, V=100000)),
     "c2": ("c2", {}),
     "c3": ("c3", {}),
+    "c4": ("c4", {}),
 }
 
 
