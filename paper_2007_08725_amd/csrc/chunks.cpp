@@ -245,7 +245,7 @@ lda_status chunked_create(lda_handle *h, const int32_t *word, const int32_t *doc
   uint32_t *wnew = s1.dt_wpos, *wkey = reinterpret_cast<uint32_t *>(s1.wt_kr), *wpos = wkey + cm.max_tok;
   HIP_TRY(h, launch_zero_split(d, p, h->stream));
   // large K: the scratch rows the W rebuild builds T in (it runs per chunk below)
-  if (p.big_k) LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(K)));
+  if (w_bits(p)) LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(K)));
   int64_t total_regions = 0;
   uint32_t max_region = 1;
   for (ChunkInfo &ci : cm.c) {

@@ -2253,13 +2253,12 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
 }
 
-// W rebuild for large K: the touched topics of a region are marked in a
-// bitmap, so the work per region follows its tokens, not K.
+// W rebuild for K >= kWBitsK: the touched topics of a region are marked in
+// a bitmap, so the work per region follows its tokens, not K.
 // Packed: two 16-bit counts per LDS word (every region shorter than 2^16
-// tokens), which halves the table and lets two workgroups share a CU at
-// K = 32,768.  Large K leaves T to k_topic_hist and k_topic_reduce: adding
-// each region's counts into T with device atomics cost more than the rest of
-// the rebuild.
+// tokens), which halves the table (two workgroups per CU at K = 32,768).
+// T is left to k_topic_hist and k_topic_reduce: adding each region's counts
+// into T with device atomics cost more than the rest of the rebuild.
 template <bool Packed>
 __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
@@ -2268,15 +2267,12 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
   const int nh = Packed ? (K + 1) / 2 : K;
   uint32_t *hist = ldsu;                              // [nh]: the region's topic counts
   uint32_t *bits = ldsu + nh;                         // [nw]: topics with a nonzero count
-  uint32_t *tloc = p.big_k ? nullptr : bits + nw;     // [K]; large K: T comes from k_topic_hist
   __shared__ uint32_t s_scan[kBlock / kWave];
   const int tid = threadIdx.x;
   uint32_t bad = 0;
   auto count = [&](int k) -> uint32_t { return Packed ? (hist[k >> 1] >> ((k & 1) << 4)) & 0xFFFFu : hist[k]; };
   for (int k = tid; k < nh; k += kBlock) hist[k] = 0u;
   for (int q = tid; q < nw; q += kBlock) bits[q] = 0u;
-  if (tloc)
-    for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
   __syncthreads();
   // regions dealt round-robin, as in k_rebuild_w
   for (int64_t r = blockIdx.x; r < p.n_regions; r += gridDim.x) {
@@ -2332,11 +2328,6 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
     __syncthreads();  // the non-split dense row reads every hist entry
     for (int q = q0; q < q1; ++q) {
       const uint32_t mq = bits[q];
-      if (tloc)
-        for (uint32_t m = mq; m; m &= m - 1u) {
-          const int k = q * 32 + __ffs(m) - 1;
-          tloc[k] += count(k);
-        }
       // cleared once both counts of a word are read (a word's two topics
       // are in the same bitmap word)
       for (uint32_t m = mq; m; m &= m - 1u) {
@@ -2347,9 +2338,6 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
     }
     __syncthreads();
   }
-  if (tloc)
-    for (int k = tid; k < K; k += kBlock)
-      if (tloc[k]) atomicAdd(&d.T[k], tloc[k]);
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
 }
 
@@ -3020,7 +3008,7 @@ hipError_t launch_rebuild_w(const DevState &d, const Params &p, hipStream_t s) {
   hipError_t err;
   // large K: the bitmap variants, whose work follows the tokens instead of K
   const size_t nwords = size_t((p.K + 31) / 32);
-  if (p.big_k) {
+  if (w_bits(p)) {
     // two 16-bit counts per word when every region is shorter than 2^16 tokens
     const bool packed = p.max_region > 0 && p.max_region < 65536;
     const size_t wlds = sizeof(uint32_t) * ((packed ? size_t(p.K + 1) / 2 : size_t(p.K)) + nwords);

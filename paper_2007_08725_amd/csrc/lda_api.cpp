@@ -224,17 +224,17 @@ lda_status create_device(lda_handle *h, const lda_options *o, const int32_t *wor
     LDA_TRY(dalloc(h, &tmp, d.topic_tmp_bytes));
     d.topic_tmp = tmp;
   }
+  uint32_t max_region = 1;
+  for (size_t r = 0; r < L.region.size(); r += 3) max_region = std::max(max_region, L.region[r + 2] - L.region[r + 1]);
+  p.max_region = int32_t(max_region);
   if (p.big_k) {
-    uint32_t max_region = 1;
-    for (size_t r = 0; r < L.region.size(); r += 3) max_region = std::max(max_region, L.region[r + 2] - L.region[r + 1]);
-    p.max_region = int32_t(max_region);
     const size_t slots = size_t(tiled_grid(p)) * size_t(max_region);
     LDA_TRY(dalloc(h, &d.ts_s, slots));
     LDA_TRY(dalloc(h, &d.ts_c1, slots));
     LDA_TRY(dalloc(h, &d.ts_code, slots));
     LDA_TRY(dalloc(h, &d.ts_list, slots));
-    LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(L.K)));
   }
+  if (w_bits(p)) LDA_TRY(dalloc(h, &d.wscratch, size_t(loglik_grid_big_k(p)) * size_t(L.K)));
   LDA_TRY(dalloc(h, &d.ll_out, 1));
   d.stats = h->stats_base;
   LDA_TRY(upload(h, d.region, L.region));

@@ -259,6 +259,11 @@ constexpr int kTiledThreads = 1024;
 // large-K LLPT kernel; the scratch slices are sized for these grids.
 inline int tiled_grid(const Params &p) { return p.grid_regions / 8 > 0 ? p.grid_regions / 8 : 1; }
 inline int loglik_grid_big_k(const Params &p) { return tiled_grid(p); }
+// The W rebuild by bitmap, with T from a histogram of the topics (and its
+// scratch rows), from this many topics on: below it a workgroup's tables of K
+// counts are small enough to keep several workgroups on a CU.
+constexpr int kWBitsK = 4096;
+inline bool w_bits(const Params &p) { return p.big_k || p.K >= kWBitsK; }
 // The count rebuild (Sec. 4.3): launch_rebuild = launch_zero_split, then
 // launch_rebuild_w and launch_rebuild_d.
 hipError_t launch_rebuild(const DevState &d, const Params &p, hipStream_t s);
