@@ -70,8 +70,23 @@ lda_status setup_device(lda_handle *h, const lda_options *o) {
                                       std::to_string(lds_max));
   }
   // the doc pass keeps a table of K 16-bit counts per wave; the D rebuild
-  // the same table plus a bitmap of the touched topics and a list of them
-  p.doc_waves = std::max(1, std::min(kBlock / 64, int(size_t(lds_max) / (sizeof(uint32_t) * d_rebuild_lds_words(p.K)))));
+  // the same table plus a bitmap of the touched topics and a list of them.
+  // Waves per workgroup: the count that keeps the most waves running on a CU
+  // (the larger on a tie), given that the LDS fits lds_max / (w * table)
+  // workgroups and the D rebuild's grid offers 4 per CU: 3 at K = 10,000,
+  // where 4 waves would fit one workgroup per CU and 3 fit two
+  {
+    const size_t wave_bytes = sizeof(uint32_t) * d_rebuild_lds_words(p.K);
+    int best = 1, best_res = 0;
+    for (int w = 1; w <= kBlock / 64; ++w) {
+      const int res = w * std::min(4, int(size_t(lds_max) / (size_t(w) * wave_bytes)));
+      if (res >= best_res && res > 0) {
+        best = w;
+        best_res = res;
+      }
+    }
+    p.doc_waves = best;
+  }
   p.grid_docs = std::max(1, cus * 8);
   return LDA_OK;
 }
