@@ -111,6 +111,25 @@ __device__ __forceinline__ double row_incl_scan(double v) {
   return v;
 }
 
+// A double from another lane by a DPP control, in the rows of row_mask only
+// (the other rows read 0).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_rows_f64(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), CTRL, ROWS, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), CTRL, ROWS, 0xF, false);
+  return __hiloint2double(hi, lo);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: a scan per row, then
+// row 0's total added to row 1 and row 2's to row 3 (row_bcast:15), then the
+// total of rows 0 and 1 added to rows 2 and 3 (row_bcast:31).
+__device__ __forceinline__ double wave_incl_scan(double v) {
+  v = row_incl_scan(v);
+  v += dpp_rows_f64<0x142, 0xA>(v);
+  v += dpp_rows_f64<0x143, 0xC>(v);
+  return v;
+}
+
 constexpr int kTop = 4;  // top values of W^[v] kept per word (a1..a4 of Eq. 9, g <= 3)
 
 struct TopN {
@@ -1849,7 +1868,7 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
     if (b == d.word_off[v])
       row_bytes += int32_t(v) < p.n_dense ? 4ull * uint64_t(K) : 4ull * d.ws_nnz[int(v) - p.n_dense];
     const WordRec rec = d.wrec[v];
-    const uint32_t K1 = rec.k1;
+    const uint32_t K1 = __builtin_amdgcn_readfirstlane(rec.k1);
     // C1 = D[d][K1] is sought only in the pass whose tile holds topic K1 (that
     // pass reads every chunk with topics of its tile); the other reads 0
     const bool k1_lo = K1 < kt;
@@ -1859,56 +1878,51 @@ __global__ __launch_bounds__(kTiledBlock) void k_sampler_tiled(DevState d, Param
       fill_tile(d, p, v, K1, tbase, tlen, kt, wt, tid, kTiledBlock);
       const TileState ts{wt, tbase, kt, 0u - tbase * 8u};
       if (pass < 2) {
-        // this tile's blocks of the Q' prefix, continuing the previous tile's
+        // this tile's blocks of the Q' prefix, continuing the previous tile's.
+        // Thread i sums blocks i and i + kTiledBlock of the tile (a tile has at
+        // most 2 * kTiledBlock blocks), the 16 topics of a block from topic
+        // i % 16 on, wrapping, so that the 16 lanes of a row read 16 different
+        // LDS bank pairs; the prefix is then a scan per wave, in registers,
+        // plus the totals of the waves before, added in wave order
         const int b0 = int(tbase) / kGroup, b1 = min(nb, int(tbase + tlen + kGroup - 1) / kGroup);
-        // block sums, one thread per block adding its topics in order; lane l
-        // starts l % 16 steps late, so that the lanes of a row read 16
-        // different topics of their blocks (16 different LDS bank pairs)
-        // instead of all the same one
-        const int skew = lane & (kGroup - 1);
-        for (int blk = b0 + tid; blk < b1; blk += kTiledBlock) {
-          const double *wb = wt + (blk - b0) * kGroup;
+        const int nblk = b1 - b0;
+        double *s_tot = s_u;  // [2 * waves]; s_u is next written in pass 1's token loop
+        // the rotation's start, opaque to the compiler: otherwise it keeps the
+        // 16 rotated addresses live (spilled) across the region loop
+        uint32_t rot;
+        asm volatile("v_mov_b32 %0, %1" : "=v"(rot) : "v"(uint32_t(li)));
+        auto block_scan = [&](int blk) {
           double sum = 0.0;
-#pragma unroll 8
-          for (int st = 0; st < 2 * kGroup - 1; ++st) {
-            const int i = st - skew;
-            const double w = wb[min(max(i, 0), kGroup - 1)];
-            sum = i >= 0 && i < kGroup ? __builtin_fma(p.alpha, w, sum) : sum;
+          if (blk < nblk) {
+            const double *wb = wt + blk * kGroup;
+#pragma unroll
+            for (uint32_t i = 0; i < uint32_t(kGroup); ++i)
+              sum = __builtin_fma(p.alpha, wb[(i + rot) & uint32_t(kGroup - 1)], sum);
           }
-          qb[blk + 1] = sum;
+          return wave_incl_scan(sum);
+        };
+        const double incl0 = block_scan(tid);
+        if (lane == kWave - 1) s_tot[wave] = incl0;
+        double incl1 = 0.0;
+        if (nblk > kTiledBlock) {
+          incl1 = block_scan(kTiledBlock + tid);
+          if (lane == kWave - 1) s_tot[waves + wave] = incl1;
         }
         __syncthreads();
-        if (wave == 0) {
-          // lane l scans a run of per consecutive blocks: their sum, a scan of
-          // the lane sums, then the running prefix over the run; the lane's
-          // block sums are read kScanBatch at a time (one LDS round trip each)
-          const int n = b1 - b0;
-          const int per = (n + kWave - 1) / kWave;
-          const int q0 = min(n, lane * per), q1 = min(n, q0 + per);
-          double sum = 0.0;
-          for (int q = q0; q < q1; q += kScanBatch) {
-            double v[kScanBatch];
-#pragma unroll
-            for (int i = 0; i < kScanBatch; ++i) v[i] = q + i < q1 ? qb[b0 + q + i + 1] : 0.0;
-#pragma unroll
-            for (int i = 0; i < kScanBatch; ++i)
-              if (q + i < q1) sum += v[i];
-          }
-          const double carry = pass == 0 ? 0.0 : qb[b0];
-          double run = carry + (group_incl_scan<kWave>(sum, lane) - sum);
-          for (int q = q0; q < q1; q += kScanBatch) {
-            double v[kScanBatch];
-#pragma unroll
-            for (int i = 0; i < kScanBatch; ++i) v[i] = q + i < q1 ? qb[b0 + q + i + 1] : 0.0;
-#pragma unroll
-            for (int i = 0; i < kScanBatch; ++i)
-              if (q + i < q1) {
-                run += v[i];
-                qb[b0 + q + i + 1] = run;
-              }
-          }
-          if (pass == 0 && lane == 0) qb[0] = 0.0;
+        double acc = pass == 0 ? 0.0 : qb[b0], own = 0.0;
+        for (int w = 0; w < waves; ++w) {
+          if (w == wave) own = acc;
+          acc += s_tot[w];
         }
+        if (tid < nblk) qb[b0 + tid + 1] = own + incl0;
+        if (nblk > kTiledBlock) {
+          for (int w = 0; w < waves; ++w) {
+            if (w == wave) own = acc;
+            acc += s_tot[waves + w];
+          }
+          if (kTiledBlock + tid < nblk) qb[b0 + kTiledBlock + tid + 1] = own + incl1;
+        }
+        if (pass == 0 && tid == 0) qb[0] = 0.0;
         __syncthreads();
       }
       const uint32_t stride = uint32_t(waves) * 4u;
@@ -2953,6 +2967,8 @@ hipError_t launch_sampler(const DevState &d, const Params &p, uint32_t t, hipStr
       return e != hipSuccess ? e : a.sharedSizeBytes == 0 ? hipSuccess : hipErrorInvalidConfiguration;
     }();
     if (lds_at_0 != hipSuccess) return lds_at_0;
+    // a tile's Q' blocks: at most two per thread
+    if (p.tile_topics / kGroup + 1 > 2 * kTiledBlock) return hipErrorInvalidValue;
     const size_t lds = tiled_lds_bytes(p.K, p.tile_topics);
     hipError_t err = allow_lds(k_sampler_tiled, lds);
     if (err != hipSuccess) return err;
