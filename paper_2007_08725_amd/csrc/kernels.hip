@@ -1470,38 +1470,55 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
         wh[K] = 0.0;  // topic of the padding entries of D rows
       }
       __syncthreads();
-      for (int blk = tid; blk < nb; blk += NB) {
+      // the Q' prefix over blocks of kGroup topics: thread i sums blocks i,
+      // i + NB, ..., then per round a scan per wave (DPP) leaves the block's
+      // prefix inside its wave in qb and the wave's total in s_u; after the
+      // barrier each block adds the totals before its wave, in round and wave
+      // order.  Without the partial-sum table a block is summed from topic
+      // i % 16 on, wrapping, so that the 16 lanes of a row read 16 different
+      // LDS bank pairs (wh past K holds zeros).
+      double *s_tot = s_u;  // [rounds * waves <= NB]; s_u is next written by the token batches
+      uint32_t rot;         // i % 16, opaque to the compiler: otherwise it keeps the 16 rotated addresses live
+      asm volatile("v_mov_b32 %0, %1" : "=v"(rot) : "v"(uint32_t(lane & (kGroup - 1))));
+      for (int r = 0; r * NB < nb; ++r) {
+        const int blk = r * NB + tid;
         double s = 0.0;
-        if (s_qw) {
-          // every topic of the block (zeros past K), as q_draw's walk adds them
-          double *pw = s_qw + blk * kQwStride;
-          int last = 0;
-          for (int i = 0; i < kGroup; ++i) {
-            pw[i] = s;
-            const double t = p.alpha * wh[blk * kGroup + i];
-            s += t;
-            last = t > 0.0 ? i : last;
+        if (blk < nb) {
+          if (s_qw) {
+            // every topic of the block (zeros past K), as q_draw's walk adds them
+            double *pw = s_qw + blk * kQwStride;
+            int last = 0;
+            for (int i = 0; i < kGroup; ++i) {
+              pw[i] = s;
+              const double t = p.alpha * wh[blk * kGroup + i];
+              s += t;
+              last = t > 0.0 ? i : last;
+            }
+            pw[kGroup] = s;
+            s_ql[blk] = uint8_t(last);
+          } else {
+            const double *wb = wh + blk * kGroup;
+#pragma unroll
+            for (uint32_t i = 0; i < uint32_t(kGroup); ++i) s += p.alpha * wb[(i + rot) & uint32_t(kGroup - 1)];
           }
-          pw[kGroup] = s;
-          s_ql[blk] = uint8_t(last);
-        } else {
-          const int k1 = min(K, (blk + 1) * kGroup);
-          for (int k = blk * kGroup; k < k1; ++k) s += p.alpha * wh[k];
         }
-        qb[blk + 1] = s;
+        const double incl = wave_incl_scan(s);
+        if (blk < nb) qb[blk + 1] = incl;
+        if (lane == kWave - 1) s_tot[r * (NB / kWave) + wave] = incl;
       }
       __syncthreads();
-      if (wave == 0) {
-        const int per = (nb + kWave - 1) / kWave;
-        const int q0 = min(nb, lane * per), q1 = min(nb, q0 + per);
-        double s = 0.0;
-        for (int q = q0; q < q1; ++q) s += qb[q + 1];
-        double run = group_incl_scan<kWave>(s, lane) - s;
-        for (int q = q0; q < q1; ++q) {
-          run += qb[q + 1];
-          qb[q + 1] = run;
+      {
+        double acc = 0.0;
+        for (int r = 0; r * NB < nb; ++r) {
+          double own = 0.0;
+          for (int w = 0; w < NB / kWave; ++w) {
+            if (w == wave) own = acc;
+            acc += s_tot[r * (NB / kWave) + w];
+          }
+          const int blk = r * NB + tid;
+          if (blk < nb) qb[blk + 1] = own + qb[blk + 1];
         }
-        if (lane == 0) qb[0] = 0.0;
+        if (tid == 0) qb[0] = 0.0;
       }
       __syncthreads();
     }
