@@ -160,6 +160,33 @@ def test_philox_matches_rocrand():
         assert got == want, c
 
 
+def test_uniform_and_init_follow_the_stated_layout():
+    """u and the initial topics as the boundary states them, from Philox words that rocRAND's
+    engine computes (not the oracle's Philox): u = ((x0 << 32 | x1) >> 11) * 2^-53 at counter
+    (i, 0, t, 0) and z0 = (x0 * K) >> 32 at counter (i, 0, 0, 1), key = seed.  A swapped
+    word, a shift by another amount or a counter slot moved would change the bits."""
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    if not os.path.exists(hipcc):
+        pytest.skip("hipcc not available")
+    exe = os.path.join(os.environ.get("TMPDIR", "/tmp"), "rocrand_philox_layout_%d" % os.getpid())
+    subprocess.run([hipcc, "-O1", "-o", exe, os.path.join(HERE, "pins", "rocrand_philox_kat.cpp")], check=True,
+                   capture_output=True)
+    rng = np.random.default_rng(11)
+    draws = [(int(rng.integers(0, 2**63)), int(rng.integers(0, 2**32)), int(rng.integers(0, 200))) for _ in range(100)]
+    inits = [(int(rng.integers(0, 2**63)), int(rng.integers(0, 2**20)), int(rng.integers(1, 40000))) for _ in range(100)]
+    inp = "".join("%d %d 0 %d 0\n" % (seed, i, t) for seed, i, t in draws)
+    inp += "".join("%d %d 0 0 1\n" % (seed, i) for seed, i, _ in inits)
+    out = subprocess.run([exe], input=inp, capture_output=True, text=True, check=True).stdout.split("\n")
+    os.unlink(exe)
+    words = [[int(x) for x in line.split()] for line in out[:len(draws) + len(inits)]]
+    for (seed, i, t), x in zip(draws, words[:len(draws)]):
+        want = float(((x[0] << 32) | x[1]) >> 11) * 2.0**-53
+        assert ora.uniform(seed, t, i) == want, (seed, i, t)
+    for (seed, i, K), x in zip(inits, words[len(draws):]):
+        z = ora.init_topics(i + 1, K, seed)
+        assert int(z[i]) == (x[0] * K) >> 32, (seed, i, K)
+
+
 def test_uniform_and_init_are_uniform():
     n = 200_000
     z = ora.init_topics(n, 16, 42)
