@@ -476,6 +476,72 @@ __global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
   if (tid == 0) write_word_records(d, p, r, top, q, sw);
 }
 
+// Step 1 for K below the sparse-word list's threshold: one wave per word,
+// four words per workgroup, no workgroup barriers.  Lane l takes topics l,
+// l + 64, ...: its top values, then a merge across the wave by exchanges at
+// distances 32 down to 1 (the top set is unique under `better`, so every lane
+// ends with the same list), then Q' and the sum of W^[v] per lane in topic
+// order, summed over the wave.  A sparse row is spread into the wave's table
+// of K counts first.
+__global__ __launch_bounds__(kBlock) void k_word_pre_wave(DevState d, Params p) {
+  extern __shared__ uint16_t wtab[];  // [kBlock / kWave][tab_stride]
+  const int K = p.K, lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int r = blockIdx.x * (kBlock / kWave) + wave;
+  if (r >= p.n_present) return;  // a whole wave; nothing below waits on the workgroup
+  const int stride = (K + 1) & ~1;
+  uint16_t *tab = wtab + size_t(wave) * size_t(stride);
+  const bool dense = r < p.n_dense;
+  const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
+  if (!dense) {
+    const int s = r - p.n_dense;
+    const uint32_t *ents = d.ws_ent + d.ws_cap[s];
+    const uint32_t nnz = d.ws_nnz[s];
+    for (int k = lane; k < K; k += kWave) tab[k] = 0;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");  // a wave's LDS accesses run in order
+    for (uint32_t q = uint32_t(lane); q < nnz; q += kWave) {
+      const uint32_t ent = ents[q];
+      tab[ent >> 16] = uint16_t(ent & 0xFFFFu);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  auto count_of = [&](int k) { return dense ? uint32_t(wrow[k]) : uint32_t(tab[k]); };
+  TopN t;
+  for (int q = 0; q < kTop; ++q) {
+    t.v[q] = -1.0;
+    t.k[q] = 0xFFFFFFFFu;
+  }
+  for (int k = lane; k < K; k += kWave) top_insert(t, what(count_of(k), p.beta, d.den[k]), uint32_t(k));
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) {
+    double pv[kTop];
+    uint32_t pk[kTop];
+#pragma unroll
+    for (int q = 0; q < kTop; ++q) {
+      pv[q] = __shfl_xor(t.v[q], o, kWave);
+      pk[q] = uint32_t(__shfl_xor(int(t.k[q]), o, kWave));
+    }
+#pragma unroll
+    for (int q = 0; q < kTop; ++q) top_insert(t, pv[q], pk[q]);
+  }
+  WordTop top;
+  top.k1 = t.k[0];
+  top.k2 = t.k[1];
+  top.k3 = t.k[2];
+  top.a1 = t.v[0];
+  top.a2 = t.v[1];
+  top.a3 = t.v[2] > 0.0 ? t.v[2] : 0.0;
+  top.a4 = t.v[3] > 0.0 ? t.v[3] : 0.0;
+  double q = 0.0, sw = 0.0;
+  for (int k = lane; k < K; k += kWave) {
+    const double w = what(count_of(k), p.beta, d.den[k]);
+    sw += w;
+    if (p.two_branch || uint32_t(k) != top.k1) q += p.alpha * w;
+  }
+  q = group_sum<kWave>(q);
+  sw = group_sum<kWave>(sw);
+  if (lane == 0) write_word_records(d, p, r, top, q, sw);
+}
+
 // Steps 2 and 3: per document, C1 = D[d][K1], C2 = D[d][K2], u, M, S_est and
 // the skip test (Eq. 7 and 9).  One wave per document; documents are handed
 // out in batches through an atomic counter.  The document's D row is spread
@@ -2908,6 +2974,12 @@ hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s) {
     if (err != hipSuccess) return err;
     err = launch_beta_sum(d, p, s);
     if (err != hipSuccess) return err;
+  }
+  if (!p.sparse_pre && p.K <= kWordTab) {
+    const size_t lds = sizeof(uint16_t) * size_t((p.K + 1) & ~1) * (kBlock / kWave);
+    const uint32_t grid = uint32_t((p.n_present + kBlock / kWave - 1) / (kBlock / kWave));
+    hipLaunchKernelGGL(k_word_pre_wave, dim3(grid), dim3(kBlock), lds, s, d, p);
+    return hipGetLastError();
   }
   hipLaunchKernelGGL(k_word_pre, dim3(uint32_t(p.n_present)), dim3(kBlock), 0, s, d, p);
   return hipGetLastError();
