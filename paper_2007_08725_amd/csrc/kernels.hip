@@ -2,7 +2,8 @@
 //
 // One synchronous iteration (Sec. 2.2, 3.2, 4.3):
 //   k_begin      den[k] = T[k] + V*beta; scheduler counters reset
-//   k_word_pre   per word: top-3 of W^[v] (K1, K2, a1..a3), Q' and sum W^   (step 1, Sec. 3.2)
+//   k_word_pre_wave (K < 4096) or k_word_pre
+//                per word: top-3 of W^[v] (K1, K2, a1..a3), Q' and sum W^   (step 1, Sec. 3.2)
 //   k_clear_skips
 //                the skip bitmap (one bit per word-ordered token) cleared
 //   k_doc_pass   per document: C1, C2 by lookup in the D row, u, M, S_est
@@ -11,7 +12,7 @@
 //                then for every token whose bit is clear C1 and S' over
 //                nz(D[d]) and the final draw over [K1 | S' | Q']; every
 //                topic slot of the region written (K1 for the skipped)     (steps 4-6, Sec. 4.3)
-//   k_zero_split, k_rebuild_w, k_rebuild_d
+//   k_zero_split, k_rebuild_w_wave, k_rebuild_d
 //                count tables of the new assignment: dense rows of W by
 //                histogram (integer atomics for split words), sparse rows of
 //                W and rows of D as packed (topic << 16 | count) entries, T
@@ -2276,77 +2277,77 @@ __global__ void k_zero_split(DevState d, Params p) {
     d.T[k] = 0u;
 }
 
-// W rebuild from the word-ordered topics: LDS histogram per region; dense
-// rows written whole (or added with atomics when the word is split), sparse
-// rows compacted to ascending packed entries; T accumulated per workgroup.
-// W rebuild for moderate K: per region a K-entry histogram, scanned in full.
 constexpr int kHistAhead = 8;  // word-ordered topic loads per thread issued together in the W rebuild
 
-__global__ __launch_bounds__(kBlock) void k_rebuild_w(DevState d, Params p) {
+// W rebuild for K below kWBitsK by one wave per region, the regions dealt
+// round-robin over the waves of the grid, with no workgroup barrier per
+// region: the region's counts in the wave's LDS table, then the dense row
+// written whole (added with atomics when the word is split) or the sparse
+// row compacted in ascending topic order, 64 topics per step by ballot; the
+// table is cleared as it is read.  T is accumulated per workgroup in LDS and
+// added to the device once at the end.
+__global__ __launch_bounds__(kBlock) void k_rebuild_w_wave(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
-  uint32_t *hist = ldsu;                           // [K]
-  uint32_t *tloc = p.big_k ? nullptr : ldsu + K;  // [K]; large K: T is added per region instead
-  __shared__ uint32_t s_scan[kBlock / kWave];
-  const int tid = threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave, tid = threadIdx.x;
+  uint32_t *tloc = ldsu;                                  // [K], the workgroup's
+  uint32_t *hist = ldsu + size_t(K) * size_t(1 + wave);  // [K], the wave's
+  for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
+  for (int k = lane; k < K; k += kWave) hist[k] = 0u;
+  __syncthreads();
   uint32_t bad = 0;
-  if (tloc)
-    for (int k = tid; k < K; k += kBlock) tloc[k] = 0u;
-  // regions dealt round-robin: every thread reads its region's record itself,
-  // so no counter atomic and no broadcast through LDS sits in front of each
-  // region's loads (the work of a region follows its tokens, and the table
-  // interleaves large and small regions well enough that the tail stays short)
-  for (int64_t r = blockIdx.x;; r += gridDim.x) {
-    for (int k = tid; k < K; k += kBlock) hist[k] = 0u;
-    __syncthreads();
-    if (r >= p.n_regions) break;
+  const int64_t nwaves = int64_t(gridDim.x) * (kBlock / kWave);
+  for (int64_t r = int64_t(blockIdx.x) * (kBlock / kWave) + wave; r < p.n_regions; r += nwaves) {
     const uint32_t v = d.region[3 * size_t(r)], b = d.region[3 * size_t(r) + 1], e = d.region[3 * size_t(r) + 2];
-    // kHistAhead topic loads per thread in flight at once
-    for (uint32_t j0 = b + tid; j0 < e; j0 += uint32_t(kHistAhead * kBlock)) {
+    for (uint32_t j0 = b + uint32_t(lane); j0 < e; j0 += uint32_t(kHistAhead * kWave)) {
       uint32_t zz[kHistAhead];
 #pragma unroll
-      for (int u = 0; u < kHistAhead; ++u) zz[u] = uint32_t(u * kBlock) < e - j0 ? uint32_t(d.z_w[j0 + u * kBlock]) : 0u;
+      for (int u = 0; u < kHistAhead; ++u) zz[u] = uint32_t(u * kWave) < e - j0 ? uint32_t(d.z_w[j0 + u * kWave]) : 0u;
 #pragma unroll
       for (int u = 0; u < kHistAhead; ++u) {
-        if (uint32_t(u * kBlock) < e - j0) {
+        if (uint32_t(u * kWave) < e - j0) {
           if (zz[u] < uint32_t(K)) atomicAdd(&hist[zz[u]], 1u);
           else bad++;
         }
       }
     }
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");  // a wave's LDS accesses run in order
     if (int32_t(v) < p.n_dense) {
       int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
-      if (d.split[v]) {
-        for (int k = tid; k < K; k += kBlock)
-          if (hist[k]) atomicAdd(&wrow[k], int32_t(hist[k]));
-      } else {
-        for (int k = tid; k < K; k += kBlock) wrow[k] = int32_t(hist[k]);
+      const bool split = d.split[v] != 0;
+      for (int k = lane; k < K; k += kWave) {
+        const uint32_t h = hist[k];
+        hist[k] = 0u;
+        if (h) atomicAdd(&tloc[k], h);
+        if (!split) wrow[k] = int32_t(h);
+        else if (h) atomicAdd(&wrow[k], int32_t(h));
       }
     } else {
       const int s = int(v) - p.n_dense;
-      const int cs = (K + kBlock - 1) / kBlock;
-      const int c0 = min(K, tid * cs), c1 = min(K, c0 + cs);
-      uint32_t cnt = 0;
-      for (int k = c0; k < c1; ++k) cnt += hist[k] ? 1u : 0u;
-      uint32_t total = 0;
-      uint32_t off = block_exclusive_u32(cnt, s_scan, &total);
       uint32_t *out = d.ws_ent + d.ws_cap[s];
-      for (int k = c0; k < c1; ++k)
-        if (hist[k]) out[off++] = (uint32_t(k) << 16) | hist[k];
-      if (tid == 0) d.ws_nnz[s] = total;
+      uint32_t base = 0;
+      for (int k0 = 0; k0 < K; k0 += kWave) {
+        const int k = k0 + lane;
+        uint32_t h = 0;
+        if (k < K) {
+          h = hist[k];
+          hist[k] = 0u;
+        }
+        const unsigned long long m = __ballot(h != 0u);
+        if (h) {
+          atomicAdd(&tloc[k], h);
+          const uint32_t rank = __builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+          out[base + rank] = (uint32_t(k) << 16) | h;
+        }
+        base += uint32_t(__popcll(m));
+      }
+      if (lane == 0) d.ws_nnz[s] = base;
     }
-    if (tloc) {
-      for (int k = tid; k < K; k += kBlock) tloc[k] += hist[k];
-    } else {
-      for (int k = tid; k < K; k += kBlock)
-        if (hist[k]) atomicAdd(&d.T[k], hist[k]);
-    }
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   }
-  if (tloc)
-    for (int k = tid; k < K; k += kBlock)
-      if (tloc[k]) atomicAdd(&d.T[k], tloc[k]);
+  __syncthreads();
+  for (int k = tid; k < K; k += kBlock)
+    if (tloc[k]) atomicAdd(&d.T[k], tloc[k]);
   if (bad) atomicAdd(&d.stats[ST_ERRORS], (unsigned long long)bad);
 }
 
@@ -2371,7 +2372,7 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_w_bits(DevState d, Params p)
   for (int k = tid; k < nh; k += kBlock) hist[k] = 0u;
   for (int q = tid; q < nw; q += kBlock) bits[q] = 0u;
   __syncthreads();
-  // regions dealt round-robin, as in k_rebuild_w
+  // regions dealt round-robin over the workgroups
   for (int64_t r = blockIdx.x; r < p.n_regions; r += gridDim.x) {
     const uint32_t v = d.region[3 * size_t(r)], b = d.region[3 * size_t(r) + 1], e = d.region[3 * size_t(r) + 2];
     // kHistAhead topic loads per thread in flight at once
@@ -3139,10 +3140,11 @@ hipError_t launch_rebuild_w(const DevState &d, const Params &p, hipStream_t s) {
     if ((err = hipGetLastError()) != hipSuccess) return err;
     hipLaunchKernelGGL(k_topic_reduce, dim3(uint32_t((p.K + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, d, p, rows, G);
   } else {
-    const size_t wlds = sizeof(uint32_t) * 2 * size_t(p.K);
-    err = allow_lds(k_rebuild_w, wlds);
+    // one wave per region: the workgroup's T table and a count table per wave
+    const size_t wlds = sizeof(uint32_t) * (1 + kBlock / kWave) * size_t(p.K);
+    err = allow_lds(k_rebuild_w_wave, wlds);
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(k_rebuild_w, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
+    hipLaunchKernelGGL(k_rebuild_w_wave, dim3(uint32_t(p.grid_regions)), dim3(kBlock), wlds, s, d, p);
   }
   return hipGetLastError();
 }
