@@ -2,7 +2,7 @@
 //
 // One synchronous iteration (Sec. 2.2, 3.2, 4.3):
 //   k_begin      den[k] = T[k] + V*beta; scheduler counters reset
-//   k_word_pre_wave (K < 4096) or k_word_pre
+//   k_word_pre_wave
 //                per word: top-3 of W^[v] (K1, K2, a1..a3), Q' and sum W^   (step 1, Sec. 3.2)
 //   k_clear_skips
 //                the skip bitmap (one bit per word-ordered token) cleared
@@ -282,35 +282,6 @@ struct WordTop {
   double a1, a2, a3, a4;
 };
 
-// Block-wide top kTop of the threads' lists (sv, sk: kBlock * kTop slots).
-__device__ void block_top(TopN &t, double *__restrict__ sv, uint32_t *__restrict__ sk, int tid, WordTop &out) {
-  for (int q = 0; q < kTop; ++q) {
-    sv[tid * kTop + q] = t.v[q];
-    sk[tid * kTop + q] = t.k[q];
-  }
-  __syncthreads();
-  for (int stride = kBlock / 2; stride > 0; stride >>= 1) {
-    if (tid < stride) {
-      for (int q = 0; q < kTop; ++q) top_insert(t, sv[(tid + stride) * kTop + q], sk[(tid + stride) * kTop + q]);
-    }
-    __syncthreads();
-    if (tid < stride) {
-      for (int q = 0; q < kTop; ++q) {
-        sv[tid * kTop + q] = t.v[q];
-        sk[tid * kTop + q] = t.k[q];
-      }
-    }
-    __syncthreads();
-  }
-  out.k1 = sk[0];
-  out.k2 = sk[1];
-  out.k3 = sk[2];
-  out.a1 = sv[0];
-  out.a2 = sv[1];
-  out.a3 = sv[2] > 0.0 ? sv[2] : 0.0;
-  out.a4 = sv[3] > 0.0 ? sv[3] : 0.0;
-}
-
 // The sampler's and the skip test's per-word records.  In two-branch mode
 // (Sec. 2.2) the max-topic branch is empty (a1 = 0, K1 = K, a topic no row
 // holds with a count) and Q' is the full Q.
@@ -339,7 +310,7 @@ __device__ void write_word_records(const DevState &d, const Params &p, int r, co
 }
 
 // Large K: the sum over all topics of beta/den[k] (one workgroup, a fixed
-// order), for the sparse words' sums in k_word_pre.
+// order), for the sparse words' sums in k_word_pre_wave.
 __global__ __launch_bounds__(kBlock) void k_beta_sum(DevState d, Params p) {
   __shared__ double red[kBlock / kWave];
   const int K = p.K;
@@ -351,167 +322,19 @@ __global__ __launch_bounds__(kBlock) void k_beta_sum(DevState d, Params p) {
   if (threadIdx.x == 0) d.beta_sum[0] = s;
 }
 
-constexpr int kWordTab = 4096;  // topics of the sparse-row count table of k_word_pre
-__global__ __launch_bounds__(kBlock) void k_word_pre(DevState d, Params p) {
-  const int r = blockIdx.x, tid = threadIdx.x;
-  const int K = p.K;
-  __shared__ uint16_t ctab[kWordTab];
-  __shared__ double sv[kBlock * kTop];
-  __shared__ uint32_t sk[kBlock * kTop];
-  __shared__ double red[kBlock / kWave];
-  const bool dense = r < p.n_dense;
-  const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
-  const uint32_t *ents = nullptr;
-  uint32_t nnz = 0;
-  if (!dense) {
-    const int s = r - p.n_dense;
-    ents = d.ws_ent + d.ws_cap[s];
-    nnz = d.ws_nnz[s];
-  }
-  // sparse rows: each thread walks a contiguous chunk of topics
-  const int cs = (K + kBlock - 1) / kBlock;
-  const int c0 = min(K, tid * cs), c1 = min(K, c0 + cs);
-  __shared__ int s_full;
-
-  TopN t;
-  for (int q = 0; q < kTop; ++q) {
-    t.v[q] = -1.0;
-    t.k[q] = 0xFFFFFFFFu;
-  }
-  if (!dense && p.sparse_pre) {
-    // Large K, sparse word: W^ = beta/den[k] on every topic outside the row.
-    // The top values come from the row's topics and from the first topics
-    // outside the row in the list of all topics by ascending T (descending
-    // beta/den[k], lowest id first on ties); the sums use the sum of
-    // beta/den[k] over all topics, corrected on the row's topics.
-    double snz = 0.0, sb = 0.0;
-    for (uint32_t q = uint32_t(tid); q < nnz; q += kBlock) {
-      const uint32_t ent = ents[q], k = ent >> 16;
-      const double w = what(ent & 0xFFFFu, p.beta, d.den[k]);
-      top_insert(t, w, k);
-      snz += w;
-      sb += d.bden[k];
-    }
-    if (tid == 0) {
-      int found = 0;
-      const int want = min(kTop, K - int(nnz));
-      for (int i = 0; i < p.top_list && found < want; ++i) {
-        const uint32_t k = d.topic_order[i];
-        const uint32_t lb = row_lower_bound(ents, nnz, k);
-        if (lb < nnz && (ents[lb] >> 16) == k) continue;
-        top_insert(t, d.bden[k], k);
-        found++;
-      }
-      s_full = found < want;  // the list ran out: scan every topic instead
-    }
-    snz = block_sum(snz, red);
-    sb = block_sum(sb, red);
-    __syncthreads();
-    if (!s_full) {
-      WordTop top;
-      block_top(t, sv, sk, tid, top);
-      if (tid == 0) {
-        const double sw = (d.beta_sum[0] - sb) + snz;
-        write_word_records(d, p, r, top, p.two_branch ? p.alpha * sw : p.alpha * (sw - top.a1), sw);
-      }
-      return;
-    }
-    for (int q = 0; q < kTop; ++q) {
-      t.v[q] = -1.0;
-      t.k[q] = 0xFFFFFFFFu;
-    }
-  }
-  // a sparse row spread into a table of counts in LDS (K up to kWordTab),
-  // so that each thread reads its topics' counts instead of searching the row
-  const bool tab = !dense && K <= kWordTab;
-  if (tab) {
-    for (int k = tid; k < K; k += kBlock) ctab[k] = 0;
-    __syncthreads();
-    for (uint32_t q = uint32_t(tid); q < nnz; q += kBlock) {
-      const uint32_t ent = ents[q];
-      ctab[ent >> 16] = uint16_t(ent & 0xFFFFu);
-    }
-    __syncthreads();
-  }
-  if (dense) {
-    for (int k = tid; k < K; k += kBlock) top_insert(t, what(uint32_t(wrow[k]), p.beta, d.den[k]), uint32_t(k));
-  } else if (tab) {
-    for (int k = c0; k < c1; ++k) top_insert(t, what(ctab[k], p.beta, d.den[k]), uint32_t(k));
-  } else {
-    uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
-    for (int k = c0; k < c1; ++k) {
-      uint32_t c = 0;
-      if (e < nnz && (ents[e] >> 16) == uint32_t(k)) c = ents[e++] & 0xFFFFu;
-      top_insert(t, what(c, p.beta, d.den[k]), uint32_t(k));
-    }
-  }
-  WordTop top;
-  block_top(t, sv, sk, tid, top);
-  const uint32_t K1 = top.k1;
-
-  double q = 0.0, sw = 0.0;
-  if (dense) {
-    for (int k = tid; k < K; k += kBlock) {
-      const double w = what(uint32_t(wrow[k]), p.beta, d.den[k]);
-      sw += w;
-      if (p.two_branch || uint32_t(k) != K1) q += p.alpha * w;
-    }
-  } else if (tab) {
-    for (int k = c0; k < c1; ++k) {
-      const double w = what(ctab[k], p.beta, d.den[k]);
-      sw += w;
-      if (p.two_branch || uint32_t(k) != K1) q += p.alpha * w;
-    }
-  } else {
-    uint32_t e = row_lower_bound(ents, nnz, uint32_t(c0));
-    for (int k = c0; k < c1; ++k) {
-      uint32_t c = 0;
-      if (e < nnz && (ents[e] >> 16) == uint32_t(k)) c = ents[e++] & 0xFFFFu;
-      const double w = what(c, p.beta, d.den[k]);
-      sw += w;
-      if (p.two_branch || uint32_t(k) != K1) q += p.alpha * w;
-    }
-  }
-  q = block_sum(q, red);
-  sw = block_sum(sw, red);
-  if (tid == 0) write_word_records(d, p, r, top, q, sw);
-}
-
-// Step 1 for K below the sparse-word list's threshold: one wave per word,
-// four words per workgroup, no workgroup barriers.  Lane l takes topics l,
-// l + 64, ...: its top values, then a merge across the wave by exchanges at
-// distances 32 down to 1 (the top set is unique under `better`, so every lane
-// ends with the same list), then Q' and the sum of W^[v] per lane in topic
-// order, summed over the wave.  A sparse row is spread into the wave's table
-// of K counts first.
-__global__ __launch_bounds__(kBlock) void k_word_pre_wave(DevState d, Params p) {
-  extern __shared__ uint16_t wtab[];  // [kBlock / kWave][tab_stride]
-  const int K = p.K, lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  const int r = blockIdx.x * (kBlock / kWave) + wave;
-  if (r >= p.n_present) return;  // a whole wave; nothing below waits on the workgroup
-  const int stride = (K + 1) & ~1;
-  uint16_t *tab = wtab + size_t(wave) * size_t(stride);
-  const bool dense = r < p.n_dense;
-  const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
-  if (!dense) {
-    const int s = r - p.n_dense;
-    const uint32_t *ents = d.ws_ent + d.ws_cap[s];
-    const uint32_t nnz = d.ws_nnz[s];
-    for (int k = lane; k < K; k += kWave) tab[k] = 0;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");  // a wave's LDS accesses run in order
-    for (uint32_t q = uint32_t(lane); q < nnz; q += kWave) {
-      const uint32_t ent = ents[q];
-      tab[ent >> 16] = uint16_t(ent & 0xFFFFu);
-    }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  }
-  auto count_of = [&](int k) { return dense ? uint32_t(wrow[k]) : uint32_t(tab[k]); };
-  TopN t;
-  for (int q = 0; q < kTop; ++q) {
-    t.v[q] = -1.0;
-    t.k[q] = 0xFFFFFFFFu;
-  }
-  for (int k = lane; k < K; k += kWave) top_insert(t, what(count_of(k), p.beta, d.den[k]), uint32_t(k));
+// Step 1, one wave per word, four words per workgroup, no workgroup
+// barriers.  Lane l takes topics l, l + 64, ...: its top values, then a merge
+// across the wave by exchanges at distances 32 down to 1 (the top set is
+// unique under `better`, so every lane ends with the same list), then Q' and
+// the sum of W^[v] per lane in topic order, summed over the wave.  Below
+// K = 4,096 a sparse row is spread into the wave's table of K counts first.
+// From K = 4,096 on (p.sparse_pre) a sparse word's W^ is beta/den[k] outside
+// its row: its top values come from the row and from the first topics
+// outside the row in the list of all topics by ascending T (descending
+// beta/den[k], lowest id first on ties), 64 candidates of the list at a time;
+// its sums from the sum of beta/den[k] over all topics, corrected on the
+// row.  Should the list run out, every topic is scanned.
+__device__ __forceinline__ void wave_top_merge(TopN &t) {
 #pragma unroll
   for (int o = kWave / 2; o > 0; o >>= 1) {
     double pv[kTop];
@@ -524,6 +347,8 @@ __global__ __launch_bounds__(kBlock) void k_word_pre_wave(DevState d, Params p) 
 #pragma unroll
     for (int q = 0; q < kTop; ++q) top_insert(t, pv[q], pk[q]);
   }
+}
+__device__ __forceinline__ WordTop word_top_of(const TopN &t) {
   WordTop top;
   top.k1 = t.k[0];
   top.k2 = t.k[1];
@@ -532,11 +357,123 @@ __global__ __launch_bounds__(kBlock) void k_word_pre_wave(DevState d, Params p) 
   top.a2 = t.v[1];
   top.a3 = t.v[2] > 0.0 ? t.v[2] : 0.0;
   top.a4 = t.v[3] > 0.0 ? t.v[3] : 0.0;
+  return top;
+}
+__global__ __launch_bounds__(kBlock) void k_word_pre_wave(DevState d, Params p) {
+  extern __shared__ uint16_t wtab[];  // below K = 4,096: [kBlock / kWave][(K + 1) & ~1]
+  const int K = p.K, lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  const int r = blockIdx.x * (kBlock / kWave) + wave;
+  if (r >= p.n_present) return;  // a whole wave; nothing below waits on the workgroup
+  const bool dense = r < p.n_dense;
+  const int32_t *wrow = dense ? d.w_dense + size_t(r) * size_t(K) : nullptr;
+  const uint32_t *ents = nullptr;
+  uint32_t nnz = 0;
+  if (!dense) {
+    const int s = r - p.n_dense;
+    ents = d.ws_ent + d.ws_cap[s];
+    nnz = d.ws_nnz[s];
+  }
+  TopN t;
+  auto reset = [&]() {
+    for (int q = 0; q < kTop; ++q) {
+      t.v[q] = -1.0;
+      t.k[q] = 0xFFFFFFFFu;
+    }
+  };
+  reset();
+  if (!dense && p.sparse_pre) {
+    double snz = 0.0, sb = 0.0;
+    for (uint32_t q = uint32_t(lane); q < nnz; q += kWave) {
+      const uint32_t ent = ents[q], k = ent >> 16;
+      const double w = what(ent & 0xFFFFu, p.beta, d.den[k]);
+      top_insert(t, w, k);
+      snz += w;
+      sb += d.bden[k];
+    }
+    const uint32_t want = uint32_t(min(kTop, K - int(nnz)));
+    uint32_t found = 0;
+    for (int i0 = 0; i0 < p.top_list && found < want; i0 += kWave) {
+      const int i = i0 + lane;
+      bool cand = false;
+      uint32_t k = 0;
+      if (i < p.top_list) {
+        k = d.topic_order[i];
+        const uint32_t lb = row_lower_bound(ents, nnz, k);
+        cand = !(lb < nnz && (ents[lb] >> 16) == k);
+      }
+      const unsigned long long m = __ballot(cand);
+      const uint32_t rank = __builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+      if (cand && rank < want - found) top_insert(t, d.bden[k], k);
+      found += min(uint32_t(__popcll(m)), want - found);
+    }
+    wave_top_merge(t);
+    snz = group_sum<kWave>(snz);
+    sb = group_sum<kWave>(sb);
+    if (found >= want) {
+      const WordTop top = word_top_of(t);
+      if (lane == 0) {
+        const double sw = (d.beta_sum[0] - sb) + snz;
+        write_word_records(d, p, r, top, p.two_branch ? p.alpha * sw : p.alpha * (sw - top.a1), sw);
+      }
+      return;
+    }
+    reset();  // the list ran out: every topic below
+  }
+  const bool tab = !dense && !p.sparse_pre;
+  uint16_t *ct = wtab + size_t(wave) * size_t((K + 1) & ~1);
+  if (tab) {
+    for (int k = lane; k < K; k += kWave) ct[k] = 0;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");  // a wave's LDS accesses run in order
+    for (uint32_t q = uint32_t(lane); q < nnz; q += kWave) {
+      const uint32_t ent = ents[q];
+      ct[ent >> 16] = uint16_t(ent & 0xFFFFu);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  // counts: the dense row, the table, or (a large-K sparse row whose topic
+  // list ran out) a search of the row
+  auto count_of = [&](int k) -> uint32_t {
+    if (dense) return uint32_t(wrow[k]);
+    if (tab) return uint32_t(ct[k]);
+    const uint32_t lb = row_lower_bound(ents, nnz, uint32_t(k));
+    return lb < nnz && (ents[lb] >> 16) == uint32_t(k) ? (ents[lb] & 0xFFFFu) : 0u;
+  };
+  // kPreAhead topics per lane at a time, their loads issued together (a
+  // dense row at K = 32,768 is 512 topics per lane)
+  constexpr int kPreAhead = 8;
+  auto batch = [&](int k0, double (&w)[kPreAhead]) {
+    uint32_t c[kPreAhead];
+    double dn[kPreAhead];
+#pragma unroll
+    for (int u = 0; u < kPreAhead; ++u) {
+      const int k = min(k0 + u * kWave, K - 1);
+      c[u] = count_of(k);
+      dn[u] = d.den[k];
+    }
+#pragma unroll
+    for (int u = 0; u < kPreAhead; ++u) w[u] = what(c[u], p.beta, dn[u]);
+  };
+  for (int k0 = lane; k0 < K; k0 += kPreAhead * kWave) {
+    double w[kPreAhead];
+    batch(k0, w);
+#pragma unroll
+    for (int u = 0; u < kPreAhead; ++u)
+      if (k0 + u * kWave < K) top_insert(t, w[u], uint32_t(k0 + u * kWave));
+  }
+  wave_top_merge(t);
+  const WordTop top = word_top_of(t);
   double q = 0.0, sw = 0.0;
-  for (int k = lane; k < K; k += kWave) {
-    const double w = what(count_of(k), p.beta, d.den[k]);
-    sw += w;
-    if (p.two_branch || uint32_t(k) != top.k1) q += p.alpha * w;
+  for (int k0 = lane; k0 < K; k0 += kPreAhead * kWave) {
+    double w[kPreAhead];
+    batch(k0, w);
+#pragma unroll
+    for (int u = 0; u < kPreAhead; ++u) {
+      const int k = k0 + u * kWave;
+      if (k < K) {
+        sw += w[u];
+        if (p.two_branch || uint32_t(k) != top.k1) q += p.alpha * w[u];
+      }
+    }
   }
   q = group_sum<kWave>(q);
   sw = group_sum<kWave>(sw);
@@ -2976,13 +2913,10 @@ hipError_t launch_word_pre(const DevState &d, const Params &p, hipStream_t s) {
     err = launch_beta_sum(d, p, s);
     if (err != hipSuccess) return err;
   }
-  if (!p.sparse_pre && p.K <= kWordTab) {
-    const size_t lds = sizeof(uint16_t) * size_t((p.K + 1) & ~1) * (kBlock / kWave);
-    const uint32_t grid = uint32_t((p.n_present + kBlock / kWave - 1) / (kBlock / kWave));
-    hipLaunchKernelGGL(k_word_pre_wave, dim3(grid), dim3(kBlock), lds, s, d, p);
-    return hipGetLastError();
-  }
-  hipLaunchKernelGGL(k_word_pre, dim3(uint32_t(p.n_present)), dim3(kBlock), 0, s, d, p);
+  // below K = 4,096 a table of K 16-bit counts per wave (at most 32 KB)
+  const size_t lds = p.sparse_pre ? 0 : sizeof(uint16_t) * size_t((p.K + 1) & ~1) * (kBlock / kWave);
+  const uint32_t grid = uint32_t((p.n_present + kBlock / kWave - 1) / (kBlock / kWave));
+  hipLaunchKernelGGL(k_word_pre_wave, dim3(grid), dim3(kBlock), lds, s, d, p);
   return hipGetLastError();
 }
 

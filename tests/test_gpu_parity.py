@@ -396,6 +396,38 @@ def test_edge_cases(name, c):
 
 
 
+def test_topic_list_running_out_follows_the_oracle():
+    """From K = 4,096 on, a sparse word's top values come from its row and from the first topics
+    outside the row in the list of the 512 topics of lowest T.  Here word 0 holds 4,094 of the
+    4,096 topics, and the two it lacks carry the most tokens, so every listed topic is in its row
+    and the per-word pass scans all topics instead; the draws are still the oracle's."""
+    K = 4096
+    rng = np.random.default_rng(31)
+    n0, n1 = K - 2, 5000
+    word = np.concatenate([np.zeros(n0, np.int32), np.ones(n1, np.int32), rng.integers(2, 60, 3000).astype(np.int32)])
+    doc = rng.integers(0, 120, word.shape[0]).astype(np.int32)
+    z = np.concatenate([rng.permutation(n0).astype(np.int32),           # word 0: topics 0..4093, once each
+                        (K - 2 + np.arange(n1) % 2).astype(np.int32),   # word 1: the two topics word 0 lacks
+                        rng.integers(0, K - 2, 3000).astype(np.int32)])
+    order = np.argsort(doc, kind="stable")
+    word, doc, z = word[order], doc[order], z[order]
+    c = _Tiny(word, doc, 60, K, 0.05)
+    kw = dict(M=c.n_docs, V=c.V, K=c.K, alpha=c.alpha, beta=c.beta)
+    T = np.bincount(z, minlength=K)
+    lowest = np.lexsort((np.arange(K), T))[:512]
+    assert np.all(lowest < K - 2)  # every listed topic is one of word 0's
+    say("topic list running out K=%d N=%d" % (K, c.N))
+    with lda_make(c) as m:
+        for t in range(2):
+            zo, flags, _ = oracle.iterate(c.word, c.doc, z, seed=SEED, t=t, **kw)
+            m.set_assignments(z, t)
+            m.iterate(1)
+            cnt = m.counts()
+            compare_draws(cnt["z"], zo, flags, c.N)
+            check_counts_are_histograms(c, cnt, c.K)
+            z = zo
+
+
 @pytest.mark.parametrize("K,marks,shuffle", [(64, 1, False), (64, 2, False), (1000, 0, False), (1000, 1, True),
                                               (20000, 0, False)])
 def test_heavy_documents_follow_the_oracle(K, marks, shuffle):
