@@ -49,35 +49,34 @@ def sampler_alg_bytes(st, N):
     return (skip + 2 * N + 12 * st["sampled"] + 4 * st["nnz_scanned"] + st["row_bytes"] + 60 * st["regions"])
 
 
-def traffic_from_profile(workload):
+def _profile_field(workload, first, last, field):
+    """A per-launch k_sampler figure from the committed counter summary, if
+    the summary covers this workload and the same iterations (first..last)
+    and was taken on the current kernel source; else None."""
+    if workload != "c3" or not os.path.exists(PMC_SUMMARY):
+        return None
+    txt = open(PMC_SUMMARY).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", txt)
+    w = re.search(r"counter_window_iterations:\s*(\d+)-(\d+)", txt)
+    b = re.search(field + r":\s*([0-9.eE+]+)", txt)
+    if not m or not w or not b or (int(w.group(1)), int(w.group(2))) != (first, last):
+        return None
+    if hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest() != m.group(1):
+        return None
+    return float(b.group(1))
+
+
+def traffic_from_profile(workload, first, last):
     """Bytes per sampler launch that the L2 requested from the memory fabric
-    (reads by request size plus writes), from the committed counter summary,
-    if it covers this workload and was taken on the current kernel source;
-    else None."""
-    if workload != "c3" or not os.path.exists(PMC_SUMMARY):
-        return None
-    txt = open(PMC_SUMMARY).read()
-    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", txt)
-    b = re.search(r"k_sampler_fabric_bytes_per_launch:\s*([0-9.eE+]+)", txt)
-    if not m or not b:
-        return None
-    sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
-    if sha != m.group(1):
-        return None
-    return float(b.group(1))
+    (reads by request size plus writes), from the committed counter summary
+    (conditions of _profile_field); else None."""
+    return _profile_field(workload, first, last, "k_sampler_fabric_bytes_per_launch")
 
 
-def valu_from_profile(workload):
+def valu_from_profile(workload, first, last):
     """k_sampler's VALU wave instructions per launch from the committed
-    counter summary (same conditions as traffic_from_profile); else None."""
-    if workload != "c3" or not os.path.exists(PMC_SUMMARY):
-        return None
-    txt = open(PMC_SUMMARY).read()
-    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", txt)
-    b = re.search(r"k_sampler_valu_per_launch:\s*([0-9.eE+]+)", txt)
-    if not m or not b or hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest() != m.group(1):
-        return None
-    return float(b.group(1))
+    counter summary (conditions of _profile_field); else None."""
+    return _profile_field(workload, first, last, "k_sampler_valu_per_launch")
 
 
 VALU_ISSUE_PER_S = 1024 * 2.4e9 / 4  # wave instructions per second: 1,024 SIMDs, 4 cycles each at 2.4 GHz
@@ -173,8 +172,8 @@ def lda_seed():
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3", choices=["c1", "c2", "c3", "c4", "c5", "c6"])
     ap.add_argument("--cpu-docs", type=int, default=200000, help="documents in the oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -242,7 +241,7 @@ def main():
                     "hbm_copy_ceiling_gbs": copy_gbs}
     else:
         achieved = alg.sum() / (ms_sampler.sum() * 1e-3) / 1e9
-        traffic = traffic_from_profile(args.workload)
+        traffic = traffic_from_profile(args.workload, args.warmup, args.warmup + args.steps - 1)
         roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                     "traffic_kind": "fabric: bytes the L2 requested from memory per launch (reads by request "
@@ -253,7 +252,7 @@ def main():
                     "copy_ceiling_gbs": copy_gbs, "frac_of_copy": achieved / copy_gbs}
         if traffic is not None:
             roofline["traffic_gbs"] = traffic / (ms_sampler.mean() * 1e-3) / 1e9
-        valu = valu_from_profile(args.workload)
+        valu = valu_from_profile(args.workload, args.warmup, args.warmup + args.steps - 1)
         if valu is not None:
             # the limit the kernel actually meets: VALU instruction issue
             roofline["valu_issue_frac"] = valu / VALU_ISSUE_PER_S / (ms_sampler.mean() * 1e-3)
