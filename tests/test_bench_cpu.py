@@ -23,20 +23,24 @@ def test_traffic_is_read_only_for_the_profiled_kernel_source(tmp_path, monkeypat
     src.write_bytes(b"// some kernel source\n")
     summary = tmp_path / "summary.md"
     sha = hashlib.sha256(src.read_bytes()).hexdigest()
-    summary.write_text("kernel_source_sha256: %s\n\nk_sampler_fabric_bytes_per_launch: 1.5e+11\n" % sha)
+    summary.write_text("kernel_source_sha256: %s\n\ncounter_window_iterations: 5-24\n\n"
+                       "k_sampler_fabric_bytes_per_launch: 1.5e+11\n" % sha)
     monkeypatch.setattr(bench, "KERNEL_SOURCE", str(src))
     monkeypatch.setattr(bench, "PMC_SUMMARY", str(summary))
-    assert bench.traffic_from_profile("c3") == 1.5e11
+    assert bench.traffic_from_profile("c3", 5, 24) == 1.5e11
     # the counters cover the c3 workload only
-    assert bench.traffic_from_profile("c5") is None
+    assert bench.traffic_from_profile("c5", 5, 24) is None
+    # and only the iterations they were taken over
+    assert bench.traffic_from_profile("c3", 1, 100) is None
     # the kernel changed since the counters were taken: no traffic figure
     src.write_bytes(b"// some other kernel source\n")
-    assert bench.traffic_from_profile("c3") is None
+    assert bench.traffic_from_profile("c3", 5, 24) is None
     # no summary at all
     monkeypatch.setattr(bench, "PMC_SUMMARY", str(tmp_path / "missing.md"))
-    assert bench.traffic_from_profile("c3") is None
+    assert bench.traffic_from_profile("c3", 5, 24) is None
 
 
 def test_committed_counter_summary_names_a_source_hash_and_a_byte_count():
     txt = open(bench.PMC_SUMMARY).read()
     assert "kernel_source_sha256:" in txt and "k_sampler_fabric_bytes_per_launch:" in txt
+    assert "counter_window_iterations:" in txt
