@@ -1424,6 +1424,10 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
   // region, word and count variables are uniform over the block (scalar registers)
   uint32_t cur = 0xFFFFFFFFu, K1 = 0;
   double a1 = 0.0, qp = 0.0;
+  // the sparse word whose row wh holds (null if a dense row or none): the
+  // next sparse word only restores that word's topics and K1 to beta/den[k]
+  const uint32_t *held = nullptr;
+  uint32_t held_nnz = 0, held_k1 = 0;
   unsigned long long n_sampled = 0, n_after_s = 0, nnz_sum = 0;
   unsigned long long n_reg = 0, n_dreg = 0, row_bytes = 0;
 
@@ -1456,16 +1460,28 @@ __device__ __forceinline__ void sampler_body(DevState d, Params p, uint32_t t, u
       if (int32_t(v) < p.n_dense) {
         const int32_t *wrow = d.w_dense + size_t(v) * size_t(K);
         for (int k = tid; k < K; k += NB) wh[k] = what(uint32_t(wrow[k]), p.beta, d.den[k]);
+        held = nullptr;
       } else {
         const int s = int(v) - p.n_dense;
         const uint32_t *ents = d.ws_ent + d.ws_cap[s];
         const uint32_t nnz = d.ws_nnz[s];
-        for (int k = tid; k < K; k += NB) wh[k] = d.bden[k];
+        if (held) {
+          for (uint32_t q = tid; q < held_nnz; q += NB) {
+            const uint32_t k = held[q] >> 16;
+            wh[k] = d.bden[k];
+          }
+          if (tid == 0 && held_k1 < uint32_t(K)) wh[held_k1] = d.bden[held_k1];  // K1 = K in two-branch mode
+        } else {
+          for (int k = tid; k < K; k += NB) wh[k] = d.bden[k];
+        }
         __syncthreads();
         for (uint32_t q = tid; q < nnz; q += NB) {
           const uint32_t ent = ents[q];
           wh[ent >> 16] = what(ent & 0xFFFFu, p.beta, d.den[ent >> 16]);
         }
+        held = ents;
+        held_nnz = nnz;
+        held_k1 = K1;
       }
       __syncthreads();
       // the max topic is its own branch: W^' has a 0 there (Eq. 5)
