@@ -1848,8 +1848,6 @@ __device__ void fill_tile(const DevState &d, const Params &p, uint32_t v, uint32
   __syncthreads();
 }
 
-constexpr int kScanBatch = 8;  // Q' block sums a lane of the prefix scan reads at a time
-
 // A token's records for one pass of the tiled sampler.
 struct TiledTok {
   uint32_t sk, rec, cn;
