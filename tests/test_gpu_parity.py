@@ -375,6 +375,9 @@ def _edge_cases():
     yield "chunk_edges", _Tiny(word, doc, 400, 301, 0.05)
     perm = rng.permutation(doc.shape[0])  # the same corpus in shuffled input order (keys are not positions)
     yield "chunk_edges_shuffled", _Tiny(word[perm], doc[perm], 400, 301, 0.05)
+    # the largest K of the table-based per-word pass and W rebuild (whose LDS then passes 64 KB)
+    r2 = np.random.default_rng(78)
+    yield "K4095", _Tiny(r2.integers(0, 300, 20000), np.sort(r2.integers(0, 200, 20000)), 300, 4095, 0.05)
 
 
 @pytest.mark.parametrize("name,c", list(_edge_cases()), ids=[e[0] for e in _edge_cases()])
