@@ -2693,6 +2693,47 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d(DevState d, Params p, int 
 // ones emit_row writes: entries in ascending topic order, padding entries
 // of topic K, the header (length << 16 | entries).
 constexpr int kSortGather = 8;  // slots per lane whose loads are in flight together
+
+// Bitonic sort (ascending) of the P = 64 * E slots of sz in registers: lane l
+// holds slots l * E .. l * E + E - 1; compare-exchanges between slots of one
+// lane stay in registers, those between lanes exchange by shuffle.  The same
+// network as the sort in LDS below, so the same result.
+template <int E>
+__device__ __forceinline__ void sort_in_registers(uint16_t *__restrict__ sz, int lane) {
+  constexpr uint32_t P = uint32_t(E) * uint32_t(kWave);
+  uint32_t x[E];
+#pragma unroll
+  for (int r = 0; r < E; ++r) x[r] = sz[lane * E + r];
+#pragma unroll
+  for (uint32_t size = 2; size <= P; size <<= 1) {
+#pragma unroll
+    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+      if (stride < uint32_t(E)) {
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+          if ((uint32_t(r) & stride) == 0u) {
+            const int q = r | int(stride);
+            const bool asc = (uint32_t(lane * E + r) & size) == 0u;
+            const uint32_t lo = min(x[r], x[q]), hi = max(x[r], x[q]);
+            x[r] = asc ? lo : hi;
+            x[q] = asc ? hi : lo;
+          }
+        }
+      } else {
+        const int dl = int(stride / uint32_t(E));        // partner lane distance
+        const bool upper = (lane & dl) != 0;             // this lane holds the higher slot
+        const bool asc = (uint32_t(lane * E) & size) == 0u;
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+          const uint32_t o = uint32_t(__shfl_xor(int(x[r]), dl, kWave));
+          x[r] = (asc != upper) ? min(x[r], o) : max(x[r], o);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < E; ++r) sz[lane * E + r] = uint16_t(x[r]);
+}
 __global__ __launch_bounds__(kBlock) void k_rebuild_d_sort(DevState d, Params p) {
   extern __shared__ uint32_t ldsu[];
   const int K = p.K;
@@ -2735,8 +2776,15 @@ __global__ __launch_bounds__(kBlock) void k_rebuild_d_sort(DevState d, Params p)
         }
       }
       __threadfence_block();
-      // bitonic sort of the P slots, ascending
-      for (uint32_t size = 2; size <= P; size <<= 1) {
+      // bitonic sort of the P slots, ascending: in registers up to 512 slots
+      if (P <= 512u) {
+        if (P == 64u) sort_in_registers<1>(sz, lane);
+        else if (P == 128u) sort_in_registers<2>(sz, lane);
+        else if (P == 256u) sort_in_registers<4>(sz, lane);
+        else sort_in_registers<8>(sz, lane);
+        __threadfence_block();
+      }
+      for (uint32_t size = 2; P > 512u && size <= P; size <<= 1) {
         for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
           for (uint32_t t = uint32_t(lane); t < P / 2; t += kWave) {
             const uint32_t i = 2 * t - (t & (stride - 1)), j = i + stride;
