@@ -276,7 +276,7 @@ __global__ void k_begin(const uint32_t *__restrict__ T, double *__restrict__ den
   }
 }
 
-// Step 1 of Sec. 3.2 and the per-word Q' of Sec. 2.2 ("Q tree once per word").
+// Step 1 of Sec. 3.2 and the per-word Q' of Sec. 2.2 (built once per word).
 struct WordTop {
   uint32_t k1, k2, k3;
   double a1, a2, a3, a4;
@@ -322,8 +322,8 @@ __global__ __launch_bounds__(kBlock) void k_beta_sum(DevState d, Params p) {
   if (threadIdx.x == 0) d.beta_sum[0] = s;
 }
 
-// Step 1, one wave per word, four words per workgroup, no workgroup
-// barriers.  Lane l takes topics l, l + 64, ...: its top values, then a merge
+// Step 1 (Sec. 3.2) and Q' (Sec. 2.2), one wave per word, four words per
+// workgroup, no workgroup barriers.  Lane l takes topics l, l + 64, ...: its top values, then a merge
 // across the wave by exchanges at distances 32 down to 1 (the top set is
 // unique under `better`, so every lane ends with the same list), then Q' and
 // the sum of W^[v] per lane in topic order, summed over the wave.  Below
@@ -2230,7 +2230,7 @@ __global__ void k_zero_split(DevState d, Params p) {
 
 constexpr int kHistAhead = 8;  // word-ordered topic loads per thread issued together in the W rebuild
 
-// W rebuild for K below kWBitsK by one wave per region, the regions dealt
+// W rebuild (Sec. 4.3) for K below kWBitsK by one wave per region, the regions dealt
 // round-robin over the waves of the grid, with no workgroup barrier per
 // region: the region's counts in the wave's LDS table, then the dense row
 // written whole (added with atomics when the word is split) or the sparse
